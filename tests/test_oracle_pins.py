@@ -1,0 +1,363 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+None of these re-types the oracle's own formula: each checks it against a
+value worked by hand (tests/golden/hand_example.json), a brute-force
+computation organised differently (per sample and slot, no sorting, no
+dedup), an invariant the paper states (Sec. 3.1: data staleness is zero in
+synchronous training and GBA keeps the global batch of synchronous training;
+Eq. 1 excludes gradients past the threshold), or a closed form of the
+optimiser rules.
+"""
+import json
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle
+from synth import counter, workload
+from synth.configs import BY_NAME
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "hand_example.json")
+
+
+def _frac(x):
+    return float(Fraction(x))
+
+
+@pytest.fixture(scope="module")
+def hand():
+    with open(GOLDEN) as f:
+        return json.load(f)
+
+
+def _hand_inputs(h):
+    grads = np.array(h["dense_grads"], np.float32)
+    ids = np.array(h["ids"], np.int64)
+    rows = np.array(h["rows"], np.float32)
+    off = np.array(h["offsets"], np.int64)
+    tag = np.full(16, -7, np.int32)            # rows never touched keep their odd value
+    for r, t in h["tag_before"].items():
+        tag[int(r)] = t
+    return grads, ids, rows, off, tag
+
+
+# ---------------------------------------------------------------- hand example
+@pytest.mark.parametrize("case", ["iota1", "iota0"])
+def test_hand_example_weights_and_dense(hand, case):
+    c = hand["cases"][case]
+    w, s, nex = oracle.token_weights(hand["tokens"], hand["step"], c["iota"])
+    assert list(s) == c["staleness"]
+    assert list(w) == c["w"]
+    assert nex == c["num_excluded"]
+    grads, *_ = _hand_inputs(hand)
+    g = oracle.aggregate_dense(grads, w)
+    np.testing.assert_array_equal(g, np.array([_frac(x) for x in c["g_bar"]], np.float32))
+
+
+@pytest.mark.parametrize("case", ["iota1", "iota0"])
+@pytest.mark.parametrize("decay", ["token", "id_tag"])
+def test_hand_example_sparse(hand, case, decay):
+    c = hand["cases"][case]
+    grads, ids, rows, off, tag = _hand_inputs(hand)
+    w, _, _ = oracle.token_weights(hand["tokens"], hand["step"], c["iota"])
+    out = oracle.aggregate_sparse(ids, rows, off, w, hand["tokens"], hand["step"], c["iota"],
+                                  tag=tag, decay=decay)
+    assert list(out["unique_ids"]) == hand["unique_ids"]
+    assert list(out["seg_offsets"]) == hand["seg_offsets"]
+    assert list(out["contrib_count"]) == hand["contrib_count"]
+    assert list(out["active_count"]) == c[decay]["active_count"]
+    np.testing.assert_array_equal(out["agg"][:, 0], np.array([_frac(x) for x in c[decay]["agg"]], np.float32))
+    if decay == "id_tag":
+        after = out["new_tag"]
+        for r, t in c["id_tag"]["tag_after"].items():
+            assert after[int(r)] == t
+        untouched = np.setdiff1d(np.arange(16), [2, 7, 9])
+        assert np.all(after[untouched] == -7)
+
+
+def test_hand_example_adagrad(hand):
+    c = hand["cases"]["iota1"]
+    a = c["adagrad"]
+    grads, ids, rows, off, tag = _hand_inputs(hand)
+    w, _, _ = oracle.token_weights(hand["tokens"], hand["step"], c["iota"])
+    g = oracle.aggregate_dense(grads, w)
+    p, acc = oracle.adagrad(np.array(a["dense_param_before"], np.float32),
+                            np.array(a["dense_accum_before"], np.float32), g, a["lr"], a["eps"])
+    np.testing.assert_allclose(p, [_frac(x) for x in a["dense_param_after"]], rtol=2e-7)
+    np.testing.assert_allclose(acc, [_frac(x) for x in a["dense_accum_after"]], rtol=2e-7)
+    # rows, through the whole-step composition
+    tr = a["token_rows"]
+    table = {int(r): v for r, v in tr["param_before"].items()}
+    accum = {int(r): v for r, v in tr["accum_before"].items()}
+    res = oracle.gba_step(hand["tokens"], hand["step"], c["iota"], grads, ids, rows, off,
+                          np.array(a["dense_param_before"], np.float32),
+                          [np.array(a["dense_accum_before"], np.float32)],
+                          lambda rr: np.array([[table[int(r)]] for r in rr], np.float32),
+                          lambda k, rr: np.array([[accum[int(r)]] for r in rr], np.float32),
+                          "adagrad", dict(lr=a["lr"], eps=a["eps"]))
+    got = {int(r): (res["table_rows"][i, 0], res["table_slot_rows"][0][i, 0])
+           for i, r in enumerate(res["active_ids"])}
+    for r in (2, 7):
+        assert got[r][0] == np.float32(_frac(tr["param_after"][str(r)]))
+        assert got[r][1] == np.float32(_frac(tr["accum_after"][str(r)]))
+    assert 9 not in got                       # inactive row: not updated
+
+
+# ------------------------------------------------------------------ Eq. 1
+def test_eq1_sync_mode_keeps_everything():
+    """Sec. 3.1: data staleness is zero in synchronous training, so every
+    gradient passes the tolerance function whatever the threshold."""
+    for iota in (0, 1, 5):
+        w, s, nex = oracle.token_weights(np.full(9, 42), 42, iota)
+        assert np.all(s == 0) and np.all(w == 1) and nex == 0
+
+
+def test_eq1_threshold_is_monotone_and_bsp_limit():
+    """Raising iota never excludes more; iota >= max staleness excludes nothing
+    (the BSP limit, Sec. 4.1); iota = -1 would exclude everything."""
+    rng = np.random.default_rng(3)
+    tok = 100 - rng.integers(0, 12, 64)
+    prev = -1
+    for iota in range(0, 13):
+        _, _, nex = oracle.token_weights(tok, 100, iota)
+        assert prev == -1 or nex <= prev
+        prev = nex
+    assert oracle.token_weights(tok, 100, 11)[2] == 0
+    assert oracle.token_weights(tok, 100, -1)[2] == 64
+
+
+def test_eq1_future_token_is_error():
+    with pytest.raises(ValueError):
+        oracle.token_weights([3, 6], 5, 2)
+
+
+# ------------------------------------------------------- brute force (sparse)
+def _brute_sparse(ids, rows, offsets, w, tokens, iota, tag, decay, norm, R):
+    """Accumulate every (contribution, slot) into a full R x D array and a
+    K x R 'seen' table, with plain loops: no sort, no dedup."""
+    K = len(offsets) - 1
+    D = rows.shape[1]
+    acc = [[Fraction(0)] * D for _ in range(R)]
+    seen = [[False] * R for _ in range(K)]
+    active = [[False] * R for _ in range(K)]
+    for m in range(K):
+        for j in range(offsets[m], offsets[m + 1]):
+            r = int(ids[j])
+            seen[m][r] = True
+            if decay == "token":
+                wt = float(w[m])
+            else:
+                st = int(tag[r]) - int(tokens[m]) + 1
+                wt = 1.0 if (st if st > 0 else 0) <= iota else 0.0
+            if wt != 0:
+                active[m][r] = True
+                for d in range(D):
+                    acc[r][d] += Fraction(float(rows[j][d])) * Fraction(wt)
+    out = {}
+    for r in range(R):
+        c = sum(seen[m][r] for m in range(K))
+        if c == 0:
+            continue
+        W = sum(active[m][r] for m in range(K))
+        div = c if norm == "per_id_count" else K
+        out[r] = (c, W, [float(a / div) for a in acc[r]])
+    return out
+
+
+@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("decay", ["token", "id_tag"])
+@pytest.mark.parametrize("norm", ["per_id_count", "by_k"])
+def test_sparse_matches_brute_force(seed, decay, norm):
+    rng = np.random.default_rng(seed)
+    K, R, D = int(rng.integers(1, 8)), int(rng.integers(1, 40)), int(rng.integers(1, 5))
+    sizes = rng.integers(0, 12, K)                    # empty contributions included
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    N = int(off[-1])
+    ids = rng.integers(0, R, N).astype(np.int64)
+    rows = (rng.integers(-128, 128, (N, D)) * 2.0 ** -8).astype(np.float32)   # dyadic: exact sums
+    step, iota = 20, int(rng.integers(0, 4))
+    tokens = step - rng.integers(0, 6, K)
+    tag = rng.integers(-1, step, R).astype(np.int32)
+    w, _, _ = oracle.token_weights(tokens, step, iota)
+    got = oracle.aggregate_sparse(ids, rows, off, w, tokens, step, iota, tag, decay, norm)
+    ref = _brute_sparse(ids, rows, off, w, tokens, iota, tag, decay, norm, R)
+    assert list(got["unique_ids"]) == sorted(ref)
+    counts = np.bincount(ids, minlength=R)
+    assert list(np.diff(got["seg_offsets"])) == [int(counts[r]) for r in sorted(ref)]
+    for i, r in enumerate(got["unique_ids"]):
+        c, W, vals = ref[int(r)]
+        assert got["contrib_count"][i] == c
+        assert got["active_count"][i] == W
+        np.testing.assert_array_equal(got["agg"][i], np.array(vals, np.float32))
+    if decay == "id_tag":
+        act = [r for r in ref if ref[r][1] > 0]
+        exp_tag = tag.copy()
+        exp_tag[act] = step
+        np.testing.assert_array_equal(got["new_tag"], exp_tag)
+
+
+def test_dedup_special_cases():
+    # one ID repeated N times across 3 contributions
+    off = np.array([0, 5, 5, 9], np.int64)
+    u, so, c = oracle.dedup(np.full(9, 17), off)
+    assert list(u) == [17] and list(so) == [0, 9] and list(c) == [2]
+    # all IDs distinct
+    ids = np.array([9, 3, 14, 0, 7, 2], np.int64)
+    u, so, c = oracle.dedup(ids, np.array([0, 2, 6], np.int64))
+    assert list(u) == sorted(ids) and list(so) == list(range(7)) and np.all(c == 1)
+    # nothing at all
+    u, so, c = oracle.dedup(np.zeros(0, np.int64), np.array([0, 0], np.int64))
+    assert u.size == 0 and list(so) == [0] and c.size == 0
+
+
+# ------------------------------------------------- sync-mode invariant (Sec. 3.1)
+def test_sync_invariant_equals_global_batch_gradient():
+    """With every token fresh (staleness 0) and K local batches of B samples,
+    the GBA aggregate equals the synchronous gradient of the global batch of
+    K * B samples (Sec. 3.1: G_a = B_a M = G_s).  The reference here is the
+    mean over all K * B per-sample gradients, computed without contributions."""
+    rng = np.random.default_rng(11)
+    K, B, L, P, R, D = 6, 5, 3, 7, 13, 4
+    per_dense = rng.normal(size=(K, B, P))
+    per_ids = rng.integers(0, R, (K, B, L))
+    per_rows = rng.normal(size=(K, B, L, D))
+    # local gradient of contribution m = mean over its B samples
+    grads = [per_dense[m].mean(axis=0).astype(np.float32) for m in range(K)]
+    ids = per_ids.reshape(-1).astype(np.int64)
+    rows = (per_rows / B).reshape(-1, D).astype(np.float32)
+    off = np.arange(K + 1, dtype=np.int64) * B * L
+    tokens = np.full(K, 9)
+    w, _, nex = oracle.token_weights(tokens, 9, iota=0)
+    assert nex == 0
+    g = oracle.aggregate_dense(grads, w)
+    sync_dense = per_dense.reshape(K * B, P).mean(axis=0)
+    np.testing.assert_allclose(g, sync_dense, rtol=2e-6, atol=1e-7)
+    sp = oracle.aggregate_sparse(ids, rows, off, w, tokens, 9, 0, norm="by_k")
+    sync_rows = np.zeros((R, D))
+    for k in range(K):
+        for b in range(B):
+            for l in range(L):
+                sync_rows[per_ids[k, b, l]] += per_rows[k, b, l]
+    sync_rows /= K * B
+    np.testing.assert_allclose(sp["agg"], sync_rows[sp["unique_ids"]], rtol=2e-6, atol=1e-7)
+    assert np.all(sp["active_count"] == sp["contrib_count"])
+
+
+# ------------------------------------------------ threshold invariant (Eq. 1)
+@pytest.mark.parametrize("decay", ["token", "id_tag"])
+def test_excluded_contributions_never_reach_the_result(decay):
+    """A contribution past the threshold is excluded (Eq. 1): filling it with
+    NaN changes nothing, while its IDs still count in c_r."""
+    w_ = BY_NAME["c0"].scaled(K=5, B=4, L=3, R=50, D=4, P=33)
+    hs = workload.host_step(w_, seed=5, staleness=[0, 4, 1, 7, 2])
+    w, _, nex = oracle.token_weights(hs.tokens, hs.step, 2)
+    assert nex == 2
+    clean = oracle.aggregate_dense(hs.grads, w)
+    sp_clean = oracle.aggregate_sparse(hs.ids, hs.rows, hs.offsets, w, hs.tokens, hs.step, 2,
+                                       hs.tags, decay)
+    grads, rows = hs.grads.copy(), hs.rows.copy()
+    grads[w == 0] = np.nan
+    weights = oracle.row_weights(w, hs.tokens, oracle.contribution_of_occurrence(hs.offsets),
+                                 hs.ids, 2, decay, hs.tags)
+    rows[weights == 0] = np.nan
+    dirty = oracle.aggregate_dense(grads, w)
+    sp_dirty = oracle.aggregate_sparse(hs.ids, rows, hs.offsets, w, hs.tokens, hs.step, 2,
+                                       hs.tags, decay)
+    assert np.all(np.isfinite(dirty)) and np.all(np.isfinite(sp_dirty["agg"]))
+    np.testing.assert_array_equal(clean, dirty)
+    for k in ("unique_ids", "seg_offsets", "contrib_count", "active_count", "agg"):
+        np.testing.assert_array_equal(sp_clean[k], sp_dirty[k])
+    # the stale contributions' IDs are still counted in c_r
+    m_of_j = oracle.contribution_of_occurrence(hs.offsets)
+    stale_ids = np.unique(hs.ids[w[m_of_j] == 0])
+    assert np.any(sp_clean["contrib_count"][np.searchsorted(sp_clean["unique_ids"], stale_ids)] >
+                  sp_clean["active_count"][np.searchsorted(sp_clean["unique_ids"], stale_ids)])
+
+
+def test_id_tag_weights_dominate_token_weights():
+    """Per-ID staleness never exceeds the token staleness (a row cannot have
+    been updated more often than the dense vector), so every contribution that
+    the token rule keeps is kept per ID; tags only move forward to k."""
+    w_ = BY_NAME["c0"].scaled(K=8, B=16, L=4, R=300, D=4, P=8)
+    hs = workload.host_step(w_, seed=9)
+    for iota in range(0, 4):
+        w, _, _ = oracle.token_weights(hs.tokens, hs.step, iota)
+        a = oracle.aggregate_sparse(hs.ids, hs.rows, hs.offsets, w, hs.tokens, hs.step, iota,
+                                    hs.tags, "token")
+        b = oracle.aggregate_sparse(hs.ids, hs.rows, hs.offsets, w, hs.tokens, hs.step, iota,
+                                    hs.tags, "id_tag")
+        assert np.all(b["active_count"] >= a["active_count"])
+        assert np.all(b["new_tag"] >= hs.tags)
+        changed = np.nonzero(b["new_tag"] != hs.tags)[0]
+        assert np.all(b["new_tag"][changed] == hs.step)
+        assert np.all(np.isin(changed, b["unique_ids"]))
+
+
+# ----------------------------------------------------- arrival-order invariance
+def test_order_of_arrival_does_not_matter():
+    """Permuting the buffer (with each gradient keeping its token) leaves the
+    step unchanged; dyadic values make float sums exact, so bitwise."""
+    w_ = BY_NAME["c0"].scaled(K=7, B=8, L=5, R=90, D=4, P=50)
+    hs = workload.host_step(w_, seed=21, value_kind=counter.KIND_DYADIC)
+    perm = np.random.default_rng(0).permutation(w_.K)
+    n = np.diff(hs.offsets)
+    off_p = np.concatenate([[0], np.cumsum(n[perm])]).astype(np.int64)
+    ids_p = np.concatenate([hs.ids[hs.offsets[m]:hs.offsets[m + 1]] for m in perm])
+    rows_p = np.concatenate([hs.rows[hs.offsets[m]:hs.offsets[m + 1]] for m in perm])
+    for decay in ("token", "id_tag"):
+        w, _, _ = oracle.token_weights(hs.tokens, hs.step, 1)
+        wp, _, _ = oracle.token_weights(hs.tokens[perm], hs.step, 1)
+        np.testing.assert_array_equal(oracle.aggregate_dense(hs.grads, w),
+                                      oracle.aggregate_dense(hs.grads[perm], wp))
+        a = oracle.aggregate_sparse(hs.ids, hs.rows, hs.offsets, w, hs.tokens, hs.step, 1, hs.tags, decay)
+        b = oracle.aggregate_sparse(ids_p, rows_p, off_p, wp, hs.tokens[perm], hs.step, 1, hs.tags, decay)
+        for k in ("unique_ids", "seg_offsets", "contrib_count", "active_count", "agg"):
+            np.testing.assert_array_equal(a[k], b[k])
+
+
+# ------------------------------------------------------- optimiser closed forms
+def test_adagrad_constant_gradient_closed_form():
+    """From a zero accumulator, T steps of a constant gradient g give
+    a_T = T g^2 and p_T = p_0 - lr sign(g) sum_{t<=T} 1/sqrt(t) (eps = 0)."""
+    g = np.array([0.25, -2.0, 3.0], np.float32)
+    p = np.array([1.0, 0.5, -1.0], np.float32)
+    a = np.zeros(3, np.float32)
+    lr, T = 0.1, 9
+    for _ in range(T):
+        p, a = oracle.adagrad(p, a, g, lr, 0.0)
+    harm = sum(1.0 / np.sqrt(t) for t in range(1, T + 1))
+    np.testing.assert_allclose(a, T * g.astype(np.float64) ** 2, rtol=1e-7)
+    np.testing.assert_allclose(p, np.array([1.0, 0.5, -1.0]) - lr * np.sign(g) * harm, rtol=1e-6)
+
+
+def test_adagrad_epsilon_sits_outside_the_root():
+    # a = 0, g = 3, eps = 1: update lr * 3 / (3 + 1)
+    p, a = oracle.adagrad(np.float32([0.0]), np.float32([0.0]), np.float32([3.0]), 1.0, 1.0)
+    assert p[0] == np.float32(-0.75) and a[0] == 9.0
+
+
+def test_adam_first_step_closed_form():
+    """Kingma and Ba: from m = v = 0 at t = 1, the bias-corrected moments are
+    g and g^2, so the step is lr g / (|g| + eps)."""
+    g = np.array([0.5, -4.0, 1e-3], np.float32)
+    z = np.zeros(3, np.float32)
+    lr, eps = 0.01, 0.5
+    p, m, v = oracle.adam(z, z, z, g, lr, 0.9, 0.999, eps, 1)
+    np.testing.assert_allclose(p, -lr * g / (np.abs(g) + eps), rtol=1e-6)
+    np.testing.assert_allclose(m, 0.1 * g, rtol=1e-6)
+    np.testing.assert_allclose(v, 0.001 * g.astype(np.float64) ** 2, rtol=1e-6)
+
+
+def test_adam_constant_gradient_closed_form():
+    """With a constant gradient the bias-corrected moments stay g and g^2 at
+    every t, so after T steps p_T = p_0 - T lr g / (|g| + eps)."""
+    g = np.array([0.5, -2.0], np.float32)
+    p = np.array([1.0, 1.0], np.float32)
+    m = np.zeros(2, np.float32)
+    v = np.zeros(2, np.float32)
+    lr, eps, T = 1e-3, 0.25, 12
+    for t in range(1, T + 1):
+        p, m, v = oracle.adam(p, m, v, g, lr, 0.9, 0.999, eps, t)
+    np.testing.assert_allclose(p, 1.0 - T * lr * g / (np.abs(g) + eps), rtol=1e-6)
