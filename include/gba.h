@@ -1,0 +1,171 @@
+/*
+ * gba.h -- C ABI of the GBA (Global Batch gradients Aggregation) push-step on
+ * one parameter-server shard, implemented with HIP kernels for gfx950 (MI355X).
+ *
+ * Paper: Wang et al., "Global Batch gradients Aggregation (GBA) for training
+ * recommendation models", arXiv 2205.11048.  Sec. 3.1 defines the token
+ * mechanism and the tolerance function (Eq. 1); Alg. 2 (PS workflow, push
+ * responder) pops the K buffered gradients of one global batch, decays them,
+ * takes the weighted sums (dense: divided by N_a; embeddings: divided by the
+ * number of workers that encountered the ID) and applies them.  K here is the
+ * paper's M = N_a, the number of local-batch gradients aggregated per step.
+ *
+ * Conventions shared by every call:
+ *  - Every array argument is a DEVICE pointer owned by the caller, except where
+ *    a comment says otherwise.  The library never allocates, frees or keeps
+ *    caller memory; scratch memory is passed in (size from a query).
+ *  - Every call only enqueues work on `stream` (0 = the null stream) and
+ *    returns without synchronising.
+ *  - Misuse the host can see (null pointer, bad size, unsupported width,
+ *    workspace too small) returns a non-zero gba_status and enqueues nothing.
+ *  - Errors that depend on device data are OR-ed into the caller's `*err`
+ *    word as GBA_DERR_* bits; the library never clears it.  When `*err` is
+ *    non-zero after the stream has drained, the outputs of that call are
+ *    undefined (but every access stayed inside the arrays described here).
+ *  - No global state is mutated; calls on different streams may overlap when
+ *    their arrays do not.
+ */
+#ifndef GBA_H
+#define GBA_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum gba_status {
+  GBA_OK = 0,
+  GBA_ERR_NULL = 1,          /* a required pointer is NULL                   */
+  GBA_ERR_INVALID_ARG = 2,   /* a size or mode is out of range               */
+  GBA_ERR_UNSUPPORTED = 3,   /* valid but not supported (e.g. width D)       */
+  GBA_ERR_WORKSPACE = 4,     /* workspace smaller than the size query asked  */
+  GBA_ERR_HIP = 5            /* a HIP launch failed                          */
+} gba_status;
+
+/* Bits OR-ed into *err by device code. */
+enum {
+  GBA_DERR_ID_RANGE = 1,      /* an embedding ID outside [0, R)                    */
+  GBA_DERR_FUTURE_TOKEN = 2,  /* a token newer than the step being applied         */
+  GBA_DERR_OFFSETS = 4,       /* contribution offsets not 0 .. N and non-decreasing */
+  GBA_DERR_ROW_RANGE = 8      /* a row index passed to a sparse apply outside [0, R) */
+};
+
+/* How embedding gradients are decayed (Alg. 2). */
+typedef enum gba_decay {
+  GBA_DECAY_TOKEN = 0,   /* every row of contribution m takes m's weight w_m          */
+  GBA_DECAY_ID_TAG = 1   /* per-ID: s = max(0, tag[r] - tau_m + 1), weight [s <= iota] */
+} gba_decay;
+
+/* Divisor of the embedding weighted sum (Alg. 2). */
+typedef enum gba_norm {
+  GBA_NORM_PER_ID_COUNT = 0, /* c_r: contributions in the buffer that contain ID r */
+  GBA_NORM_BY_K = 1          /* K: the synchronous global-batch mean               */
+} gba_norm;
+
+const char* gba_status_string(gba_status status);
+
+/* Largest supported sizes. */
+#define GBA_MAX_K 4096       /* contributions per call                        */
+#define GBA_MAX_D 256        /* embedding width; D must be a multiple of 4    */
+
+/*
+ * Token weights -- Eq. 1 (Sec. 3.1).
+ *   s_m = step - tokens[m];  w[m] = 1.0f if s_m <= iota, else 0.0f (excluded).
+ * tokens     [K] int64, the global step at which contribution m's batch was issued.
+ * w          [K] float out.
+ * staleness  [K] int64 out, may be NULL.
+ * num_excluded  one int32 out (count of w[m] == 0), may be NULL.
+ * err        device error word; GBA_DERR_FUTURE_TOKEN when some s_m < 0 (that
+ *            contribution then gets weight 0).
+ * 1 <= K <= GBA_MAX_K.
+ */
+gba_status gba_token_weights(const int64_t* tokens, int32_t K, int64_t step, int64_t iota,
+                             float* w, int64_t* staleness, int32_t* num_excluded,
+                             int32_t* err, hipStream_t stream);
+
+/*
+ * Dense weighted sum divided by N_a -- Alg. 2 (push responder).
+ *   out[i] = (sum over m with w[m] != 0 of w[m] * grads[m][i]) / K
+ * accumulated in float64 in buffer order, rounded to float once.  A gradient
+ * whose weight is 0 is never read (so it may hold anything, NaN included).
+ * grads   DEVICE array of K device pointers, each to P floats.
+ * w       [K] float (from gba_token_weights).
+ * out     [P] float.
+ * 1 <= K <= GBA_MAX_K, P >= 0.
+ */
+gba_status gba_aggregate_dense(const float* const* grads, const float* w, int32_t K, int64_t P,
+                               float* out, hipStream_t stream);
+
+/* Bytes of workspace gba_aggregate_sparse needs for these sizes. */
+gba_status gba_aggregate_sparse_workspace_size(int64_t N, int32_t K, int32_t D, int64_t R,
+                                               size_t* bytes /* host out */);
+
+/*
+ * Embedding gradients by ID -- Alg. 2 (push responder): dedup by ID, per-ID
+ * decay, weighted sum divided by the number of contributions that hold the ID.
+ * ids              [N] int64 embedding IDs in [0, R), contribution-major.
+ * rows             [N][D] float, row j is the gradient of occurrence j.
+ * contrib_offsets  [K+1] int64, occurrences of contribution m are
+ *                  [offsets[m], offsets[m+1]); offsets[0] = 0, offsets[K] = N.
+ * w, tokens        [K] token weights and tokens of the contributions.
+ * tag              [R] int32, the last step each row was updated (-1: never).
+ *                  Read and rewritten in GBA_DECAY_ID_TAG mode (every row with a
+ *                  non-zero weight gets tag = step after all reads); ignored
+ *                  (may be NULL) in GBA_DECAY_TOKEN mode.
+ * Outputs, with U = number of distinct IDs (U <= N; size them for N):
+ *   unique_ids     [U]   distinct IDs, ascending.
+ *   seg_offsets    [U+1] exclusive prefix of the occurrence counts per ID.
+ *   contrib_count  [U]   c_r, contributions that contain the ID.
+ *   active_count   [U]   W_r, contributions with a non-zero weight for the ID.
+ *   agg            [U][D] float, sum of the weighted rows of the ID (float64
+ *                  accumulation) divided by c_r (or by K); 0 when W_r = 0.
+ *   num_unique     one int64, U.
+ * workspace        device scratch of at least the queried size.
+ * Limits: 1 <= K <= GBA_MAX_K, 0 <= N < 2^31, 1 <= R <= 2^32,
+ * D % 4 == 0 and 4 <= D <= GBA_MAX_D.
+ */
+gba_status gba_aggregate_sparse(const int64_t* ids, const float* rows,
+                                const int64_t* contrib_offsets, int32_t K, int64_t N, int32_t D,
+                                int64_t R, const float* w, const int64_t* tokens, int64_t step,
+                                int64_t iota, int32_t* tag, gba_decay decay, gba_norm norm,
+                                int64_t* unique_ids, int64_t* seg_offsets, int32_t* contrib_count,
+                                int32_t* active_count, float* agg, int64_t* num_unique,
+                                void* workspace, size_t workspace_bytes, int32_t* err,
+                                hipStream_t stream);
+
+/*
+ * Optimiser apply (Table 1 names Adagrad and Adam; rules of Duchi et al. 2011
+ * and Kingma and Ba 2015).  Arithmetic in float64 from the float32 state,
+ * each stored value rounded once.
+ *
+ * Dense form (rows == NULL): elementwise over n elements of param/state/grad.
+ * Row form (rows != NULL): for i < *num_rows (device int64, <= n), when
+ * active == NULL or active[i] > 0, update table row r = rows[i] (param, state
+ * are [R][D], grad is [n][D], row i of grad goes to row r).  Rows not listed
+ * are untouched.  An r outside [0, R) sets GBA_DERR_ROW_RANGE and is skipped.
+ * The row indices must be distinct (as gba_aggregate_sparse's unique_ids are).
+ *
+ * Adagrad: a' = a + g^2;  p' = p - lr * g / (sqrt(a') + eps).
+ */
+gba_status gba_apply_adagrad(float* param, float* accum, const float* grad, const int64_t* rows,
+                             const int32_t* active, const int64_t* num_rows, int64_t n, int32_t D,
+                             int64_t R, double lr, double eps, int32_t* err, hipStream_t stream);
+
+/*
+ * Adam with bias correction at step count t >= 1 (shared by the dense vector
+ * and the rows; rows are updated only when listed, i.e. lazily):
+ *   m' = b1 m + (1-b1) g;  v' = b2 v + (1-b2) g^2;
+ *   p' = p - lr * (m' / (1 - b1^t)) / (sqrt(v' / (1 - b2^t)) + eps).
+ */
+gba_status gba_apply_adam(float* param, float* m, float* v, const float* grad, const int64_t* rows,
+                          const int32_t* active, const int64_t* num_rows, int64_t n, int32_t D,
+                          int64_t R, double lr, double beta1, double beta2, double eps, int64_t t,
+                          int32_t* err, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* GBA_H */

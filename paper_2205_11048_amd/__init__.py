@@ -1,0 +1,196 @@
+"""Python binding of libgba.so, the GBA push-step for MI355X (gfx950).
+
+Each function has the name of the C entry point it calls (include/gba.h)
+and does argument marshalling only: it reads sizes off torch tensors that
+already live on the GPU, passes their device pointers and the current HIP
+stream, and raises ``GBAError`` on a non-zero status.  Every step of the
+computation runs in the library's HIP kernels; there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+__all__ = [
+    "GBAError", "lib", "gba_token_weights", "gba_aggregate_dense", "gba_aggregate_sparse",
+    "gba_aggregate_sparse_workspace_size", "gba_apply_adagrad", "gba_apply_adam",
+    "pointer_table", "DECAY_TOKEN", "DECAY_ID_TAG", "NORM_PER_ID_COUNT", "NORM_BY_K",
+    "DERR_ID_RANGE", "DERR_FUTURE_TOKEN", "DERR_OFFSETS", "DERR_ROW_RANGE", "MAX_K", "MAX_D",
+    "LIB_PATH",
+]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libgba.so")
+
+DECAY_TOKEN, DECAY_ID_TAG = 0, 1
+NORM_PER_ID_COUNT, NORM_BY_K = 0, 1
+DERR_ID_RANGE, DERR_FUTURE_TOKEN, DERR_OFFSETS, DERR_ROW_RANGE = 1, 2, 4, 8
+MAX_K, MAX_D = 4096, 256
+
+_P = ctypes.c_void_p
+_I32 = ctypes.c_int32
+_I64 = ctypes.c_int64
+_F64 = ctypes.c_double
+
+_SIGNATURES = {
+    "gba_status_string": ([_I32], ctypes.c_char_p),
+    "gba_token_weights": ([_P, _I32, _I64, _I64, _P, _P, _P, _P, _P], _I32),
+    "gba_aggregate_dense": ([_P, _P, _I32, _I64, _P, _P], _I32),
+    "gba_aggregate_sparse_workspace_size": ([_I64, _I32, _I32, _I64, ctypes.POINTER(ctypes.c_size_t)], _I32),
+    "gba_aggregate_sparse": ([_P, _P, _P, _I32, _I64, _I32, _I64, _P, _P, _I64, _I64, _P, _I32, _I32,
+                              _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P, _P], _I32),
+    "gba_apply_adagrad": ([_P, _P, _P, _P, _P, _P, _I64, _I32, _I64, _F64, _F64, _P, _P], _I32),
+    "gba_apply_adam": ([_P, _P, _P, _P, _P, _P, _P, _I64, _I32, _I64, _F64, _F64, _F64, _F64, _I64,
+                        _P, _P], _I32),
+}
+
+_LIB = None
+
+
+class GBAError(RuntimeError):
+    pass
+
+
+def lib() -> ctypes.CDLL:
+    """Load libgba.so (built in-tree by ``python -m paper_2205_11048_amd.build``)."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise GBAError(f"{LIB_PATH} is missing: build it with `python -m paper_2205_11048_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (args, res) in _SIGNATURES.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = res
+        _LIB = L
+    return _LIB
+
+
+def _check(status: int):
+    if status != 0:
+        raise GBAError(f"status {status}: {lib().gba_status_string(status).decode()}")
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _need(t, dtype, name, numel=None):
+    if t is None:
+        return
+    if not t.is_cuda or t.dtype != dtype or not t.is_contiguous():
+        raise GBAError(f"{name}: expected a contiguous {dtype} tensor on the GPU")
+    if numel is not None and t.numel() < numel:
+        raise GBAError(f"{name}: expected at least {numel} elements, got {t.numel()}")
+
+
+def pointer_table(tensors, device=None) -> torch.Tensor:
+    """Device int64 array of the tensors' device pointers (the `grads` argument)."""
+    for i, t in enumerate(tensors):
+        _need(t, torch.float32, f"grads[{i}]")
+    device = device or tensors[0].device
+    return torch.tensor([t.data_ptr() for t in tensors], dtype=torch.int64, device=device)
+
+
+def gba_token_weights(tokens, step, iota, w, staleness=None, num_excluded=None, err=None, stream=None):
+    K = tokens.numel()
+    _need(tokens, torch.int64, "tokens")
+    _need(w, torch.float32, "w", K)
+    _need(staleness, torch.int64, "staleness", K)
+    _need(num_excluded, torch.int32, "num_excluded", 1)
+    _need(err, torch.int32, "err", 1)
+    _check(lib().gba_token_weights(_ptr(tokens), K, int(step), int(iota), _ptr(w), _ptr(staleness),
+                                   _ptr(num_excluded), _ptr(err), _stream(stream)))
+
+
+def gba_aggregate_dense(grads, w, P, out, stream=None):
+    """``grads``: device int64 tensor of K gradient pointers (see pointer_table)."""
+    K = grads.numel()
+    _need(grads, torch.int64, "grads")
+    _need(w, torch.float32, "w", K)
+    _need(out, torch.float32, "out", P)
+    _check(lib().gba_aggregate_dense(_ptr(grads), _ptr(w), K, int(P), _ptr(out), _stream(stream)))
+
+
+def gba_aggregate_sparse_workspace_size(N, K, D, R) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib().gba_aggregate_sparse_workspace_size(int(N), int(K), int(D), int(R), ctypes.byref(n)))
+    return int(n.value)
+
+
+def gba_aggregate_sparse(ids, rows, contrib_offsets, R, w, tokens, step, iota, tag, decay, norm,
+                         unique_ids, seg_offsets, contrib_count, active_count, agg, num_unique,
+                         workspace, err=None, stream=None):
+    N = ids.numel()
+    K = contrib_offsets.numel() - 1
+    D = rows.shape[-1]
+    _need(ids, torch.int64, "ids")
+    _need(rows, torch.float32, "rows", N * D)
+    _need(contrib_offsets, torch.int64, "contrib_offsets")
+    _need(w, torch.float32, "w", K)
+    _need(tokens, torch.int64, "tokens", K)
+    _need(tag, torch.int32, "tag", R if tag is not None else None)
+    _need(unique_ids, torch.int64, "unique_ids", N)
+    _need(seg_offsets, torch.int64, "seg_offsets", N + 1)
+    _need(contrib_count, torch.int32, "contrib_count", N)
+    _need(active_count, torch.int32, "active_count", N)
+    _need(agg, torch.float32, "agg", N * D)
+    _need(num_unique, torch.int64, "num_unique", 1)
+    _need(workspace, torch.uint8, "workspace")
+    _need(err, torch.int32, "err", 1)
+    _check(lib().gba_aggregate_sparse(
+        _ptr(ids), _ptr(rows), _ptr(contrib_offsets), K, N, D, int(R), _ptr(w), _ptr(tokens), int(step),
+        int(iota), _ptr(tag), int(decay), int(norm), _ptr(unique_ids), _ptr(seg_offsets),
+        _ptr(contrib_count), _ptr(active_count), _ptr(agg), _ptr(num_unique), _ptr(workspace),
+        workspace.numel(), _ptr(err), _stream(stream)))
+
+
+def gba_apply_adagrad(param, accum, grad, lr, eps, rows=None, active=None, num_rows=None, R=0,
+                      err=None, stream=None):
+    """Dense form when ``rows`` is None, else the row form over [R, D] tables."""
+    _need(param, torch.float32, "param")
+    _need(accum, torch.float32, "accum")
+    _need(grad, torch.float32, "grad")
+    _need(rows, torch.int64, "rows")
+    _need(active, torch.int32, "active")
+    _need(num_rows, torch.int64, "num_rows", 1 if rows is not None else None)
+    _need(err, torch.int32, "err", 1)
+    if rows is None:
+        n, D = grad.numel(), 0
+        if param.numel() < n or accum.numel() < n:
+            raise GBAError("param/accum shorter than grad")
+    else:
+        n, D = rows.numel(), param.shape[-1]
+        if grad.numel() < n * D or param.numel() < R * D or accum.numel() < R * D:
+            raise GBAError("row-form sizes do not match")
+    _check(lib().gba_apply_adagrad(_ptr(param), _ptr(accum), _ptr(grad), _ptr(rows), _ptr(active),
+                                   _ptr(num_rows), n, D, int(R), float(lr), float(eps), _ptr(err),
+                                   _stream(stream)))
+
+
+def gba_apply_adam(param, m, v, grad, lr, beta1, beta2, eps, t, rows=None, active=None, num_rows=None,
+                   R=0, err=None, stream=None):
+    for name, x in (("param", param), ("m", m), ("v", v), ("grad", grad)):
+        _need(x, torch.float32, name)
+    _need(rows, torch.int64, "rows")
+    _need(active, torch.int32, "active")
+    _need(num_rows, torch.int64, "num_rows", 1 if rows is not None else None)
+    _need(err, torch.int32, "err", 1)
+    if rows is None:
+        n, D = grad.numel(), 0
+        if min(param.numel(), m.numel(), v.numel()) < n:
+            raise GBAError("param/m/v shorter than grad")
+    else:
+        n, D = rows.numel(), param.shape[-1]
+        if grad.numel() < n * D or min(param.numel(), m.numel(), v.numel()) < R * D:
+            raise GBAError("row-form sizes do not match")
+    _check(lib().gba_apply_adam(_ptr(param), _ptr(m), _ptr(v), _ptr(grad), _ptr(rows), _ptr(active),
+                                _ptr(num_rows), n, D, int(R), float(lr), float(beta1), float(beta2),
+                                float(eps), int(t), _ptr(err), _stream(stream)))

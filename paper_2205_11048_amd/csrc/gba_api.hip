@@ -1,0 +1,166 @@
+// C ABI of the GBA push-step (declared in include/gba.h): argument checks,
+// workspace layout and launch order.  No allocation, no synchronisation.
+#include <cmath>
+#include <cstdint>
+
+#include "gba_internal.hpp"
+
+using namespace gba;
+
+namespace {
+
+constexpr int64_t kMaxN = (int64_t(1) << 31) - 1;
+
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+inline size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
+
+inline gba_status from_hip(hipError_t e) { return e == hipSuccess ? GBA_OK : GBA_ERR_HIP; }
+
+bool width_ok(int32_t D) { return D >= 4 && D <= GBA_MAX_D && D % 4 == 0; }
+
+size_t sparse_bytes(int64_t N, int32_t D, int64_t R, SortPlan* plan_out) {
+  const SortPlan plan = plan_sort(N, R);
+  if (plan_out) *plan_out = plan;
+  return align_up(plan.bytes) + align_up(segments_workspace_bytes(N, D));
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* gba_status_string(gba_status s) {
+  switch (s) {
+    case GBA_OK: return "ok";
+    case GBA_ERR_NULL: return "a required pointer is NULL";
+    case GBA_ERR_INVALID_ARG: return "an argument is out of range";
+    case GBA_ERR_UNSUPPORTED: return "unsupported size or width";
+    case GBA_ERR_WORKSPACE: return "workspace too small";
+    case GBA_ERR_HIP: return "a HIP launch failed";
+  }
+  return "unknown status";
+}
+
+gba_status gba_token_weights(const int64_t* tokens, int32_t K, int64_t step, int64_t iota, float* w,
+                             int64_t* staleness, int32_t* num_excluded, int32_t* err,
+                             hipStream_t stream) {
+  if (!tokens || !w) return GBA_ERR_NULL;
+  if (K < 1 || K > GBA_MAX_K) return GBA_ERR_INVALID_ARG;
+  return from_hip(launch_token_weights(tokens, K, step, iota, w, staleness, num_excluded, err, stream));
+}
+
+gba_status gba_aggregate_dense(const float* const* grads, const float* w, int32_t K, int64_t P,
+                               float* out, hipStream_t stream) {
+  if (K < 1 || K > GBA_MAX_K || P < 0) return GBA_ERR_INVALID_ARG;
+  if (P == 0) return GBA_OK;
+  if (!grads || !w || !out) return GBA_ERR_NULL;
+  return from_hip(launch_aggregate_dense(grads, w, K, P, out, stream));
+}
+
+gba_status gba_aggregate_sparse_workspace_size(int64_t N, int32_t K, int32_t D, int64_t R,
+                                               size_t* bytes) {
+  if (!bytes) return GBA_ERR_NULL;
+  if (K < 1 || K > GBA_MAX_K || N < 0 || N > kMaxN || R < 1 || R > (int64_t(1) << 32))
+    return GBA_ERR_INVALID_ARG;
+  if (!width_ok(D)) return GBA_ERR_UNSUPPORTED;
+  *bytes = sparse_bytes(N, D, R, nullptr);
+  return GBA_OK;
+}
+
+gba_status gba_aggregate_sparse(const int64_t* ids, const float* rows, const int64_t* contrib_offsets,
+                                int32_t K, int64_t N, int32_t D, int64_t R, const float* w,
+                                const int64_t* tokens, int64_t step, int64_t iota, int32_t* tag,
+                                gba_decay decay, gba_norm norm, int64_t* unique_ids,
+                                int64_t* seg_offsets, int32_t* contrib_count, int32_t* active_count,
+                                float* agg, int64_t* num_unique, void* workspace,
+                                size_t workspace_bytes, int32_t* err, hipStream_t stream) {
+  if (K < 1 || K > GBA_MAX_K || N < 0 || N > kMaxN || R < 1 || R > (int64_t(1) << 32))
+    return GBA_ERR_INVALID_ARG;
+  if (decay != GBA_DECAY_TOKEN && decay != GBA_DECAY_ID_TAG) return GBA_ERR_INVALID_ARG;
+  if (norm != GBA_NORM_PER_ID_COUNT && norm != GBA_NORM_BY_K) return GBA_ERR_INVALID_ARG;
+  if (!width_ok(D)) return GBA_ERR_UNSUPPORTED;
+  if (!contrib_offsets || !w || !tokens || !seg_offsets || !num_unique || !workspace)
+    return GBA_ERR_NULL;
+  if (N > 0 && (!ids || !rows || !unique_ids || !contrib_count || !active_count || !agg))
+    return GBA_ERR_NULL;
+  if (decay == GBA_DECAY_ID_TAG) {
+    if (!tag) return GBA_ERR_NULL;
+    if (step < INT32_MIN || step > INT32_MAX) return GBA_ERR_INVALID_ARG;
+  }
+  if ((rows && !aligned16(rows)) || (agg && !aligned16(agg)) || !aligned16(workspace))
+    return GBA_ERR_INVALID_ARG;
+  SortPlan plan;
+  const size_t need = sparse_bytes(N, D, R, &plan);
+  if (workspace_bytes < need) return GBA_ERR_WORKSPACE;
+
+  char* ws = static_cast<char*>(workspace);
+  const uint32_t* keys = nullptr;
+  const uint32_t* vals = nullptr;
+  hipError_t e = launch_sort_ids(ids, N, R, plan, ws, &keys, &vals, err, stream);
+  if (e != hipSuccess) return GBA_ERR_HIP;
+
+  SegmentArgs a;
+  a.keys = keys;
+  a.vals = vals;
+  a.rows = rows;
+  a.offsets = contrib_offsets;
+  a.w = w;
+  a.tokens = tokens;
+  a.tag = tag;
+  a.N = N;
+  a.R = R;
+  a.step = step;
+  a.iota = iota;
+  a.K = K;
+  a.D = D;
+  a.decay = (int)decay;
+  a.norm = (int)norm;
+  a.unique_ids = unique_ids;
+  a.seg_offsets = seg_offsets;
+  a.contrib_count = contrib_count;
+  a.active_count = active_count;
+  a.agg = agg;
+  a.num_unique = num_unique;
+  a.err = err;
+  return from_hip(launch_segments(a, ws + align_up(plan.bytes), stream));
+}
+
+gba_status gba_apply_adagrad(float* param, float* accum, const float* grad, const int64_t* rows,
+                             const int32_t* active, const int64_t* num_rows, int64_t n, int32_t D,
+                             int64_t R, double lr, double eps, int32_t* err, hipStream_t stream) {
+  if (n < 0) return GBA_ERR_INVALID_ARG;
+  if (n == 0) return GBA_OK;
+  if (!param || !accum || !grad) return GBA_ERR_NULL;
+  if (!rows) return from_hip(launch_dense_adagrad(param, accum, grad, n, lr, eps, stream));
+  if (!num_rows) return GBA_ERR_NULL;
+  if (!width_ok(D)) return GBA_ERR_UNSUPPORTED;
+  if (R < 1) return GBA_ERR_INVALID_ARG;
+  if (!aligned16(param) || !aligned16(accum) || !aligned16(grad)) return GBA_ERR_INVALID_ARG;
+  return from_hip(
+      launch_rows_adagrad(param, accum, grad, rows, active, num_rows, n, D, R, lr, eps, err, stream));
+}
+
+gba_status gba_apply_adam(float* param, float* m, float* v, const float* grad, const int64_t* rows,
+                          const int32_t* active, const int64_t* num_rows, int64_t n, int32_t D,
+                          int64_t R, double lr, double beta1, double beta2, double eps, int64_t t,
+                          int32_t* err, hipStream_t stream) {
+  if (n < 0 || t < 1 || !(beta1 >= 0.0 && beta1 < 1.0) || !(beta2 >= 0.0 && beta2 < 1.0))
+    return GBA_ERR_INVALID_ARG;
+  if (n == 0) return GBA_OK;
+  if (!param || !m || !v || !grad) return GBA_ERR_NULL;
+  AdamParams hp;
+  hp.lr = lr;
+  hp.beta1 = beta1;
+  hp.beta2 = beta2;
+  hp.eps = eps;
+  hp.bc1 = 1.0 - std::pow(beta1, (double)t);
+  hp.bc2 = 1.0 - std::pow(beta2, (double)t);
+  if (!rows) return from_hip(launch_dense_adam(param, m, v, grad, n, hp, stream));
+  if (!num_rows) return GBA_ERR_NULL;
+  if (!width_ok(D)) return GBA_ERR_UNSUPPORTED;
+  if (R < 1) return GBA_ERR_INVALID_ARG;
+  if (!aligned16(param) || !aligned16(m) || !aligned16(v) || !aligned16(grad))
+    return GBA_ERR_INVALID_ARG;
+  return from_hip(launch_rows_adam(param, m, v, grad, rows, active, num_rows, n, D, R, hp, err, stream));
+}
+
+}  // extern "C"

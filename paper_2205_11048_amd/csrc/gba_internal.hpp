@@ -1,0 +1,82 @@
+// Host-side launchers of the GBA kernels, shared between the kernel sources
+// and the C ABI layer.  Every launcher only enqueues on `stream` and returns
+// the launch status; argument checks happen in the C ABI layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/gba.h"
+
+namespace gba {
+
+// ---- token weights (Eq. 1)
+hipError_t launch_token_weights(const int64_t* tokens, int32_t K, int64_t step, int64_t iota,
+                                float* w, int64_t* staleness, int32_t* num_excluded, int32_t* err,
+                                hipStream_t stream);
+
+// ---- dense weighted sum / N_a (Alg. 2)
+hipError_t launch_aggregate_dense(const float* const* grads, const float* w, int32_t K, int64_t P,
+                                  float* out, hipStream_t stream);
+
+// ---- dense and row optimiser apply
+struct AdamParams {
+  double lr, beta1, beta2, eps, bc1, bc2;   // bc = 1 - beta^t
+};
+hipError_t launch_dense_adagrad(float* p, float* a, const float* g, int64_t n, double lr, double eps,
+                                hipStream_t stream);
+hipError_t launch_dense_adam(float* p, float* m, float* v, const float* g, int64_t n,
+                             const AdamParams& hp, hipStream_t stream);
+hipError_t launch_rows_adagrad(float* p, float* a, const float* g, const int64_t* rows,
+                               const int32_t* active, const int64_t* num_rows, int64_t n, int32_t D,
+                               int64_t R, double lr, double eps, int32_t* err, hipStream_t stream);
+hipError_t launch_rows_adam(float* p, float* m, float* v, const float* g, const int64_t* rows,
+                            const int32_t* active, const int64_t* num_rows, int64_t n, int32_t D,
+                            int64_t R, const AdamParams& hp, int32_t* err, hipStream_t stream);
+
+// ---- device-wide exclusive scan of uint32 (in place allowed)
+size_t scan_workspace_bytes(int64_t n);
+hipError_t launch_exclusive_scan_u32(const uint32_t* in, uint32_t* out, int64_t n, uint32_t* total,
+                                     void* ws, hipStream_t stream);
+
+// ---- LSD radix sort of (u32 key, u32 occurrence index) pairs
+struct SortPlan {
+  int64_t n;
+  int key_bits;          // significant key bits (>= 1)
+  int passes;
+  int64_t blocks;        // tiles per pass
+  size_t bytes;          // workspace bytes
+};
+SortPlan plan_sort(int64_t n, int64_t R);
+// Sorts ids (int64 [n], each checked against [0, R)) by value, stably.  The
+// sorted keys and original occurrence indices are returned through
+// *keys_out / *vals_out, which point into `ws`.
+hipError_t launch_sort_ids(const int64_t* ids, int64_t n, int64_t R, const SortPlan& plan, void* ws,
+                           const uint32_t** keys_out, const uint32_t** vals_out, int32_t* err,
+                           hipStream_t stream);
+
+// ---- segments over the sorted keys: dedup, counts, decayed weighted sums
+struct SegmentArgs {
+  const uint32_t* keys;        // sorted IDs [N]
+  const uint32_t* vals;        // occurrence index of each sorted entry [N]
+  const float* rows;           // [N][D]
+  const int64_t* offsets;      // [K+1]
+  const float* w;              // [K]
+  const int64_t* tokens;       // [K]
+  int32_t* tag;                // [R] or null
+  int64_t N, R, step, iota;
+  int32_t K, D;
+  int decay, norm;
+  int64_t* unique_ids;
+  int64_t* seg_offsets;
+  int32_t* contrib_count;
+  int32_t* active_count;
+  float* agg;
+  int64_t* num_unique;
+  int32_t* err;
+};
+size_t segments_workspace_bytes(int64_t N, int32_t D);
+hipError_t launch_segments(const SegmentArgs& a, void* ws, hipStream_t stream);
+
+}  // namespace gba

@@ -1,0 +1,112 @@
+// Optimiser apply over the touched embedding rows only: gather the row and
+// its optimiser state, update with the row's aggregated gradient, scatter
+// back.  Rows without a non-zero-weight contribution are skipped (they are
+// not updated at this global step; Alg. 2 updates embeddings by ID).
+//
+// A group of LPR lanes owns one row at a time and moves it as 16-byte
+// vectors; the grid is persistent and reads the row count from device memory,
+// so no host round trip sits between the aggregation and the apply.
+#include "gba_device.hpp"
+#include "gba_internal.hpp"
+#include "optim.hpp"
+
+namespace gba {
+
+constexpr int kRowsBlock = 256;
+constexpr int64_t kRowsMaxBlocks = 4096;
+
+static inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+template <int LPR, bool ADAM>
+__global__ void __launch_bounds__(kRowsBlock)
+rows_apply_kernel(float* __restrict__ p, float* __restrict__ s1, float* __restrict__ s2,
+                  const float* __restrict__ g, const int64_t* __restrict__ rows,
+                  const int32_t* __restrict__ active, const int64_t* __restrict__ num_rows,
+                  int64_t n, int D, int64_t R, double lr, double eps, double b1, double b2,
+                  double bc1, double bc2, int32_t* __restrict__ err) {
+  constexpr int G = kRowsBlock / LPR;
+  const int lane = threadIdx.x % LPR;
+  const int grp = threadIdx.x / LPR;
+  int64_t count = *num_rows;
+  if (count > n) count = n;
+  bool bad = false;
+  const int64_t stride = (int64_t)gridDim.x * G;
+  for (int64_t i = (int64_t)blockIdx.x * G + grp; i < count; i += stride) {
+    if (active && active[i] <= 0) continue;
+    const int64_t r = rows[i];
+    if (r < 0 || r >= R) {
+      bad = true;
+      continue;
+    }
+    for (int c = lane * 4; c < D; c += LPR * 4) {
+      const int64_t at = r * (int64_t)D + c;
+      const f32x4 pv = *reinterpret_cast<const f32x4*>(p + at);
+      const f32x4 av = *reinterpret_cast<const f32x4*>(s1 + at);
+      const f32x4 gv = *reinterpret_cast<const f32x4*>(g + i * (int64_t)D + c);
+      float pe[4] = {pv.x, pv.y, pv.z, pv.w};
+      float ae[4] = {av.x, av.y, av.z, av.w};
+      const float ge[4] = {gv.x, gv.y, gv.z, gv.w};
+      if (ADAM) {
+        const f32x4 vv = *reinterpret_cast<const f32x4*>(s2 + at);
+        float ve[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) adam_update(pe[k], ae[k], ve[k], ge[k], lr, b1, b2, eps, bc1, bc2);
+        *reinterpret_cast<f32x4*>(s2 + at) = f32x4{ve[0], ve[1], ve[2], ve[3]};
+      } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) adagrad_update(pe[k], ae[k], ge[k], lr, eps);
+      }
+      *reinterpret_cast<f32x4*>(p + at) = f32x4{pe[0], pe[1], pe[2], pe[3]};
+      *reinterpret_cast<f32x4*>(s1 + at) = f32x4{ae[0], ae[1], ae[2], ae[3]};
+    }
+  }
+  if (bad) raise_error(err, GBA_DERR_ROW_RANGE);
+}
+
+template <bool ADAM>
+static hipError_t launch_rows(float* p, float* s1, float* s2, const float* g, const int64_t* rows,
+                              const int32_t* active, const int64_t* num_rows, int64_t n, int32_t D,
+                              int64_t R, double lr, double eps, double b1, double b2, double bc1,
+                              double bc2, int32_t* err, hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  int lpr = 1;
+  while (lpr < 64 && lpr * 4 < D) lpr <<= 1;
+  const int G = kRowsBlock / lpr;
+  int64_t blocks = ceil_div(n, G);
+  if (blocks > kRowsMaxBlocks) blocks = kRowsMaxBlocks;
+  const dim3 grid((unsigned)blocks), block(kRowsBlock);
+#define GBA_ROWS_CASE(L)                                                                          \
+  case L:                                                                                         \
+    hipLaunchKernelGGL((rows_apply_kernel<L, ADAM>), grid, block, 0, stream, p, s1, s2, g, rows,  \
+                       active, num_rows, n, (int)D, R, lr, eps, b1, b2, bc1, bc2, err);           \
+    break;
+  switch (lpr) {
+    GBA_ROWS_CASE(1)
+    GBA_ROWS_CASE(2)
+    GBA_ROWS_CASE(4)
+    GBA_ROWS_CASE(8)
+    GBA_ROWS_CASE(16)
+    GBA_ROWS_CASE(32)
+    GBA_ROWS_CASE(64)
+    default:
+      return hipErrorInvalidValue;
+  }
+#undef GBA_ROWS_CASE
+  return hipGetLastError();
+}
+
+hipError_t launch_rows_adagrad(float* p, float* a, const float* g, const int64_t* rows,
+                               const int32_t* active, const int64_t* num_rows, int64_t n, int32_t D,
+                               int64_t R, double lr, double eps, int32_t* err, hipStream_t stream) {
+  return launch_rows<false>(p, a, nullptr, g, rows, active, num_rows, n, D, R, lr, eps, 0.0, 0.0,
+                            1.0, 1.0, err, stream);
+}
+
+hipError_t launch_rows_adam(float* p, float* m, float* v, const float* g, const int64_t* rows,
+                            const int32_t* active, const int64_t* num_rows, int64_t n, int32_t D,
+                            int64_t R, const AdamParams& hp, int32_t* err, hipStream_t stream) {
+  return launch_rows<true>(p, m, v, g, rows, active, num_rows, n, D, R, hp.lr, hp.eps, hp.beta1,
+                           hp.beta2, hp.bc1, hp.bc2, err, stream);
+}
+
+}  // namespace gba

@@ -1,0 +1,60 @@
+"""The C ABI library loads and exports every entry point its header declares
+(CPU only: nothing here launches a kernel)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2205_11048_amd as gba
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "gba.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w[\w\s\*]*?\b(gba_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_header_declares_the_five_calls():
+    names = declared_functions()
+    for n in ("gba_token_weights", "gba_aggregate_dense", "gba_aggregate_sparse",
+              "gba_apply_adagrad", "gba_apply_adam"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    if not os.path.exists(gba.LIB_PATH):
+        pytest.fail("libgba.so is not built (python -m paper_2205_11048_amd.build)")
+    L = ctypes.CDLL(gba.LIB_PATH)
+    for n in declared_functions():
+        assert hasattr(L, n), n
+
+
+def test_status_strings_and_workspace_query():
+    L = gba.lib()
+    assert L.gba_status_string(0) == b"ok"
+    assert b"workspace" in L.gba_status_string(4)
+    # pure host queries: sizes grow with N and D, bad widths are refused
+    a = gba.gba_aggregate_sparse_workspace_size(1000, 4, 16, 10_000)
+    b = gba.gba_aggregate_sparse_workspace_size(100_000, 4, 16, 10_000)
+    c = gba.gba_aggregate_sparse_workspace_size(100_000, 4, 64, 10_000)
+    assert 0 < a < b < c
+    assert gba.gba_aggregate_sparse_workspace_size(0, 1, 4, 1) > 0
+    for bad in [(10, 4, 6, 100), (10, 4, 260, 100), (10, 0, 8, 100), (10, 5000, 8, 100),
+                (10, 4, 8, 0), (-1, 4, 8, 100), (10, 4, 8, (1 << 32) + 1)]:
+        with pytest.raises(gba.GBAError):
+            gba.gba_aggregate_sparse_workspace_size(*bad)
+
+
+def test_host_checks_return_before_any_launch():
+    L = gba.lib()
+    # null pointers and bad sizes are refused on the host, without touching a GPU
+    assert L.gba_token_weights(None, 4, 0, 0, None, None, None, None, None) == 1
+    assert L.gba_token_weights(None, 0, 0, 0, None, None, None, None, None) == 1
+    assert L.gba_aggregate_dense(None, None, 0, 10, None, None) == 2
+    assert L.gba_aggregate_dense(None, None, 3, 0, None, None) == 0
+    assert L.gba_apply_adagrad(None, None, None, None, None, None, 0, 0, 0, 0.1, 0.0, None, None) == 0
+    assert L.gba_apply_adam(None, None, None, None, None, None, None, 10, 0, 0, 0.1, 0.9, 0.999, 0.0, 0,
+                            None, None) == 2

@@ -1,0 +1,411 @@
+"""Parity of every C-ABI entry point with the CPU oracle, on seeded inputs
+at sizes that span several tiles and ragged tails, plus the degenerate
+cases of the method (empty contributions, a single hot ID, all IDs
+distinct, every contribution excluded, nothing at all)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2205_11048_amd as gba
+from compare import assert_exact, assert_rule_t, exact_fraction
+from paper_2205_11048_amd.step import GBAStep
+from synth import counter, workload
+from synth.configs import BY_NAME
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def dev(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).to(DEV)
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+# ------------------------------------------------------------------ Eq. 1
+@pytest.mark.parametrize("K", [1, 2, 63, 64, 65, 1000, 4096])
+def test_token_weights(K):
+    rng = np.random.default_rng(K)
+    step, iota = 777, int(rng.integers(0, 6))
+    tokens = step - rng.integers(0, 12, K)
+    w = torch.empty(K, dtype=torch.float32, device=DEV)
+    s = torch.empty(K, dtype=torch.int64, device=DEV)
+    nex = torch.zeros(1, dtype=torch.int32, device=DEV)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    gba.gba_token_weights(dev(tokens), step, iota, w, s, nex, err)
+    rw, rs, rn = oracle.token_weights(tokens, step, iota)
+    assert_exact(host(w), rw, "w")
+    assert_exact(host(s), rs, "staleness")
+    assert int(host(nex)[0]) == rn
+    assert int(host(err)[0]) == 0
+
+
+def test_future_token_is_reported():
+    tokens = np.array([5, 9, 4], np.int64)
+    w = torch.empty(3, dtype=torch.float32, device=DEV)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    gba.gba_token_weights(dev(tokens), 6, 2, w, err=err)
+    assert int(host(err)[0]) & gba.DERR_FUTURE_TOKEN
+    assert host(w)[1] == 0.0
+
+
+# ------------------------------------------------------------ dense, Alg. 2
+@pytest.mark.parametrize("K,P", [(1, 1), (3, 5), (4, 65536), (37, 100003), (256, 4099), (9, 3)])
+def test_aggregate_dense(K, P):
+    rng = np.random.default_rng(K * 1000 + P)
+    grads = [counter.values_range(17, counter.STREAM_DENSE_GRAD_BASE + m, 0, P, counter.KIND_GRAD,
+                                  counter.grad_scale(1e-2)) for m in range(K)]
+    tokens = 50 - rng.integers(0, 6, K)
+    w, _, _ = oracle.token_weights(tokens, 50, 3)
+    ref = oracle.aggregate_dense(grads, w)
+    poisoned = [g.copy() if w[m] != 0 else np.full(P, np.nan, np.float32) for m, g in enumerate(grads)]
+    g_dev = [dev(g) for g in poisoned]
+    out = torch.empty(P, dtype=torch.float32, device=DEV)
+    gba.gba_aggregate_dense(gba.pointer_table(g_dev), dev(w), P, out)
+    got = host(out)
+    assert_rule_t(got, ref, oracle.aggregate_dense_magnitude(grads, w), "g_bar")
+    assert_exact(got, ref, "g_bar (float64 accumulation in buffer order is exact)")
+
+
+def test_aggregate_dense_unaligned_and_fractional_weights():
+    K, P = 5, 1001
+    base = [dev(counter.values_range(3, 100 + m, 0, P + 1, counter.KIND_GRAD, counter.grad_scale(1e-2)))
+            for m in range(K)]
+    views = [b[1:] for b in base]                  # 4-byte offset: no 16-byte loads possible
+    w = np.array([1.0, 0.5, 0.0, 0.25, 1.0], np.float32)
+    out = torch.empty(P, dtype=torch.float32, device=DEV)
+    gba.gba_aggregate_dense(gba.pointer_table(views), dev(w), P, out)
+    ref = oracle.aggregate_dense([host(v) for v in views], w)
+    assert_exact(host(out), ref, "g_bar")
+
+
+def test_aggregate_dense_all_excluded():
+    K, P = 4, 777
+    g_dev = [torch.full((P,), float("nan"), device=DEV) for _ in range(K)]
+    out = torch.full((P,), 7.0, device=DEV)
+    gba.gba_aggregate_dense(gba.pointer_table(g_dev), torch.zeros(K, device=DEV), P, out)
+    assert_exact(host(out), np.zeros(P, np.float32), "g_bar")
+
+
+# ----------------------------------------------------------- sparse, Alg. 2
+def _run_sparse(ids, rows, offsets, w, tokens, step, iota, R, tag=None, decay="token", norm="per_id_count"):
+    N, D = rows.shape
+    K = len(offsets) - 1
+    cap = max(N, 1)
+    out = dict(unique_ids=torch.full((cap,), -5, dtype=torch.int64, device=DEV),
+               seg_offsets=torch.full((cap + 1,), -5, dtype=torch.int64, device=DEV),
+               contrib_count=torch.full((cap,), -5, dtype=torch.int32, device=DEV),
+               active_count=torch.full((cap,), -5, dtype=torch.int32, device=DEV),
+               agg=torch.full((cap, D), float("nan"), dtype=torch.float32, device=DEV),
+               num_unique=torch.full((1,), -5, dtype=torch.int64, device=DEV))
+    ws = torch.empty(gba.gba_aggregate_sparse_workspace_size(N, K, D, R), dtype=torch.uint8, device=DEV)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    tag_d = dev(tag) if tag is not None else None
+    gba.gba_aggregate_sparse(dev(ids), dev(rows.reshape(N, D)) if N else torch.empty((0, D), device=DEV),
+                             dev(offsets), R, dev(w), dev(tokens), step, iota, tag_d,
+                             gba.DECAY_ID_TAG if decay == "id_tag" else gba.DECAY_TOKEN,
+                             gba.NORM_BY_K if norm == "by_k" else gba.NORM_PER_ID_COUNT,
+                             out["unique_ids"], out["seg_offsets"], out["contrib_count"],
+                             out["active_count"], out["agg"], out["num_unique"], ws, err)
+    res = {k: host(v) for k, v in out.items()}
+    res["err"] = int(host(err)[0])
+    res["tag"] = host(tag_d) if tag_d is not None else None
+    return res
+
+
+def _check_sparse(res, ids, rows, offsets, w, tokens, step, iota, tag=None, decay="token",
+                  norm="per_id_count", expect_exact=False):
+    ref = oracle.aggregate_sparse(ids, rows, offsets, w, tokens, step, iota, tag, decay, norm)
+    U = ref["num_unique"]
+    assert res["err"] == 0
+    assert int(res["num_unique"][0]) == U
+    assert_exact(res["unique_ids"][:U], ref["unique_ids"], "unique_ids")
+    assert_exact(res["seg_offsets"][:U + 1], ref["seg_offsets"], "seg_offsets")
+    assert_exact(res["contrib_count"][:U], ref["contrib_count"], "contrib_count")
+    assert_exact(res["active_count"][:U], ref["active_count"], "active_count")
+    assert_rule_t(res["agg"][:U], ref["agg"], ref["agg_mu"], "agg")
+    if expect_exact:
+        assert_exact(res["agg"][:U], ref["agg"], "agg (dyadic inputs)")
+    if decay == "id_tag":
+        assert_exact(res["tag"], ref["new_tag"], "tag")
+    return ref
+
+
+def _case(K, sizes, R, D, seed, zipf_s=1.1, kind=counter.KIND_GRAD, step=1000, stale_hi=5):
+    rng = np.random.default_rng(seed)
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    N = int(off[-1])
+    from synth.zipf import ZipfRejectionInversion, rank_to_row
+    ids = rank_to_row(ZipfRejectionInversion(R, zipf_s).ranks(seed, np.arange(N)) - 1, R) if N else \
+        np.zeros(0, np.int64)
+    rows = counter.values_range(seed, counter.STREAM_ROWS, 0, N * D, kind,
+                                counter.grad_scale(1e-2)).reshape(N, D)
+    tokens = step - rng.integers(0, stale_hi + 1, K)
+    tag = workload.tag_values(seed, np.arange(R), step) if R <= 50_000_000 else None
+    return ids.astype(np.int64), rows, off, tokens, tag
+
+
+@pytest.mark.parametrize("D", [4, 8, 12, 16, 20, 32, 64, 128, 256])
+@pytest.mark.parametrize("decay", ["token", "id_tag"])
+def test_sparse_widths(D, decay):
+    K = 7
+    sizes = np.array([900, 0, 1733, 17, 1200, 0, 611])
+    ids, rows, off, tokens, tag = _case(K, sizes, 3000, D, seed=D)
+    w, _, _ = oracle.token_weights(tokens, 1000, 2)
+    res = _run_sparse(ids, rows, off, w, tokens, 1000, 2, 3000, tag, decay)
+    _check_sparse(res, ids, rows, off, w, tokens, 1000, 2, tag, decay)
+
+
+@pytest.mark.parametrize("norm", ["per_id_count", "by_k"])
+@pytest.mark.parametrize("decay", ["token", "id_tag"])
+def test_sparse_c0_full_size(norm, decay):
+    c = BY_NAME["c0"]
+    hs = workload.host_step(c, value_kind=counter.KIND_DYADIC)
+    w, _, _ = oracle.token_weights(hs.tokens, hs.step, c.iota)
+    res = _run_sparse(hs.ids, hs.rows, hs.offsets, w, hs.tokens, hs.step, c.iota, c.R, hs.tags, decay, norm)
+    _check_sparse(res, hs.ids, hs.rows, hs.offsets, w, hs.tokens, hs.step, c.iota, hs.tags, decay, norm,
+                  expect_exact=True)
+
+
+@pytest.mark.parametrize("D", [4, 32, 256])
+def test_sparse_one_hot_id_spans_many_blocks(D):
+    """One ID holds most occurrences, so its segment crosses many blocks and
+    the per-block partial sums must be joined."""
+    K, n = 6, 40_000
+    rng = np.random.default_rng(D)
+    N = K * n
+    ids = np.where(rng.random(N) < 0.7, 4242, rng.integers(0, 10_000, N)).astype(np.int64)
+    ids[: n // 2] = 4242                           # a long run inside the first contribution
+    off = np.arange(K + 1, dtype=np.int64) * n
+    rows = counter.values_range(9, counter.STREAM_ROWS, 0, N * D, counter.KIND_DYADIC).reshape(N, D)
+    tokens = 100 - np.array([0, 1, 4, 0, 2, 7])
+    w, _, _ = oracle.token_weights(tokens, 100, 3)
+    res = _run_sparse(ids, rows, off, w, tokens, 100, 3, 10_000)
+    _check_sparse(res, ids, rows, off, w, tokens, 100, 3, expect_exact=True)
+
+
+def test_sparse_single_id_everywhere():
+    K, n, D = 3, 50_000, 16
+    ids = np.full(K * n, 7, np.int64)
+    off = np.arange(K + 1, dtype=np.int64) * n
+    rows = counter.values_range(4, counter.STREAM_ROWS, 0, K * n * D, counter.KIND_DYADIC).reshape(-1, D)
+    tokens = np.array([10, 10, 3])
+    w, _, _ = oracle.token_weights(tokens, 10, 2)
+    res = _run_sparse(ids, rows, off, w, tokens, 10, 2, 8)
+    ref = _check_sparse(res, ids, rows, off, w, tokens, 10, 2, expect_exact=True)
+    assert ref["num_unique"] == 1 and list(ref["contrib_count"]) == [3] and list(ref["active_count"]) == [2]
+
+
+def test_sparse_all_distinct():
+    K, D, R = 4, 32, 1 << 20
+    rng = np.random.default_rng(1)
+    ids = rng.permutation(R)[:9999].astype(np.int64)
+    off = np.array([0, 2500, 5000, 7500, 9999], np.int64)
+    rows = counter.values_range(5, counter.STREAM_ROWS, 0, 9999 * D, counter.KIND_GRAD,
+                                counter.grad_scale(1e-2)).reshape(-1, D)
+    tokens = np.array([9, 9, 8, 1])
+    w, _, _ = oracle.token_weights(tokens, 9, 3)
+    res = _run_sparse(ids, rows, off, w, tokens, 9, 3, R)
+    ref = _check_sparse(res, ids, rows, off, w, tokens, 9, 3)
+    assert ref["num_unique"] == 9999 and np.all(ref["contrib_count"] == 1)
+
+
+def test_sparse_empty():
+    K, D = 3, 8
+    off = np.zeros(K + 1, np.int64)
+    res = _run_sparse(np.zeros(0, np.int64), np.zeros((0, D), np.float32), off, np.ones(K, np.float32),
+                      np.array([1, 1, 1]), 1, 0, 100)
+    assert int(res["num_unique"][0]) == 0 and int(res["seg_offsets"][0]) == 0 and res["err"] == 0
+
+
+def test_sparse_all_excluded():
+    K, sizes, R, D = 5, np.array([300, 200, 0, 50, 450]), 500, 16
+    ids, rows, off, tokens, tag = _case(K, sizes, R, D, seed=77, stale_hi=0)
+    tokens = tokens - 10                                     # every contribution too stale
+    w, _, nex = oracle.token_weights(tokens, 1000, 2)
+    assert nex == K
+    res = _run_sparse(ids, rows, off, w, tokens, 1000, 2, R)
+    ref = _check_sparse(res, ids, rows, off, w, tokens, 1000, 2)
+    assert np.all(ref["active_count"] == 0) and np.all(res["agg"][:ref["num_unique"]] == 0)
+
+
+def test_sparse_table_of_one_row_and_full_32bit_ids():
+    K, D = 2, 4
+    off = np.array([0, 3000, 7000], np.int64)
+    rows = counter.values_range(6, counter.STREAM_ROWS, 0, 7000 * D, counter.KIND_DYADIC).reshape(-1, D)
+    tokens = np.array([4, 4])
+    w = np.ones(K, np.float32)
+    ids = np.zeros(7000, np.int64)
+    res = _run_sparse(ids, rows, off, w, tokens, 4, 0, 1)
+    _check_sparse(res, ids, rows, off, w, tokens, 4, 0, expect_exact=True)
+    R = 1 << 32
+    rng = np.random.default_rng(2)
+    ids = np.concatenate([rng.integers(0, R, 6000), np.full(1000, R - 1)]).astype(np.int64)
+    res = _run_sparse(ids, rows, off, w, tokens, 4, 0, R)
+    _check_sparse(res, ids, rows, off, w, tokens, 4, 0, expect_exact=True)
+
+
+def test_sparse_many_small_contributions():
+    K, D, R = 4096, 8, 5000
+    rng = np.random.default_rng(3)
+    sizes = rng.integers(0, 6, K)
+    ids, rows, off, tokens, tag = _case(K, sizes, R, D, seed=3)
+    w, _, _ = oracle.token_weights(tokens, 1000, 3)
+    for decay in ("token", "id_tag"):
+        res = _run_sparse(ids, rows, off, w, tokens, 1000, 3, R, tag, decay)
+        _check_sparse(res, ids, rows, off, w, tokens, 1000, 3, tag, decay)
+
+
+def test_sparse_device_errors():
+    K, D, R = 2, 4, 100
+    off = np.array([0, 3, 6], np.int64)
+    rows = np.ones((6, D), np.float32)
+    ids = np.array([1, 2, 300, 4, 5, 6], np.int64)          # 300 is outside [0, R)
+    res = _run_sparse(ids, rows, off, np.ones(K, np.float32), np.array([1, 1]), 1, 0, R)
+    assert res["err"] & gba.DERR_ID_RANGE
+    ids = np.array([1, 2, 3, 4, 5, 6], np.int64)
+    res = _run_sparse(ids, rows, np.array([0, 4, 3], np.int64), np.ones(K, np.float32),
+                      np.array([1, 1]), 1, 0, R)
+    assert res["err"] & gba.DERR_OFFSETS
+
+
+def test_host_checks_enqueue_nothing():
+    with pytest.raises(gba.GBAError):
+        gba.gba_aggregate_sparse_workspace_size(10, 2, 6, 100)      # D not a multiple of 4
+    with pytest.raises(gba.GBAError):
+        gba.gba_aggregate_sparse_workspace_size(10, 0, 8, 100)      # K = 0
+    ws = torch.empty(16, dtype=torch.uint8, device=DEV)
+    z64 = torch.zeros(8, dtype=torch.int64, device=DEV)
+    z32 = torch.zeros(8, dtype=torch.int32, device=DEV)
+    with pytest.raises(gba.GBAError):                                  # workspace too small
+        gba.gba_aggregate_sparse(z64, torch.zeros((8, 4), device=DEV), torch.tensor([0, 8], device=DEV),
+                                 100, torch.ones(1, device=DEV), z64[:1], 0, 0, None, 0, 0, z64,
+                                 torch.zeros(9, dtype=torch.int64, device=DEV), z32, z32,
+                                 torch.zeros((8, 4), device=DEV), z64[:1], ws)
+
+
+# ------------------------------------------------------------ optimisers
+@pytest.mark.parametrize("n", [1, 5, 100_003])
+def test_apply_dense_adagrad(n):
+    p = counter.values_range(1, 1, 0, n, counter.KIND_PARAM)
+    a = counter.values_range(1, 2, 0, n, counter.KIND_ACCUM)
+    g = counter.values_range(1, 3, 0, n, counter.KIND_GRAD, counter.grad_scale(1e-2))
+    pd, ad = dev(p), dev(a)
+    gba.gba_apply_adagrad(pd, ad, dev(g), 0.01, 1e-8)
+    rp, ra = oracle.adagrad(p, a, g, 0.01, 1e-8)
+    mp, ma = oracle.adagrad_magnitude(p, a, g, np.abs(g), 0.01, 1e-8)
+    assert_rule_t(host(pd), rp, mp, "param")
+    assert_rule_t(host(ad), ra, ma, "accum")
+    assert exact_fraction(host(pd), rp) > 0.999
+
+
+@pytest.mark.parametrize("n", [1, 7, 100_003])
+def test_apply_dense_adam(n):
+    p = counter.values_range(2, 1, 0, n, counter.KIND_PARAM)
+    m = counter.values_range(2, 2, 0, n, counter.KIND_ADAM_M)
+    v = counter.values_range(2, 3, 0, n, counter.KIND_ADAM_V)
+    g = counter.values_range(2, 4, 0, n, counter.KIND_GRAD, counter.grad_scale(1e-2))
+    pd, md, vd = dev(p), dev(m), dev(v)
+    gba.gba_apply_adam(pd, md, vd, dev(g), 1e-3, 0.9, 0.999, 1e-8, 1001)
+    rp, rm, rv = oracle.adam(p, m, v, g, 1e-3, 0.9, 0.999, 1e-8, 1001)
+    mp, mm, mv = oracle.adam_magnitude(p, m, v, g, np.abs(g), 1e-3, 0.9, 0.999, 1e-8, 1001)
+    assert_rule_t(host(pd), rp, mp, "param")
+    assert_rule_t(host(md), rm, mm, "m")
+    assert_rule_t(host(vd), rv, mv, "v")
+    assert exact_fraction(host(pd), rp) > 0.999
+
+
+@pytest.mark.parametrize("opt", ["adagrad", "adam"])
+@pytest.mark.parametrize("D", [4, 16, 24, 64, 256])
+def test_apply_rows(opt, D):
+    R, n = 3000, 1200
+    rng = np.random.default_rng(D)
+    rows = rng.permutation(R)[:n].astype(np.int64)
+    active = (rng.random(n) < 0.8).astype(np.int32)
+    count = 1000                                     # entries past the count are ignored
+    table = counter.values_range(3, counter.STREAM_TABLE, 0, R * D, counter.KIND_PARAM).reshape(R, D)
+    s1 = counter.values_range(3, 5, 0, R * D, counter.KIND_ACCUM if opt == "adagrad" else counter.KIND_ADAM_M).reshape(R, D)
+    s2 = counter.values_range(3, 6, 0, R * D, counter.KIND_ADAM_V).reshape(R, D)
+    g = counter.values_range(3, 7, 0, n * D, counter.KIND_GRAD, counter.grad_scale(1e-2)).reshape(n, D)
+    td, s1d, s2d = dev(table), dev(s1), dev(s2)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    num = torch.tensor([count], dtype=torch.int64, device=DEV)
+    if opt == "adagrad":
+        gba.gba_apply_adagrad(td, s1d, dev(g), 0.01, 1e-8, rows=dev(rows), active=dev(active), num_rows=num,
+                              R=R, err=err)
+    else:
+        gba.gba_apply_adam(td, s1d, s2d, dev(g), 1e-3, 0.9, 0.999, 1e-8, 7, rows=dev(rows), active=dev(active),
+                           num_rows=num, R=R, err=err)
+    upd = np.zeros(R, bool)
+    sel = np.nonzero(active[:count] > 0)[0]
+    upd[rows[sel]] = True
+    et, e1, e2 = table.copy(), s1.copy(), s2.copy()
+    if opt == "adagrad":
+        et[rows[sel]], e1[rows[sel]] = oracle.adagrad(table[rows[sel]], s1[rows[sel]], g[sel], 0.01, 1e-8)
+    else:
+        et[rows[sel]], e1[rows[sel]], e2[rows[sel]] = oracle.adam(table[rows[sel]], s1[rows[sel]], s2[rows[sel]],
+                                                                  g[sel], 1e-3, 0.9, 0.999, 1e-8, 7)
+    gt, g1, g2 = host(td), host(s1d), host(s2d)
+    assert_exact(gt[~upd], table[~upd], "untouched rows")
+    assert_exact(g1[~upd], s1[~upd], "untouched state")
+    assert_rule_t(gt, et, None, "table")
+    assert_rule_t(g1, e1, None, "slot1")
+    if opt == "adam":
+        assert_rule_t(g2, e2, None, "slot2")
+    assert int(host(err)[0]) == 0
+
+
+def test_apply_rows_out_of_range_is_reported():
+    R, D = 10, 4
+    td = torch.zeros((R, D), device=DEV)
+    ad = torch.ones((R, D), device=DEV)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    gba.gba_apply_adagrad(td, ad, torch.ones((2, D), device=DEV), 0.1, 0.0,
+                          rows=torch.tensor([3, 10], device=DEV), num_rows=torch.tensor([2], device=DEV),
+                          R=R, err=err)
+    assert int(host(err)[0]) & gba.DERR_ROW_RANGE
+    t = host(td)
+    assert np.all(t[3] != 0) and np.all(np.delete(t, 3, axis=0) == 0)
+
+
+# ------------------------------------------------------------ whole step
+@pytest.mark.parametrize("decay", ["token", "id_tag"])
+@pytest.mark.parametrize("opt", ["adagrad", "adam"])
+def test_full_step_small(decay, opt):
+    c = BY_NAME["c0"].scaled(optimizer=opt, lr=0.01 if opt == "adagrad" else 1e-3)
+    hs = workload.host_step(c)
+    stepper = GBAStep(c.K, c.N, c.D, c.R, c.P)
+    grads = [dev(g) for g in hs.grads]
+    param, table = dev(hs.param), dev(hs.table)
+    dslots = [dev(s) for s in hs.dense_slots]
+    tslots = [dev(s) for s in hs.table_slots]
+    tag = dev(hs.tags)
+    stepper.run(tokens=dev(hs.tokens), step=hs.step, iota=c.iota, grads=grads, ids=dev(hs.ids),
+                rows=dev(hs.rows), offsets=dev(hs.offsets), param=param, dense_slots=dslots, table=table,
+                table_slots=tslots, optimizer=opt, lr=c.lr, eps=c.eps, t=c.adam_t, tag=tag,
+                decay=gba.DECAY_ID_TAG if decay == "id_tag" else gba.DECAY_TOKEN)
+    hp = dict(lr=c.lr, eps=c.eps, beta1=c.beta1, beta2=c.beta2)
+    ref = oracle.gba_step(hs.tokens, hs.step, c.iota, hs.grads, hs.ids, hs.rows, hs.offsets, hs.param,
+                          hs.dense_slots, lambda r: hs.table[r], lambda k, r: hs.table_slots[k][r], opt, hp,
+                          tag=hs.tags, decay=decay, t=c.adam_t)
+    assert int(host(stepper.err)[0]) == 0
+    assert_exact(host(stepper.w), ref["w"], "w")
+    assert int(host(stepper.num_excluded)[0]) == ref["num_excluded"]
+    assert_exact(host(stepper.g_bar), ref["g_bar"], "g_bar")
+    assert_rule_t(host(param), ref["param"], None, "param")
+    for k, s in enumerate(ref["dense_slots"]):
+        assert_rule_t(host(dslots[k]), s, None, f"dense slot {k}")
+    t_after = host(table)
+    act = ref["active_ids"]
+    assert_rule_t(t_after[act], ref["table_rows"], None, "table rows")
+    untouched = np.ones(c.R, bool)
+    untouched[act] = False
+    assert_exact(t_after[untouched], hs.table[untouched], "untouched rows")
+    for k, s in enumerate(ref["table_slot_rows"]):
+        assert_rule_t(host(tslots[k])[act], s, None, f"table slot {k}")
+    if decay == "id_tag":
+        assert_exact(host(tag), ref["sparse"]["new_tag"], "tag")
