@@ -1,0 +1,273 @@
+"""Throughput of the GBA push-step on one MI355X.
+
+A step is one pass of the whole path over one global batch of K buffered
+contributions: token weights (Eq. 1), dense weighted sum / K, embedding
+dedup + decayed weighted sum / c_r (Alg. 2, push responder), and the
+optimiser apply on the dense vector and the touched rows.  Inputs are
+seeded synthetic recommendation-shaped workloads resident in HBM before the
+timed region starts.
+
+Prints ONE JSON line.  `value` is global batches (steps) per second on the
+headline workload (c4: K=256 contributions of 256 x 1000 Zipf IDs over a
+500M x 32 table, 16M dense parameters, Adagrad); embedding-grad rows/s and
+the achieved algorithmic HBM bandwidth against the 8 TB/s peak are reported
+beside it, and the same figures for the dense-heavy workload c3 under
+`other_workloads`.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="c4")
+    ap.add_argument("--also", default="c3", help="comma list of extra workloads ('' for none)")
+    ap.add_argument("--decay", default="token", choices=["token", "id_tag"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample", type=int, default=16, help="1/S of the workload for the oracle timing")
+    return ap.parse_args()
+
+
+def algorithmic_bytes(w, K_eff, N_act, U, U_act, id_tag):
+    """Bytes the step must move at least once (inputs read, state read and
+    written, outputs written); sort passes and intermediate round trips are
+    overhead and are not counted."""
+    S = 1 if w.optimizer == "adagrad" else 2
+    dense = K_eff * w.P * 4 + (2 + 2 * S) * w.P * 4
+    sparse = (w.N * 8 + N_act * w.D * 4 + U_act * (2 + 2 * S) * w.D * 4 + U * 24)
+    if id_tag:
+        sparse += U * 4 + U_act * 4
+    return dense, sparse
+
+
+def kernel_source_sha(path):
+    with open(os.path.join(ROOT, path), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic(kernel, workload_name):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they
+    were taken on the current source of the kernel; else None."""
+    p = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(p):
+        return None
+    with open(p) as f:
+        data = json.load(f)
+    e = data.get(f"{kernel}@{workload_name}")
+    if not e or e.get("source_sha256_16") != kernel_source_sha(e["source"]):
+        return None
+    return e["bytes_per_launch"]
+
+
+def run_workload(name, args, torch, gba_step_mod, sdev, gba):
+    from synth.configs import BY_NAME
+    w = BY_NAME[name]
+    t0 = time.time()
+    ds = sdev.make_device_step(w, with_tags=(args.decay == "id_tag"))
+    torch.cuda.synchronize()
+    setup_s = time.time() - t0
+    print(f"[bench] {name}: inputs resident in HBM after {setup_s:.1f} s", file=sys.stderr, flush=True)
+    st = gba_step_mod.GBAStep(w.K, w.N, w.D, w.R, w.P)
+    decay = gba.DECAY_ID_TAG if args.decay == "id_tag" else gba.DECAY_TOKEN
+    stream = torch.cuda.current_stream()
+    names = ["token_weights", "aggregate_dense", "aggregate_sparse", "apply_dense", "apply_rows"]
+
+    def one_step(ev=None):
+        kw = dict(stream=stream)
+        if ev is not None:
+            ev[0].record(stream)
+        gba.gba_token_weights(ds.tokens, ds.step, w.iota, st.w, st.staleness, st.num_excluded, st.err, **kw)
+        if ev is not None:
+            ev[1].record(stream)
+        gba.gba_aggregate_dense(st.grad_table(ds.grads), st.w, w.P, st.g_bar, **kw)
+        if ev is not None:
+            ev[2].record(stream)
+        gba.gba_aggregate_sparse(ds.ids, ds.rows, ds.offsets, w.R, st.w, ds.tokens, ds.step, w.iota,
+                                 ds.tags, decay, gba.NORM_PER_ID_COUNT, st.unique_ids, st.seg_offsets,
+                                 st.contrib_count, st.active_count, st.agg, st.num_unique, st.workspace,
+                                 st.err, **kw)
+        if ev is not None:
+            ev[3].record(stream)
+        if w.optimizer == "adagrad":
+            gba.gba_apply_adagrad(ds.param, ds.dense_slots[0], st.g_bar, w.lr, w.eps, **kw)
+            if ev is not None:
+                ev[4].record(stream)
+            gba.gba_apply_adagrad(ds.table, ds.table_slots[0], st.agg, w.lr, w.eps, rows=st.unique_ids,
+                                  active=st.active_count, num_rows=st.num_unique, R=w.R, err=st.err, **kw)
+        else:
+            gba.gba_apply_adam(ds.param, ds.dense_slots[0], ds.dense_slots[1], st.g_bar, w.lr, w.beta1,
+                               w.beta2, w.eps, w.adam_t, **kw)
+            if ev is not None:
+                ev[4].record(stream)
+            gba.gba_apply_adam(ds.table, ds.table_slots[0], ds.table_slots[1], st.agg, w.lr, w.beta1,
+                               w.beta2, w.eps, w.adam_t, rows=st.unique_ids, active=st.active_count,
+                               num_rows=st.num_unique, R=w.R, err=st.err, **kw)
+        if ev is not None:
+            ev[5].record(stream)
+
+    for _ in range(args.warmup):
+        one_step()
+    torch.cuda.synchronize()
+    if int(st.err.item()) != 0:
+        raise RuntimeError(f"device error bits {int(st.err.item())}")
+
+    # timed region: K whole steps, no host synchronisation inside
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    start.record(stream)
+    for i in range(args.steps):
+        one_step(evs[i])
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t_wall) * 1e3
+    print(f"[bench] {name}: {args.steps} steps timed", file=sys.stderr, flush=True)
+    total_ms = start.elapsed_time(end)
+    ms = total_ms / args.steps
+    breakdown = {n: float(np.mean([e[k].elapsed_time(e[k + 1]) for e in evs])) for k, n in enumerate(names)}
+
+    # realised sizes (the same every step: the batch is re-applied)
+    w_h = st.w.cpu().numpy()
+    K_eff = int((w_h != 0).sum())
+    m_of_j = np.repeat(np.arange(w.K), np.diff(ds.offsets_host))
+    N_act = int((w_h[m_of_j] != 0).sum()) if args.decay == "token" else None
+    U = int(st.num_unique.item())
+    act = st.active_count[:U]
+    U_act = int((act > 0).sum().item())
+    if N_act is None:
+        N_act = w.N  # upper bound for the per-ID mode (weights differ per row)
+    dense_b, sparse_b = algorithmic_bytes(w, K_eff, N_act, U, U_act, args.decay == "id_tag")
+    step_gbs = (dense_b + sparse_b) / (ms * 1e-3) / 1e9
+
+    # dominant kernel: the dense reduction (one launch per call)
+    dense_kernel_bytes = K_eff * w.P * 4 + w.P * 4
+    dk_ms = breakdown["aggregate_dense"]
+    dk_gbs = dense_kernel_bytes / (dk_ms * 1e-3) / 1e9
+    traffic = measured_traffic("aggregate_dense_kernel", name)
+    res = dict(
+        workload=name, ms_per_step=ms, wall_ms_per_step=wall_ms / args.steps,
+        global_batches_per_s=1000.0 / ms, embedding_grad_rows_per_s=w.N / (ms * 1e-3),
+        samples_per_s=w.K * w.B / (ms * 1e-3),
+        step_alg_bytes=dense_b + sparse_b, step_alg_gbs=step_gbs, step_frac_of_hbm_peak=step_gbs / HBM_PEAK_GBS,
+        breakdown_ms=breakdown, K_eff=K_eff, N=w.N, N_act=N_act, U=U, U_act=U_act, setup_s=setup_s,
+        roofline=dict(kernel="aggregate_dense_kernel", bound="hbm", achieved=dk_gbs, peak=HBM_PEAK_GBS,
+                      unit="GB/s", frac=dk_gbs / HBM_PEAK_GBS, traffic=traffic,
+                      alg_bytes_per_launch=dense_kernel_bytes, avg_launch_ms=dk_ms),
+    )
+    del ds, st
+    torch.cuda.empty_cache()
+    return res
+
+
+def cpu_baseline(name, S):
+    """The oracle, untuned, on 1/S of the workload (all K contributions, B/S
+    samples each, P/S dense parameters), one host thread; the measured time is
+    scaled by S to a whole step."""
+    import oracle
+    from synth import counter, workload
+    from synth.configs import BY_NAME, seed_of
+    w = BY_NAME[name]
+    ws = w.scaled(B=max(1, w.B // S), P=max(1, w.P // S))
+    seed = seed_of(name)
+    ids = workload.embedding_ids(ws, seed)
+    off = workload.contrib_offsets(ws)
+    rows = workload.row_values(ws, seed, 0, ws.N)
+    grads = np.stack([workload.dense_grad(ws, seed, m) for m in range(ws.K)])
+    tok = workload.tokens_from_staleness(workload.staleness_draws(ws, seed))
+    param = counter.values_range(seed, counter.STREAM_DENSE_PARAM, 0, ws.P, counter.KIND_PARAM)
+    kinds = workload.state_kinds(ws.optimizer)
+    dslots = [counter.values_range(seed, ds_, 0, ws.P, kind) for ds_, _, kind in kinds]
+    uniq = np.unique(ids)
+    trows = {}
+    idx = (uniq[:, None] * ws.D + np.arange(ws.D)[None, :]).reshape(-1)
+    trows["E"] = counter.values(seed, counter.STREAM_TABLE, idx, counter.KIND_PARAM).reshape(-1, ws.D)
+    for k, (_, ts, kind) in enumerate(kinds):
+        trows[k] = counter.values(seed, ts, idx, kind).reshape(-1, ws.D)
+
+    def rows_of(r):
+        return trows["E"][np.searchsorted(uniq, r)]
+
+    def slot_rows_of(k, r):
+        return trows[k][np.searchsorted(uniq, r)]
+
+    hp = dict(lr=ws.lr, eps=ws.eps, beta1=ws.beta1, beta2=ws.beta2)
+    t0 = time.perf_counter()
+    oracle.gba_step(tok, 1000, ws.iota, grads, ids, rows, off, param, dslots, rows_of, slot_rows_of,
+                    ws.optimizer, hp, t=ws.adam_t)
+    dt = time.perf_counter() - t0
+    full_s = dt * S
+    return dict(value=1.0 / full_s, unit="global batches/s", cores=1, kind="oracle",
+                sample=f"{name} at 1/{S}: K={ws.K} contributions of B={ws.B} samples x L={ws.L} IDs "
+                       f"(N={ws.N}), P={ws.P} dense params, same Zipf law and R; oracle time {dt:.2f} s x {S}",
+                seconds_measured=dt, host=platform.processor() or platform.machine(),
+                nproc=os.cpu_count())
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU: this build holds one PS shard per GPU and has no multi-GPU "
+              "path (run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2205_11048_amd as gba
+    from paper_2205_11048_amd import step as gba_step_mod
+    from synth import device as sdev
+
+    torch.cuda.set_device(0)
+    head = run_workload(args.workload, args, torch, gba_step_mod, sdev, gba)
+    others = [run_workload(n, args, torch, gba_step_mod, sdev, gba) for n in args.also.split(",") if n and n != args.workload]
+    from synth.configs import BY_NAME
+    w = BY_NAME[args.workload]
+    out = {
+        "metric": "global batches/sec and embedding-grad rows/sec; achieved HBM GB/s vs peak",
+        "value": head["global_batches_per_s"],
+        "unit": "global batches/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": head["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32 (f64 accumulation)",
+        "data": "synthetic (seeded; Zipf IDs, counter-based gradients; no dataset)",
+        "config": {"workload": f"{args.workload}: K={w.K} contributions, local batch {w.B}, "
+                               f"{w.L} IDs/sample Zipf s={w.zipf_s} over {w.R}x{w.D} fp32 table, "
+                               f"{w.P} dense params, {w.optimizer}, decay={args.decay}",
+                   "global_batch": w.K * w.B, "K": w.K, "N": w.N, "R": w.R, "D": w.D, "P": w.P,
+                   "parallelism": "one PS shard on one GPU"},
+        "embedding_grad_rows_per_s": head["embedding_grad_rows_per_s"],
+        "step_alg_gbs": head["step_alg_gbs"],
+        "step_frac_of_hbm_peak": head["step_frac_of_hbm_peak"],
+        "breakdown_ms": head["breakdown_ms"],
+        "realised": {k: head[k] for k in ("K_eff", "N", "N_act", "U", "U_act", "step_alg_bytes")},
+        "roofline": head["roofline"],
+        "other_workloads": others,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_sample)
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

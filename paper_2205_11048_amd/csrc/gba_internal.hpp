@@ -7,7 +7,7 @@
 #include <stddef.h>
 #include <stdint.h>
 
-#include "../../include/gba.h"
+#include "gba.h"
 
 namespace gba {
 

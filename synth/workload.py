@@ -54,6 +54,16 @@ def embedding_ids(w: Workload, seed: int, start: int = 0, count: int | None = No
     """
     if count is None:
         count = w.N - start
+    chunk = 1 << 21
+    if count > 2 * chunk:
+        # independent chunks (every ID depends only on its index): run them on threads
+        import os
+        from concurrent.futures import ThreadPoolExecutor
+        starts = list(range(start, start + count, chunk))
+        with ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1)) as ex:
+            parts = list(ex.map(lambda s0: embedding_ids(w, seed, s0, min(chunk, start + count - s0)),
+                                starts))
+        return np.concatenate(parts)
     j = np.arange(start, start + count, dtype=np.int64)
     if w.one_hot_fields:
         field_rows = w.R // w.L
