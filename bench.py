@@ -41,6 +41,8 @@ def parse():
     ap.add_argument("--also", default="c3", help="comma list of extra workloads ('' for none)")
     ap.add_argument("--decay", default="token", choices=["token", "id_tag"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--overlap", action="store_true",
+                    help="run the dense path on a second stream, concurrently with the sparse path")
     ap.add_argument("--cpu-sample", type=int, default=16, help="1/S of the workload for the oracle timing")
     return ap.parse_args()
 
@@ -87,40 +89,56 @@ def run_workload(name, args, torch, gba_step_mod, sdev, gba):
     st = gba_step_mod.GBAStep(w.K, w.N, w.D, w.R, w.P)
     decay = gba.DECAY_ID_TAG if args.decay == "id_tag" else gba.DECAY_TOKEN
     stream = torch.cuda.current_stream()
+    # the dense path (token weights -> dense sum -> dense apply) runs on its own
+    # stream, concurrently with the sparse path; both wait only for the weights
+    dstream = torch.cuda.Stream() if args.overlap else stream
     names = ["token_weights", "aggregate_dense", "aggregate_sparse", "apply_dense", "apply_rows"]
 
     def one_step(ev=None):
         kw = dict(stream=stream)
+        dkw = dict(stream=dstream)
         if ev is not None:
-            ev[0].record(stream)
+            ev["t0"].record(stream)
         gba.gba_token_weights(ds.tokens, ds.step, w.iota, st.w, st.staleness, st.num_excluded, st.err, **kw)
         if ev is not None:
-            ev[1].record(stream)
-        gba.gba_aggregate_dense(st.grad_table(ds.grads), st.w, w.P, st.g_bar, **kw)
+            ev["t1"].record(stream)
+        if args.overlap:
+            w_ready = torch.cuda.Event()
+            w_ready.record(stream)
+            dstream.wait_event(w_ready)
         if ev is not None:
-            ev[2].record(stream)
+            ev["d0"].record(dstream)
+        gba.gba_aggregate_dense(st.grad_table(ds.grads), st.w, w.P, st.g_bar, **dkw)
+        if ev is not None:
+            ev["d1"].record(dstream)
+        if w.optimizer == "adagrad":
+            gba.gba_apply_adagrad(ds.param, ds.dense_slots[0], st.g_bar, w.lr, w.eps, **dkw)
+        else:
+            gba.gba_apply_adam(ds.param, ds.dense_slots[0], ds.dense_slots[1], st.g_bar, w.lr, w.beta1,
+                               w.beta2, w.eps, w.adam_t, **dkw)
+        if ev is not None:
+            ev["d2"].record(dstream)
+        if ev is not None:
+            ev["s0"].record(stream)
         gba.gba_aggregate_sparse(ds.ids, ds.rows, ds.offsets, w.R, st.w, ds.tokens, ds.step, w.iota,
                                  ds.tags, decay, gba.NORM_PER_ID_COUNT, st.unique_ids, st.seg_offsets,
                                  st.contrib_count, st.active_count, st.agg, st.num_unique, st.workspace,
                                  st.err, **kw)
         if ev is not None:
-            ev[3].record(stream)
+            ev["s1"].record(stream)
         if w.optimizer == "adagrad":
-            gba.gba_apply_adagrad(ds.param, ds.dense_slots[0], st.g_bar, w.lr, w.eps, **kw)
-            if ev is not None:
-                ev[4].record(stream)
             gba.gba_apply_adagrad(ds.table, ds.table_slots[0], st.agg, w.lr, w.eps, rows=st.unique_ids,
                                   active=st.active_count, num_rows=st.num_unique, R=w.R, err=st.err, **kw)
         else:
-            gba.gba_apply_adam(ds.param, ds.dense_slots[0], ds.dense_slots[1], st.g_bar, w.lr, w.beta1,
-                               w.beta2, w.eps, w.adam_t, **kw)
-            if ev is not None:
-                ev[4].record(stream)
             gba.gba_apply_adam(ds.table, ds.table_slots[0], ds.table_slots[1], st.agg, w.lr, w.beta1,
                                w.beta2, w.eps, w.adam_t, rows=st.unique_ids, active=st.active_count,
                                num_rows=st.num_unique, R=w.R, err=st.err, **kw)
         if ev is not None:
-            ev[5].record(stream)
+            ev["s2"].record(stream)
+        if args.overlap:
+            d_done = torch.cuda.Event()
+            d_done.record(dstream)
+            stream.wait_event(d_done)
 
     for _ in range(args.warmup):
         one_step()
@@ -129,7 +147,8 @@ def run_workload(name, args, torch, gba_step_mod, sdev, gba):
         raise RuntimeError(f"device error bits {int(st.err.item())}")
 
     # timed region: K whole steps, no host synchronisation inside
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+    evs = [{k: torch.cuda.Event(enable_timing=True) for k in ("t0", "t1", "d0", "d1", "d2", "s0", "s1", "s2")}
+           for _ in range(args.steps)]
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -143,7 +162,9 @@ def run_workload(name, args, torch, gba_step_mod, sdev, gba):
     print(f"[bench] {name}: {args.steps} steps timed", file=sys.stderr, flush=True)
     total_ms = start.elapsed_time(end)
     ms = total_ms / args.steps
-    breakdown = {n: float(np.mean([e[k].elapsed_time(e[k + 1]) for e in evs])) for k, n in enumerate(names)}
+    spans = {"token_weights": ("t0", "t1"), "aggregate_dense": ("d0", "d1"), "apply_dense": ("d1", "d2"),
+             "aggregate_sparse": ("s0", "s1"), "apply_rows": ("s1", "s2")}
+    breakdown = {n: float(np.mean([e[a].elapsed_time(e[b]) for e in evs])) for n, (a, b) in spans.items()}
 
     # realised sizes (the same every step: the batch is re-applied)
     w_h = st.w.cpu().numpy()
@@ -168,7 +189,7 @@ def run_workload(name, args, torch, gba_step_mod, sdev, gba):
         global_batches_per_s=1000.0 / ms, embedding_grad_rows_per_s=w.N / (ms * 1e-3),
         samples_per_s=w.K * w.B / (ms * 1e-3),
         step_alg_bytes=dense_b + sparse_b, step_alg_gbs=step_gbs, step_frac_of_hbm_peak=step_gbs / HBM_PEAK_GBS,
-        breakdown_ms=breakdown, K_eff=K_eff, N=w.N, N_act=N_act, U=U, U_act=U_act, setup_s=setup_s,
+        breakdown_ms=breakdown, overlap=args.overlap, K_eff=K_eff, N=w.N, N_act=N_act, U=U, U_act=U_act, setup_s=setup_s,
         roofline=dict(kernel="aggregate_dense_kernel", bound="hbm", achieved=dk_gbs, peak=HBM_PEAK_GBS,
                       unit="GB/s", frac=dk_gbs / HBM_PEAK_GBS, traffic=traffic,
                       alg_bytes_per_launch=dense_kernel_bytes, avg_launch_ms=dk_ms),

@@ -50,7 +50,8 @@ enum {
   GBA_DERR_ID_RANGE = 1,      /* an embedding ID outside [0, R)                    */
   GBA_DERR_FUTURE_TOKEN = 2,  /* a token newer than the step being applied         */
   GBA_DERR_OFFSETS = 4,       /* contribution offsets not 0 .. N and non-decreasing */
-  GBA_DERR_ROW_RANGE = 8      /* a row index passed to a sparse apply outside [0, R) */
+  GBA_DERR_ROW_RANGE = 8,     /* a row index passed to a sparse apply outside [0, R) */
+  GBA_DERR_INTERNAL = 16      /* a bounded wait between tiles gave up (outputs invalid) */
 };
 
 /* How embedding gradients are decayed (Alg. 2). */
@@ -124,7 +125,7 @@ gba_status gba_aggregate_sparse_workspace_size(int64_t N, int32_t K, int32_t D, 
  *                  accumulation) divided by c_r (or by K); 0 when W_r = 0.
  *   num_unique     one int64, U.
  * workspace        device scratch of at least the queried size.
- * Limits: 1 <= K <= GBA_MAX_K, 0 <= N < 2^31, 1 <= R <= 2^32,
+ * Limits: 1 <= K <= GBA_MAX_K, 0 <= N < 2^30, 1 <= R <= 2^32,
  * D % 4 == 0 and 4 <= D <= GBA_MAX_D.
  */
 gba_status gba_aggregate_sparse(const int64_t* ids, const float* rows,

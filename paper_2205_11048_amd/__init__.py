@@ -17,15 +17,18 @@ __all__ = [
     "GBAError", "lib", "gba_token_weights", "gba_aggregate_dense", "gba_aggregate_sparse",
     "gba_aggregate_sparse_workspace_size", "gba_apply_adagrad", "gba_apply_adam",
     "pointer_table", "DECAY_TOKEN", "DECAY_ID_TAG", "NORM_PER_ID_COUNT", "NORM_BY_K",
-    "DERR_ID_RANGE", "DERR_FUTURE_TOKEN", "DERR_OFFSETS", "DERR_ROW_RANGE", "MAX_K", "MAX_D",
+    "DERR_ID_RANGE", "DERR_FUTURE_TOKEN", "DERR_OFFSETS", "DERR_ROW_RANGE", "DERR_INTERNAL", "MAX_K", "MAX_D",
     "LIB_PATH",
 ]
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libgba.so")
+# GBA_LIBRARY may name another build of the library (for example one made for
+# a different launch configuration); by default the in-tree build is used.
+LIB_PATH = os.environ.get("GBA_LIBRARY") or os.path.join(os.path.dirname(os.path.abspath(__file__)),
+                                                         "libgba.so")
 
 DECAY_TOKEN, DECAY_ID_TAG = 0, 1
 NORM_PER_ID_COUNT, NORM_BY_K = 0, 1
-DERR_ID_RANGE, DERR_FUTURE_TOKEN, DERR_OFFSETS, DERR_ROW_RANGE = 1, 2, 4, 8
+DERR_ID_RANGE, DERR_FUTURE_TOKEN, DERR_OFFSETS, DERR_ROW_RANGE, DERR_INTERNAL = 1, 2, 4, 8, 16
 MAX_K, MAX_D = 4096, 256
 
 _P = ctypes.c_void_p

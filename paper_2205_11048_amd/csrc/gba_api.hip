@@ -9,7 +9,7 @@ using namespace gba;
 
 namespace {
 
-constexpr int64_t kMaxN = (int64_t(1) << 31) - 1;
+constexpr int64_t kMaxN = (int64_t(1) << 30) - 1;
 
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 inline size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }

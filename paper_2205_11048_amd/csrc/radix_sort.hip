@@ -3,12 +3,13 @@
 // push-step can deduplicate them and reduce their rows (Alg. 2: gradients of
 // the embedding parameters are processed by ID).
 //
-// Each pass over one digit (<= 8 bits) is three launches: a per-tile digit
-// histogram, a device-wide exclusive scan of the histograms (digit-major, so
-// the scan yields each tile's global offset per digit), and a scatter that
-// ranks the tile stably in LDS before writing runs of equal digits together.
+// Each 8-bit digit takes three steps: a histogram per tile of 4096 keys
+// (written tile-major, 1 KB per tile), a column scan that turns the per-tile
+// counts into each tile's global offset per digit value (tile-major again, so
+// a tile reads its 256 offsets as one contiguous line), and a scatter that
+// ranks the tile stably in LDS and writes runs of equal digits together.
 // Ranks inside a wave come from ballots that match lanes holding the same
-// digit, so skewed (Zipf) keys cost no LDS atomics on hot bins.
+// digit, so skewed (Zipf) keys cost no LDS atomics on hot bins in the scatter.
 #include "gba_device.hpp"
 #include "gba_internal.hpp"
 
@@ -16,13 +17,34 @@ namespace gba {
 
 constexpr int kSortBlock = 256;
 constexpr int kSortWaves = kSortBlock / kWave;
-constexpr int kSortItems = 16;                        // per lane
+constexpr int kSortItems = 16;                         // per lane
 constexpr int kSortWaveTile = kWave * kSortItems;      // 1024 keys per wave
-constexpr int64_t kSortTile = kSortBlock * kSortItems; // 4096 keys per block
+constexpr int64_t kSortTile = kSortBlock * kSortItems; // 4096 keys per tile
 constexpr int kRadix = 256;
+constexpr int kChunk = 32;                             // tiles per column-scan chunk
 
 static inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 static inline size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
+
+struct SortLayout {
+  size_t arr, off_keys0, off_keys1, off_vals0, off_vals1, off_hist, off_chunk, off_base, bytes;
+};
+
+static SortLayout sort_layout(int64_t n, int64_t tiles) {
+  SortLayout L{};
+  L.arr = align_up((size_t)(n > 0 ? n : 1) * sizeof(uint32_t));
+  const size_t nt = (size_t)(tiles > 0 ? tiles : 1);
+  size_t o = 0;
+  L.off_keys0 = o; o += L.arr;
+  L.off_keys1 = o; o += L.arr;
+  L.off_vals0 = o; o += L.arr;
+  L.off_vals1 = o; o += L.arr;
+  L.off_hist = o;  o += align_up(nt * kRadix * 4);                       // [tile][digit]
+  L.off_chunk = o; o += align_up((size_t)ceil_div((int64_t)nt, kChunk) * kRadix * 4);
+  L.off_base = o;  o += align_up(kRadix * 4);
+  L.bytes = o;
+  return L;
+}
 
 // Mask of the active lanes whose digit equals this lane's digit.
 __device__ __forceinline__ uint64_t match_digit(uint32_t digit, int bits, bool active) {
@@ -50,40 +72,104 @@ __device__ __forceinline__ uint32_t load_key(const void* src, int64_t i, int64_t
   return static_cast<const uint32_t*>(src)[i];
 }
 
+// Digit counts of one tile, one 1 KB row per tile.  Each wave adds one count
+// per run of equal digits among its 64 lanes, so the long runs of a hot ID
+// (contiguous after the first pass) cost one LDS add, not 64 colliding ones.
 template <bool FIRST>
 __global__ void __launch_bounds__(kSortBlock)
-sort_histogram_kernel(const void* __restrict__ keys_in, int64_t n, int shift, int bits, int64_t R,
-                      int64_t num_tiles, uint32_t* __restrict__ hist, int32_t* __restrict__ err) {
-  __shared__ uint32_t cnt[kSortWaves][kRadix];
-  for (int i = threadIdx.x; i < kSortWaves * kRadix; i += kSortBlock) (&cnt[0][0])[i] = 0;
+sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n, int shift, int bits, int64_t R,
+                      uint32_t* __restrict__ hist, int32_t* __restrict__ err) {
+  __shared__ uint32_t h[kSortWaves][kRadix];
+  for (int i = threadIdx.x; i < kSortWaves * kRadix; i += kSortBlock) (&h[0][0])[i] = 0u;
   __syncthreads();
   const int w = threadIdx.x / kWave;
-  const int64_t base = (int64_t)blockIdx.x * kSortTile + (int64_t)w * kSortWaveTile + lane_id();
+  const int lane = lane_id();
+  const int64_t base = (int64_t)blockIdx.x * kSortTile + (int64_t)w * kSortWaveTile + lane;
   const uint32_t mask = (1u << bits) - 1u;
   bool bad = false;
+  uint32_t digit[kSortItems];
+#pragma unroll
   for (int r = 0; r < kSortItems; ++r) {
     const int64_t i = base + (int64_t)r * kWave;
-    const bool active = i < n;
-    const uint32_t key = active ? load_key<FIRST>(keys_in, i, R, &bad) : 0u;
-    const uint32_t digit = (key >> shift) & mask;
-    const uint64_t m = match_digit(digit, bits, active);
-    if (active && (m & lanemask_lt()) == 0) cnt[w][digit] += (uint32_t)__popcll(m);
+    digit[r] = i < n ? (load_key<FIRST>(keys_in, i, R, &bad) >> shift) & mask : 0u;
+  }
+#pragma unroll
+  for (int r = 0; r < kSortItems; ++r) {
+    const bool active = base + (int64_t)r * kWave < n;   // active lanes are a prefix of the wave
+    const uint32_t prev = __shfl_up(digit[r], 1, kWave);
+    const bool head = active && (lane == 0 || digit[r] != prev);
+    const uint64_t heads = __ballot(head);
+    const int na = __popcll(__ballot(active));
+    if (head) {
+      const uint64_t above = lane == 63 ? 0ull : heads & (~0ull << (lane + 1));
+      const int next = above ? __builtin_ctzll(above) : na;
+      atomicAdd(&h[w][digit[r]], (uint32_t)(next - lane));
+    }
   }
   if (FIRST && bad) raise_error(err, GBA_DERR_ID_RANGE);
   __syncthreads();
   const int d = threadIdx.x;   // kSortBlock == kRadix
   uint32_t s = 0;
 #pragma unroll
-  for (int k = 0; k < kSortWaves; ++k) s += cnt[k][d];
-  hist[(int64_t)d * num_tiles + blockIdx.x] = s;
+  for (int k = 0; k < kSortWaves; ++k) s += h[k][d];
+  hist[(int64_t)blockIdx.x * kRadix + d] = s;
+}
+
+// Column sums of chunks of kChunk tiles (the rows are read together).
+__global__ void __launch_bounds__(kSortBlock)
+sort_chunk_sum_kernel(const uint32_t* __restrict__ hist, int64_t tiles, uint32_t* __restrict__ chunk) {
+  const int d = threadIdx.x;
+  const int64_t t0 = (int64_t)blockIdx.x * kChunk;
+  uint32_t s = 0;
+#pragma unroll
+  for (int k = 0; k < kChunk; ++k)
+    if (t0 + k < tiles) s += hist[(t0 + k) * kRadix + d];
+  chunk[(int64_t)blockIdx.x * kRadix + d] = s;
+}
+
+// Per digit: exclusive prefix over chunks; across digits: where each digit starts.
+__global__ void __launch_bounds__(kSortBlock)
+sort_chunk_scan_kernel(uint32_t* __restrict__ chunk, int64_t nchunks, uint32_t* __restrict__ base) {
+  constexpr int kStep = 16;
+  __shared__ uint32_t tmp[kSortBlock / kWave + 1];
+  const int d = threadIdx.x;
+  uint32_t run = 0;
+  for (int64_t c0 = 0; c0 < nchunks; c0 += kStep) {
+    uint32_t v[kStep];
+#pragma unroll
+    for (int k = 0; k < kStep; ++k) v[k] = (c0 + k < nchunks) ? chunk[(c0 + k) * kRadix + d] : 0u;
+#pragma unroll
+    for (int k = 0; k < kStep; ++k) {
+      if (c0 + k < nchunks) chunk[(c0 + k) * kRadix + d] = run;
+      run += v[k];
+    }
+  }
+  uint32_t total;
+  base[d] = block_exclusive_scan<kSortBlock>(run, tmp, &total);
+}
+
+// hist[tile][d] becomes the global position of the tile's first key with digit d.
+__global__ void __launch_bounds__(kSortBlock)
+sort_chunk_apply_kernel(uint32_t* __restrict__ hist, int64_t tiles, const uint32_t* __restrict__ chunk,
+                        const uint32_t* __restrict__ base) {
+  const int d = threadIdx.x;
+  const int64_t t0 = (int64_t)blockIdx.x * kChunk;
+  uint32_t run = base[d] + chunk[(int64_t)blockIdx.x * kRadix + d];
+  uint32_t v[kChunk];
+#pragma unroll
+  for (int k = 0; k < kChunk; ++k) v[k] = (t0 + k < tiles) ? hist[(t0 + k) * kRadix + d] : 0u;
+#pragma unroll
+  for (int k = 0; k < kChunk; ++k) {
+    if (t0 + k < tiles) hist[(t0 + k) * kRadix + d] = run;
+    run += v[k];
+  }
 }
 
 template <bool FIRST>
 __global__ void __launch_bounds__(kSortBlock)
 sort_scatter_kernel(const void* __restrict__ keys_in, const uint32_t* __restrict__ vals_in,
                     uint32_t* __restrict__ keys_out, uint32_t* __restrict__ vals_out, int64_t n,
-                    int shift, int bits, int64_t R, int64_t num_tiles,
-                    const uint32_t* __restrict__ offsets) {
+                    int shift, int bits, int64_t R, const uint32_t* __restrict__ offsets) {
   __shared__ uint32_t cnt[kSortWaves][kRadix];
   __shared__ uint32_t digit_start[kRadix];
   __shared__ uint32_t global_base[kRadix];
@@ -91,6 +177,7 @@ sort_scatter_kernel(const void* __restrict__ keys_in, const uint32_t* __restrict
   __shared__ uint32_t s_keys[kSortTile];
   __shared__ uint32_t s_vals[kSortTile];
   for (int i = threadIdx.x; i < kSortWaves * kRadix; i += kSortBlock) (&cnt[0][0])[i] = 0;
+  global_base[threadIdx.x] = offsets[(int64_t)blockIdx.x * kRadix + threadIdx.x];
   __syncthreads();
   const int w = threadIdx.x / kWave;
   const int64_t tile0 = (int64_t)blockIdx.x * kSortTile;
@@ -107,6 +194,7 @@ sort_scatter_kernel(const void* __restrict__ keys_in, const uint32_t* __restrict
     key[r] = active ? load_key<FIRST>(keys_in, i, R, &bad) : 0u;
     val[r] = active ? (FIRST ? (uint32_t)i : vals_in[i]) : 0u;
   }
+  (void)bad;   // range errors are reported by the histogram launch
   // Stable rank within (wave, digit): rounds in index order, lanes in order.
 #pragma unroll
   for (int r = 0; r < kSortItems; ++r) {
@@ -141,7 +229,6 @@ sort_scatter_kernel(const void* __restrict__ keys_in, const uint32_t* __restrict
       cnt[k][d] = run;
       run += c[k];
     }
-    global_base[d] = offsets[(int64_t)d * num_tiles + blockIdx.x];
   }
   __syncthreads();
 #pragma unroll
@@ -160,7 +247,7 @@ sort_scatter_kernel(const void* __restrict__ keys_in, const uint32_t* __restrict
     const uint32_t k = s_keys[i];
     const uint32_t digit = (k >> shift) & mask;
     const uint32_t g = global_base[digit] + ((uint32_t)i - digit_start[digit]);
-    if ((int64_t)g < n) {   // always true when the histograms are consistent
+    if ((int64_t)g < n) {   // always true when the counts are consistent
       keys_out[g] = k;
       vals_out[g] = s_vals[i];
     }
@@ -175,54 +262,53 @@ SortPlan plan_sort(int64_t n, int64_t R) {
   p.key_bits = bits;
   p.passes = (bits + 7) / 8;
   p.blocks = n > 0 ? ceil_div(n, kSortTile) : 0;
-  const size_t arr = align_up((size_t)(n > 0 ? n : 1) * sizeof(uint32_t));
-  const size_t hist_words = (size_t)kRadix * (size_t)(p.blocks > 0 ? p.blocks : 1);
-  p.bytes = 4 * arr + align_up(hist_words * sizeof(uint32_t)) +
-            align_up(scan_workspace_bytes((int64_t)hist_words));
+  p.bytes = sort_layout(n, p.blocks).bytes;
   return p;
 }
 
 hipError_t launch_sort_ids(const int64_t* ids, int64_t n, int64_t R, const SortPlan& plan, void* ws,
                            const uint32_t** keys_out, const uint32_t** vals_out, int32_t* err,
                            hipStream_t stream) {
+  const SortLayout L = sort_layout(n, plan.blocks);
   char* p = static_cast<char*>(ws);
-  const size_t arr = align_up((size_t)(n > 0 ? n : 1) * sizeof(uint32_t));
-  uint32_t* keys[2] = {reinterpret_cast<uint32_t*>(p), reinterpret_cast<uint32_t*>(p + arr)};
-  uint32_t* vals[2] = {reinterpret_cast<uint32_t*>(p + 2 * arr), reinterpret_cast<uint32_t*>(p + 3 * arr)};
-  const size_t hist_words = (size_t)kRadix * (size_t)(plan.blocks > 0 ? plan.blocks : 1);
-  uint32_t* hist = reinterpret_cast<uint32_t*>(p + 4 * arr);
-  void* scan_ws = p + 4 * arr + align_up(hist_words * sizeof(uint32_t));
+  uint32_t* keys[2] = {reinterpret_cast<uint32_t*>(p + L.off_keys0), reinterpret_cast<uint32_t*>(p + L.off_keys1)};
+  uint32_t* vals[2] = {reinterpret_cast<uint32_t*>(p + L.off_vals0), reinterpret_cast<uint32_t*>(p + L.off_vals1)};
+  uint32_t* hist = reinterpret_cast<uint32_t*>(p + L.off_hist);
+  uint32_t* chunk = reinterpret_cast<uint32_t*>(p + L.off_chunk);
+  uint32_t* base = reinterpret_cast<uint32_t*>(p + L.off_base);
   *keys_out = keys[0];
   *vals_out = vals[0];
   if (n <= 0) return hipSuccess;
-  const dim3 grid((unsigned)plan.blocks), block(kSortBlock);
+  const int64_t tiles = plan.blocks;
+  const int64_t nchunks = ceil_div(tiles, kChunk);
+  const dim3 grid((unsigned)tiles), block(kSortBlock);
+  hipError_t e;
   int cur = 0;
   for (int pass = 0; pass < plan.passes; ++pass) {
     const int shift = 8 * pass;
     const int bits = (plan.key_bits - shift) < 8 ? (plan.key_bits - shift) : 8;
     const int out = pass == 0 ? 0 : 1 - cur;
-    if (pass == 0) {
-      hipLaunchKernelGGL(sort_histogram_kernel<true>, grid, block, 0, stream, (const void*)ids, n,
-                         shift, bits, R, plan.blocks, hist, err);
-    } else {
-      hipLaunchKernelGGL(sort_histogram_kernel<false>, grid, block, 0, stream,
-                         (const void*)keys[cur], n, shift, bits, R, plan.blocks, hist, err);
-    }
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    e = launch_exclusive_scan_u32(hist, hist, (int64_t)kRadix * plan.blocks, nullptr, scan_ws, stream);
-    if (e != hipSuccess) return e;
-    if (pass == 0) {
-      hipLaunchKernelGGL(sort_scatter_kernel<true>, grid, block, 0, stream, (const void*)ids,
-                         (const uint32_t*)nullptr, keys[out], vals[out], n, shift, bits, R,
-                         plan.blocks, (const uint32_t*)hist);
-    } else {
-      hipLaunchKernelGGL(sort_scatter_kernel<false>, grid, block, 0, stream, (const void*)keys[cur],
-                         (const uint32_t*)vals[cur], keys[out], vals[out], n, shift, bits, R,
-                         plan.blocks, (const uint32_t*)hist);
-    }
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    const void* kin = pass == 0 ? (const void*)ids : (const void*)keys[cur];
+    if (pass == 0)
+      hipLaunchKernelGGL(sort_tile_hist_kernel<true>, grid, block, 0, stream, kin, n, shift, bits, R, hist, err);
+    else
+      hipLaunchKernelGGL(sort_tile_hist_kernel<false>, grid, block, 0, stream, kin, n, shift, bits, R, hist, err);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(sort_chunk_sum_kernel, dim3((unsigned)nchunks), block, 0, stream,
+                       (const uint32_t*)hist, tiles, chunk);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(sort_chunk_scan_kernel, dim3(1), block, 0, stream, chunk, nchunks, base);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(sort_chunk_apply_kernel, dim3((unsigned)nchunks), block, 0, stream, hist, tiles,
+                       (const uint32_t*)chunk, (const uint32_t*)base);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (pass == 0)
+      hipLaunchKernelGGL(sort_scatter_kernel<true>, grid, block, 0, stream, kin, (const uint32_t*)nullptr,
+                         keys[out], vals[out], n, shift, bits, R, (const uint32_t*)hist);
+    else
+      hipLaunchKernelGGL(sort_scatter_kernel<false>, grid, block, 0, stream, kin, (const uint32_t*)vals[cur],
+                         keys[out], vals[out], n, shift, bits, R, (const uint32_t*)hist);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
     cur = out;
   }
   *keys_out = keys[cur];

@@ -31,6 +31,7 @@ constexpr int kRounds = kWaveSpan / kWave;                   // 4
 constexpr int64_t kSegTile = (int64_t)kSegWaves * kWaveSpan; // 1024 positions per tile
 constexpr int kTileWords = (int)(kSegTile / 32);             // bit-mask words per tile
 constexpr int kBatch = 8;                                    // row gathers in flight per group
+static_assert(32 % kBatch == 0 && kBatch < 32, "a batch must not straddle a mask word");
 constexpr int kMaxBuckets = 1024;                            // contribution lookup buckets
 
 enum : uint32_t { kValid = 1, kOpen = 2, kPass = 4 };            // group flags
@@ -157,7 +158,9 @@ __global__ void check_offsets_kernel(const int64_t* __restrict__ off, int K, int
 
 // bucket[b] = contribution of occurrence b << q
 __global__ void contrib_buckets_kernel(const int64_t* __restrict__ off, int K, int64_t N, int q,
-                                       int nb, int32_t* __restrict__ bucket) {
+                                       int nb, int32_t* __restrict__ bucket,
+                                       uint32_t* __restrict__ tile_ctr) {
+  if (threadIdx.x == 0) *tile_ctr = 0u;   // the reduction's tile counter starts at zero
   for (int b = threadIdx.x; b < nb; b += blockDim.x) {
     const int64_t j = (int64_t)b << q;
     int lo = 1, len = K;
@@ -204,7 +207,7 @@ template <int LPR>
 __global__ void __launch_bounds__(kSegBlock)
 seg_reduce_kernel(SegmentArgs a, const uint32_t* __restrict__ tile_seg_base,
                   const int32_t* __restrict__ buckets, int q, int nbuckets, int64_t num_tiles,
-                  SegPartials part) {
+                  uint32_t* __restrict__ tile_ctr, SegPartials part) {
   constexpr int GW = kWave / LPR;            // groups per wave
   constexpr int G = kSegWaves * GW;          // groups per block
   constexpr int PG = kWaveSpan / GW;         // positions per group
@@ -219,6 +222,7 @@ seg_reduce_kernel(SegmentArgs a, const uint32_t* __restrict__ tile_seg_base,
   __shared__ uint32_t s_seg[G], s_flags[G];
   __shared__ uint32_t s_tmp[kSegBlock / kWave + 1];
   __shared__ uint32_t s_bflags;
+  __shared__ uint32_t s_next;
 
   const int K = a.K;
   const int64_t N = a.N;
@@ -248,7 +252,11 @@ seg_reduce_kernel(SegmentArgs a, const uint32_t* __restrict__ tile_seg_base,
   const bool lane_on = gl * 4 < a.D;
   const int D = a.D;
 
-  for (int64_t tile = blockIdx.x; tile < num_tiles; tile += gridDim.x) {
+  // Tiles are taken from a counter, so blocks that become resident late (the
+  // GPU may be shared with another stream's kernels) simply take fewer.
+  if (threadIdx.x == 0) s_next = atomicAdd(tile_ctr, 1u);
+  __syncthreads();
+  for (int64_t tile = s_next; tile < num_tiles; tile = s_next) {
     const int64_t tile0 = tile * kSegTile;
     if (threadIdx.x == 0) {
       s_bflags = 0;
@@ -370,8 +378,9 @@ seg_reduce_kernel(SegmentArgs a, const uint32_t* __restrict__ tile_seg_base,
           rv[u] = *reinterpret_cast<const f32x4*>(a.rows + (int64_t)jv * D + gl * 4);
       }
       const int b0 = gpos0 + i0;
-      const uint32_t hb = (s_hb[b0 >> 5] >> (b0 & 31)) & 0xFFu;
-      const uint32_t nb = (s_nb[b0 >> 5] >> (b0 & 31)) & 0xFFu;
+      constexpr uint32_t kBatchMask = (1u << kBatch) - 1u;   // kBatch divides 32
+      const uint32_t hb = (s_hb[b0 >> 5] >> (b0 & 31)) & kBatchMask;
+      const uint32_t nb = (s_nb[b0 >> 5] >> (b0 & 31)) & kBatchMask;
 #pragma unroll
       for (int u = 0; u < kBatch; ++u) {
         const int i = i0 + u;
@@ -472,7 +481,10 @@ seg_reduce_kernel(SegmentArgs a, const uint32_t* __restrict__ tile_seg_base,
       }
     }
     __syncthreads();
-    if (threadIdx.x == 0) part.flags[tile] = s_bflags;
+    if (threadIdx.x == 0) {
+      part.flags[tile] = s_bflags;
+      s_next = atomicAdd(tile_ctr, 1u);
+    }
     __syncthreads();
   }
 }
@@ -534,7 +546,8 @@ tag_update_kernel(const int64_t* __restrict__ unique_ids, const int32_t* __restr
 
 template <int LPR>
 static hipError_t launch_reduce(const SegmentArgs& a, const uint32_t* tile_base, const int32_t* buckets,
-                                int q, int nb, SegPartials part, int64_t tiles, hipStream_t stream) {
+                                int q, int nb, uint32_t* tile_ctr, SegPartials part, int64_t tiles,
+                                hipStream_t stream) {
   const size_t lds = (size_t)(3 * a.K + 1 + nb) * sizeof(int32_t);
   int dev = 0, cus = 0, per_cu = 0;
   hipError_t e = hipGetDevice(&dev);
@@ -545,7 +558,7 @@ static hipError_t launch_reduce(const SegmentArgs& a, const uint32_t* tile_base,
   int64_t grid = (int64_t)(per_cu > 0 ? per_cu : 1) * (cus > 0 ? cus : 1);
   if (grid > tiles) grid = tiles;
   hipLaunchKernelGGL(seg_reduce_kernel<LPR>, dim3((unsigned)grid), dim3(kSegBlock), lds, stream, a,
-                     tile_base, buckets, q, nb, tiles, part);
+                     tile_base, buckets, q, nb, tiles, tile_ctr, part);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   hipLaunchKernelGGL(seg_fixup_kernel<LPR>, dim3((unsigned)tiles), dim3(kSegBlock), 0, stream, a, part);
   return hipGetLastError();
@@ -558,6 +571,7 @@ hipError_t launch_segments(const SegmentArgs& a, void* ws, hipStream_t stream) {
   uint32_t* total = reinterpret_cast<uint32_t*>(base + L.off_total);
   void* scan_ws = base + L.off_scan;
   int32_t* buckets = reinterpret_cast<int32_t*>(base + L.off_buckets);
+  uint32_t* tile_ctr = total + 1;
   SegPartials part;
   part.flags = reinterpret_cast<uint32_t*>(base + L.off_flags);
   part.last_seg = reinterpret_cast<uint32_t*>(base + L.off_last_seg);
@@ -586,16 +600,16 @@ hipError_t launch_segments(const SegmentArgs& a, void* ws, hipStream_t stream) {
     const int q = bucket_shift(a.N);
     const int nb = (int)(((a.N - 1) >> q) + 1);
     hipLaunchKernelGGL(contrib_buckets_kernel, dim3(1), dim3(256), 0, stream, a.offsets, a.K, a.N, q,
-                       nb, buckets);
+                       nb, buckets, tile_ctr);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     switch (lanes_per_row(a.D)) {
-      case 1: e = launch_reduce<1>(a, heads, buckets, q, nb, part, L.tiles, stream); break;
-      case 2: e = launch_reduce<2>(a, heads, buckets, q, nb, part, L.tiles, stream); break;
-      case 4: e = launch_reduce<4>(a, heads, buckets, q, nb, part, L.tiles, stream); break;
-      case 8: e = launch_reduce<8>(a, heads, buckets, q, nb, part, L.tiles, stream); break;
-      case 16: e = launch_reduce<16>(a, heads, buckets, q, nb, part, L.tiles, stream); break;
-      case 32: e = launch_reduce<32>(a, heads, buckets, q, nb, part, L.tiles, stream); break;
-      case 64: e = launch_reduce<64>(a, heads, buckets, q, nb, part, L.tiles, stream); break;
+      case 1: e = launch_reduce<1>(a, heads, buckets, q, nb, tile_ctr, part, L.tiles, stream); break;
+      case 2: e = launch_reduce<2>(a, heads, buckets, q, nb, tile_ctr, part, L.tiles, stream); break;
+      case 4: e = launch_reduce<4>(a, heads, buckets, q, nb, tile_ctr, part, L.tiles, stream); break;
+      case 8: e = launch_reduce<8>(a, heads, buckets, q, nb, tile_ctr, part, L.tiles, stream); break;
+      case 16: e = launch_reduce<16>(a, heads, buckets, q, nb, tile_ctr, part, L.tiles, stream); break;
+      case 32: e = launch_reduce<32>(a, heads, buckets, q, nb, tile_ctr, part, L.tiles, stream); break;
+      case 64: e = launch_reduce<64>(a, heads, buckets, q, nb, tile_ctr, part, L.tiles, stream); break;
       default: return hipErrorInvalidValue;
     }
     if (e != hipSuccess) return e;
