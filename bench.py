@@ -41,9 +41,12 @@ def parse():
     ap.add_argument("--also", default="c3", help="comma list of extra workloads ('' for none)")
     ap.add_argument("--decay", default="token", choices=["token", "id_tag"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="also run a plain 1 GiB device copy (torch), the known-size reference for "
+                         "calibrating HBM byte counters")
     ap.add_argument("--overlap", action="store_true",
                     help="run the dense path on a second stream, concurrently with the sparse path")
-    ap.add_argument("--cpu-sample", type=int, default=16, help="1/S of the workload for the oracle timing")
+    ap.add_argument("--cpu-sample", type=int, default=4, help="1/S of the workload for the oracle timing")
     return ap.parse_args()
 
 
@@ -255,6 +258,13 @@ def main():
     from synth import device as sdev
 
     torch.cuda.set_device(0)
+    if args.copy_probe:
+        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(2):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     head = run_workload(args.workload, args, torch, gba_step_mod, sdev, gba)
     others = [run_workload(n, args, torch, gba_step_mod, sdev, gba) for n in args.also.split(",") if n and n != args.workload]
     from synth.configs import BY_NAME
