@@ -107,7 +107,8 @@ gba_status gba_aggregate_sparse_workspace_size(int64_t N, int32_t K, int32_t D, 
 /*
  * Embedding gradients by ID -- Alg. 2 (push responder): dedup by ID, per-ID
  * decay, weighted sum divided by the number of contributions that hold the ID.
- * ids              [N] int64 embedding IDs in [0, R), contribution-major.
+ * ids              [N] int64 embedding IDs in [0, R), contribution-major; ids, rows
+ *                  and agg must be 16-byte aligned.
  * rows             [N][D] float, row j is the gradient of occurrence j.
  * contrib_offsets  [K+1] int64, occurrences of contribution m are
  *                  [offsets[m], offsets[m+1]); offsets[0] = 0, offsets[K] = N.
@@ -125,7 +126,7 @@ gba_status gba_aggregate_sparse_workspace_size(int64_t N, int32_t K, int32_t D, 
  *                  accumulation) divided by c_r (or by K); 0 when W_r = 0.
  *   num_unique     one int64, U.
  * workspace        device scratch of at least the queried size.
- * Limits: 1 <= K <= GBA_MAX_K, 0 <= N < 2^30, 1 <= R <= 2^32,
+ * Limits: 1 <= K <= GBA_MAX_K, 0 <= N < 2^28, 1 <= R <= 2^32,
  * D % 4 == 0 and 4 <= D <= GBA_MAX_D.
  */
 gba_status gba_aggregate_sparse(const int64_t* ids, const float* rows,

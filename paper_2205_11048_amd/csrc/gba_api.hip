@@ -9,7 +9,7 @@ using namespace gba;
 
 namespace {
 
-constexpr int64_t kMaxN = (int64_t(1) << 30) - 1;
+constexpr int64_t kMaxN = (int64_t(1) << 28) - 1;
 
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 inline size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
@@ -86,7 +86,8 @@ gba_status gba_aggregate_sparse(const int64_t* ids, const float* rows, const int
     if (!tag) return GBA_ERR_NULL;
     if (step < INT32_MIN || step > INT32_MAX) return GBA_ERR_INVALID_ARG;
   }
-  if ((rows && !aligned16(rows)) || (agg && !aligned16(agg)) || !aligned16(workspace))
+  if ((ids && !aligned16(ids)) || (rows && !aligned16(rows)) || (agg && !aligned16(agg)) ||
+      !aligned16(workspace))
     return GBA_ERR_INVALID_ARG;
   SortPlan plan;
   const size_t need = sparse_bytes(N, D, R, &plan);

@@ -72,47 +72,80 @@ __device__ __forceinline__ uint32_t load_key(const void* src, int64_t i, int64_t
   return static_cast<const uint32_t*>(src)[i];
 }
 
-// Digit counts of one tile, one 1 KB row per tile.  Each wave adds one count
-// per run of equal digits among its 64 lanes, so the long runs of a hot ID
-// (contiguous after the first pass) cost one LDS add, not 64 colliding ones.
+// Digit counts of one tile, one 1 KB row per tile.  One wave takes a whole
+// tile (64 keys per lane, loaded as 16-byte vectors, so many bytes are in
+// flight per wave) and adds one count per run of equal digits among its 64
+// lanes: the long runs of a hot ID cost one LDS add, not 64 colliding ones.
+constexpr int kHistKeys = kSortTile / kWave;   // 64 keys per lane
 template <bool FIRST>
 __global__ void __launch_bounds__(kSortBlock)
-sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n, int shift, int bits, int64_t R,
-                      uint32_t* __restrict__ hist, int32_t* __restrict__ err) {
+sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n, int64_t tiles, int shift, int bits,
+                      int64_t R, uint32_t* __restrict__ hist, int32_t* __restrict__ err) {
   __shared__ uint32_t h[kSortWaves][kRadix];
-  for (int i = threadIdx.x; i < kSortWaves * kRadix; i += kSortBlock) (&h[0][0])[i] = 0u;
-  __syncthreads();
   const int w = threadIdx.x / kWave;
   const int lane = lane_id();
-  const int64_t base = (int64_t)blockIdx.x * kSortTile + (int64_t)w * kSortWaveTile + lane;
+  for (int i = lane; i < kRadix; i += kWave) h[w][i] = 0u;
+  __builtin_amdgcn_wave_barrier();
+  const int64_t tile = (int64_t)blockIdx.x * kSortWaves + w;
+  if (tile >= tiles) return;   // whole waves leave; no block-wide barrier follows
   const uint32_t mask = (1u << bits) - 1u;
+  // lane l holds keys tile0 + 4 * (l + 64 * c) + e, c < 16, e < 4: each
+  // vector load of the wave covers 1 KB of consecutive keys
+  const int64_t tile0 = tile * kSortTile;
   bool bad = false;
-  uint32_t digit[kSortItems];
+  uint32_t digit[kHistKeys];
 #pragma unroll
-  for (int r = 0; r < kSortItems; ++r) {
-    const int64_t i = base + (int64_t)r * kWave;
-    digit[r] = i < n ? (load_key<FIRST>(keys_in, i, R, &bad) >> shift) & mask : 0u;
-  }
+  for (int c = 0; c < kHistKeys / 4; ++c) {
+    const int64_t i0 = tile0 + 4 * ((int64_t)lane + (int64_t)kWave * c);
+    if (i0 + 3 < n) {
+      uint32_t k4[4];
+      if (FIRST) {
+        const int64_t* ids = static_cast<const int64_t*>(keys_in);
+        typedef int64_t i64x2 __attribute__((ext_vector_type(2)));
+        const i64x2 a = *reinterpret_cast<const i64x2*>(ids + i0);
+        const i64x2 b = *reinterpret_cast<const i64x2*>(ids + i0 + 2);
+        const int64_t v[4] = {a.x, a.y, b.x, b.y};
 #pragma unroll
-  for (int r = 0; r < kSortItems; ++r) {
-    const bool active = base + (int64_t)r * kWave < n;   // active lanes are a prefix of the wave
-    const uint32_t prev = __shfl_up(digit[r], 1, kWave);
-    const bool head = active && (lane == 0 || digit[r] != prev);
-    const uint64_t heads = __ballot(head);
-    const int na = __popcll(__ballot(active));
-    if (head) {
-      const uint64_t above = lane == 63 ? 0ull : heads & (~0ull << (lane + 1));
-      const int next = above ? __builtin_ctzll(above) : na;
-      atomicAdd(&h[w][digit[r]], (uint32_t)(next - lane));
+        for (int e = 0; e < 4; ++e) {
+          const bool out = v[e] < 0 || v[e] >= R;
+          bad |= out;
+          k4[e] = out ? 0u : (uint32_t)v[e];
+        }
+      } else {
+        const u32x4 v = *reinterpret_cast<const u32x4*>(static_cast<const uint32_t*>(keys_in) + i0);
+        k4[0] = v.x; k4[1] = v.y; k4[2] = v.z; k4[3] = v.w;
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) digit[4 * c + e] = (k4[e] >> shift) & mask;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        digit[4 * c + e] = (i0 + e < n) ? (load_key<FIRST>(keys_in, i0 + e, R, &bad) >> shift) & mask : 0u;
     }
   }
-  if (FIRST && bad) raise_error(err, GBA_DERR_ID_RANGE);
-  __syncthreads();
-  const int d = threadIdx.x;   // kSortBlock == kRadix
-  uint32_t s = 0;
+  // one LDS add per run of equal digits among each lane's 4 consecutive keys
 #pragma unroll
-  for (int k = 0; k < kSortWaves; ++k) s += h[k][d];
-  hist[(int64_t)blockIdx.x * kRadix + d] = s;
+  for (int c = 0; c < kHistKeys / 4; ++c) {
+    const int64_t i0 = tile0 + 4 * ((int64_t)lane + (int64_t)kWave * c);
+    uint32_t cur = digit[4 * c];
+    uint32_t len = i0 < n ? 1u : 0u;
+#pragma unroll
+    for (int e = 1; e < 4; ++e) {
+      if (i0 + e < n) {
+        if (digit[4 * c + e] == cur) {
+          ++len;
+        } else {
+          atomicAdd(&h[w][cur], len);
+          cur = digit[4 * c + e];
+          len = 1;
+        }
+      }
+    }
+    if (len) atomicAdd(&h[w][cur], len);
+  }
+  __builtin_amdgcn_wave_barrier();
+  for (int d = lane; d < kRadix; d += kWave) hist[tile * kRadix + d] = h[w][d];
+  if (FIRST && bad) raise_error(err, GBA_DERR_ID_RANGE);
 }
 
 // Column sums of chunks of kChunk tiles (the rows are read together).
@@ -127,25 +160,49 @@ sort_chunk_sum_kernel(const uint32_t* __restrict__ hist, int64_t tiles, uint32_t
   chunk[(int64_t)blockIdx.x * kRadix + d] = s;
 }
 
-// Per digit: exclusive prefix over chunks; across digits: where each digit starts.
-__global__ void __launch_bounds__(kSortBlock)
+// Per digit: exclusive prefix over chunks; across digits: where each digit
+// starts.  Four threads share a digit, each scanning a quarter of the chunks.
+constexpr int kScanParts = 4;
+__global__ void __launch_bounds__(kSortBlock * kScanParts)
 sort_chunk_scan_kernel(uint32_t* __restrict__ chunk, int64_t nchunks, uint32_t* __restrict__ base) {
   constexpr int kStep = 16;
-  __shared__ uint32_t tmp[kSortBlock / kWave + 1];
-  const int d = threadIdx.x;
-  uint32_t run = 0;
-  for (int64_t c0 = 0; c0 < nchunks; c0 += kStep) {
+  __shared__ uint32_t part_sum[kScanParts][kRadix];
+  __shared__ uint32_t tmp[kSortBlock * kScanParts / kWave + 1];
+  const int d = threadIdx.x % kRadix;
+  const int qp = threadIdx.x / kRadix;
+  const int64_t per = (nchunks + kScanParts - 1) / kScanParts;
+  const int64_t c_lo = qp * per;
+  const int64_t c_hi = (c_lo + per < nchunks) ? c_lo + per : nchunks;
+  uint32_t s = 0;
+  for (int64_t c0 = c_lo; c0 < c_hi; c0 += kStep) {
     uint32_t v[kStep];
 #pragma unroll
-    for (int k = 0; k < kStep; ++k) v[k] = (c0 + k < nchunks) ? chunk[(c0 + k) * kRadix + d] : 0u;
+    for (int k = 0; k < kStep; ++k) v[k] = (c0 + k < c_hi) ? chunk[(c0 + k) * kRadix + d] : 0u;
+#pragma unroll
+    for (int k = 0; k < kStep; ++k) s += v[k];
+  }
+  part_sum[qp][d] = s;
+  __syncthreads();
+  uint32_t run = 0, total_d = 0;
+  for (int k = 0; k < kScanParts; ++k) {
+    if (k < qp) run += part_sum[k][d];
+    total_d += part_sum[k][d];
+  }
+  for (int64_t c0 = c_lo; c0 < c_hi; c0 += kStep) {
+    uint32_t v[kStep];
+#pragma unroll
+    for (int k = 0; k < kStep; ++k) v[k] = (c0 + k < c_hi) ? chunk[(c0 + k) * kRadix + d] : 0u;
 #pragma unroll
     for (int k = 0; k < kStep; ++k) {
-      if (c0 + k < nchunks) chunk[(c0 + k) * kRadix + d] = run;
+      if (c0 + k < c_hi) chunk[(c0 + k) * kRadix + d] = run;
       run += v[k];
     }
   }
+  // every thread takes part in the block scan; threads of the first quarter
+  // come first in thread order and carry the digit totals
   uint32_t total;
-  base[d] = block_exclusive_scan<kSortBlock>(run, tmp, &total);
+  const uint32_t ex = block_exclusive_scan<kSortBlock * kScanParts>(qp == 0 ? total_d : 0u, tmp, &total);
+  if (qp == 0) base[d] = ex;
 }
 
 // hist[tile][d] becomes the global position of the tile's first key with digit d.
@@ -284,20 +341,27 @@ hipError_t launch_sort_ids(const int64_t* ids, int64_t n, int64_t R, const SortP
   const dim3 grid((unsigned)tiles), block(kSortBlock);
   hipError_t e;
   int cur = 0;
+  // the narrowest digit goes first: the first pass sees keys in arrival order,
+  // and fewer bins there mean longer runs of equal digits to write
+  const int first_bits = plan.key_bits - 8 * (plan.passes - 1);
   for (int pass = 0; pass < plan.passes; ++pass) {
-    const int shift = 8 * pass;
-    const int bits = (plan.key_bits - shift) < 8 ? (plan.key_bits - shift) : 8;
+    const int shift = pass == 0 ? 0 : first_bits + 8 * (pass - 1);
+    const int bits = pass == 0 ? first_bits : 8;
     const int out = pass == 0 ? 0 : 1 - cur;
     const void* kin = pass == 0 ? (const void*)ids : (const void*)keys[cur];
+    const dim3 hgrid((unsigned)ceil_div(tiles, kSortWaves));
     if (pass == 0)
-      hipLaunchKernelGGL(sort_tile_hist_kernel<true>, grid, block, 0, stream, kin, n, shift, bits, R, hist, err);
+      hipLaunchKernelGGL(sort_tile_hist_kernel<true>, hgrid, block, 0, stream, kin, n, tiles, shift, bits, R,
+                         hist, err);
     else
-      hipLaunchKernelGGL(sort_tile_hist_kernel<false>, grid, block, 0, stream, kin, n, shift, bits, R, hist, err);
+      hipLaunchKernelGGL(sort_tile_hist_kernel<false>, hgrid, block, 0, stream, kin, n, tiles, shift, bits, R,
+                         hist, err);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(sort_chunk_sum_kernel, dim3((unsigned)nchunks), block, 0, stream,
                        (const uint32_t*)hist, tiles, chunk);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(sort_chunk_scan_kernel, dim3(1), block, 0, stream, chunk, nchunks, base);
+    hipLaunchKernelGGL(sort_chunk_scan_kernel, dim3(1), dim3(kSortBlock * kScanParts), 0, stream, chunk,
+                       nchunks, base);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(sort_chunk_apply_kernel, dim3((unsigned)nchunks), block, 0, stream, hist, tiles,
                        (const uint32_t*)chunk, (const uint32_t*)base);

@@ -409,3 +409,15 @@ def test_full_step_small(decay, opt):
         assert_rule_t(host(tslots[k])[act], s, None, f"table slot {k}")
     if decay == "id_tag":
         assert_exact(host(tag), ref["sparse"]["new_tag"], "tag")
+
+
+@pytest.mark.parametrize("D", [8, 32])
+def test_sparse_fractional_token_weights(D):
+    """Weights other than 0 and 1 (other decay strategies than Eq. 1's) scale
+    the rows they weigh; a zero weight still excludes."""
+    K = 5
+    sizes = np.array([700, 300, 0, 900, 450])
+    ids, rows, off, tokens, tag = _case(K, sizes, 800, D, seed=41, kind=counter.KIND_DYADIC)
+    w = np.array([1.0, 0.5, 0.0, 0.25, 0.0], np.float32)
+    res = _run_sparse(ids, rows, off, w, tokens, 1000, 2, 800)
+    _check_sparse(res, ids, rows, off, w, tokens, 1000, 2, expect_exact=True)
