@@ -45,7 +45,7 @@ struct SortPlan {
   int64_t n;
   int key_bits;          // significant key bits (>= 1)
   int passes;
-  int64_t blocks;        // tiles per pass
+  int64_t blocks;        // tiles of the first pass (the most of any pass)
   size_t bytes;          // workspace bytes
 };
 SortPlan plan_sort(int64_t n, int64_t R);

@@ -3,8 +3,8 @@
 // push-step can deduplicate them and reduce their rows (Alg. 2: gradients of
 // the embedding parameters are processed by ID).
 //
-// Each 8-bit digit takes three steps: a histogram per tile of 4096 keys
-// (written tile-major, 1 KB per tile), a column scan that turns the per-tile
+// Each digit takes three steps: a histogram per tile (written tile-major,
+// 1 KB per tile), a column scan that turns the per-tile
 // counts into each tile's global offset per digit value (tile-major again, so
 // a tile reads its 256 offsets as one contiguous line), and a scatter that
 // ranks the tile stably in LDS and writes runs of equal digits together.
@@ -17,9 +17,14 @@ namespace gba {
 
 constexpr int kSortBlock = 256;
 constexpr int kSortWaves = kSortBlock / kWave;
-constexpr int kSortItems = 16;                         // per lane
-constexpr int kSortWaveTile = kWave * kSortItems;      // 1024 keys per wave
-constexpr int64_t kSortTile = kSortBlock * kSortItems; // 4096 keys per tile
+// Keys per lane in the scatter: 16 (4096-key tiles) on the 8-bit passes, whose
+// writes need long runs of equal digits; 8 (2048-key tiles) on the first,
+// narrow-digit pass, where runs are long anyway and more resident blocks hide
+// the latency of the 8-byte ID loads better.
+constexpr int kItemsFirst = 8;
+constexpr int kItemsRest = 16;
+template <int ITEMS>
+constexpr int64_t tile_keys() { return (int64_t)kSortBlock * ITEMS; }
 constexpr int kRadix = 256;
 constexpr int kChunk = 32;                             // tiles per column-scan chunk
 
@@ -30,6 +35,7 @@ struct SortLayout {
   size_t arr, off_keys0, off_keys1, off_vals0, off_vals1, off_hist, off_chunk, off_base, bytes;
 };
 
+// tiles: the largest tile count of any pass (the first pass's)
 static SortLayout sort_layout(int64_t n, int64_t tiles) {
   SortLayout L{};
   L.arr = align_up((size_t)(n > 0 ? n : 1) * sizeof(uint32_t));
@@ -73,11 +79,10 @@ __device__ __forceinline__ uint32_t load_key(const void* src, int64_t i, int64_t
 }
 
 // Digit counts of one tile, one 1 KB row per tile.  One wave takes a whole
-// tile (64 keys per lane, loaded as 16-byte vectors, so many bytes are in
-// flight per wave) and adds one count per run of equal digits among its 64
-// lanes: the long runs of a hot ID cost one LDS add, not 64 colliding ones.
-constexpr int kHistKeys = kSortTile / kWave;   // 64 keys per lane
-template <bool FIRST>
+// tile (4 ITEMS keys per lane, loaded as 16-byte vectors, so many bytes are in
+// flight per wave) and adds one count per run of equal digits among each
+// lane's 4 consecutive keys.
+template <bool FIRST, int ITEMS>
 __global__ void __launch_bounds__(kSortBlock)
 sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n, int64_t tiles, int shift, int bits,
                       int64_t R, uint32_t* __restrict__ hist, int32_t* __restrict__ err) {
@@ -88,10 +93,11 @@ sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n, int64_t tiles
   __builtin_amdgcn_wave_barrier();
   const int64_t tile = (int64_t)blockIdx.x * kSortWaves + w;
   if (tile >= tiles) return;   // whole waves leave; no block-wide barrier follows
+  constexpr int kHistKeys = 4 * ITEMS;   // keys per lane
   const uint32_t mask = (1u << bits) - 1u;
-  // lane l holds keys tile0 + 4 * (l + 64 * c) + e, c < 16, e < 4: each
+  // lane l holds keys tile0 + 4 * (l + 64 * c) + e, c < ITEMS, e < 4: each
   // vector load of the wave covers 1 KB of consecutive keys
-  const int64_t tile0 = tile * kSortTile;
+  const int64_t tile0 = tile * tile_keys<ITEMS>();
   bool bad = false;
   uint32_t digit[kHistKeys];
 #pragma unroll
@@ -222,7 +228,7 @@ sort_chunk_apply_kernel(uint32_t* __restrict__ hist, int64_t tiles, const uint32
   }
 }
 
-template <bool FIRST>
+template <bool FIRST, int ITEMS>
 __global__ void __launch_bounds__(kSortBlock)
 sort_scatter_kernel(const void* __restrict__ keys_in, const uint32_t* __restrict__ vals_in,
                     uint32_t* __restrict__ keys_out, uint32_t* __restrict__ vals_out, int64_t n,
@@ -231,21 +237,22 @@ sort_scatter_kernel(const void* __restrict__ keys_in, const uint32_t* __restrict
   __shared__ uint32_t digit_start[kRadix];
   __shared__ uint32_t global_base[kRadix];
   __shared__ uint32_t tmp[kSortBlock / kWave + 1];
-  __shared__ uint32_t s_keys[kSortTile];
-  __shared__ uint32_t s_vals[kSortTile];
+  constexpr int64_t kTile = tile_keys<ITEMS>();
+  __shared__ uint32_t s_keys[kTile];
+  __shared__ uint32_t s_vals[kTile];
   for (int i = threadIdx.x; i < kSortWaves * kRadix; i += kSortBlock) (&cnt[0][0])[i] = 0;
   global_base[threadIdx.x] = offsets[(int64_t)blockIdx.x * kRadix + threadIdx.x];
   __syncthreads();
   const int w = threadIdx.x / kWave;
-  const int64_t tile0 = (int64_t)blockIdx.x * kSortTile;
-  const int64_t base = tile0 + (int64_t)w * kSortWaveTile + lane_id();
+  const int64_t tile0 = (int64_t)blockIdx.x * kTile;
+  const int64_t base = tile0 + (int64_t)w * (kWave * ITEMS) + lane_id();
   const uint32_t mask = (1u << bits) - 1u;
   const uint64_t lt = lanemask_lt();
 
-  uint32_t key[kSortItems], val[kSortItems], rank[kSortItems];
+  uint32_t key[ITEMS], val[ITEMS], rank[ITEMS];
   bool bad = false;
 #pragma unroll
-  for (int r = 0; r < kSortItems; ++r) {
+  for (int r = 0; r < ITEMS; ++r) {
     const int64_t i = base + (int64_t)r * kWave;
     const bool active = i < n;
     key[r] = active ? load_key<FIRST>(keys_in, i, R, &bad) : 0u;
@@ -254,7 +261,7 @@ sort_scatter_kernel(const void* __restrict__ keys_in, const uint32_t* __restrict
   (void)bad;   // range errors are reported by the histogram launch
   // Stable rank within (wave, digit): rounds in index order, lanes in order.
 #pragma unroll
-  for (int r = 0; r < kSortItems; ++r) {
+  for (int r = 0; r < ITEMS; ++r) {
     const int64_t i = base + (int64_t)r * kWave;
     const bool active = i < n;
     const uint32_t digit = (key[r] >> shift) & mask;
@@ -289,7 +296,7 @@ sort_scatter_kernel(const void* __restrict__ keys_in, const uint32_t* __restrict
   }
   __syncthreads();
 #pragma unroll
-  for (int r = 0; r < kSortItems; ++r) {
+  for (int r = 0; r < ITEMS; ++r) {
     const int64_t i = base + (int64_t)r * kWave;
     if (i < n) {
       const uint32_t digit = (key[r] >> shift) & mask;
@@ -299,7 +306,7 @@ sort_scatter_kernel(const void* __restrict__ keys_in, const uint32_t* __restrict
     }
   }
   __syncthreads();
-  const int64_t tile_n = (n - tile0) < kSortTile ? (n - tile0) : kSortTile;
+  const int64_t tile_n = (n - tile0) < kTile ? (n - tile0) : kTile;
   for (int i = threadIdx.x; i < tile_n; i += kSortBlock) {
     const uint32_t k = s_keys[i];
     const uint32_t digit = (k >> shift) & mask;
@@ -318,7 +325,7 @@ SortPlan plan_sort(int64_t n, int64_t R) {
   while (bits < 32 && ((int64_t)1 << bits) < R) ++bits;
   p.key_bits = bits;
   p.passes = (bits + 7) / 8;
-  p.blocks = n > 0 ? ceil_div(n, kSortTile) : 0;
+  p.blocks = n > 0 ? ceil_div(n, tile_keys<kItemsFirst>()) : 0;
   p.bytes = sort_layout(n, p.blocks).bytes;
   return p;
 }
@@ -336,9 +343,6 @@ hipError_t launch_sort_ids(const int64_t* ids, int64_t n, int64_t R, const SortP
   *keys_out = keys[0];
   *vals_out = vals[0];
   if (n <= 0) return hipSuccess;
-  const int64_t tiles = plan.blocks;
-  const int64_t nchunks = ceil_div(tiles, kChunk);
-  const dim3 grid((unsigned)tiles), block(kSortBlock);
   hipError_t e;
   int cur = 0;
   // the narrowest digit goes first: the first pass sees keys in arrival order,
@@ -349,13 +353,16 @@ hipError_t launch_sort_ids(const int64_t* ids, int64_t n, int64_t R, const SortP
     const int bits = pass == 0 ? first_bits : 8;
     const int out = pass == 0 ? 0 : 1 - cur;
     const void* kin = pass == 0 ? (const void*)ids : (const void*)keys[cur];
+    const int64_t tiles = ceil_div(n, pass == 0 ? tile_keys<kItemsFirst>() : tile_keys<kItemsRest>());
+    const int64_t nchunks = ceil_div(tiles, kChunk);
+    const dim3 grid((unsigned)tiles), block(kSortBlock);
     const dim3 hgrid((unsigned)ceil_div(tiles, kSortWaves));
     if (pass == 0)
-      hipLaunchKernelGGL(sort_tile_hist_kernel<true>, hgrid, block, 0, stream, kin, n, tiles, shift, bits, R,
-                         hist, err);
+      hipLaunchKernelGGL((sort_tile_hist_kernel<true, kItemsFirst>), hgrid, block, 0, stream, kin, n, tiles,
+                         shift, bits, R, hist, err);
     else
-      hipLaunchKernelGGL(sort_tile_hist_kernel<false>, hgrid, block, 0, stream, kin, n, tiles, shift, bits, R,
-                         hist, err);
+      hipLaunchKernelGGL((sort_tile_hist_kernel<false, kItemsRest>), hgrid, block, 0, stream, kin, n, tiles,
+                         shift, bits, R, hist, err);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(sort_chunk_sum_kernel, dim3((unsigned)nchunks), block, 0, stream,
                        (const uint32_t*)hist, tiles, chunk);
@@ -367,11 +374,12 @@ hipError_t launch_sort_ids(const int64_t* ids, int64_t n, int64_t R, const SortP
                        (const uint32_t*)chunk, (const uint32_t*)base);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (pass == 0)
-      hipLaunchKernelGGL(sort_scatter_kernel<true>, grid, block, 0, stream, kin, (const uint32_t*)nullptr,
-                         keys[out], vals[out], n, shift, bits, R, (const uint32_t*)hist);
+      hipLaunchKernelGGL((sort_scatter_kernel<true, kItemsFirst>), grid, block, 0, stream, kin,
+                         (const uint32_t*)nullptr, keys[out], vals[out], n, shift, bits, R, (const uint32_t*)hist);
     else
-      hipLaunchKernelGGL(sort_scatter_kernel<false>, grid, block, 0, stream, kin, (const uint32_t*)vals[cur],
-                         keys[out], vals[out], n, shift, bits, R, (const uint32_t*)hist);
+      hipLaunchKernelGGL((sort_scatter_kernel<false, kItemsRest>), grid, block, 0, stream, kin,
+                         (const uint32_t*)vals[cur], keys[out], vals[out], n, shift, bits, R,
+                         (const uint32_t*)hist);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     cur = out;
   }

@@ -210,22 +210,41 @@ __global__ void contrib_buckets_kernel(const int64_t* __restrict__ off, int K, i
   }
 }
 
-// Run heads per 1024-position tile, kHeadTilesPerBlock tiles per block.
-constexpr int kHeadTilesPerBlock = 8;
+// Run heads per 1024-position tile, one wave per tile.  Lane l holds
+// positions t0 + 4 (l + 64 c) + e (c, e < 4): each 16-byte load of the wave
+// covers 1 KB of consecutive keys, and the key before a lane's first one is
+// the last key of the lane before it.
 __global__ void __launch_bounds__(kSegBlock)
 seg_heads_kernel(const uint32_t* __restrict__ keys, int64_t N, int64_t tiles, uint32_t* __restrict__ heads) {
-  __shared__ uint32_t tmp[kSegBlock / kWave + 1];
-  for (int k = 0; k < kHeadTilesPerBlock; ++k) {
-    const int64_t tile = (int64_t)blockIdx.x * kHeadTilesPerBlock + k;
-    if (tile >= tiles) break;
-    const int64_t t0 = tile * kMetaTile;
-    const int64_t t1 = (t0 + kMetaTile < N) ? t0 + kMetaTile : N;
-    uint32_t c = 0;
-    for (int64_t p = t0 + threadIdx.x; p < t1; p += kSegBlock) c += (p == 0 || keys[p] != keys[p - 1]);
-    uint32_t total;
-    block_exclusive_scan<kSegBlock>(c, tmp, &total);
-    if (threadIdx.x == 0) heads[tile] = total;
+  const int lane = lane_id();
+  const int64_t tile = (int64_t)blockIdx.x * kSegWaves + threadIdx.x / kWave;
+  if (tile >= tiles) return;   // whole waves leave; no block-wide barrier follows
+  const int64_t t0 = tile * kMetaTile;
+  uint32_t carry = t0 > 0 ? keys[t0 - 1] : 0u;   // position 0 is always a head
+  uint32_t cnt = 0;
+#pragma unroll
+  for (int c = 0; c < kRounds; ++c) {
+    const int64_t i0 = t0 + 4 * ((int64_t)lane + (int64_t)kWave * c);
+    uint32_t k[4] = {0u, 0u, 0u, 0u};
+    if (i0 + 3 < N) {
+      const u32x4 v = *reinterpret_cast<const u32x4*>(keys + i0);
+      k[0] = v.x; k[1] = v.y; k[2] = v.z; k[3] = v.w;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) k[e] = (i0 + e < N) ? keys[i0 + e] : 0u;
+    }
+    uint32_t prev = __shfl_up(k[3], 1, kWave);
+    if (lane == 0) prev = carry;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int64_t p = i0 + e;
+      if (p < N) cnt += (p == 0 || k[e] != prev) ? 1u : 0u;
+      prev = k[e];
+    }
+    carry = __shfl(k[3], kWave - 1, kWave);
   }
+  const uint32_t total = wave_sum(cnt);
+  if (lane == 0) heads[tile] = total;
 }
 
 __global__ void seg_finish_kernel(const uint32_t* __restrict__ total, int64_t N,
@@ -590,7 +609,7 @@ hipError_t launch_segments(const SegmentArgs& a, void* ws, hipStream_t stream) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (a.N > 0) {
-    hipLaunchKernelGGL(seg_heads_kernel, dim3((unsigned)ceil_div(L.meta_tiles, kHeadTilesPerBlock)),
+    hipLaunchKernelGGL(seg_heads_kernel, dim3((unsigned)ceil_div(L.meta_tiles, kSegWaves)),
                        dim3(kSegBlock), 0, stream, a.keys, a.N, L.meta_tiles, heads);
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
