@@ -3,11 +3,12 @@
 // push-step can deduplicate them and reduce their rows (Alg. 2: gradients of
 // the embedding parameters are processed by ID).
 //
-// Each digit takes three steps: a histogram per tile (written tile-major,
-// 1 KB per tile), a column scan that turns the per-tile
-// counts into each tile's global offset per digit value (tile-major again, so
-// a tile reads its 256 offsets as one contiguous line), and a scatter that
-// ranks the tile stably in LDS and writes runs of equal digits together.
+// Each digit takes three launches: digit counts per tile (1 KB per tile,
+// tile-major) and per chunk of four tiles; an exclusive scan of every digit's
+// chunk counts, one block per digit; and a scatter in which each tile adds up
+// its own offsets (digit start + chunk prefix + the tiles before it in its
+// chunk), ranks its keys stably in LDS and writes runs of equal digits
+// together.
 // Ranks inside a wave come from ballots that match lanes holding the same
 // digit, so skewed (Zipf) keys cost no LDS atomics on hot bins in the scatter.
 #include "gba_device.hpp"
@@ -26,13 +27,13 @@ constexpr int kItemsRest = 16;
 template <int ITEMS>
 constexpr int64_t tile_keys() { return (int64_t)kSortBlock * ITEMS; }
 constexpr int kRadix = 256;
-constexpr int kChunk = 32;                             // tiles per column-scan chunk
+constexpr int kChunk = kSortWaves;                     // tiles per chunk: one hist block
 
-static inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+__host__ __device__ static inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 static inline size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
 
 struct SortLayout {
-  size_t arr, off_keys0, off_keys1, off_vals0, off_vals1, off_hist, off_chunk, off_base, bytes;
+  size_t arr, off_keys0, off_keys1, off_vals0, off_vals1, off_hist, off_chunk, off_total, bytes;
 };
 
 // tiles: the largest tile count of any pass (the first pass's)
@@ -46,8 +47,8 @@ static SortLayout sort_layout(int64_t n, int64_t tiles) {
   L.off_vals0 = o; o += L.arr;
   L.off_vals1 = o; o += L.arr;
   L.off_hist = o;  o += align_up(nt * kRadix * 4);                       // [tile][digit]
-  L.off_chunk = o; o += align_up((size_t)ceil_div((int64_t)nt, kChunk) * kRadix * 4);
-  L.off_base = o;  o += align_up(kRadix * 4);
+  L.off_chunk = o; o += align_up((size_t)ceil_div((int64_t)nt, kChunk) * kRadix * 4);   // [chunk][digit]
+  L.off_total = o; o += align_up(kRadix * 4);
   L.bytes = o;
   return L;
 }
@@ -85,154 +86,128 @@ __device__ __forceinline__ uint32_t load_key(const void* src, int64_t i, int64_t
 template <bool FIRST, int ITEMS>
 __global__ void __launch_bounds__(kSortBlock)
 sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n, int64_t tiles, int shift, int bits,
-                      int64_t R, uint32_t* __restrict__ hist, int32_t* __restrict__ err) {
+                      int64_t R, uint32_t* __restrict__ hist, uint32_t* __restrict__ chunk,
+                      int32_t* __restrict__ err) {
   __shared__ uint32_t h[kSortWaves][kRadix];
   const int w = threadIdx.x / kWave;
   const int lane = lane_id();
   for (int i = lane; i < kRadix; i += kWave) h[w][i] = 0u;
   __builtin_amdgcn_wave_barrier();
   const int64_t tile = (int64_t)blockIdx.x * kSortWaves + w;
-  if (tile >= tiles) return;   // whole waves leave; no block-wide barrier follows
-  constexpr int kHistKeys = 4 * ITEMS;   // keys per lane
-  const uint32_t mask = (1u << bits) - 1u;
-  // lane l holds keys tile0 + 4 * (l + 64 * c) + e, c < ITEMS, e < 4: each
-  // vector load of the wave covers 1 KB of consecutive keys
-  const int64_t tile0 = tile * tile_keys<ITEMS>();
   bool bad = false;
-  uint32_t digit[kHistKeys];
+  if (tile < tiles) {
+    constexpr int kHistKeys = 4 * ITEMS;   // keys per lane
+    const uint32_t mask = (1u << bits) - 1u;
+    // lane l holds keys tile0 + 4 * (l + 64 * c) + e, c < ITEMS, e < 4: each
+    // vector load of the wave covers 1 KB of consecutive keys
+    const int64_t tile0 = tile * tile_keys<ITEMS>();
+    uint32_t digit[kHistKeys];
 #pragma unroll
-  for (int c = 0; c < kHistKeys / 4; ++c) {
-    const int64_t i0 = tile0 + 4 * ((int64_t)lane + (int64_t)kWave * c);
-    if (i0 + 3 < n) {
-      uint32_t k4[4];
-      if (FIRST) {
-        const int64_t* ids = static_cast<const int64_t*>(keys_in);
-        typedef int64_t i64x2 __attribute__((ext_vector_type(2)));
-        const i64x2 a = *reinterpret_cast<const i64x2*>(ids + i0);
-        const i64x2 b = *reinterpret_cast<const i64x2*>(ids + i0 + 2);
-        const int64_t v[4] = {a.x, a.y, b.x, b.y};
+    for (int c = 0; c < kHistKeys / 4; ++c) {
+      const int64_t i0 = tile0 + 4 * ((int64_t)lane + (int64_t)kWave * c);
+      if (i0 + 3 < n) {
+        uint32_t k4[4];
+        if (FIRST) {
+          const int64_t* ids = static_cast<const int64_t*>(keys_in);
+          typedef int64_t i64x2 __attribute__((ext_vector_type(2)));
+          const i64x2 a = *reinterpret_cast<const i64x2*>(ids + i0);
+          const i64x2 b = *reinterpret_cast<const i64x2*>(ids + i0 + 2);
+          const int64_t v[4] = {a.x, a.y, b.x, b.y};
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const bool out = v[e] < 0 || v[e] >= R;
-          bad |= out;
-          k4[e] = out ? 0u : (uint32_t)v[e];
-        }
-      } else {
-        const u32x4 v = *reinterpret_cast<const u32x4*>(static_cast<const uint32_t*>(keys_in) + i0);
-        k4[0] = v.x; k4[1] = v.y; k4[2] = v.z; k4[3] = v.w;
-      }
-#pragma unroll
-      for (int e = 0; e < 4; ++e) digit[4 * c + e] = (k4[e] >> shift) & mask;
-    } else {
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        digit[4 * c + e] = (i0 + e < n) ? (load_key<FIRST>(keys_in, i0 + e, R, &bad) >> shift) & mask : 0u;
-    }
-  }
-  // one LDS add per run of equal digits among each lane's 4 consecutive keys
-#pragma unroll
-  for (int c = 0; c < kHistKeys / 4; ++c) {
-    const int64_t i0 = tile0 + 4 * ((int64_t)lane + (int64_t)kWave * c);
-    uint32_t cur = digit[4 * c];
-    uint32_t len = i0 < n ? 1u : 0u;
-#pragma unroll
-    for (int e = 1; e < 4; ++e) {
-      if (i0 + e < n) {
-        if (digit[4 * c + e] == cur) {
-          ++len;
+          for (int e = 0; e < 4; ++e) {
+            const bool out = v[e] < 0 || v[e] >= R;
+            bad |= out;
+            k4[e] = out ? 0u : (uint32_t)v[e];
+          }
         } else {
-          atomicAdd(&h[w][cur], len);
-          cur = digit[4 * c + e];
-          len = 1;
+          const u32x4 v = *reinterpret_cast<const u32x4*>(static_cast<const uint32_t*>(keys_in) + i0);
+          k4[0] = v.x; k4[1] = v.y; k4[2] = v.z; k4[3] = v.w;
         }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) digit[4 * c + e] = (k4[e] >> shift) & mask;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          digit[4 * c + e] = (i0 + e < n) ? (load_key<FIRST>(keys_in, i0 + e, R, &bad) >> shift) & mask : 0u;
       }
     }
-    if (len) atomicAdd(&h[w][cur], len);
+    // one LDS add per run of equal digits among each lane's 4 consecutive keys
+#pragma unroll
+    for (int c = 0; c < kHistKeys / 4; ++c) {
+      const int64_t i0 = tile0 + 4 * ((int64_t)lane + (int64_t)kWave * c);
+      uint32_t cur = digit[4 * c];
+      uint32_t len = i0 < n ? 1u : 0u;
+#pragma unroll
+      for (int e = 1; e < 4; ++e) {
+        if (i0 + e < n) {
+          if (digit[4 * c + e] == cur) {
+            ++len;
+          } else {
+            atomicAdd(&h[w][cur], len);
+            cur = digit[4 * c + e];
+            len = 1;
+          }
+        }
+      }
+      if (len) atomicAdd(&h[w][cur], len);
+    }
+    __builtin_amdgcn_wave_barrier();
+    for (int d = lane; d < kRadix; d += kWave) hist[tile * kRadix + d] = h[w][d];
   }
-  __builtin_amdgcn_wave_barrier();
-  for (int d = lane; d < kRadix; d += kWave) hist[tile * kRadix + d] = h[w][d];
+  __syncthreads();
+  // the block's tiles form one chunk
+  {
+    const int d = threadIdx.x;
+    uint32_t s = 0;
+#pragma unroll
+    for (int k = 0; k < kSortWaves; ++k) s += h[k][d];
+    chunk[(int64_t)blockIdx.x * kRadix + d] = s;
+  }
   if (FIRST && bad) raise_error(err, GBA_DERR_ID_RANGE);
 }
 
-// Column sums of chunks of kChunk tiles (the rows are read together).
+// One block per digit value: exclusive prefix of the digit's chunk counts, in
+// place, and the digit's total.  Blocks of one XCD (block b runs on XCD b % 8)
+// take 32 consecutive digits, so each 128-byte line of a chunk row is read by
+// one XCD only.
+constexpr int kXcds = 8;
+constexpr int kDigitScanBatch = 8;
 __global__ void __launch_bounds__(kSortBlock)
-sort_chunk_sum_kernel(const uint32_t* __restrict__ hist, int64_t tiles, uint32_t* __restrict__ chunk) {
-  const int d = threadIdx.x;
-  const int64_t t0 = (int64_t)blockIdx.x * kChunk;
-  uint32_t s = 0;
-#pragma unroll
-  for (int k = 0; k < kChunk; ++k)
-    if (t0 + k < tiles) s += hist[(t0 + k) * kRadix + d];
-  chunk[(int64_t)blockIdx.x * kRadix + d] = s;
-}
-
-// Per digit: exclusive prefix over chunks; across digits: where each digit
-// starts.  Four threads share a digit, each scanning a quarter of the chunks.
-constexpr int kScanParts = 4;
-__global__ void __launch_bounds__(kSortBlock * kScanParts)
-sort_chunk_scan_kernel(uint32_t* __restrict__ chunk, int64_t nchunks, uint32_t* __restrict__ base) {
-  constexpr int kStep = 16;
-  __shared__ uint32_t part_sum[kScanParts][kRadix];
-  __shared__ uint32_t tmp[kSortBlock * kScanParts / kWave + 1];
-  const int d = threadIdx.x % kRadix;
-  const int qp = threadIdx.x / kRadix;
-  const int64_t per = (nchunks + kScanParts - 1) / kScanParts;
-  const int64_t c_lo = qp * per;
+sort_digit_scan_kernel(uint32_t* __restrict__ chunk, int64_t nchunks, uint32_t* __restrict__ total) {
+  __shared__ uint32_t tmp[kSortBlock / kWave + 1];
+  const int d = (int)(blockIdx.x % kXcds) * (kRadix / kXcds) + (int)(blockIdx.x / kXcds);
+  const int64_t per = ceil_div(nchunks, kSortBlock);
+  const int64_t c_lo = (int64_t)threadIdx.x * per;
   const int64_t c_hi = (c_lo + per < nchunks) ? c_lo + per : nchunks;
   uint32_t s = 0;
-  for (int64_t c0 = c_lo; c0 < c_hi; c0 += kStep) {
-    uint32_t v[kStep];
+  for (int64_t c0 = c_lo; c0 < c_hi; c0 += kDigitScanBatch) {
+    uint32_t v[kDigitScanBatch];
 #pragma unroll
-    for (int k = 0; k < kStep; ++k) v[k] = (c0 + k < c_hi) ? chunk[(c0 + k) * kRadix + d] : 0u;
+    for (int k = 0; k < kDigitScanBatch; ++k) v[k] = (c0 + k < c_hi) ? chunk[(c0 + k) * kRadix + d] : 0u;
 #pragma unroll
-    for (int k = 0; k < kStep; ++k) s += v[k];
+    for (int k = 0; k < kDigitScanBatch; ++k) s += v[k];
   }
-  part_sum[qp][d] = s;
-  __syncthreads();
-  uint32_t run = 0, total_d = 0;
-  for (int k = 0; k < kScanParts; ++k) {
-    if (k < qp) run += part_sum[k][d];
-    total_d += part_sum[k][d];
-  }
-  for (int64_t c0 = c_lo; c0 < c_hi; c0 += kStep) {
-    uint32_t v[kStep];
+  uint32_t all;
+  uint32_t run = block_exclusive_scan<kSortBlock>(s, tmp, &all);
+  for (int64_t c0 = c_lo; c0 < c_hi; c0 += kDigitScanBatch) {
+    uint32_t v[kDigitScanBatch];
 #pragma unroll
-    for (int k = 0; k < kStep; ++k) v[k] = (c0 + k < c_hi) ? chunk[(c0 + k) * kRadix + d] : 0u;
+    for (int k = 0; k < kDigitScanBatch; ++k) v[k] = (c0 + k < c_hi) ? chunk[(c0 + k) * kRadix + d] : 0u;
 #pragma unroll
-    for (int k = 0; k < kStep; ++k) {
+    for (int k = 0; k < kDigitScanBatch; ++k) {
       if (c0 + k < c_hi) chunk[(c0 + k) * kRadix + d] = run;
       run += v[k];
     }
   }
-  // every thread takes part in the block scan; threads of the first quarter
-  // come first in thread order and carry the digit totals
-  uint32_t total;
-  const uint32_t ex = block_exclusive_scan<kSortBlock * kScanParts>(qp == 0 ? total_d : 0u, tmp, &total);
-  if (qp == 0) base[d] = ex;
-}
-
-// hist[tile][d] becomes the global position of the tile's first key with digit d.
-__global__ void __launch_bounds__(kSortBlock)
-sort_chunk_apply_kernel(uint32_t* __restrict__ hist, int64_t tiles, const uint32_t* __restrict__ chunk,
-                        const uint32_t* __restrict__ base) {
-  const int d = threadIdx.x;
-  const int64_t t0 = (int64_t)blockIdx.x * kChunk;
-  uint32_t run = base[d] + chunk[(int64_t)blockIdx.x * kRadix + d];
-  uint32_t v[kChunk];
-#pragma unroll
-  for (int k = 0; k < kChunk; ++k) v[k] = (t0 + k < tiles) ? hist[(t0 + k) * kRadix + d] : 0u;
-#pragma unroll
-  for (int k = 0; k < kChunk; ++k) {
-    if (t0 + k < tiles) hist[(t0 + k) * kRadix + d] = run;
-    run += v[k];
-  }
+  if (threadIdx.x == 0) total[d] = all;
 }
 
 template <bool FIRST, int ITEMS>
 __global__ void __launch_bounds__(kSortBlock)
 sort_scatter_kernel(const void* __restrict__ keys_in, const uint32_t* __restrict__ vals_in,
                     uint32_t* __restrict__ keys_out, uint32_t* __restrict__ vals_out, int64_t n,
-                    int shift, int bits, int64_t R, const uint32_t* __restrict__ offsets) {
+                    int shift, int bits, int64_t R, const uint32_t* __restrict__ hist,
+                    const uint32_t* __restrict__ chunk, const uint32_t* __restrict__ total) {
   __shared__ uint32_t cnt[kSortWaves][kRadix];
   __shared__ uint32_t digit_start[kRadix];
   __shared__ uint32_t global_base[kRadix];
@@ -241,8 +216,18 @@ sort_scatter_kernel(const void* __restrict__ keys_in, const uint32_t* __restrict
   __shared__ uint32_t s_keys[kTile];
   __shared__ uint32_t s_vals[kTile];
   for (int i = threadIdx.x; i < kSortWaves * kRadix; i += kSortBlock) (&cnt[0][0])[i] = 0;
-  global_base[threadIdx.x] = offsets[(int64_t)blockIdx.x * kRadix + threadIdx.x];
-  __syncthreads();
+  {
+    // global position of the tile's first key of each digit value: where the
+    // digit starts, plus its count in earlier chunks, plus in earlier tiles of
+    // this tile's chunk
+    const int d = threadIdx.x;
+    const int64_t c = (int64_t)blockIdx.x / kChunk;
+    uint32_t off = chunk[c * kRadix + d];
+    for (int64_t t = c * kChunk; t < (int64_t)blockIdx.x; ++t) off += hist[t * kRadix + d];
+    uint32_t all;
+    const uint32_t start = block_exclusive_scan<kSortBlock>(total[d], tmp, &all);   // also publishes cnt = 0
+    global_base[d] = start + off;
+  }
   const int w = threadIdx.x / kWave;
   const int64_t tile0 = (int64_t)blockIdx.x * kTile;
   const int64_t base = tile0 + (int64_t)w * (kWave * ITEMS) + lane_id();
@@ -339,7 +324,7 @@ hipError_t launch_sort_ids(const int64_t* ids, int64_t n, int64_t R, const SortP
   uint32_t* vals[2] = {reinterpret_cast<uint32_t*>(p + L.off_vals0), reinterpret_cast<uint32_t*>(p + L.off_vals1)};
   uint32_t* hist = reinterpret_cast<uint32_t*>(p + L.off_hist);
   uint32_t* chunk = reinterpret_cast<uint32_t*>(p + L.off_chunk);
-  uint32_t* base = reinterpret_cast<uint32_t*>(p + L.off_base);
+  uint32_t* total = reinterpret_cast<uint32_t*>(p + L.off_total);
   *keys_out = keys[0];
   *vals_out = vals[0];
   if (n <= 0) return hipSuccess;
@@ -356,30 +341,23 @@ hipError_t launch_sort_ids(const int64_t* ids, int64_t n, int64_t R, const SortP
     const int64_t tiles = ceil_div(n, pass == 0 ? tile_keys<kItemsFirst>() : tile_keys<kItemsRest>());
     const int64_t nchunks = ceil_div(tiles, kChunk);
     const dim3 grid((unsigned)tiles), block(kSortBlock);
-    const dim3 hgrid((unsigned)ceil_div(tiles, kSortWaves));
     if (pass == 0)
-      hipLaunchKernelGGL((sort_tile_hist_kernel<true, kItemsFirst>), hgrid, block, 0, stream, kin, n, tiles,
-                         shift, bits, R, hist, err);
+      hipLaunchKernelGGL((sort_tile_hist_kernel<true, kItemsFirst>), dim3((unsigned)nchunks), block, 0, stream,
+                         kin, n, tiles, shift, bits, R, hist, chunk, err);
     else
-      hipLaunchKernelGGL((sort_tile_hist_kernel<false, kItemsRest>), hgrid, block, 0, stream, kin, n, tiles,
-                         shift, bits, R, hist, err);
+      hipLaunchKernelGGL((sort_tile_hist_kernel<false, kItemsRest>), dim3((unsigned)nchunks), block, 0, stream,
+                         kin, n, tiles, shift, bits, R, hist, chunk, err);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(sort_chunk_sum_kernel, dim3((unsigned)nchunks), block, 0, stream,
-                       (const uint32_t*)hist, tiles, chunk);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(sort_chunk_scan_kernel, dim3(1), dim3(kSortBlock * kScanParts), 0, stream, chunk,
-                       nchunks, base);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(sort_chunk_apply_kernel, dim3((unsigned)nchunks), block, 0, stream, hist, tiles,
-                       (const uint32_t*)chunk, (const uint32_t*)base);
+    hipLaunchKernelGGL(sort_digit_scan_kernel, dim3(kRadix), block, 0, stream, chunk, nchunks, total);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (pass == 0)
       hipLaunchKernelGGL((sort_scatter_kernel<true, kItemsFirst>), grid, block, 0, stream, kin,
-                         (const uint32_t*)nullptr, keys[out], vals[out], n, shift, bits, R, (const uint32_t*)hist);
+                         (const uint32_t*)nullptr, keys[out], vals[out], n, shift, bits, R, (const uint32_t*)hist,
+                         (const uint32_t*)chunk, (const uint32_t*)total);
     else
       hipLaunchKernelGGL((sort_scatter_kernel<false, kItemsRest>), grid, block, 0, stream, kin,
                          (const uint32_t*)vals[cur], keys[out], vals[out], n, shift, bits, R,
-                         (const uint32_t*)hist);
+                         (const uint32_t*)hist, (const uint32_t*)chunk, (const uint32_t*)total);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     cur = out;
   }
