@@ -289,12 +289,20 @@ def test_host_checks_enqueue_nothing():
 
 
 # ------------------------------------------------------------ optimisers
-@pytest.mark.parametrize("n", [1, 5, 100_003])
-def test_apply_dense_adagrad(n):
+def dev_at(x, offset):
+    """Device copy of x that starts `offset` floats into its allocation."""
+    buf = torch.zeros(x.size + offset, dtype=torch.float32, device=DEV)
+    view = buf[offset:]
+    view.copy_(torch.from_numpy(np.ascontiguousarray(x)))
+    return view
+
+
+@pytest.mark.parametrize("n,offset", [(1, 0), (5, 0), (100_003, 0), (100_003, 1), (64, 3)])
+def test_apply_dense_adagrad(n, offset):
     p = counter.values_range(1, 1, 0, n, counter.KIND_PARAM)
     a = counter.values_range(1, 2, 0, n, counter.KIND_ACCUM)
     g = counter.values_range(1, 3, 0, n, counter.KIND_GRAD, counter.grad_scale(1e-2))
-    pd, ad = dev(p), dev(a)
+    pd, ad = dev_at(p, offset), dev(a)
     gba.gba_apply_adagrad(pd, ad, dev(g), 0.01, 1e-8)
     rp, ra = oracle.adagrad(p, a, g, 0.01, 1e-8)
     mp, ma = oracle.adagrad_magnitude(p, a, g, np.abs(g), 0.01, 1e-8)
@@ -303,13 +311,13 @@ def test_apply_dense_adagrad(n):
     assert exact_fraction(host(pd), rp) > 0.999
 
 
-@pytest.mark.parametrize("n", [1, 7, 100_003])
-def test_apply_dense_adam(n):
+@pytest.mark.parametrize("n,offset", [(1, 0), (7, 0), (100_003, 0), (100_003, 2), (64, 1)])
+def test_apply_dense_adam(n, offset):
     p = counter.values_range(2, 1, 0, n, counter.KIND_PARAM)
     m = counter.values_range(2, 2, 0, n, counter.KIND_ADAM_M)
     v = counter.values_range(2, 3, 0, n, counter.KIND_ADAM_V)
     g = counter.values_range(2, 4, 0, n, counter.KIND_GRAD, counter.grad_scale(1e-2))
-    pd, md, vd = dev(p), dev(m), dev(v)
+    pd, md, vd = dev(p), dev(m), dev_at(v, offset)
     gba.gba_apply_adam(pd, md, vd, dev(g), 1e-3, 0.9, 0.999, 1e-8, 1001)
     rp, rm, rv = oracle.adam(p, m, v, g, 1e-3, 0.9, 0.999, 1e-8, 1001)
     mp, mm, mv = oracle.adam_magnitude(p, m, v, g, np.abs(g), 1e-3, 0.9, 0.999, 1e-8, 1001)
