@@ -46,6 +46,8 @@ def parse():
                          "calibrating HBM byte counters")
     ap.add_argument("--overlap", action="store_true",
                     help="run the dense path on a second stream, concurrently with the sparse path")
+    ap.add_argument("--separate-dense", action="store_true",
+                    help="dense sum and dense optimiser as two calls instead of the fused one")
     ap.add_argument("--cpu-sample", type=int, default=4, help="1/S of the workload for the oracle timing")
     return ap.parse_args()
 
@@ -111,14 +113,26 @@ def run_workload(name, args, torch, gba_step_mod, sdev, gba):
             dstream.wait_event(w_ready)
         if ev is not None:
             ev["d0"].record(dstream)
-        gba.gba_aggregate_dense(st.grad_table(ds.grads), st.w, w.P, st.g_bar, **dkw)
-        if ev is not None:
-            ev["d1"].record(dstream)
-        if w.optimizer == "adagrad":
-            gba.gba_apply_adagrad(ds.param, ds.dense_slots[0], st.g_bar, w.lr, w.eps, **dkw)
+        if args.separate_dense:
+            gba.gba_aggregate_dense(st.grad_table(ds.grads), st.w, w.P, st.g_bar, **dkw)
+            if ev is not None:
+                ev["d1"].record(dstream)
+            if w.optimizer == "adagrad":
+                gba.gba_apply_adagrad(ds.param, ds.dense_slots[0], st.g_bar, w.lr, w.eps, **dkw)
+            else:
+                gba.gba_apply_adam(ds.param, ds.dense_slots[0], ds.dense_slots[1], st.g_bar, w.lr, w.beta1,
+                                   w.beta2, w.eps, w.adam_t, **dkw)
         else:
-            gba.gba_apply_adam(ds.param, ds.dense_slots[0], ds.dense_slots[1], st.g_bar, w.lr, w.beta1,
-                               w.beta2, w.eps, w.adam_t, **dkw)
+            # the weighted sum and the dense optimiser in one pass; g_bar is not stored
+            if w.optimizer == "adagrad":
+                gba.gba_aggregate_apply_dense_adagrad(st.grad_table(ds.grads), st.w, w.P, ds.param,
+                                                      ds.dense_slots[0], w.lr, w.eps, **dkw)
+            else:
+                gba.gba_aggregate_apply_dense_adam(st.grad_table(ds.grads), st.w, w.P, ds.param, ds.dense_slots[0],
+                                                   ds.dense_slots[1], w.lr, w.beta1, w.beta2, w.eps, w.adam_t,
+                                                   **dkw)
+            if ev is not None:
+                ev["d1"].record(dstream)
         if ev is not None:
             ev["d2"].record(dstream)
         if ev is not None:
@@ -165,8 +179,11 @@ def run_workload(name, args, torch, gba_step_mod, sdev, gba):
     print(f"[bench] {name}: {args.steps} steps timed", file=sys.stderr, flush=True)
     total_ms = start.elapsed_time(end)
     ms = total_ms / args.steps
-    spans = {"token_weights": ("t0", "t1"), "aggregate_dense": ("d0", "d1"), "apply_dense": ("d1", "d2"),
-             "aggregate_sparse": ("s0", "s1"), "apply_rows": ("s1", "s2")}
+    spans = {"token_weights": ("t0", "t1"), "aggregate_sparse": ("s0", "s1"), "apply_rows": ("s1", "s2")}
+    if args.separate_dense:
+        spans.update(aggregate_dense=("d0", "d1"), apply_dense=("d1", "d2"))
+    else:
+        spans.update(aggregate_apply_dense=("d0", "d1"))
     breakdown = {n: float(np.mean([e[a].elapsed_time(e[b]) for e in evs])) for n, (a, b) in spans.items()}
 
     # realised sizes (the same every step: the batch is re-applied)
@@ -182,18 +199,26 @@ def run_workload(name, args, torch, gba_step_mod, sdev, gba):
     dense_b, sparse_b = algorithmic_bytes(w, K_eff, N_act, U, U_act, args.decay == "id_tag")
     step_gbs = (dense_b + sparse_b) / (ms * 1e-3) / 1e9
 
-    # dominant kernel: the dense reduction (one launch per call)
-    dense_kernel_bytes = K_eff * w.P * 4 + w.P * 4
-    dk_ms = breakdown["aggregate_dense"]
+    # dominant kernel: the dense reduction (one launch per call), fused with
+    # the dense optimiser unless --separate-dense
+    S = 1 if w.optimizer == "adagrad" else 2
+    if args.separate_dense:
+        dense_kernel_bytes = K_eff * w.P * 4 + w.P * 4
+        dk_ms = breakdown["aggregate_dense"]
+        kname = "aggregate_dense_kernel<0>"
+    else:
+        dense_kernel_bytes = K_eff * w.P * 4 + (2 + 2 * S) * w.P * 4
+        dk_ms = breakdown["aggregate_apply_dense"]
+        kname = f"aggregate_dense_kernel<{S}>"
     dk_gbs = dense_kernel_bytes / (dk_ms * 1e-3) / 1e9
-    traffic = measured_traffic("aggregate_dense_kernel", name)
+    traffic = measured_traffic(kname, name)
     res = dict(
         workload=name, ms_per_step=ms, wall_ms_per_step=wall_ms / args.steps,
         global_batches_per_s=1000.0 / ms, embedding_grad_rows_per_s=w.N / (ms * 1e-3),
         samples_per_s=w.K * w.B / (ms * 1e-3),
         step_alg_bytes=dense_b + sparse_b, step_alg_gbs=step_gbs, step_frac_of_hbm_peak=step_gbs / HBM_PEAK_GBS,
-        breakdown_ms=breakdown, overlap=args.overlap, K_eff=K_eff, N=w.N, N_act=N_act, U=U, U_act=U_act, setup_s=setup_s,
-        roofline=dict(kernel="aggregate_dense_kernel", bound="hbm", achieved=dk_gbs, peak=HBM_PEAK_GBS,
+        breakdown_ms=breakdown, overlap=args.overlap, fused_dense=not args.separate_dense, K_eff=K_eff, N=w.N, N_act=N_act, U=U, U_act=U_act, setup_s=setup_s,
+        roofline=dict(kernel=kname, bound="hbm", achieved=dk_gbs, peak=HBM_PEAK_GBS,
                       unit="GB/s", frac=dk_gbs / HBM_PEAK_GBS, traffic=traffic,
                       alg_bytes_per_launch=dense_kernel_bytes, avg_launch_ms=dk_ms),
     )

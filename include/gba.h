@@ -167,6 +167,29 @@ gba_status gba_apply_adam(float* param, float* m, float* v, const float* grad, c
                           int64_t R, double lr, double beta1, double beta2, double eps, int64_t t,
                           int32_t* err, hipStream_t stream);
 
+/*
+ * gba_aggregate_dense followed by the dense form of gba_apply_adagrad /
+ * gba_apply_adam, in one pass over memory (Alg. 2: the weighted sum of the
+ * dense gradients divided by K, then the Table 1 optimiser on the dense
+ * parameters).  Each element's sum is rounded to float and applied exactly
+ * as the two separate calls would, so param and state come out bitwise equal
+ * to theirs; the sum itself never makes a round trip through memory.
+ * grads, w, K, P   as for gba_aggregate_dense.
+ * out              [P] float, receives the sum as gba_aggregate_dense would;
+ *                  may be NULL.
+ * param, accum / m, v   [P] float, updated in place.
+ * lr, eps, beta1, beta2, t   as for gba_apply_adagrad / gba_apply_adam.
+ * 16-byte-aligned buffers take the vector path; others work, more slowly.
+ */
+gba_status gba_aggregate_apply_dense_adagrad(const float* const* grads, const float* w, int32_t K,
+                                             int64_t P, float* out, float* param, float* accum,
+                                             double lr, double eps, hipStream_t stream);
+
+gba_status gba_aggregate_apply_dense_adam(const float* const* grads, const float* w, int32_t K,
+                                          int64_t P, float* out, float* param, float* m, float* v,
+                                          double lr, double beta1, double beta2, double eps,
+                                          int64_t t, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

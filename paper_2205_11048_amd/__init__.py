@@ -16,6 +16,7 @@ import torch
 __all__ = [
     "GBAError", "lib", "gba_token_weights", "gba_aggregate_dense", "gba_aggregate_sparse",
     "gba_aggregate_sparse_workspace_size", "gba_apply_adagrad", "gba_apply_adam",
+    "gba_aggregate_apply_dense_adagrad", "gba_aggregate_apply_dense_adam",
     "pointer_table", "DECAY_TOKEN", "DECAY_ID_TAG", "NORM_PER_ID_COUNT", "NORM_BY_K",
     "DERR_ID_RANGE", "DERR_FUTURE_TOKEN", "DERR_OFFSETS", "DERR_ROW_RANGE", "DERR_INTERNAL", "MAX_K", "MAX_D",
     "LIB_PATH",
@@ -43,6 +44,9 @@ _SIGNATURES = {
     "gba_aggregate_sparse_workspace_size": ([_I64, _I32, _I32, _I64, ctypes.POINTER(ctypes.c_size_t)], _I32),
     "gba_aggregate_sparse": ([_P, _P, _P, _I32, _I64, _I32, _I64, _P, _P, _I64, _I64, _P, _I32, _I32,
                               _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P, _P], _I32),
+    "gba_aggregate_apply_dense_adagrad": ([_P, _P, _I32, _I64, _P, _P, _P, _F64, _F64, _P], _I32),
+    "gba_aggregate_apply_dense_adam": ([_P, _P, _I32, _I64, _P, _P, _P, _P, _F64, _F64, _F64, _F64, _I64, _P],
+                                       _I32),
     "gba_apply_adagrad": ([_P, _P, _P, _P, _P, _P, _I64, _I32, _I64, _F64, _F64, _P, _P], _I32),
     "gba_apply_adam": ([_P, _P, _P, _P, _P, _P, _P, _I64, _I32, _I64, _F64, _F64, _F64, _F64, _I64,
                         _P, _P], _I32),
@@ -120,6 +124,33 @@ def gba_aggregate_dense(grads, w, P, out, stream=None):
     _need(w, torch.float32, "w", K)
     _need(out, torch.float32, "out", P)
     _check(lib().gba_aggregate_dense(_ptr(grads), _ptr(w), K, int(P), _ptr(out), _stream(stream)))
+
+
+def _dense_common(grads, w, P, out, **state):
+    K = grads.numel()
+    _need(grads, torch.int64, "grads")
+    _need(w, torch.float32, "w", K)
+    _need(out, torch.float32, "out", P)
+    for name, x in state.items():
+        if x is None:
+            raise GBAError(f"{name} is required")
+        _need(x, torch.float32, name, P)
+    return K
+
+
+def gba_aggregate_apply_dense_adagrad(grads, w, P, param, accum, lr, eps, out=None, stream=None):
+    """gba_aggregate_dense + dense Adagrad in one pass; ``out`` (the sum) may be None."""
+    K = _dense_common(grads, w, P, out, param=param, accum=accum)
+    _check(lib().gba_aggregate_apply_dense_adagrad(_ptr(grads), _ptr(w), K, int(P), _ptr(out), _ptr(param),
+                                                   _ptr(accum), float(lr), float(eps), _stream(stream)))
+
+
+def gba_aggregate_apply_dense_adam(grads, w, P, param, m, v, lr, beta1, beta2, eps, t, out=None, stream=None):
+    """gba_aggregate_dense + dense Adam in one pass; ``out`` (the sum) may be None."""
+    K = _dense_common(grads, w, P, out, param=param, m=m, v=v)
+    _check(lib().gba_aggregate_apply_dense_adam(_ptr(grads), _ptr(w), K, int(P), _ptr(out), _ptr(param), _ptr(m),
+                                                _ptr(v), float(lr), float(beta1), float(beta2), float(eps), int(t),
+                                                _stream(stream)))
 
 
 def gba_aggregate_sparse_workspace_size(N, K, D, R) -> int:

@@ -1,6 +1,6 @@
 // Dense part of the push-step: the decayed weighted sum of the K dense
 // gradients divided by N_a (Alg. 2), and the elementwise optimiser updates
-// (Adagrad, Adam; Table 1 names them).
+// (Adagrad, Adam; Table 1 names them), separately or fused.
 //
 // The reduction streams K_eff * P floats from HBM.  A block owns 64 KB of
 // the output at a time; each of its waves reads 16 KB of one gradient as 16
@@ -58,9 +58,93 @@ __device__ __forceinline__ int build_kept_list(const float* const* grads, const 
   return (int)total;
 }
 
+// What the reduction does with each finished element g = sum / K: store it
+// (kStoreOnly), and/or apply Adagrad or Adam to the dense parameters right
+// away, which spares the round trip of g through memory.  In the apply modes
+// `out` may be null.
+enum DenseMode : int { kStoreOnly = 0, kApplyAdagrad = 1, kApplyAdam = 2 };
+struct DenseState {
+  float* p;
+  float* s1;   // Adagrad accumulator or Adam m
+  float* s2;   // Adam v
+  double lr, eps, beta1, beta2, bc1, bc2;
+};
+
+template <int MODE>
+__device__ __forceinline__ void finish_element(float g, int64_t e, float* out, const DenseState& st) {
+  if (out) out[e] = g;
+  if (MODE == kApplyAdagrad) {
+    float pe = st.p[e], ae = st.s1[e];
+    adagrad_update(pe, ae, g, st.lr, st.eps);
+    st.p[e] = pe;
+    st.s1[e] = ae;
+  } else if (MODE == kApplyAdam) {
+    float pe = st.p[e], me = st.s1[e], ve = st.s2[e];
+    adam_update(pe, me, ve, g, st.lr, st.beta1, st.beta2, st.eps, st.bc1, st.bc2);
+    st.p[e] = pe;
+    st.s1[e] = me;
+    st.s2[e] = ve;
+  }
+}
+
+// Vectors q[j] = vb + 64 j (j < kDenseVecs, q < nvec) are finished: g in
+// float first (which frees the float64 sums), then the optimiser, with the
+// state of a whole group of vectors requested at once (16 for Adagrad, 8 for
+// Adam: what fits the registers the sums held), so a block's finishing costs
+// one or two memory latencies, not one per vector.
+template <int MODE>
+__device__ __forceinline__ void finish_vectors(const f64x4* acc, double denom, int64_t vb, int64_t nvec,
+                                               float* out, const DenseState& st) {
+  f32x4 g[kDenseVecs];
+#pragma unroll
+  for (int j = 0; j < kDenseVecs; ++j) g[j] = narrow(acc[j] / denom);
+  if (out) {
+#pragma unroll
+    for (int j = 0; j < kDenseVecs; ++j)
+      if (vb + kWave * j < nvec) store_stream(reinterpret_cast<f32x4*>(out) + vb + kWave * j, g[j]);
+  }
+  if (MODE == kStoreOnly) return;
+  constexpr int kGroup = (MODE == kApplyAdam) ? 8 : 16;
+#pragma unroll
+  for (int j0 = 0; j0 < kDenseVecs; j0 += kGroup) {
+    f32x4 pv[kGroup], sv[kGroup], vv[kGroup];
+#pragma unroll
+    for (int jj = 0; jj < kGroup; ++jj) {
+      const int64_t q = vb + kWave * (j0 + jj);
+      if (q < nvec) {
+        pv[jj] = load_stream(reinterpret_cast<const f32x4*>(st.p) + q);
+        sv[jj] = load_stream(reinterpret_cast<const f32x4*>(st.s1) + q);
+        if (MODE == kApplyAdam) vv[jj] = load_stream(reinterpret_cast<const f32x4*>(st.s2) + q);
+      }
+    }
+#pragma unroll
+    for (int jj = 0; jj < kGroup; ++jj) {
+      const int64_t q = vb + kWave * (j0 + jj);
+      if (q >= nvec) continue;
+      const f32x4 gj = g[j0 + jj];
+      float pe[4] = {pv[jj].x, pv[jj].y, pv[jj].z, pv[jj].w};
+      float se[4] = {sv[jj].x, sv[jj].y, sv[jj].z, sv[jj].w};
+      const float ge[4] = {gj.x, gj.y, gj.z, gj.w};
+      if (MODE == kApplyAdam) {
+        float ve[4] = {vv[jj].x, vv[jj].y, vv[jj].z, vv[jj].w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          adam_update(pe[k], se[k], ve[k], ge[k], st.lr, st.beta1, st.beta2, st.eps, st.bc1, st.bc2);
+        store_stream(reinterpret_cast<f32x4*>(st.s2) + q, f32x4{ve[0], ve[1], ve[2], ve[3]});
+      } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) adagrad_update(pe[k], se[k], ge[k], st.lr, st.eps);
+      }
+      store_stream(reinterpret_cast<f32x4*>(st.p) + q, f32x4{pe[0], pe[1], pe[2], pe[3]});
+      store_stream(reinterpret_cast<f32x4*>(st.s1) + q, f32x4{se[0], se[1], se[2], se[3]});
+    }
+  }
+}
+
+template <int MODE>
 __global__ void __launch_bounds__(kDenseBlock)
 aggregate_dense_kernel(const float* const* __restrict__ grads, const float* __restrict__ w, int K,
-                       int64_t P, float* __restrict__ out) {
+                       int64_t P, float* __restrict__ out, DenseState st) {
   __shared__ uint16_t kept[GBA_MAX_K];
   __shared__ float kw[GBA_MAX_K];
   __shared__ uint32_t tmp[kDenseBlock / kWave + 1];
@@ -68,7 +152,10 @@ aggregate_dense_kernel(const float* const* __restrict__ grads, const float* __re
   const int nk = build_kept_list(grads, w, K, kept, kw, tmp, &aligned);
   const double denom = (double)K;
   const int64_t stride = (int64_t)gridDim.x * kDenseBlock;
-  if (aligned) {
+  const bool outputs_aligned = ((reinterpret_cast<uintptr_t>(out) | reinterpret_cast<uintptr_t>(st.p) |
+                                 reinterpret_cast<uintptr_t>(st.s1) | reinterpret_cast<uintptr_t>(st.s2)) &
+                                15u) == 0;   // null pointers count as aligned
+  if (aligned && outputs_aligned) {
     const int64_t nvec = P / 4;
     for (int64_t b0 = (int64_t)blockIdx.x * kDenseSpan; b0 < nvec; b0 += (int64_t)gridDim.x * kDenseSpan) {
       // wave w covers vectors [b0 + w * 1024, +1024): lane l takes l, l + 64, ...
@@ -86,10 +173,7 @@ aggregate_dense_kernel(const float* const* __restrict__ grads, const float* __re
 #pragma unroll
         for (int j = 0; j < kDenseVecs; ++j) acc[j] += wi * widen(x[j]);
       }
-#pragma unroll
-      for (int j = 0; j < kDenseVecs; ++j)
-        if (vb + kWave * j < nvec)
-          store_stream(reinterpret_cast<f32x4*>(out) + vb + kWave * j, narrow(acc[j] / denom));
+      finish_vectors<MODE>(acc, denom, vb, nvec, out, st);
     }
     // the last P % 4 elements
     const int64_t tail0 = nvec * 4;
@@ -97,28 +181,52 @@ aggregate_dense_kernel(const float* const* __restrict__ grads, const float* __re
       const int64_t e = tail0 + threadIdx.x;
       double acc = 0.0;
       for (int i = 0; i < nk; ++i) acc += (double)kw[i] * (double)grads[kept[i]][e];
-      out[e] = (float)(acc / denom);
+      finish_element<MODE>((float)(acc / denom), e, out, st);
     }
   } else {
     for (int64_t e = (int64_t)blockIdx.x * kDenseBlock + threadIdx.x; e < P; e += stride) {
       double acc = 0.0;
       for (int i = 0; i < nk; ++i) acc += (double)kw[i] * (double)grads[kept[i]][e];
-      out[e] = (float)(acc / denom);
+      finish_element<MODE>((float)(acc / denom), e, out, st);
     }
   }
 }
 
-hipError_t launch_aggregate_dense(const float* const* grads, const float* w, int32_t K, int64_t P,
-                                  float* out, hipStream_t stream) {
+template <int MODE>
+static hipError_t launch_dense_mode(const float* const* grads, const float* w, int32_t K, int64_t P,
+                                    float* out, const DenseState& st, hipStream_t stream) {
   if (P <= 0) return hipSuccess;
   // one block step per block where possible; unaligned buffers fall back to
   // a grid-stride loop over single elements
   int64_t blocks = ceil_div(ceil_div(P, 4), kDenseSpan);
   if (blocks > kDenseMaxBlocks) blocks = kDenseMaxBlocks;
   if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(aggregate_dense_kernel, dim3((unsigned)blocks), dim3(kDenseBlock), 0, stream,
-                     grads, w, (int)K, P, out);
+  hipLaunchKernelGGL(aggregate_dense_kernel<MODE>, dim3((unsigned)blocks), dim3(kDenseBlock), 0, stream,
+                     grads, w, (int)K, P, out, st);
   return hipGetLastError();
+}
+
+hipError_t launch_aggregate_dense(const float* const* grads, const float* w, int32_t K, int64_t P,
+                                  float* out, hipStream_t stream) {
+  return launch_dense_mode<kStoreOnly>(grads, w, K, P, out, DenseState{}, stream);
+}
+
+hipError_t launch_aggregate_apply_dense_adagrad(const float* const* grads, const float* w, int32_t K,
+                                                int64_t P, float* out, float* p, float* a, double lr,
+                                                double eps, hipStream_t stream) {
+  DenseState st{};
+  st.p = p;
+  st.s1 = a;
+  st.lr = lr;
+  st.eps = eps;
+  return launch_dense_mode<kApplyAdagrad>(grads, w, K, P, out, st, stream);
+}
+
+hipError_t launch_aggregate_apply_dense_adam(const float* const* grads, const float* w, int32_t K,
+                                             int64_t P, float* out, float* p, float* m, float* v,
+                                             const AdamParams& hp, hipStream_t stream) {
+  DenseState st{p, m, v, hp.lr, hp.eps, hp.beta1, hp.beta2, hp.bc1, hp.bc2};
+  return launch_dense_mode<kApplyAdam>(grads, w, K, P, out, st, stream);
 }
 
 // ---------------------------------------------------------------- optimisers

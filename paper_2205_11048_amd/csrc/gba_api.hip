@@ -24,6 +24,21 @@ size_t sparse_bytes(int64_t N, int32_t D, int64_t R, SortPlan* plan_out) {
   return align_up(plan.bytes) + align_up(segments_workspace_bytes(N, D));
 }
 
+bool adam_args_ok(double beta1, double beta2, int64_t t) {
+  return t >= 1 && beta1 >= 0.0 && beta1 < 1.0 && beta2 >= 0.0 && beta2 < 1.0;
+}
+
+AdamParams adam_params(double lr, double beta1, double beta2, double eps, int64_t t) {
+  AdamParams hp;
+  hp.lr = lr;
+  hp.beta1 = beta1;
+  hp.beta2 = beta2;
+  hp.eps = eps;
+  hp.bc1 = 1.0 - std::pow(beta1, (double)t);
+  hp.bc2 = 1.0 - std::pow(beta2, (double)t);
+  return hp;
+}
+
 }  // namespace
 
 extern "C" {
@@ -54,6 +69,26 @@ gba_status gba_aggregate_dense(const float* const* grads, const float* w, int32_
   if (P == 0) return GBA_OK;
   if (!grads || !w || !out) return GBA_ERR_NULL;
   return from_hip(launch_aggregate_dense(grads, w, K, P, out, stream));
+}
+
+gba_status gba_aggregate_apply_dense_adagrad(const float* const* grads, const float* w, int32_t K,
+                                             int64_t P, float* out, float* param, float* accum, double lr,
+                                             double eps, hipStream_t stream) {
+  if (K < 1 || K > GBA_MAX_K || P < 0) return GBA_ERR_INVALID_ARG;
+  if (P == 0) return GBA_OK;
+  if (!grads || !w || !param || !accum) return GBA_ERR_NULL;
+  return from_hip(launch_aggregate_apply_dense_adagrad(grads, w, K, P, out, param, accum, lr, eps, stream));
+}
+
+gba_status gba_aggregate_apply_dense_adam(const float* const* grads, const float* w, int32_t K, int64_t P,
+                                          float* out, float* param, float* m, float* v, double lr,
+                                          double beta1, double beta2, double eps, int64_t t,
+                                          hipStream_t stream) {
+  if (K < 1 || K > GBA_MAX_K || P < 0 || !adam_args_ok(beta1, beta2, t)) return GBA_ERR_INVALID_ARG;
+  if (P == 0) return GBA_OK;
+  if (!grads || !w || !param || !m || !v) return GBA_ERR_NULL;
+  return from_hip(launch_aggregate_apply_dense_adam(grads, w, K, P, out, param, m, v,
+                                                    adam_params(lr, beta1, beta2, eps, t), stream));
 }
 
 gba_status gba_aggregate_sparse_workspace_size(int64_t N, int32_t K, int32_t D, int64_t R,
@@ -144,17 +179,10 @@ gba_status gba_apply_adam(float* param, float* m, float* v, const float* grad, c
                           const int32_t* active, const int64_t* num_rows, int64_t n, int32_t D,
                           int64_t R, double lr, double beta1, double beta2, double eps, int64_t t,
                           int32_t* err, hipStream_t stream) {
-  if (n < 0 || t < 1 || !(beta1 >= 0.0 && beta1 < 1.0) || !(beta2 >= 0.0 && beta2 < 1.0))
-    return GBA_ERR_INVALID_ARG;
+  if (n < 0 || !adam_args_ok(beta1, beta2, t)) return GBA_ERR_INVALID_ARG;
   if (n == 0) return GBA_OK;
   if (!param || !m || !v || !grad) return GBA_ERR_NULL;
-  AdamParams hp;
-  hp.lr = lr;
-  hp.beta1 = beta1;
-  hp.beta2 = beta2;
-  hp.eps = eps;
-  hp.bc1 = 1.0 - std::pow(beta1, (double)t);
-  hp.bc2 = 1.0 - std::pow(beta2, (double)t);
+  const AdamParams hp = adam_params(lr, beta1, beta2, eps, t);
   if (!rows) return from_hip(launch_dense_adam(param, m, v, grad, n, hp, stream));
   if (!num_rows) return GBA_ERR_NULL;
   if (!width_ok(D)) return GBA_ERR_UNSUPPORTED;

@@ -26,8 +26,15 @@ struct AdamParams {
 };
 hipError_t launch_dense_adagrad(float* p, float* a, const float* g, int64_t n, double lr, double eps,
                                 hipStream_t stream);
+// the weighted sum and the optimiser in one pass; out (the sum) may be null
+hipError_t launch_aggregate_apply_dense_adagrad(const float* const* grads, const float* w, int32_t K,
+                                                int64_t P, float* out, float* p, float* a, double lr,
+                                                double eps, hipStream_t stream);
 hipError_t launch_dense_adam(float* p, float* m, float* v, const float* g, int64_t n,
                              const AdamParams& hp, hipStream_t stream);
+hipError_t launch_aggregate_apply_dense_adam(const float* const* grads, const float* w, int32_t K,
+                                             int64_t P, float* out, float* p, float* m, float* v,
+                                             const AdamParams& hp, hipStream_t stream);
 hipError_t launch_rows_adagrad(float* p, float* a, const float* g, const int64_t* rows,
                                const int32_t* active, const int64_t* num_rows, int64_t n, int32_t D,
                                int64_t R, double lr, double eps, int32_t* err, hipStream_t stream);

@@ -5,16 +5,18 @@ token weights (Eq. 1) -> dense weighted sum / K -> embedding dedup, per-ID
 decay and weighted sum / c_r -> optimiser apply on the dense vector and on
 the touched rows.  This class owns only the output and scratch buffers of the
 step (allocated once, reused every step); inputs and PS state are the
-caller's tensors.  All five calls are enqueued on one stream with no host
-synchronisation in between.
+caller's tensors.  All calls are enqueued on one stream with no host
+synchronisation in between.  The dense sum and the dense optimiser run as one
+fused call by default (``fused_dense=False`` makes them two).
 """
 from __future__ import annotations
 
 import torch
 
-from . import (DECAY_ID_TAG, DECAY_TOKEN, NORM_PER_ID_COUNT, gba_aggregate_dense,
-               gba_aggregate_sparse, gba_aggregate_sparse_workspace_size, gba_apply_adagrad,
-               gba_apply_adam, gba_token_weights, pointer_table)
+from . import (DECAY_ID_TAG, DECAY_TOKEN, NORM_PER_ID_COUNT, gba_aggregate_apply_dense_adagrad,
+               gba_aggregate_apply_dense_adam, gba_aggregate_dense, gba_aggregate_sparse,
+               gba_aggregate_sparse_workspace_size, gba_apply_adagrad, gba_apply_adam, gba_token_weights,
+               pointer_table)
 
 
 class GBAStep:
@@ -48,24 +50,37 @@ class GBAStep:
 
     def run(self, *, tokens, step, iota, grads, ids, rows, offsets, param, dense_slots, table,
             table_slots, optimizer, lr, eps, beta1=0.9, beta2=0.999, t=1, tag=None,
-            decay=DECAY_TOKEN, norm=NORM_PER_ID_COUNT, stream=None):
+            decay=DECAY_TOKEN, norm=NORM_PER_ID_COUNT, stream=None, fused_dense=True, keep_g_bar=True):
+        """One push-step.  On the fused dense path, ``keep_g_bar`` also stores
+        the dense sum in ``self.g_bar`` (the separate path always does)."""
+        if optimizer not in ("adagrad", "adam"):
+            raise ValueError(optimizer)
         gba_token_weights(tokens, step, iota, self.w, self.staleness, self.num_excluded, self.err,
                           stream=stream)
-        gba_aggregate_dense(self.grad_table(grads), self.w, self.P, self.g_bar, stream=stream)
+        table_grads = self.grad_table(grads)
+        g_out = self.g_bar if keep_g_bar else None
+        if fused_dense and optimizer == "adagrad":
+            gba_aggregate_apply_dense_adagrad(table_grads, self.w, self.P, param, dense_slots[0], lr, eps,
+                                              out=g_out, stream=stream)
+        elif fused_dense:
+            gba_aggregate_apply_dense_adam(table_grads, self.w, self.P, param, dense_slots[0], dense_slots[1], lr,
+                                           beta1, beta2, eps, t, out=g_out, stream=stream)
+        else:
+            gba_aggregate_dense(table_grads, self.w, self.P, self.g_bar, stream=stream)
+            if optimizer == "adagrad":
+                gba_apply_adagrad(param, dense_slots[0], self.g_bar, lr, eps, stream=stream)
+            else:
+                gba_apply_adam(param, dense_slots[0], dense_slots[1], self.g_bar, lr, beta1, beta2, eps, t,
+                               stream=stream)
         gba_aggregate_sparse(ids, rows, offsets, self.R, self.w, tokens, step, iota,
                              tag if decay == DECAY_ID_TAG else None, decay, norm, self.unique_ids,
                              self.seg_offsets, self.contrib_count, self.active_count, self.agg,
                              self.num_unique, self.workspace, self.err, stream=stream)
         if optimizer == "adagrad":
-            gba_apply_adagrad(param, dense_slots[0], self.g_bar, lr, eps, stream=stream)
             gba_apply_adagrad(table, table_slots[0], self.agg, lr, eps, rows=self.unique_ids,
                               active=self.active_count, num_rows=self.num_unique, R=self.R,
                               err=self.err, stream=stream)
-        elif optimizer == "adam":
-            gba_apply_adam(param, dense_slots[0], dense_slots[1], self.g_bar, lr, beta1, beta2, eps, t,
-                           stream=stream)
+        else:
             gba_apply_adam(table, table_slots[0], table_slots[1], self.agg, lr, beta1, beta2, eps, t,
                            rows=self.unique_ids, active=self.active_count, num_rows=self.num_unique,
                            R=self.R, err=self.err, stream=stream)
-        else:
-            raise ValueError(optimizer)

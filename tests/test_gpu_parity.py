@@ -381,9 +381,10 @@ def test_apply_rows_out_of_range_is_reported():
 
 
 # ------------------------------------------------------------ whole step
+@pytest.mark.parametrize("fused_dense", [True, False])
 @pytest.mark.parametrize("decay", ["token", "id_tag"])
 @pytest.mark.parametrize("opt", ["adagrad", "adam"])
-def test_full_step_small(decay, opt):
+def test_full_step_small(decay, opt, fused_dense):
     c = BY_NAME["c0"].scaled(optimizer=opt, lr=0.01 if opt == "adagrad" else 1e-3)
     hs = workload.host_step(c)
     stepper = GBAStep(c.K, c.N, c.D, c.R, c.P)
@@ -395,7 +396,7 @@ def test_full_step_small(decay, opt):
     stepper.run(tokens=dev(hs.tokens), step=hs.step, iota=c.iota, grads=grads, ids=dev(hs.ids),
                 rows=dev(hs.rows), offsets=dev(hs.offsets), param=param, dense_slots=dslots, table=table,
                 table_slots=tslots, optimizer=opt, lr=c.lr, eps=c.eps, t=c.adam_t, tag=tag,
-                decay=gba.DECAY_ID_TAG if decay == "id_tag" else gba.DECAY_TOKEN)
+                decay=gba.DECAY_ID_TAG if decay == "id_tag" else gba.DECAY_TOKEN, fused_dense=fused_dense)
     hp = dict(lr=c.lr, eps=c.eps, beta1=c.beta1, beta2=c.beta2)
     ref = oracle.gba_step(hs.tokens, hs.step, c.iota, hs.grads, hs.ids, hs.rows, hs.offsets, hs.param,
                           hs.dense_slots, lambda r: hs.table[r], lambda k, r: hs.table_slots[k][r], opt, hp,
@@ -429,3 +430,64 @@ def test_sparse_fractional_token_weights(D):
     w = np.array([1.0, 0.5, 0.0, 0.25, 0.0], np.float32)
     res = _run_sparse(ids, rows, off, w, tokens, 1000, 2, 800)
     _check_sparse(res, ids, rows, off, w, tokens, 1000, 2, expect_exact=True)
+
+
+# ------------------------------------------------ fused dense sum + optimiser
+@pytest.mark.parametrize("opt", ["adagrad", "adam"])
+@pytest.mark.parametrize("K,P,offset,keep_out", [(1, 1, 0, True), (3, 5, 0, False), (37, 100_003, 0, True),
+                                                 (9, 4096 * 16 * 3 + 7, 0, False), (64, 70_001, 1, True),
+                                                 (200, 8193, 3, False), (5, 262_144, 0, False)])
+def test_fused_dense_matches_separate_calls(opt, K, P, offset, keep_out):
+    """The fused call gives bitwise the parameters, state and (if asked) sum of
+    gba_aggregate_dense followed by the dense optimiser, aligned or not."""
+    rng = np.random.default_rng(K * 7 + P)
+    grads = [dev_at(counter.values_range(5, 300 + m, 0, P, counter.KIND_GRAD, counter.grad_scale(1e-2)), offset)
+             for m in range(K)]
+    tokens = 80 - rng.integers(0, 7, K)
+    w, _, _ = oracle.token_weights(tokens, 80, 4)
+    table, w_d = gba.pointer_table(grads), dev(w)
+    p0 = counter.values_range(6, 1, 0, P, counter.KIND_PARAM)
+    kinds = workload.state_kinds(opt)
+    s0 = [counter.values_range(6, 2 + k, 0, P, kind) for k, (_, _, kind) in enumerate(kinds)]
+    # separate
+    pa, sa = dev_at(p0, offset), [dev(x) for x in s0]
+    g_bar = torch.empty(P, device=DEV)
+    gba.gba_aggregate_dense(table, w_d, P, g_bar)
+    if opt == "adagrad":
+        gba.gba_apply_adagrad(pa, sa[0], g_bar, 0.01, 1e-8)
+    else:
+        gba.gba_apply_adam(pa, sa[0], sa[1], g_bar, 1e-3, 0.9, 0.999, 1e-8, 1001)
+    # fused
+    pb, sb = dev_at(p0, offset), [dev(x) for x in s0]
+    out = torch.full((P,), float("nan"), device=DEV) if keep_out else None
+    if opt == "adagrad":
+        gba.gba_aggregate_apply_dense_adagrad(table, w_d, P, pb, sb[0], 0.01, 1e-8, out=out)
+    else:
+        gba.gba_aggregate_apply_dense_adam(table, w_d, P, pb, sb[0], sb[1], 1e-3, 0.9, 0.999, 1e-8, 1001, out=out)
+    assert_exact(host(pb), host(pa), "param")
+    for k in range(len(sa)):
+        assert_exact(host(sb[k]), host(sa[k]), f"state {k}")
+    if keep_out:
+        assert_exact(host(out), host(g_bar), "sum")
+    # and the sum itself against the oracle
+    g_host = [host(g) for g in grads]
+    assert_exact(host(g_bar), oracle.aggregate_dense(g_host, w), "g_bar vs oracle")
+
+
+def test_fused_dense_host_checks():
+    P = 16
+    g = [torch.ones(P, device=DEV)]
+    table, w = gba.pointer_table(g), torch.ones(1, device=DEV)
+    p, a = torch.zeros(P, device=DEV), torch.ones(P, device=DEV)
+    L = gba.lib()
+    st = torch.cuda.current_stream().cuda_stream
+    assert L.gba_aggregate_apply_dense_adagrad(table.data_ptr(), w.data_ptr(), 1, P, None, None, a.data_ptr(),
+                                               0.1, 0.0, st) == 1
+    assert L.gba_aggregate_apply_dense_adagrad(table.data_ptr(), w.data_ptr(), 0, P, None, p.data_ptr(),
+                                               a.data_ptr(), 0.1, 0.0, st) == 2
+    assert L.gba_aggregate_apply_dense_adam(table.data_ptr(), w.data_ptr(), 1, P, None, p.data_ptr(), a.data_ptr(),
+                                            a.data_ptr(), 1e-3, 0.9, 0.999, 1e-8, 0, st) == 2
+    assert L.gba_aggregate_apply_dense_adam(table.data_ptr(), w.data_ptr(), 1, P, None, p.data_ptr(), a.data_ptr(),
+                                            None, 1e-3, 0.9, 0.999, 1e-8, 1, st) == 1
+    torch.cuda.synchronize()
+    assert np.all(host(p) == 0) and np.all(host(a) == 1)
