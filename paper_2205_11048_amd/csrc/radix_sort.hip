@@ -27,6 +27,7 @@ constexpr int kItemsRest = 16;
 template <int ITEMS>
 constexpr int64_t tile_keys() { return (int64_t)kSortBlock * ITEMS; }
 constexpr int kRadix = 256;
+constexpr int kXcds = 8;   // MI355X: 8 accelerator dies, each with its own L2
 constexpr int kChunk = kSortWaves;                     // tiles per chunk: one hist block
 
 __host__ __device__ static inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -101,55 +102,63 @@ sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n, int64_t tiles
     // lane l holds keys tile0 + 4 * (l + 64 * c) + e, c < ITEMS, e < 4: each
     // vector load of the wave covers 1 KB of consecutive keys
     const int64_t tile0 = tile * tile_keys<ITEMS>();
-    uint32_t digit[kHistKeys];
+    // four vectors (16 keys) per lane per phase: few registers, so eight waves
+    // per SIMD keep loads in flight while others count
+    constexpr int kVecs = 4;
 #pragma unroll
-    for (int c = 0; c < kHistKeys / 4; ++c) {
-      const int64_t i0 = tile0 + 4 * ((int64_t)lane + (int64_t)kWave * c);
-      if (i0 + 3 < n) {
-        uint32_t k4[4];
-        if (FIRST) {
-          const int64_t* ids = static_cast<const int64_t*>(keys_in);
-          typedef int64_t i64x2 __attribute__((ext_vector_type(2)));
-          const i64x2 a = *reinterpret_cast<const i64x2*>(ids + i0);
-          const i64x2 b = *reinterpret_cast<const i64x2*>(ids + i0 + 2);
-          const int64_t v[4] = {a.x, a.y, b.x, b.y};
+    for (int ph = 0; ph < kHistKeys / 4 / kVecs; ++ph) {
+      uint32_t digit[4 * kVecs];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const bool out = v[e] < 0 || v[e] >= R;
-            bad |= out;
-            k4[e] = out ? 0u : (uint32_t)v[e];
-          }
-        } else {
-          const u32x4 v = *reinterpret_cast<const u32x4*>(static_cast<const uint32_t*>(keys_in) + i0);
-          k4[0] = v.x; k4[1] = v.y; k4[2] = v.z; k4[3] = v.w;
-        }
+      for (int cc = 0; cc < kVecs; ++cc) {
+        const int c = ph * kVecs + cc;
+        const int64_t i0 = tile0 + 4 * ((int64_t)lane + (int64_t)kWave * c);
+        if (i0 + 3 < n) {
+          uint32_t k4[4];
+          if (FIRST) {
+            const int64_t* ids = static_cast<const int64_t*>(keys_in);
+            typedef int64_t i64x2 __attribute__((ext_vector_type(2)));
+            const i64x2 a = *reinterpret_cast<const i64x2*>(ids + i0);
+            const i64x2 b = *reinterpret_cast<const i64x2*>(ids + i0 + 2);
+            const int64_t v[4] = {a.x, a.y, b.x, b.y};
 #pragma unroll
-        for (int e = 0; e < 4; ++e) digit[4 * c + e] = (k4[e] >> shift) & mask;
-      } else {
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          digit[4 * c + e] = (i0 + e < n) ? (load_key<FIRST>(keys_in, i0 + e, R, &bad) >> shift) & mask : 0u;
-      }
-    }
-    // one LDS add per run of equal digits among each lane's 4 consecutive keys
-#pragma unroll
-    for (int c = 0; c < kHistKeys / 4; ++c) {
-      const int64_t i0 = tile0 + 4 * ((int64_t)lane + (int64_t)kWave * c);
-      uint32_t cur = digit[4 * c];
-      uint32_t len = i0 < n ? 1u : 0u;
-#pragma unroll
-      for (int e = 1; e < 4; ++e) {
-        if (i0 + e < n) {
-          if (digit[4 * c + e] == cur) {
-            ++len;
+            for (int e = 0; e < 4; ++e) {
+              const bool out = v[e] < 0 || v[e] >= R;
+              bad |= out;
+              k4[e] = out ? 0u : (uint32_t)v[e];
+            }
           } else {
-            atomicAdd(&h[w][cur], len);
-            cur = digit[4 * c + e];
-            len = 1;
+            const u32x4 v = *reinterpret_cast<const u32x4*>(static_cast<const uint32_t*>(keys_in) + i0);
+            k4[0] = v.x; k4[1] = v.y; k4[2] = v.z; k4[3] = v.w;
           }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) digit[4 * cc + e] = (k4[e] >> shift) & mask;
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            digit[4 * cc + e] = (i0 + e < n) ? (load_key<FIRST>(keys_in, i0 + e, R, &bad) >> shift) & mask : 0u;
         }
       }
-      if (len) atomicAdd(&h[w][cur], len);
+      // one LDS add per run of equal digits among each lane's 4 consecutive keys
+#pragma unroll
+      for (int cc = 0; cc < kVecs; ++cc) {
+        const int c = ph * kVecs + cc;
+        const int64_t i0 = tile0 + 4 * ((int64_t)lane + (int64_t)kWave * c);
+        uint32_t cur = digit[4 * cc];
+        uint32_t len = i0 < n ? 1u : 0u;
+#pragma unroll
+        for (int e = 1; e < 4; ++e) {
+          if (i0 + e < n) {
+            if (digit[4 * cc + e] == cur) {
+              ++len;
+            } else {
+              atomicAdd(&h[w][cur], len);
+              cur = digit[4 * cc + e];
+              len = 1;
+            }
+          }
+        }
+        if (len) atomicAdd(&h[w][cur], len);
+      }
     }
     __builtin_amdgcn_wave_barrier();
     for (int d = lane; d < kRadix; d += kWave) hist[tile * kRadix + d] = h[w][d];
@@ -170,7 +179,6 @@ sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n, int64_t tiles
 // place, and the digit's total.  Blocks of one XCD (block b runs on XCD b % 8)
 // take 32 consecutive digits, so each 128-byte line of a chunk row is read by
 // one XCD only.
-constexpr int kXcds = 8;
 constexpr int kDigitScanBatch = 8;
 __global__ void __launch_bounds__(kSortBlock)
 sort_digit_scan_kernel(uint32_t* __restrict__ chunk, int64_t nchunks, uint32_t* __restrict__ total) {
@@ -202,6 +210,15 @@ sort_digit_scan_kernel(uint32_t* __restrict__ chunk, int64_t nchunks, uint32_t* 
   if (threadIdx.x == 0) total[d] = all;
 }
 
+// Tile of scatter block b.  Blocks are dispatched round-robin over the 8 XCDs
+// (block b on XCD b % 8); giving XCD x the x-th eighth of the tiles, in order,
+// puts neighbouring tiles on one L2, which then merges their partial-line
+// writes into the same digit bucket before they reach HBM.
+__device__ __forceinline__ int64_t xcd_tile(int64_t b, int64_t tiles) {
+  const int64_t x = b % kXcds, i = b / kXcds, q = tiles / kXcds, r = tiles % kXcds;
+  return x * q + (x < r ? x : r) + i;
+}
+
 template <bool FIRST, int ITEMS>
 __global__ void __launch_bounds__(kSortBlock)
 sort_scatter_kernel(const void* __restrict__ keys_in, const uint32_t* __restrict__ vals_in,
@@ -216,20 +233,21 @@ sort_scatter_kernel(const void* __restrict__ keys_in, const uint32_t* __restrict
   __shared__ uint32_t s_keys[kTile];
   __shared__ uint32_t s_vals[kTile];
   for (int i = threadIdx.x; i < kSortWaves * kRadix; i += kSortBlock) (&cnt[0][0])[i] = 0;
+  const int64_t tile = xcd_tile(blockIdx.x, gridDim.x);   // the grid has one block per tile
   {
     // global position of the tile's first key of each digit value: where the
     // digit starts, plus its count in earlier chunks, plus in earlier tiles of
     // this tile's chunk
     const int d = threadIdx.x;
-    const int64_t c = (int64_t)blockIdx.x / kChunk;
+    const int64_t c = tile / kChunk;
     uint32_t off = chunk[c * kRadix + d];
-    for (int64_t t = c * kChunk; t < (int64_t)blockIdx.x; ++t) off += hist[t * kRadix + d];
+    for (int64_t t = c * kChunk; t < tile; ++t) off += hist[t * kRadix + d];
     uint32_t all;
     const uint32_t start = block_exclusive_scan<kSortBlock>(total[d], tmp, &all);   // also publishes cnt = 0
     global_base[d] = start + off;
   }
   const int w = threadIdx.x / kWave;
-  const int64_t tile0 = (int64_t)blockIdx.x * kTile;
+  const int64_t tile0 = tile * kTile;
   const int64_t base = tile0 + (int64_t)w * (kWave * ITEMS) + lane_id();
   const uint32_t mask = (1u << bits) - 1u;
   const uint64_t lt = lanemask_lt();
