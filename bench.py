@@ -48,6 +48,9 @@ def parse():
                     help="run the dense path on a second stream, concurrently with the sparse path")
     ap.add_argument("--separate-dense", action="store_true",
                     help="dense sum and dense optimiser as two calls instead of the fused one")
+    ap.add_argument("--early-sum", default="16",
+                    help="comma list of J: also time the step with the dense sum taken early, J arriving "
+                         "contributions folded per call ('' for none)")
     ap.add_argument("--cpu-sample", type=int, default=4, help="1/S of the workload for the oracle timing")
     return ap.parse_args()
 
@@ -97,9 +100,27 @@ def run_workload(name, args, torch, gba_step_mod, sdev, gba):
     # the dense path (token weights -> dense sum -> dense apply) runs on its own
     # stream, concurrently with the sparse path; both wait only for the weights
     dstream = torch.cuda.Stream() if args.overlap else stream
-    names = ["token_weights", "aggregate_dense", "aggregate_sparse", "apply_dense", "apply_rows"]
 
-    def one_step(ev=None):
+    run = None       # float64 running sum of the early weighted sum, allocated on first use
+    early_tables = {}
+
+    def dense_early(J, dkw):
+        """The dense path with the weighted sum taken early (App. B): K/J calls
+        that fold J arriving contributions each, then one finishing call."""
+        nonlocal run
+        if run is None:
+            run = torch.zeros(w.P, dtype=torch.float64, device="cuda")
+        if J not in early_tables:
+            early_tables[J] = [(lo, gba.pointer_table(ds.grads[lo:lo + J])) for lo in range(0, w.K, J)]
+        for lo, tab in early_tables[J]:
+            gba.gba_accumulate_dense(tab, st.w[lo:lo + tab.numel()], w.P, run, **dkw)
+        if w.optimizer == "adagrad":
+            gba.gba_finalize_apply_dense_adagrad(run, w.K, w.P, ds.param, ds.dense_slots[0], w.lr, w.eps, **dkw)
+        else:
+            gba.gba_finalize_apply_dense_adam(run, w.K, w.P, ds.param, ds.dense_slots[0], ds.dense_slots[1], w.lr,
+                                              w.beta1, w.beta2, w.eps, w.adam_t, **dkw)
+
+    def one_step(ev=None, early_J=0):
         kw = dict(stream=stream)
         dkw = dict(stream=dstream)
         if ev is not None:
@@ -113,7 +134,11 @@ def run_workload(name, args, torch, gba_step_mod, sdev, gba):
             dstream.wait_event(w_ready)
         if ev is not None:
             ev["d0"].record(dstream)
-        if args.separate_dense:
+        if early_J:
+            dense_early(early_J, dkw)
+            if ev is not None:
+                ev["d1"].record(dstream)
+        elif args.separate_dense:
             gba.gba_aggregate_dense(st.grad_table(ds.grads), st.w, w.P, st.g_bar, **dkw)
             if ev is not None:
                 ev["d1"].record(dstream)
@@ -222,6 +247,26 @@ def run_workload(name, args, torch, gba_step_mod, sdev, gba):
                       unit="GB/s", frac=dk_gbs / HBM_PEAK_GBS, traffic=traffic,
                       alg_bytes_per_launch=dense_kernel_bytes, avg_launch_ms=dk_ms),
     )
+    # the same step with the dense sum taken early, for each J asked for
+    res["early_sum"] = []
+    for J in [int(x) for x in args.early_sum.split(",") if x.strip()]:
+        for _ in range(2):
+            one_step(early_J=J)
+        torch.cuda.synchronize()
+        n = max(3, args.steps // 2)
+        evs = [{k: torch.cuda.Event(enable_timing=True) for k in ("t0", "t1", "d0", "d1", "d2", "s0", "s1", "s2")}
+               for _ in range(n)]
+        start.record(stream)
+        for i in range(n):
+            one_step(evs[i], early_J=J)
+        end.record(stream)
+        torch.cuda.synchronize()
+        res["early_sum"].append(dict(
+            J=J, calls_per_step=-(-w.K // J) + 1, ms_per_step=start.elapsed_time(end) / n,
+            dense_ms=float(np.mean([e["d0"].elapsed_time(e["d1"]) for e in evs])),
+            running_sum_bytes=w.P * 8, buffered_gradient_bytes_saved=w.K * w.P * 4 - w.P * 8))
+    if int(st.err.item()) != 0:
+        raise RuntimeError(f"device error bits {int(st.err.item())}")
     del ds, st
     torch.cuda.empty_cache()
     return res
@@ -318,6 +363,7 @@ def main():
         "breakdown_ms": head["breakdown_ms"],
         "realised": {k: head[k] for k in ("K_eff", "N", "N_act", "U", "U_act", "step_alg_bytes")},
         "roofline": head["roofline"],
+        "early_weighted_sum": head["early_sum"],
         "other_workloads": others,
     }
     if not args.no_cpu_baseline:

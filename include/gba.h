@@ -50,8 +50,7 @@ enum {
   GBA_DERR_ID_RANGE = 1,      /* an embedding ID outside [0, R)                    */
   GBA_DERR_FUTURE_TOKEN = 2,  /* a token newer than the step being applied         */
   GBA_DERR_OFFSETS = 4,       /* contribution offsets not 0 .. N and non-decreasing */
-  GBA_DERR_ROW_RANGE = 8,     /* a row index passed to a sparse apply outside [0, R) */
-  GBA_DERR_INTERNAL = 16      /* a bounded wait between tiles gave up (outputs invalid) */
+  GBA_DERR_ROW_RANGE = 8      /* a row index passed to a sparse apply outside [0, R) */
 };
 
 /* How embedding gradients are decayed (Alg. 2). */
@@ -189,6 +188,43 @@ gba_status gba_aggregate_apply_dense_adam(const float* const* grads, const float
                                           int64_t P, float* out, float* param, float* m, float* v,
                                           double lr, double beta1, double beta2, double eps,
                                           int64_t t, hipStream_t stream);
+
+/*
+ * Early weighted sum of the dense gradients (App. B, with Alg. 2: the weighted
+ * sum can be taken over some gradients in advance, from their tokens).  The
+ * weight of a contribution depends only on its token and the step it will be
+ * applied at, both known when it arrives, so it can be folded into a running
+ * sum right away and the buffer holds P doubles instead of K gradients.
+ *
+ * gba_accumulate_dense: run[i] += w_j * g_j[i] for j = 0..J-1 in order, in
+ * float64, skipping w_j == 0 (such gradients are never read).
+ *   grads  device array of J gradient pointers, each [P] float.
+ *   w      [J] float device weights (for example gba_token_weights of the J tokens).
+ *   run    [P] double, device, caller-owned; all zero before the first
+ *          contribution of a step (gba_finalize_* with reset != 0 leaves it so).
+ *   1 <= J <= GBA_MAX_K.
+ * gba_finalize_dense: out[i] = (float)(run[i] / K), K = the step's number of
+ * contributions; run is cleared when reset != 0.
+ * gba_finalize_apply_dense_*: the same sum, then the dense optimiser as in
+ * gba_apply_adagrad / gba_apply_adam; out may be NULL.
+ * Folding the contributions in buffer order, in any grouping into calls,
+ * gives bitwise the results of gba_aggregate_dense / _apply_dense_* over the
+ * whole buffer.  A 32-byte-aligned run and 16-byte-aligned arrays take the
+ * vector path; others work, more slowly.
+ */
+gba_status gba_accumulate_dense(const float* const* grads, const float* w, int32_t J, int64_t P,
+                                double* run, hipStream_t stream);
+
+gba_status gba_finalize_dense(double* run, int32_t K, int64_t P, float* out, int32_t reset,
+                              hipStream_t stream);
+
+gba_status gba_finalize_apply_dense_adagrad(double* run, int32_t K, int64_t P, float* out,
+                                            float* param, float* accum, double lr, double eps,
+                                            int32_t reset, hipStream_t stream);
+
+gba_status gba_finalize_apply_dense_adam(double* run, int32_t K, int64_t P, float* out, float* param,
+                                         float* m, float* v, double lr, double beta1, double beta2,
+                                         double eps, int64_t t, int32_t reset, hipStream_t stream);
 
 #ifdef __cplusplus
 }

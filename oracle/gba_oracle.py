@@ -16,6 +16,8 @@ recommendation models" (arXiv 2205.11048).
   token, decay embedding gradients by the ID tag and the token, sum the dense
   gradients with the weights and divide by N_a, sum the embedding gradients
   with the weights and divide by the number of workers that encountered the ID.
+* App. B (workflows of GBA): the weighted sum may be taken over some
+  gradients in advance, from their tokens (the early weighted sum).
 * Table 1 (Sec. 4.1): GBA runs with Adam; the asynchronous baseline with
   Adagrad.  The update rules are the textbook ones (Duchi, Hazan and Singer,
   JMLR 2011; Kingma and Ba, ICLR 2015), since the paper names them only.
@@ -45,6 +47,12 @@ design notes of the repository, with its reason):
       dense vector and for rows (rows are updated lazily).
 * R8  A token newer than the step being applied (tau_m > k) cannot occur by
       construction; it is an error.
+* R9  The early weighted sum folds each arriving dense gradient, with its
+      token weight for the step it will be applied at, into a float64 running
+      sum in arrival order; the buffer order is the arrival order, so the
+      result equals the one-shot sum bit for bit.  Embedding rows are kept as
+      they arrive (their buffer is already O(sum of n_m D)) and reduced at the
+      step.
 """
 from __future__ import annotations
 
@@ -98,6 +106,28 @@ def aggregate_dense_magnitude(grads, w):
         if w[m] != 0:
             acc += abs(np.float64(w[m])) * np.abs(np.asarray(grads[m], dtype=np.float64))
     return acc / K
+
+
+# --------------------------------------------------------------------------
+# App. B: the early weighted sum (contributions folded in as they arrive)
+# --------------------------------------------------------------------------
+def accumulate_dense(run, grads, w):
+    """Fold arriving contributions into the float64 running sum, in arrival
+    order: run += w_j * g_j for every j with w_j != 0 (App. B notes that the
+    weighted sum may be taken over some gradients in advance, from their
+    tokens; a weight depends only on the token and the step it is applied at).
+    ``run`` is updated in place and returned."""
+    for j in range(len(grads)):
+        if w[j] != 0:                               # excluded: never read (R2)
+            run += np.float64(w[j]) * np.asarray(grads[j], dtype=np.float64)
+    return run
+
+
+def finalize_dense(run, K: int):
+    """g_bar = run / K, rounded to float32 once (Alg. 2's divisor N_a = K)."""
+    if K <= 0:
+        raise ValueError("K must be positive")
+    return (run / K).astype(np.float32)
 
 
 # --------------------------------------------------------------------------

@@ -16,9 +16,10 @@ import torch
 __all__ = [
     "GBAError", "lib", "gba_token_weights", "gba_aggregate_dense", "gba_aggregate_sparse",
     "gba_aggregate_sparse_workspace_size", "gba_apply_adagrad", "gba_apply_adam",
-    "gba_aggregate_apply_dense_adagrad", "gba_aggregate_apply_dense_adam",
+    "gba_aggregate_apply_dense_adagrad", "gba_aggregate_apply_dense_adam", "gba_accumulate_dense",
+    "gba_finalize_dense", "gba_finalize_apply_dense_adagrad", "gba_finalize_apply_dense_adam",
     "pointer_table", "DECAY_TOKEN", "DECAY_ID_TAG", "NORM_PER_ID_COUNT", "NORM_BY_K",
-    "DERR_ID_RANGE", "DERR_FUTURE_TOKEN", "DERR_OFFSETS", "DERR_ROW_RANGE", "DERR_INTERNAL", "MAX_K", "MAX_D",
+    "DERR_ID_RANGE", "DERR_FUTURE_TOKEN", "DERR_OFFSETS", "DERR_ROW_RANGE", "MAX_K", "MAX_D",
     "LIB_PATH",
 ]
 
@@ -29,7 +30,7 @@ LIB_PATH = os.environ.get("GBA_LIBRARY") or os.path.join(os.path.dirname(os.path
 
 DECAY_TOKEN, DECAY_ID_TAG = 0, 1
 NORM_PER_ID_COUNT, NORM_BY_K = 0, 1
-DERR_ID_RANGE, DERR_FUTURE_TOKEN, DERR_OFFSETS, DERR_ROW_RANGE, DERR_INTERNAL = 1, 2, 4, 8, 16
+DERR_ID_RANGE, DERR_FUTURE_TOKEN, DERR_OFFSETS, DERR_ROW_RANGE = 1, 2, 4, 8
 MAX_K, MAX_D = 4096, 256
 
 _P = ctypes.c_void_p
@@ -47,6 +48,11 @@ _SIGNATURES = {
     "gba_aggregate_apply_dense_adagrad": ([_P, _P, _I32, _I64, _P, _P, _P, _F64, _F64, _P], _I32),
     "gba_aggregate_apply_dense_adam": ([_P, _P, _I32, _I64, _P, _P, _P, _P, _F64, _F64, _F64, _F64, _I64, _P],
                                        _I32),
+    "gba_accumulate_dense": ([_P, _P, _I32, _I64, _P, _P], _I32),
+    "gba_finalize_dense": ([_P, _I32, _I64, _P, _I32, _P], _I32),
+    "gba_finalize_apply_dense_adagrad": ([_P, _I32, _I64, _P, _P, _P, _F64, _F64, _I32, _P], _I32),
+    "gba_finalize_apply_dense_adam": ([_P, _I32, _I64, _P, _P, _P, _P, _F64, _F64, _F64, _F64, _I64, _I32, _P],
+                                      _I32),
     "gba_apply_adagrad": ([_P, _P, _P, _P, _P, _P, _I64, _I32, _I64, _F64, _F64, _P, _P], _I32),
     "gba_apply_adam": ([_P, _P, _P, _P, _P, _P, _P, _I64, _I32, _I64, _F64, _F64, _F64, _F64, _I64,
                         _P, _P], _I32),
@@ -151,6 +157,42 @@ def gba_aggregate_apply_dense_adam(grads, w, P, param, m, v, lr, beta1, beta2, e
     _check(lib().gba_aggregate_apply_dense_adam(_ptr(grads), _ptr(w), K, int(P), _ptr(out), _ptr(param), _ptr(m),
                                                 _ptr(v), float(lr), float(beta1), float(beta2), float(eps), int(t),
                                                 _stream(stream)))
+
+
+def gba_accumulate_dense(grads, w, P, run, stream=None):
+    """Early weighted sum: run += sum_j w_j g_j in float64, in order.
+    ``grads``: device int64 tensor of J gradient pointers; ``run``: float64 [P]."""
+    J = grads.numel()
+    _need(grads, torch.int64, "grads")
+    _need(w, torch.float32, "w", J)
+    _need(run, torch.float64, "run", P)
+    _check(lib().gba_accumulate_dense(_ptr(grads), _ptr(w), J, int(P), _ptr(run), _stream(stream)))
+
+
+def gba_finalize_dense(run, K, P, out, reset=True, stream=None):
+    _need(run, torch.float64, "run", P)
+    _need(out, torch.float32, "out", P)
+    _check(lib().gba_finalize_dense(_ptr(run), int(K), int(P), _ptr(out), int(bool(reset)), _stream(stream)))
+
+
+def gba_finalize_apply_dense_adagrad(run, K, P, param, accum, lr, eps, out=None, reset=True, stream=None):
+    _need(run, torch.float64, "run", P)
+    _need(out, torch.float32, "out", P)
+    for name, x in (("param", param), ("accum", accum)):
+        _need(x, torch.float32, name, P)
+    _check(lib().gba_finalize_apply_dense_adagrad(_ptr(run), int(K), int(P), _ptr(out), _ptr(param), _ptr(accum),
+                                                  float(lr), float(eps), int(bool(reset)), _stream(stream)))
+
+
+def gba_finalize_apply_dense_adam(run, K, P, param, m, v, lr, beta1, beta2, eps, t, out=None, reset=True,
+                                  stream=None):
+    _need(run, torch.float64, "run", P)
+    _need(out, torch.float32, "out", P)
+    for name, x in (("param", param), ("m", m), ("v", v)):
+        _need(x, torch.float32, name, P)
+    _check(lib().gba_finalize_apply_dense_adam(_ptr(run), int(K), int(P), _ptr(out), _ptr(param), _ptr(m), _ptr(v),
+                                               float(lr), float(beta1), float(beta2), float(eps), int(t),
+                                               int(bool(reset)), _stream(stream)))
 
 
 def gba_aggregate_sparse_workspace_size(N, K, D, R) -> int:

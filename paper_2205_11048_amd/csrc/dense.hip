@@ -60,9 +60,10 @@ __device__ __forceinline__ int build_kept_list(const float* const* grads, const 
 
 // What the reduction does with each finished element g = sum / K: store it
 // (kStoreOnly), and/or apply Adagrad or Adam to the dense parameters right
-// away, which spares the round trip of g through memory.  In the apply modes
-// `out` may be null.
-enum DenseMode : int { kStoreOnly = 0, kApplyAdagrad = 1, kApplyAdam = 2 };
+// away, which spares the round trip of g through memory (in the apply modes
+// `out` may be null); or, for the early weighted sum, nothing yet: the
+// float64 running sum is stored back (kAccumulate).
+enum DenseMode : int { kStoreOnly = 0, kApplyAdagrad = 1, kApplyAdam = 2, kAccumulate = 3 };
 struct DenseState {
   float* p;
   float* s1;   // Adagrad accumulator or Adam m
@@ -84,6 +85,21 @@ __device__ __forceinline__ void finish_element(float g, int64_t e, float* out, c
     st.p[e] = pe;
     st.s1[e] = me;
     st.s2[e] = ve;
+  }
+}
+
+// One element, for the last P % 4 and for buffers that are not 16-byte aligned.
+template <int MODE, bool CARRY>
+__device__ __forceinline__ void finish_scalar(const float* const* grads, const uint16_t* kept, const float* kw,
+                                              int nk, int64_t e, float* out, const DenseState& st,
+                                              double* run, double denom, int reset) {
+  double acc = CARRY ? run[e] : 0.0;
+  for (int i = 0; i < nk; ++i) acc += (double)kw[i] * (double)grads[kept[i]][e];
+  if (MODE == kAccumulate) {
+    run[e] = acc;
+  } else {
+    finish_element<MODE>((float)(acc / denom), e, out, st);
+    if (CARRY && reset) run[e] = 0.0;
   }
 }
 
@@ -141,20 +157,26 @@ __device__ __forceinline__ void finish_vectors(const f64x4* acc, double denom, i
   }
 }
 
-template <int MODE>
+// The weighted sum of the kept gradients, added in buffer order to a float64
+// running sum that starts at 0 (the whole buffer at once) or at run[] (the
+// early weighted sum, CARRY: contributions folded in as they arrive, in
+// arrival order, so the result is bitwise the one-shot sum).  Then the
+// MODE's finishing; with CARRY, `reset` clears run[] for the next step.
+template <int MODE, bool CARRY>
 __global__ void __launch_bounds__(kDenseBlock)
 aggregate_dense_kernel(const float* const* __restrict__ grads, const float* __restrict__ w, int K,
-                       int64_t P, float* __restrict__ out, DenseState st) {
+                       int64_t P, float* __restrict__ out, DenseState st, double* __restrict__ run,
+                       double denom, int reset) {
   __shared__ uint16_t kept[GBA_MAX_K];
   __shared__ float kw[GBA_MAX_K];
   __shared__ uint32_t tmp[kDenseBlock / kWave + 1];
   __shared__ int aligned;
   const int nk = build_kept_list(grads, w, K, kept, kw, tmp, &aligned);
-  const double denom = (double)K;
   const int64_t stride = (int64_t)gridDim.x * kDenseBlock;
   const bool outputs_aligned = ((reinterpret_cast<uintptr_t>(out) | reinterpret_cast<uintptr_t>(st.p) |
                                  reinterpret_cast<uintptr_t>(st.s1) | reinterpret_cast<uintptr_t>(st.s2)) &
-                                15u) == 0;   // null pointers count as aligned
+                                15u) == 0 &&
+                               (reinterpret_cast<uintptr_t>(run) & 31u) == 0;   // null pointers count as aligned
   if (aligned && outputs_aligned) {
     const int64_t nvec = P / 4;
     for (int64_t b0 = (int64_t)blockIdx.x * kDenseSpan; b0 < nvec; b0 += (int64_t)gridDim.x * kDenseSpan) {
@@ -162,7 +184,10 @@ aggregate_dense_kernel(const float* const* __restrict__ grads, const float* __re
       const int64_t vb = b0 + (int64_t)(threadIdx.x / kWave) * (kWave * kDenseVecs) + (threadIdx.x % kWave);
       f64x4 acc[kDenseVecs];
 #pragma unroll
-      for (int j = 0; j < kDenseVecs; ++j) acc[j] = f64x4{0.0, 0.0, 0.0, 0.0};
+      for (int j = 0; j < kDenseVecs; ++j) {
+        acc[j] = f64x4{0.0, 0.0, 0.0, 0.0};
+        if (CARRY && vb + kWave * j < nvec) acc[j] = reinterpret_cast<const f64x4*>(run)[vb + kWave * j];
+      }
       for (int i = 0; i < nk; ++i) {
         const f32x4* g = reinterpret_cast<const f32x4*>(grads[kept[i]]) + vb;
         f32x4 x[kDenseVecs];
@@ -173,60 +198,96 @@ aggregate_dense_kernel(const float* const* __restrict__ grads, const float* __re
 #pragma unroll
         for (int j = 0; j < kDenseVecs; ++j) acc[j] += wi * widen(x[j]);
       }
-      finish_vectors<MODE>(acc, denom, vb, nvec, out, st);
+      if (MODE == kAccumulate) {
+#pragma unroll
+        for (int j = 0; j < kDenseVecs; ++j)
+          if (vb + kWave * j < nvec) reinterpret_cast<f64x4*>(run)[vb + kWave * j] = acc[j];
+      } else {
+        finish_vectors<MODE>(acc, denom, vb, nvec, out, st);
+        if (CARRY && reset) {
+#pragma unroll
+          for (int j = 0; j < kDenseVecs; ++j)
+            if (vb + kWave * j < nvec) reinterpret_cast<f64x4*>(run)[vb + kWave * j] = f64x4{0.0, 0.0, 0.0, 0.0};
+        }
+      }
     }
     // the last P % 4 elements
     const int64_t tail0 = nvec * 4;
-    if (blockIdx.x == 0 && threadIdx.x < P - tail0) {
-      const int64_t e = tail0 + threadIdx.x;
-      double acc = 0.0;
-      for (int i = 0; i < nk; ++i) acc += (double)kw[i] * (double)grads[kept[i]][e];
-      finish_element<MODE>((float)(acc / denom), e, out, st);
-    }
+    if (blockIdx.x == 0 && threadIdx.x < P - tail0)
+      finish_scalar<MODE, CARRY>(grads, kept, kw, nk, tail0 + threadIdx.x, out, st, run, denom, reset);
   } else {
-    for (int64_t e = (int64_t)blockIdx.x * kDenseBlock + threadIdx.x; e < P; e += stride) {
-      double acc = 0.0;
-      for (int i = 0; i < nk; ++i) acc += (double)kw[i] * (double)grads[kept[i]][e];
-      finish_element<MODE>((float)(acc / denom), e, out, st);
-    }
+    for (int64_t e = (int64_t)blockIdx.x * kDenseBlock + threadIdx.x; e < P; e += stride)
+      finish_scalar<MODE, CARRY>(grads, kept, kw, nk, e, out, st, run, denom, reset);
   }
 }
 
-template <int MODE>
+template <int MODE, bool CARRY>
 static hipError_t launch_dense_mode(const float* const* grads, const float* w, int32_t K, int64_t P,
-                                    float* out, const DenseState& st, hipStream_t stream) {
+                                    float* out, const DenseState& st, double* run, double denom, int reset,
+                                    hipStream_t stream) {
   if (P <= 0) return hipSuccess;
   // one block step per block where possible; unaligned buffers fall back to
   // a grid-stride loop over single elements
   int64_t blocks = ceil_div(ceil_div(P, 4), kDenseSpan);
   if (blocks > kDenseMaxBlocks) blocks = kDenseMaxBlocks;
   if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(aggregate_dense_kernel<MODE>, dim3((unsigned)blocks), dim3(kDenseBlock), 0, stream,
-                     grads, w, (int)K, P, out, st);
+  hipLaunchKernelGGL((aggregate_dense_kernel<MODE, CARRY>), dim3((unsigned)blocks), dim3(kDenseBlock), 0, stream,
+                     grads, w, (int)K, P, out, st, run, denom, reset);
   return hipGetLastError();
 }
 
 hipError_t launch_aggregate_dense(const float* const* grads, const float* w, int32_t K, int64_t P,
                                   float* out, hipStream_t stream) {
-  return launch_dense_mode<kStoreOnly>(grads, w, K, P, out, DenseState{}, stream);
+  return launch_dense_mode<kStoreOnly, false>(grads, w, K, P, out, DenseState{}, nullptr, (double)K, 0, stream);
 }
 
-hipError_t launch_aggregate_apply_dense_adagrad(const float* const* grads, const float* w, int32_t K,
-                                                int64_t P, float* out, float* p, float* a, double lr,
-                                                double eps, hipStream_t stream) {
+static DenseState adagrad_state(float* p, float* a, double lr, double eps) {
   DenseState st{};
   st.p = p;
   st.s1 = a;
   st.lr = lr;
   st.eps = eps;
-  return launch_dense_mode<kApplyAdagrad>(grads, w, K, P, out, st, stream);
+  return st;
+}
+
+static DenseState adam_state(float* p, float* m, float* v, const AdamParams& hp) {
+  return DenseState{p, m, v, hp.lr, hp.eps, hp.beta1, hp.beta2, hp.bc1, hp.bc2};
+}
+
+hipError_t launch_aggregate_apply_dense_adagrad(const float* const* grads, const float* w, int32_t K,
+                                                int64_t P, float* out, float* p, float* a, double lr,
+                                                double eps, hipStream_t stream) {
+  return launch_dense_mode<kApplyAdagrad, false>(grads, w, K, P, out, adagrad_state(p, a, lr, eps), nullptr,
+                                                 (double)K, 0, stream);
 }
 
 hipError_t launch_aggregate_apply_dense_adam(const float* const* grads, const float* w, int32_t K,
                                              int64_t P, float* out, float* p, float* m, float* v,
                                              const AdamParams& hp, hipStream_t stream) {
-  DenseState st{p, m, v, hp.lr, hp.eps, hp.beta1, hp.beta2, hp.bc1, hp.bc2};
-  return launch_dense_mode<kApplyAdam>(grads, w, K, P, out, st, stream);
+  return launch_dense_mode<kApplyAdam, false>(grads, w, K, P, out, adam_state(p, m, v, hp), nullptr, (double)K, 0,
+                                              stream);
+}
+
+hipError_t launch_accumulate_dense(const float* const* grads, const float* w, int32_t J, int64_t P, double* run,
+                                   hipStream_t stream) {
+  return launch_dense_mode<kAccumulate, true>(grads, w, J, P, nullptr, DenseState{}, run, 1.0, 0, stream);
+}
+
+hipError_t launch_finalize_dense(double* run, int32_t K, int64_t P, float* out, int reset, hipStream_t stream) {
+  return launch_dense_mode<kStoreOnly, true>(nullptr, nullptr, 0, P, out, DenseState{}, run, (double)K, reset,
+                                             stream);
+}
+
+hipError_t launch_finalize_apply_dense_adagrad(double* run, int32_t K, int64_t P, float* out, float* p, float* a,
+                                               double lr, double eps, int reset, hipStream_t stream) {
+  return launch_dense_mode<kApplyAdagrad, true>(nullptr, nullptr, 0, P, out, adagrad_state(p, a, lr, eps), run,
+                                                (double)K, reset, stream);
+}
+
+hipError_t launch_finalize_apply_dense_adam(double* run, int32_t K, int64_t P, float* out, float* p, float* m,
+                                            float* v, const AdamParams& hp, int reset, hipStream_t stream) {
+  return launch_dense_mode<kApplyAdam, true>(nullptr, nullptr, 0, P, out, adam_state(p, m, v, hp), run, (double)K,
+                                             reset, stream);
 }
 
 // ---------------------------------------------------------------- optimisers

@@ -91,6 +91,40 @@ gba_status gba_aggregate_apply_dense_adam(const float* const* grads, const float
                                                     adam_params(lr, beta1, beta2, eps, t), stream));
 }
 
+gba_status gba_accumulate_dense(const float* const* grads, const float* w, int32_t J, int64_t P, double* run,
+                                hipStream_t stream) {
+  if (J < 1 || J > GBA_MAX_K || P < 0) return GBA_ERR_INVALID_ARG;
+  if (P == 0) return GBA_OK;
+  if (!grads || !w || !run) return GBA_ERR_NULL;
+  return from_hip(launch_accumulate_dense(grads, w, J, P, run, stream));
+}
+
+gba_status gba_finalize_dense(double* run, int32_t K, int64_t P, float* out, int32_t reset, hipStream_t stream) {
+  if (K < 1 || P < 0) return GBA_ERR_INVALID_ARG;
+  if (P == 0) return GBA_OK;
+  if (!run || !out) return GBA_ERR_NULL;
+  return from_hip(launch_finalize_dense(run, K, P, out, reset != 0, stream));
+}
+
+gba_status gba_finalize_apply_dense_adagrad(double* run, int32_t K, int64_t P, float* out, float* param,
+                                            float* accum, double lr, double eps, int32_t reset,
+                                            hipStream_t stream) {
+  if (K < 1 || P < 0) return GBA_ERR_INVALID_ARG;
+  if (P == 0) return GBA_OK;
+  if (!run || !param || !accum) return GBA_ERR_NULL;
+  return from_hip(launch_finalize_apply_dense_adagrad(run, K, P, out, param, accum, lr, eps, reset != 0, stream));
+}
+
+gba_status gba_finalize_apply_dense_adam(double* run, int32_t K, int64_t P, float* out, float* param, float* m,
+                                         float* v, double lr, double beta1, double beta2, double eps, int64_t t,
+                                         int32_t reset, hipStream_t stream) {
+  if (K < 1 || P < 0 || !adam_args_ok(beta1, beta2, t)) return GBA_ERR_INVALID_ARG;
+  if (P == 0) return GBA_OK;
+  if (!run || !param || !m || !v) return GBA_ERR_NULL;
+  return from_hip(launch_finalize_apply_dense_adam(run, K, P, out, param, m, v,
+                                                   adam_params(lr, beta1, beta2, eps, t), reset != 0, stream));
+}
+
 gba_status gba_aggregate_sparse_workspace_size(int64_t N, int32_t K, int32_t D, int64_t R,
                                                size_t* bytes) {
   if (!bytes) return GBA_ERR_NULL;

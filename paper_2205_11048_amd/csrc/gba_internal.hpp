@@ -35,6 +35,15 @@ hipError_t launch_dense_adam(float* p, float* m, float* v, const float* g, int64
 hipError_t launch_aggregate_apply_dense_adam(const float* const* grads, const float* w, int32_t K,
                                              int64_t P, float* out, float* p, float* m, float* v,
                                              const AdamParams& hp, hipStream_t stream);
+// early weighted sum: fold J gradients into the float64 running sum run[P];
+// then finish (divide by K, optionally apply) and optionally clear run
+hipError_t launch_accumulate_dense(const float* const* grads, const float* w, int32_t J, int64_t P, double* run,
+                                   hipStream_t stream);
+hipError_t launch_finalize_dense(double* run, int32_t K, int64_t P, float* out, int reset, hipStream_t stream);
+hipError_t launch_finalize_apply_dense_adagrad(double* run, int32_t K, int64_t P, float* out, float* p, float* a,
+                                               double lr, double eps, int reset, hipStream_t stream);
+hipError_t launch_finalize_apply_dense_adam(double* run, int32_t K, int64_t P, float* out, float* p, float* m,
+                                            float* v, const AdamParams& hp, int reset, hipStream_t stream);
 hipError_t launch_rows_adagrad(float* p, float* a, const float* g, const int64_t* rows,
                                const int32_t* active, const int64_t* num_rows, int64_t n, int32_t D,
                                int64_t R, double lr, double eps, int32_t* err, hipStream_t stream);

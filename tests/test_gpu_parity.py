@@ -491,3 +491,69 @@ def test_fused_dense_host_checks():
                                             None, 1e-3, 0.9, 0.999, 1e-8, 1, st) == 1
     torch.cuda.synchronize()
     assert np.all(host(p) == 0) and np.all(host(a) == 1)
+
+
+# ------------------------------------------------ early weighted sum (App. B)
+@pytest.mark.parametrize("opt", [None, "adagrad", "adam"])
+@pytest.mark.parametrize("K,P,groups,offset", [(1, 5, [1], 0), (37, 100_003, [5, 1, 31], 0),
+                                               (9, 4096 * 16 * 3 + 7, [3, 3, 3], 0), (64, 70_001, [64], 1),
+                                               (200, 8193, [100, 99, 1], 0)])
+def test_early_sum_matches_one_shot(opt, K, P, groups, offset):
+    """Folding the contributions in as they arrive, in any grouping into calls,
+    gives bitwise the one-shot sum (and parameters and state when the
+    optimiser is applied at the end), and the oracle's running sum."""
+    assert sum(groups) == K
+    rng = np.random.default_rng(K + P)
+    host_g = [counter.values_range(12, 900 + m, 0, P, counter.KIND_GRAD, counter.grad_scale(1e-2)) for m in range(K)]
+    tokens = 70 - rng.integers(0, 7, K)
+    w, _, _ = oracle.token_weights(tokens, 70, 4)
+    grads = [dev_at(g if w[m] != 0 else np.full(P, np.nan, np.float32), offset) for m, g in enumerate(host_g)]
+    run = torch.zeros(P, dtype=torch.float64, device=DEV)
+    lo = 0
+    for n in groups:
+        gba.gba_accumulate_dense(gba.pointer_table(grads[lo:lo + n]), dev(w[lo:lo + n]), P, run)
+        lo += n
+    ref_run = oracle.accumulate_dense(np.zeros(P, np.float64), host_g, w)
+    assert_exact(host(run), ref_run, "running sum vs oracle")
+    table, w_d = gba.pointer_table(grads), dev(w)
+    if opt is None:
+        out, one_shot = torch.empty(P, device=DEV), torch.empty(P, device=DEV)
+        gba.gba_finalize_dense(run, K, P, out, reset=True)
+        gba.gba_aggregate_dense(table, w_d, P, one_shot)
+        assert_exact(host(out), host(one_shot), "g_bar vs one-shot")
+        assert_exact(host(out), oracle.finalize_dense(ref_run, K), "g_bar vs oracle")
+        assert not host(run).any(), "reset leaves the running sum at zero"
+        return
+    p0 = counter.values_range(13, 1, 0, P, counter.KIND_PARAM)
+    kinds = workload.state_kinds(opt)
+    s0 = [counter.values_range(13, 2 + k, 0, P, kind) for k, (_, _, kind) in enumerate(kinds)]
+    pa, sa, pb, sb = dev(p0), [dev(x) for x in s0], dev(p0), [dev(x) for x in s0]
+    out = torch.full((P,), float("nan"), device=DEV)
+    if opt == "adagrad":
+        gba.gba_finalize_apply_dense_adagrad(run, K, P, pa, sa[0], 0.01, 1e-8, out=out, reset=False)
+        gba.gba_aggregate_apply_dense_adagrad(table, w_d, P, pb, sb[0], 0.01, 1e-8)
+    else:
+        gba.gba_finalize_apply_dense_adam(run, K, P, pa, sa[0], sa[1], 1e-3, 0.9, 0.999, 1e-8, 1001, out=out,
+                                          reset=False)
+        gba.gba_aggregate_apply_dense_adam(table, w_d, P, pb, sb[0], sb[1], 1e-3, 0.9, 0.999, 1e-8, 1001)
+    assert_exact(host(pa), host(pb), "param")
+    for k in range(len(sa)):
+        assert_exact(host(sa[k]), host(sb[k]), f"state {k}")
+    assert_exact(host(out), oracle.finalize_dense(ref_run, K), "g_bar vs oracle")
+    assert_exact(host(run), ref_run, "reset=False keeps the running sum")
+
+
+def test_early_sum_host_checks():
+    P = 8
+    g = [torch.ones(P, device=DEV)]
+    table, w = gba.pointer_table(g), torch.ones(1, device=DEV)
+    run = torch.zeros(P, dtype=torch.float64, device=DEV)
+    L = gba.lib()
+    st = torch.cuda.current_stream().cuda_stream
+    assert L.gba_accumulate_dense(table.data_ptr(), w.data_ptr(), 0, P, run.data_ptr(), st) == 2
+    assert L.gba_accumulate_dense(table.data_ptr(), w.data_ptr(), 1, P, None, st) == 1
+    assert L.gba_finalize_dense(run.data_ptr(), 0, P, run.data_ptr(), 1, st) == 2
+    assert L.gba_finalize_apply_dense_adam(run.data_ptr(), 4, P, None, run.data_ptr(), run.data_ptr(), None, 1e-3,
+                                           0.9, 0.999, 1e-8, 1, 1, st) == 1
+    torch.cuda.synchronize()
+    assert not host(run).any()

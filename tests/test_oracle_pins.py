@@ -361,3 +361,38 @@ def test_adam_constant_gradient_closed_form():
     for t in range(1, T + 1):
         p, m, v = oracle.adam(p, m, v, g, lr, 0.9, 0.999, eps, t)
     np.testing.assert_allclose(p, 1.0 - T * lr * g / (np.abs(g) + eps), rtol=1e-6)
+
+
+# ------------------------------------------------------------------ App. B
+@pytest.mark.parametrize("seed", range(6))
+def test_early_sum_equals_exact_rational_mean(seed):
+    """Folding dyadic contributions in as they arrive, in any grouping, gives
+    the exact weighted sum / K (computed here in rational arithmetic)."""
+    rng = np.random.default_rng(seed)
+    K, P = int(rng.integers(1, 12)), int(rng.integers(1, 9))
+    grads = [counter.values_range(seed, 700 + m, 0, P, counter.KIND_DYADIC) for m in range(K)]
+    w = (rng.random(K) < 0.7).astype(np.float32)
+    run = np.zeros(P, np.float64)
+    cuts = np.sort(rng.choice(np.arange(1, K), size=min(K - 1, int(rng.integers(0, 4))), replace=False)) \
+        if K > 1 else np.zeros(0, int)
+    for lo, hi in zip(np.r_[0, cuts], np.r_[cuts, K]):
+        oracle.accumulate_dense(run, grads[lo:hi], w[lo:hi])
+    got = oracle.finalize_dense(run, K)
+    for i in range(P):
+        exact = sum(Fraction(float(w[m])) * Fraction(float(grads[m][i])) for m in range(K)) / K
+        assert got[i] == np.float32(float(exact)), (i, got[i], exact)
+
+
+def test_early_sum_is_bitwise_the_one_shot_sum_and_skips_excluded():
+    """Arrival order is buffer order, so the running sum is the one-shot sum
+    bit for bit (non-dyadic values too); an excluded gradient is never read."""
+    rng = np.random.default_rng(3)
+    K, P = 37, 1001
+    grads = [counter.values_range(9, 800 + m, 0, P, counter.KIND_GRAD, counter.grad_scale(1e-2)) for m in range(K)]
+    tokens = 50 - rng.integers(0, 6, K)
+    w, _, _ = oracle.token_weights(tokens, 50, 3)
+    poisoned = [g if w[m] != 0 else np.full(P, np.nan, np.float32) for m, g in enumerate(grads)]
+    run = np.zeros(P, np.float64)
+    for lo in range(0, K, 5):
+        oracle.accumulate_dense(run, poisoned[lo:lo + 5], w[lo:lo + 5])
+    assert np.array_equal(oracle.finalize_dense(run, K), oracle.aggregate_dense(grads, w))
