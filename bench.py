@@ -265,6 +265,30 @@ def run_workload(name, args, torch, gba_step_mod, sdev, gba):
             J=J, calls_per_step=-(-w.K // J) + 1, ms_per_step=start.elapsed_time(end) / n,
             dense_ms=float(np.mean([e["d0"].elapsed_time(e["d1"]) for e in evs])),
             running_sum_bytes=w.P * 8, buffered_gradient_bytes_saved=w.K * w.P * 4 - w.P * 8))
+    # pull side: one worker's request (the IDs of one contribution), rows looked
+    # up once per distinct ID
+    n_req = int(ds.offsets_host[1] - ds.offsets_host[0])
+    req = ds.ids[:n_req]
+    pu = torch.empty(n_req, dtype=torch.int64, device="cuda")
+    pinv = torch.empty(n_req, dtype=torch.int32, device="cuda")
+    prows = torch.empty((n_req, w.D), dtype=torch.float32, device="cuda")
+    pnu = torch.zeros(1, dtype=torch.int64, device="cuda")
+    pws = torch.empty(gba.gba_pull_workspace_size(n_req, w.R), dtype=torch.uint8, device="cuda")
+    for _ in range(3):
+        gba.gba_pull_rows(req, ds.table, pu, pinv, prows, pnu, pws, st.err)
+    torch.cuda.synchronize()
+    n_pull = 20
+    start.record(stream)
+    for _ in range(n_pull):
+        gba.gba_pull_rows(req, ds.table, pu, pinv, prows, pnu, pws, st.err)
+    end.record(stream)
+    torch.cuda.synchronize()
+    pull_ms = start.elapsed_time(end) / n_pull
+    U_req = int(pnu.item())
+    pull_bytes = n_req * 8 + U_req * w.D * 4 * 2 + U_req * 8 + n_req * 4
+    res["pull"] = dict(ids_per_request=n_req, distinct=U_req, us_per_request=pull_ms * 1e3,
+                       requests_per_s=1e3 / pull_ms, alg_gbs=pull_bytes / (pull_ms * 1e-3) / 1e9)
+    del pu, pinv, prows, pws
     if int(st.err.item()) != 0:
         raise RuntimeError(f"device error bits {int(st.err.item())}")
     del ds, st
@@ -364,6 +388,7 @@ def main():
         "realised": {k: head[k] for k in ("K_eff", "N", "N_act", "U", "U_act", "step_alg_bytes")},
         "roofline": head["roofline"],
         "early_weighted_sum": head["early_sum"],
+        "pull": head["pull"],
         "other_workloads": others,
     }
     if not args.no_cpu_baseline:

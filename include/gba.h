@@ -226,6 +226,36 @@ gba_status gba_finalize_apply_dense_adam(double* run, int32_t K, int64_t P, floa
                                          float* m, float* v, double lr, double beta1, double beta2,
                                          double eps, int64_t t, int32_t reset, hipStream_t stream);
 
+/*
+ * Pull side (Sec. 3.1 token list; Alg. 2, pull responder).
+ *
+ * gba_token_of_batch (host function, no device work): the token handed out
+ * with the i-th batch of the data list, t_i = floor(i / M) with M = K the
+ * number of gradients aggregated per step: tokens start at 0 and each value
+ * repeats M times, in ascending order.  (The paper prints floor(i / K) with K
+ * the number of updates, which contradicts "each value repeats M times"; the
+ * repetition rule is the one followed.)  Returns -1 if i < 0 or M < 1.
+ *
+ * gba_pull_rows: the embedding rows for a worker's request, looked up once per
+ * distinct ID.
+ *   ids         [n] int64 IDs in [0, R) of the request (16-byte aligned).
+ *   table       [R][D] float embedding rows (16-byte aligned).
+ *   unique_ids  [U] int64 out, the distinct IDs ascending (size it for n).
+ *   inverse     [n] int32 out, ids[i] == unique_ids[inverse[i]].
+ *   rows        [U][D] float out, rows[s] = table[unique_ids[s]] (16-byte aligned).
+ *   num_unique  one int64 out, U.
+ *   workspace   device scratch of gba_pull_workspace_size bytes.
+ *   err         GBA_DERR_ID_RANGE for an ID outside [0, R) (outputs then undefined).
+ * Limits: 0 <= n < 2^28, 1 <= R <= 2^32, D % 4 == 0 and 4 <= D <= GBA_MAX_D.
+ */
+int64_t gba_token_of_batch(int64_t i, int32_t M);
+
+gba_status gba_pull_workspace_size(int64_t n, int64_t R, size_t* bytes /* host out */);
+
+gba_status gba_pull_rows(const int64_t* ids, int64_t n, int64_t R, const float* table, int32_t D,
+                         int64_t* unique_ids, int32_t* inverse, float* rows, int64_t* num_unique,
+                         void* workspace, size_t workspace_bytes, int32_t* err, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -53,6 +53,9 @@ design notes of the repository, with its reason):
       result equals the one-shot sum bit for bit.  Embedding rows are kept as
       they arrive (their buffer is already O(sum of n_m D)) and reduced at the
       step.
+* R10 The token of the i-th batch is floor(i / M): the text says each token
+      value repeats M times and the values ascend, while the printed formula
+      divides by K, the number of updates; the repetition rule is followed.
 """
 from __future__ import annotations
 
@@ -243,6 +246,26 @@ def aggregate_sparse_occurrences(ids, m_of_j, rows, K: int, w, tokens, step: int
         new_tag[unique_ids[active_count > 0]] = step
         out["new_tag"] = new_tag
     return out
+
+
+# --------------------------------------------------------------------------
+# Sec. 3.1 token list and Alg. 2 pull responder
+# --------------------------------------------------------------------------
+def token_of_batch(i: int, M: int) -> int:
+    """Token attached to the i-th batch of the data list: values start at 0
+    and each repeats M times, in ascending order (Sec. 3.1; R10)."""
+    if i < 0 or M < 1:
+        raise ValueError("i >= 0 and M >= 1 required")
+    return i // M
+
+
+def pull_rows(ids, table):
+    """Rows of a worker's request, looked up once per distinct ID (Alg. 2,
+    pull responder): the distinct IDs ascending, for each request position
+    the index of its ID among them, and the table rows of the distinct IDs."""
+    ids = np.asarray(ids, dtype=np.int64)
+    unique_ids, inverse = np.unique(ids, return_inverse=True)
+    return unique_ids, inverse.astype(np.int32), np.asarray(table)[unique_ids]
 
 
 # --------------------------------------------------------------------------

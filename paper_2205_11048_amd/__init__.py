@@ -18,6 +18,7 @@ __all__ = [
     "gba_aggregate_sparse_workspace_size", "gba_apply_adagrad", "gba_apply_adam",
     "gba_aggregate_apply_dense_adagrad", "gba_aggregate_apply_dense_adam", "gba_accumulate_dense",
     "gba_finalize_dense", "gba_finalize_apply_dense_adagrad", "gba_finalize_apply_dense_adam",
+    "gba_token_of_batch", "gba_pull_workspace_size", "gba_pull_rows",
     "pointer_table", "DECAY_TOKEN", "DECAY_ID_TAG", "NORM_PER_ID_COUNT", "NORM_BY_K",
     "DERR_ID_RANGE", "DERR_FUTURE_TOKEN", "DERR_OFFSETS", "DERR_ROW_RANGE", "MAX_K", "MAX_D",
     "LIB_PATH",
@@ -53,6 +54,9 @@ _SIGNATURES = {
     "gba_finalize_apply_dense_adagrad": ([_P, _I32, _I64, _P, _P, _P, _F64, _F64, _I32, _P], _I32),
     "gba_finalize_apply_dense_adam": ([_P, _I32, _I64, _P, _P, _P, _P, _F64, _F64, _F64, _F64, _I64, _I32, _P],
                                       _I32),
+    "gba_token_of_batch": ([_I64, _I32], _I64),
+    "gba_pull_workspace_size": ([_I64, _I64, ctypes.POINTER(ctypes.c_size_t)], _I32),
+    "gba_pull_rows": ([_P, _I64, _I64, _P, _I32, _P, _P, _P, _P, _P, ctypes.c_size_t, _P, _P], _I32),
     "gba_apply_adagrad": ([_P, _P, _P, _P, _P, _P, _I64, _I32, _I64, _F64, _F64, _P, _P], _I32),
     "gba_apply_adam": ([_P, _P, _P, _P, _P, _P, _P, _I64, _I32, _I64, _F64, _F64, _F64, _F64, _I64,
                         _P, _P], _I32),
@@ -193,6 +197,34 @@ def gba_finalize_apply_dense_adam(run, K, P, param, m, v, lr, beta1, beta2, eps,
     _check(lib().gba_finalize_apply_dense_adam(_ptr(run), int(K), int(P), _ptr(out), _ptr(param), _ptr(m), _ptr(v),
                                                float(lr), float(beta1), float(beta2), float(eps), int(t),
                                                int(bool(reset)), _stream(stream)))
+
+
+def gba_token_of_batch(i, M) -> int:
+    """Token of the i-th batch handed out: floor(i / M), each value M times."""
+    return int(lib().gba_token_of_batch(int(i), int(M)))
+
+
+def gba_pull_workspace_size(n, R) -> int:
+    b = ctypes.c_size_t(0)
+    _check(lib().gba_pull_workspace_size(int(n), int(R), ctypes.byref(b)))
+    return int(b.value)
+
+
+def gba_pull_rows(ids, table, unique_ids, inverse, rows, num_unique, workspace, err=None, stream=None):
+    """Rows of a worker's request, once per distinct ID: table[unique_ids] and
+    the inverse map (ids == unique_ids[inverse])."""
+    n = ids.numel()
+    R, D = table.shape
+    _need(ids, torch.int64, "ids")
+    _need(table, torch.float32, "table")
+    _need(unique_ids, torch.int64, "unique_ids", n)
+    _need(inverse, torch.int32, "inverse", n)
+    _need(rows, torch.float32, "rows", n * D)
+    _need(num_unique, torch.int64, "num_unique", 1)
+    _need(workspace, torch.uint8, "workspace")
+    _need(err, torch.int32, "err", 1)
+    _check(lib().gba_pull_rows(_ptr(ids), n, int(R), _ptr(table), int(D), _ptr(unique_ids), _ptr(inverse), _ptr(rows),
+                               _ptr(num_unique), _ptr(workspace), workspace.numel(), _ptr(err), _stream(stream)))
 
 
 def gba_aggregate_sparse_workspace_size(N, K, D, R) -> int:

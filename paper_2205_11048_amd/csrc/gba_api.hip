@@ -194,6 +194,49 @@ gba_status gba_aggregate_sparse(const int64_t* ids, const float* rows, const int
   return from_hip(launch_segments(a, ws + align_up(plan.bytes), stream));
 }
 
+int64_t gba_token_of_batch(int64_t i, int32_t M) {
+  if (i < 0 || M < 1) return -1;
+  return i / M;
+}
+
+gba_status gba_pull_workspace_size(int64_t n, int64_t R, size_t* bytes) {
+  if (!bytes) return GBA_ERR_NULL;
+  if (n < 0 || n > kMaxN || R < 1 || R > (int64_t(1) << 32)) return GBA_ERR_INVALID_ARG;
+  *bytes = align_up(plan_sort(n, R).bytes) + align_up(pull_workspace_bytes(n));
+  return GBA_OK;
+}
+
+gba_status gba_pull_rows(const int64_t* ids, int64_t n, int64_t R, const float* table, int32_t D,
+                         int64_t* unique_ids, int32_t* inverse, float* rows, int64_t* num_unique, void* workspace,
+                         size_t workspace_bytes, int32_t* err, hipStream_t stream) {
+  if (n < 0 || n > kMaxN || R < 1 || R > (int64_t(1) << 32)) return GBA_ERR_INVALID_ARG;
+  if (!width_ok(D)) return GBA_ERR_UNSUPPORTED;
+  if (!num_unique || !workspace) return GBA_ERR_NULL;
+  if (n > 0 && (!ids || !table || !unique_ids || !inverse || !rows)) return GBA_ERR_NULL;
+  if ((ids && !aligned16(ids)) || (table && !aligned16(table)) || (rows && !aligned16(rows)) ||
+      !aligned16(workspace))
+    return GBA_ERR_INVALID_ARG;
+  const SortPlan plan = plan_sort(n, R);
+  if (workspace_bytes < align_up(plan.bytes) + align_up(pull_workspace_bytes(n))) return GBA_ERR_WORKSPACE;
+  char* ws = static_cast<char*>(workspace);
+  const uint32_t* keys = nullptr;
+  const uint32_t* vals = nullptr;
+  hipError_t e = launch_sort_ids(ids, n, R, plan, ws, &keys, &vals, err, stream);
+  if (e != hipSuccess) return GBA_ERR_HIP;
+  PullArgs a;
+  a.keys = keys;
+  a.vals = vals;
+  a.n = n;
+  a.R = R;
+  a.table = table;
+  a.D = D;
+  a.unique_ids = unique_ids;
+  a.inverse = inverse;
+  a.rows = rows;
+  a.num_unique = num_unique;
+  return from_hip(launch_pull(a, ws + align_up(plan.bytes), stream));
+}
+
 gba_status gba_apply_adagrad(float* param, float* accum, const float* grad, const int64_t* rows,
                              const int32_t* active, const int64_t* num_rows, int64_t n, int32_t D,
                              int64_t R, double lr, double eps, int32_t* err, hipStream_t stream) {

@@ -95,4 +95,26 @@ struct SegmentArgs {
 size_t segments_workspace_bytes(int64_t N, int32_t D);
 hipError_t launch_segments(const SegmentArgs& a, void* ws, hipStream_t stream);
 
+// ---- runs of equal keys in sorted keys[N]: per 1024-position tile, the number
+// of runs that start before it (tile_base[ceil(N/1024)]); *total = number of runs
+constexpr int64_t kRunTile = 1024;
+size_t run_heads_workspace_bytes(int64_t N);
+hipError_t launch_run_heads(const uint32_t* keys, int64_t N, uint32_t* tile_base, uint32_t* total, void* scan_ws,
+                            hipStream_t stream);
+
+// ---- pull side: distinct IDs of a worker's request, the inverse map, the rows
+struct PullArgs {
+  const uint32_t* keys;   // sorted IDs [n]
+  const uint32_t* vals;   // request position of each sorted entry [n]
+  int64_t n, R;
+  const float* table;     // [R][D]
+  int32_t D;
+  int64_t* unique_ids;    // [U] ascending
+  int32_t* inverse;       // [n] index into unique_ids of each request position
+  float* rows;            // [U][D]
+  int64_t* num_unique;
+};
+size_t pull_workspace_bytes(int64_t n);
+hipError_t launch_pull(const PullArgs& a, void* ws, hipStream_t stream);
+
 }  // namespace gba

@@ -30,6 +30,7 @@ constexpr int kSegBlock = 256;
 constexpr int kSegWaves = kSegBlock / kWave;                 // 4
 constexpr int kRounds = 4;                                   // positions per lane in seg_meta
 constexpr int64_t kMetaTile = (int64_t)kSegBlock * kRounds;  // 1024 positions
+static_assert(kMetaTile == kRunTile, "run-head tiles are the per-position tiles");
 constexpr int kGroupSpan = 128;                              // positions per lane group in seg_rows
 constexpr int kBatch = 8;                                    // row gathers in flight per group
 constexpr int kMaxBuckets = 1024;                            // contribution lookup buckets
@@ -88,7 +89,7 @@ static SegLayout seg_layout(int64_t N, int32_t D) {
   size_t o = 0;
   L.off_heads = o;     o += align_up(mt * 4);
   L.off_total = o;     o += 256;                     // head total
-  L.off_scan = o;      o += align_up(scan_workspace_bytes(L.meta_tiles));
+  L.off_scan = o;      o += align_up(run_heads_workspace_bytes(N));
   L.off_buckets = o;   o += align_up(kMaxBuckets * 4);
   L.off_packed = o;    o += align_up((n + kGroupSpan) * 4);   // padded: whole-group vector loads stay inside
   L.off_base32 = o;    o += align_up((n / kGroupSpan + 2) * 4);
@@ -574,6 +575,22 @@ tag_update_kernel(const int64_t* __restrict__ unique_ids, const int32_t* __restr
     if (active_count[s] > 0) tag[unique_ids[s]] = step;
 }
 
+size_t run_heads_workspace_bytes(int64_t N) {
+  return scan_workspace_bytes(N > 0 ? ceil_div(N, kMetaTile) : 1);
+}
+
+hipError_t launch_run_heads(const uint32_t* keys, int64_t N, uint32_t* tile_base, uint32_t* total, void* scan_ws,
+                            hipStream_t stream) {
+  const int64_t tiles = N > 0 ? ceil_div(N, kMetaTile) : 0;
+  if (N > 0) {
+    hipLaunchKernelGGL(seg_heads_kernel, dim3((unsigned)ceil_div(tiles, kSegWaves)), dim3(kSegBlock), 0, stream,
+                       keys, N, tiles, tile_base);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return launch_exclusive_scan_u32(tile_base, tile_base, tiles, total, scan_ws, stream);
+}
+
 template <int LPR>
 static hipError_t launch_rows(const SegmentArgs& a, const uint32_t* packed, const uint32_t* base32,
                               SegPartials part, int64_t tiles, hipStream_t stream) {
@@ -608,12 +625,7 @@ hipError_t launch_segments(const SegmentArgs& a, void* ws, hipStream_t stream) {
   hipLaunchKernelGGL(check_offsets_kernel, dim3(1), dim3(256), 0, stream, a.offsets, a.K, a.N, a.err);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (a.N > 0) {
-    hipLaunchKernelGGL(seg_heads_kernel, dim3((unsigned)ceil_div(L.meta_tiles, kSegWaves)),
-                       dim3(kSegBlock), 0, stream, a.keys, a.N, L.meta_tiles, heads);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-  }
-  e = launch_exclusive_scan_u32(heads, heads, a.N > 0 ? L.meta_tiles : 0, total, scan_ws, stream);
+  e = launch_run_heads(a.keys, a.N, heads, total, scan_ws, stream);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(seg_finish_kernel, dim3(1), dim3(1), 0, stream, (const uint32_t*)total, a.N,
                      a.num_unique, a.seg_offsets);

@@ -58,3 +58,12 @@ def test_host_checks_return_before_any_launch():
     assert L.gba_apply_adagrad(None, None, None, None, None, None, 0, 0, 0, 0.1, 0.0, None, None) == 0
     assert L.gba_apply_adam(None, None, None, None, None, None, None, 10, 0, 0, 0.1, 0.9, 0.999, 0.0, 0,
                             None, None) == 2
+
+
+def test_token_of_batch_host_function():
+    """The token rule is a host function of the library: no GPU needed."""
+    import oracle
+    for M in (1, 4, 32):
+        for i in (0, 1, M - 1, M, 5 * M + 2):
+            assert gba.gba_token_of_batch(i, M) == oracle.token_of_batch(i, M)
+    assert gba.gba_token_of_batch(-1, 4) == -1 and gba.gba_token_of_batch(3, 0) == -1

@@ -557,3 +557,66 @@ def test_early_sum_host_checks():
                                            0.9, 0.999, 1e-8, 1, 1, st) == 1
     torch.cuda.synchronize()
     assert not host(run).any()
+
+
+# ------------------------------------------------ pull side (Alg. 2 pull responder)
+def _pull(ids, table_d, R):
+    n = ids.size
+    D = table_d.shape[1]
+    cap = max(n, 1)
+    out = dict(u=torch.full((cap,), -5, dtype=torch.int64, device=DEV),
+               inv=torch.full((cap,), -5, dtype=torch.int32, device=DEV),
+               rows=torch.full((cap, D), float("nan"), device=DEV),
+               nu=torch.full((1,), -5, dtype=torch.int64, device=DEV))
+    ws = torch.empty(gba.gba_pull_workspace_size(n, R), dtype=torch.uint8, device=DEV)
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    ids_d = dev(ids) if n else torch.empty(0, dtype=torch.int64, device=DEV)
+    gba.gba_pull_rows(ids_d, table_d, out["u"], out["inv"], out["rows"], out["nu"], ws, err)
+    return {k: host(v) for k, v in out.items()}, int(host(err)[0])
+
+
+@pytest.mark.parametrize("n,R,D,kind", [(0, 10, 4, "zipf"), (1, 10, 4, "zipf"), (1023, 3000, 16, "zipf"),
+                                        (1025, 3000, 32, "zipf"), (256_000, 500_000_000 // 1000, 32, "zipf"),
+                                        (70_001, 100_000, 64, "distinct"), (50_000, 50, 256, "zipf"),
+                                        (40_000, 1 << 20, 8, "one")])
+def test_pull_rows(n, R, D, kind):
+    rng = np.random.default_rng(n + D)
+    if kind == "zipf":
+        from synth.zipf import ZipfRejectionInversion, rank_to_row
+        ids = rank_to_row(ZipfRejectionInversion(R, 1.1).ranks(n + 1, np.arange(n)) - 1, R).astype(np.int64) \
+            if n else np.zeros(0, np.int64)
+    elif kind == "distinct":
+        ids = rng.permutation(R)[:n].astype(np.int64)
+    else:
+        ids = np.full(n, R - 1, np.int64)
+    table = counter.values_range(n + 1, counter.STREAM_TABLE, 0, R * D, counter.KIND_PARAM).reshape(R, D)
+    got, err = _pull(ids, dev(table), R)
+    assert err == 0
+    u, inv, rows = oracle.pull_rows(ids, table)
+    U = int(got["nu"][0])
+    assert U == u.size
+    assert_exact(got["u"][:U], u, "unique_ids")
+    assert_exact(got["inv"][:n], inv, "inverse")
+    assert_exact(got["rows"][:U], rows, "rows")
+
+
+def test_pull_rows_reports_out_of_range_ids():
+    R, D = 100, 4
+    ids = np.array([3, 100, 7, -1, 3], np.int64)
+    _, err = _pull(ids, torch.zeros((R, D), device=DEV), R)
+    assert err & gba.DERR_ID_RANGE
+
+
+def test_pull_rows_host_checks():
+    L = gba.lib()
+    t = torch.zeros((10, 6), device=DEV)          # D = 6 is not a multiple of 4
+    ids = torch.zeros(4, dtype=torch.int64, device=DEV)
+    nu = torch.zeros(1, dtype=torch.int64, device=DEV)
+    ws = torch.empty(gba.gba_pull_workspace_size(4, 10), dtype=torch.uint8, device=DEV)
+    st = torch.cuda.current_stream().cuda_stream
+    assert L.gba_pull_rows(ids.data_ptr(), 4, 10, t.data_ptr(), 6, t.data_ptr(), t.data_ptr(), t.data_ptr(),
+                           nu.data_ptr(), ws.data_ptr(), ws.numel(), None, st) == 3
+    assert L.gba_pull_rows(ids.data_ptr(), 4, 10, t.data_ptr(), 4, None, t.data_ptr(), t.data_ptr(),
+                           nu.data_ptr(), ws.data_ptr(), ws.numel(), None, st) == 1
+    assert L.gba_pull_rows(ids.data_ptr(), 4, 10, t.data_ptr(), 4, t.data_ptr(), t.data_ptr(), t.data_ptr(),
+                           nu.data_ptr(), ws.data_ptr(), 16, None, st) == 4

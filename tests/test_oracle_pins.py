@@ -396,3 +396,30 @@ def test_early_sum_is_bitwise_the_one_shot_sum_and_skips_excluded():
     for lo in range(0, K, 5):
         oracle.accumulate_dense(run, poisoned[lo:lo + 5], w[lo:lo + 5])
     assert np.array_equal(oracle.finalize_dense(run, K), oracle.aggregate_dense(grads, w))
+
+
+# ------------------------------------------------- Sec. 3.1, Alg. 2 pull side
+def test_token_list_repeats_each_value_m_times_in_ascending_order():
+    """Sec. 3.1: tokens start from zero, each value repeats M times, and the
+    list ascends; with Q batches there are ceil(Q / M) distinct values."""
+    for M in (1, 3, 4, 64):
+        Q = 10 * M + 3
+        toks = [oracle.token_of_batch(i, M) for i in range(Q)]
+        assert toks[0] == 0 and all(b - a in (0, 1) for a, b in zip(toks, toks[1:]))
+        values, counts = np.unique(toks, return_counts=True)
+        assert values.size == -(-Q // M)
+        assert np.all(counts[:-1] == M) and counts[-1] == Q - M * (values.size - 1)
+
+
+@pytest.mark.parametrize("n,R", [(1, 5), (50, 7), (1000, 100_000), (500, 1)])
+def test_pull_rows_reconstructs_the_request(n, R):
+    """Looking rows up once per distinct ID loses nothing: rows[inverse] is
+    the plain per-position lookup, and the distinct IDs are sorted and unique."""
+    rng = np.random.default_rng(n)
+    ids = rng.integers(0, R, n).astype(np.int64)
+    table = rng.standard_normal((R, 4)).astype(np.float32)
+    u, inv, rows = oracle.pull_rows(ids, table)
+    assert np.all(np.diff(u) > 0)
+    assert np.array_equal(u[inv], ids)
+    assert np.array_equal(rows[inv], table[ids])
+    assert set(u.tolist()) == set(ids.tolist())
