@@ -2,8 +2,8 @@
 // gradients divided by N_a (Alg. 2), and the elementwise optimiser updates
 // (Adagrad, Adam; Table 1 names them), separately or fused.
 //
-// The reduction streams K_eff * P floats from HBM.  A block owns 64 KB of
-// the output at a time; each of its waves reads 16 KB of one gradient as 16
+// The reduction streams K_eff * P floats from HBM.  A block of 8 waves owns
+// 128 KB of the output at a time; each wave reads 16 KB of one gradient as 16
 // consecutive 1 KB loads before moving to the next gradient, so the memory
 // system sees long contiguous runs per gradient wherever the caller placed
 // the K buffers (short runs from many buffers at once were measured to lose
@@ -16,9 +16,10 @@
 
 namespace gba {
 
-constexpr int kDenseBlock = 256;
+constexpr int kDenseBlock = 256;                                      // elementwise optimiser kernels
+constexpr int kSumBlock = 512;                                        // the reduction: 8 waves
 constexpr int kDenseVecs = 16;                                        // f32x4 per thread
-constexpr int64_t kDenseSpan = (int64_t)kDenseBlock * kDenseVecs;     // vectors per block step
+constexpr int64_t kDenseSpan = (int64_t)kSumBlock * kDenseVecs;       // vectors per block step
 constexpr int64_t kDenseMaxBlocks = 65535;
 constexpr int64_t kApplyMaxBlocks = 8192;
 
@@ -30,7 +31,7 @@ static inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 __device__ __forceinline__ int build_kept_list(const float* const* grads, const float* w, int K,
                                                uint16_t* kept, float* kw, uint32_t* tmp,
                                                int* aligned) {
-  constexpr int kPer = (GBA_MAX_K + kDenseBlock - 1) / kDenseBlock;
+  constexpr int kPer = (GBA_MAX_K + kSumBlock - 1) / kSumBlock;
   const int lo = threadIdx.x * kPer;
   uint32_t c = 0;
   bool al = true;
@@ -45,7 +46,7 @@ __device__ __forceinline__ int build_kept_list(const float* const* grads, const 
   __syncthreads();
   if (!al) *aligned = 0;
   uint32_t total;
-  uint32_t pos = block_exclusive_scan<kDenseBlock>(c, tmp, &total);
+  uint32_t pos = block_exclusive_scan<kSumBlock>(c, tmp, &total);
   for (int k = 0; k < kPer; ++k) {
     const int m = lo + k;
     if (m < K && w[m] != 0.0f) {
@@ -163,16 +164,16 @@ __device__ __forceinline__ void finish_vectors(const f64x4* acc, double denom, i
 // arrival order, so the result is bitwise the one-shot sum).  Then the
 // MODE's finishing; with CARRY, `reset` clears run[] for the next step.
 template <int MODE, bool CARRY>
-__global__ void __launch_bounds__(kDenseBlock)
+__global__ void __launch_bounds__(kSumBlock)
 aggregate_dense_kernel(const float* const* __restrict__ grads, const float* __restrict__ w, int K,
                        int64_t P, float* __restrict__ out, DenseState st, double* __restrict__ run,
                        double denom, int reset) {
   __shared__ uint16_t kept[GBA_MAX_K];
   __shared__ float kw[GBA_MAX_K];
-  __shared__ uint32_t tmp[kDenseBlock / kWave + 1];
+  __shared__ uint32_t tmp[kSumBlock / kWave + 1];
   __shared__ int aligned;
   const int nk = build_kept_list(grads, w, K, kept, kw, tmp, &aligned);
-  const int64_t stride = (int64_t)gridDim.x * kDenseBlock;
+  const int64_t stride = (int64_t)gridDim.x * kSumBlock;
   const bool outputs_aligned = ((reinterpret_cast<uintptr_t>(out) | reinterpret_cast<uintptr_t>(st.p) |
                                  reinterpret_cast<uintptr_t>(st.s1) | reinterpret_cast<uintptr_t>(st.s2)) &
                                 15u) == 0 &&
@@ -216,7 +217,7 @@ aggregate_dense_kernel(const float* const* __restrict__ grads, const float* __re
     if (blockIdx.x == 0 && threadIdx.x < P - tail0)
       finish_scalar<MODE, CARRY>(grads, kept, kw, nk, tail0 + threadIdx.x, out, st, run, denom, reset);
   } else {
-    for (int64_t e = (int64_t)blockIdx.x * kDenseBlock + threadIdx.x; e < P; e += stride)
+    for (int64_t e = (int64_t)blockIdx.x * kSumBlock + threadIdx.x; e < P; e += stride)
       finish_scalar<MODE, CARRY>(grads, kept, kw, nk, e, out, st, run, denom, reset);
   }
 }
@@ -231,7 +232,7 @@ static hipError_t launch_dense_mode(const float* const* grads, const float* w, i
   int64_t blocks = ceil_div(ceil_div(P, 4), kDenseSpan);
   if (blocks > kDenseMaxBlocks) blocks = kDenseMaxBlocks;
   if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL((aggregate_dense_kernel<MODE, CARRY>), dim3((unsigned)blocks), dim3(kDenseBlock), 0, stream,
+  hipLaunchKernelGGL((aggregate_dense_kernel<MODE, CARRY>), dim3((unsigned)blocks), dim3(kSumBlock), 0, stream,
                      grads, w, (int)K, P, out, st, run, denom, reset);
   return hipGetLastError();
 }
