@@ -40,14 +40,14 @@ rows_apply_kernel(float* __restrict__ p, float* __restrict__ s1, float* __restri
     }
     for (int c = lane * 4; c < D; c += LPR * 4) {
       const int64_t at = r * (int64_t)D + c;
-      const f32x4 pv = *reinterpret_cast<const f32x4*>(p + at);
-      const f32x4 av = *reinterpret_cast<const f32x4*>(s1 + at);
-      const f32x4 gv = *reinterpret_cast<const f32x4*>(g + i * (int64_t)D + c);
+      const f32x4 pv = load_stream(reinterpret_cast<const f32x4*>(p + at));
+      const f32x4 av = load_stream(reinterpret_cast<const f32x4*>(s1 + at));
+      const f32x4 gv = load_stream(reinterpret_cast<const f32x4*>(g + i * (int64_t)D + c));
       float pe[4] = {pv.x, pv.y, pv.z, pv.w};
       float ae[4] = {av.x, av.y, av.z, av.w};
       const float ge[4] = {gv.x, gv.y, gv.z, gv.w};
       if (ADAM) {
-        const f32x4 vv = *reinterpret_cast<const f32x4*>(s2 + at);
+        const f32x4 vv = load_stream(reinterpret_cast<const f32x4*>(s2 + at));
         float ve[4] = {vv.x, vv.y, vv.z, vv.w};
 #pragma unroll
         for (int k = 0; k < 4; ++k) adam_update(pe[k], ae[k], ve[k], ge[k], lr, b1, b2, eps, bc1, bc2);
