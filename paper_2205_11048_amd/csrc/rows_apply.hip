@@ -4,8 +4,10 @@
 // not updated at this global step; Alg. 2 updates embeddings by ID).
 //
 // A group of LPR lanes owns one row at a time and moves it as 16-byte
-// vectors; the grid is persistent and reads the row count from device memory,
-// so no host round trip sits between the aggregation and the apply.
+// non-temporal vectors (every row, state and gradient is touched once, so the
+// L2 is left to the kernels that reuse lines); the grid is persistent and
+// reads the row count from device memory, so no host round trip sits between
+// the aggregation and the apply.
 #include "gba_device.hpp"
 #include "gba_internal.hpp"
 #include "optim.hpp"
@@ -51,13 +53,13 @@ rows_apply_kernel(float* __restrict__ p, float* __restrict__ s1, float* __restri
         float ve[4] = {vv.x, vv.y, vv.z, vv.w};
 #pragma unroll
         for (int k = 0; k < 4; ++k) adam_update(pe[k], ae[k], ve[k], ge[k], lr, b1, b2, eps, bc1, bc2);
-        *reinterpret_cast<f32x4*>(s2 + at) = f32x4{ve[0], ve[1], ve[2], ve[3]};
+        store_stream(reinterpret_cast<f32x4*>(s2 + at), f32x4{ve[0], ve[1], ve[2], ve[3]});
       } else {
 #pragma unroll
         for (int k = 0; k < 4; ++k) adagrad_update(pe[k], ae[k], ge[k], lr, eps);
       }
-      *reinterpret_cast<f32x4*>(p + at) = f32x4{pe[0], pe[1], pe[2], pe[3]};
-      *reinterpret_cast<f32x4*>(s1 + at) = f32x4{ae[0], ae[1], ae[2], ae[3]};
+      store_stream(reinterpret_cast<f32x4*>(p + at), f32x4{pe[0], pe[1], pe[2], pe[3]});
+      store_stream(reinterpret_cast<f32x4*>(s1 + at), f32x4{ae[0], ae[1], ae[2], ae[3]});
     }
   }
   if (bad) raise_error(err, GBA_DERR_ROW_RANGE);

@@ -154,7 +154,7 @@ __device__ __forceinline__ void finalize_segment(const SegmentArgs& a, int64_t s
   if (seg < 0 || seg >= a.N) return;   // unreachable when the numbering is consistent
   const double div = (a.norm == GBA_NORM_BY_K) ? (double)a.K : (double)cc;
   if (lane_on)
-    *reinterpret_cast<f32x4*>(a.agg + seg * (int64_t)a.D + lane * 4) = narrow(acc / div);
+    store_stream(reinterpret_cast<f32x4*>(a.agg + seg * (int64_t)a.D + lane * 4), narrow(acc / div));   // read once, by the apply
   if (lane == 0) {
     a.contrib_count[seg] = cc;
     a.active_count[seg] = ww;
