@@ -51,6 +51,8 @@ def parse():
     ap.add_argument("--early-sum", default="16",
                     help="comma list of J: also time the step with the dense sum taken early, J arriving "
                          "contributions folded per call ('' for none)")
+    ap.add_argument("--no-hash-storage", dest="hash_storage", action="store_false",
+                    help="skip the leg that runs the step on storage keyed by 64-bit IDs")
     ap.add_argument("--cpu-sample", type=int, default=4, help="1/S of the workload for the oracle timing")
     return ap.parse_args()
 
@@ -265,6 +267,11 @@ def run_workload(name, args, torch, gba_step_mod, sdev, gba):
             J=J, calls_per_step=-(-w.K // J) + 1, ms_per_step=start.elapsed_time(end) / n,
             dense_ms=float(np.mean([e["d0"].elapsed_time(e["d1"]) for e in evs])),
             running_sum_bytes=w.P * 8, buffered_gradient_bytes_saved=w.K * w.P * 4 - w.P * 8))
+    # storage keyed by 64-bit IDs: the same step with the IDs scrambled over the
+    # whole 64-bit range and mapped to rows of a pool by the hash index first
+    if args.hash_storage:
+        res["hash_storage"] = hash_leg(w, ds, st, gba, torch, stream, decay, start, end, max(3, args.steps // 2))
+
     # pull side: one worker's request (the IDs of one contribution), rows looked
     # up once per distinct ID
     n_req = int(ds.offsets_host[1] - ds.offsets_host[0])
@@ -294,6 +301,61 @@ def run_workload(name, args, torch, gba_step_mod, sdev, gba):
     del ds, st
     torch.cuda.empty_cache()
     return res
+
+
+def hash_leg(w, ds, st, gba, torch, stream, decay, start, end, n):
+    """Time the step on storage keyed by 64-bit IDs; after the first step every
+    ID is known, so the timed steps look IDs up without inserting."""
+    ids64 = ds.ids * -0x61C8864680B583EB + 12345          # a bijection of the 64-bit range
+    cap = 1 << max(20, (2 * w.N - 1).bit_length() - 2)   # index for N/2 distinct IDs at load <= 0.5
+    slot_ids = torch.empty(cap, dtype=torch.int64, device="cuda")
+    slot_rows = torch.empty(cap, dtype=torch.int32, device="cuda")
+    gba.gba_hash_clear(slot_ids, slot_rows)
+    pool_rows = min(cap // 2, w.R)     # rows of the pool (the table's first rows); index load <= 0.5
+    num_rows = torch.zeros(1, dtype=torch.int64, device="cuda")
+    rows_of = torch.empty(w.N, dtype=torch.int64, device="cuda")
+    hws = torch.empty(gba.gba_hash_workspace_size(w.N), dtype=torch.uint8, device="cuda")
+    sws = torch.empty(gba.gba_aggregate_sparse_workspace_size(w.N, w.K, w.D, pool_rows), dtype=torch.uint8,
+                      device="cuda")
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+
+    def step(e=None):
+        gba.gba_token_weights(ds.tokens, ds.step, w.iota, st.w, st.staleness, st.num_excluded, st.err)
+        if w.optimizer == "adagrad":
+            gba.gba_aggregate_apply_dense_adagrad(st.grad_table(ds.grads), st.w, w.P, ds.param, ds.dense_slots[0],
+                                                  w.lr, w.eps)
+        else:
+            gba.gba_aggregate_apply_dense_adam(st.grad_table(ds.grads), st.w, w.P, ds.param, ds.dense_slots[0],
+                                               ds.dense_slots[1], w.lr, w.beta1, w.beta2, w.eps, w.adam_t)
+        if e is not None:
+            e[0].record(stream)
+        gba.gba_hash_find_or_insert(slot_ids, slot_rows, ids64, rows_of, num_rows, pool_rows, hws, err=st.err)
+        if e is not None:
+            e[1].record(stream)
+        gba.gba_aggregate_sparse(rows_of, ds.rows, ds.offsets, pool_rows, st.w, ds.tokens, ds.step, w.iota,
+                                 ds.tags, decay, gba.NORM_PER_ID_COUNT, st.unique_ids, st.seg_offsets,
+                                 st.contrib_count, st.active_count, st.agg, st.num_unique, sws, st.err)
+        if w.optimizer == "adagrad":
+            gba.gba_apply_adagrad(ds.table, ds.table_slots[0], st.agg, w.lr, w.eps, rows=st.unique_ids,
+                                  active=st.active_count, num_rows=st.num_unique, R=pool_rows, err=st.err)
+        else:
+            gba.gba_apply_adam(ds.table, ds.table_slots[0], ds.table_slots[1], st.agg, w.lr, w.beta1, w.beta2, w.eps,
+                               w.adam_t, rows=st.unique_ids, active=st.active_count, num_rows=st.num_unique,
+                               R=pool_rows, err=st.err)
+
+    for _ in range(2):
+        step()
+    torch.cuda.synchronize()
+    start.record(stream)
+    for i in range(n):
+        step(ev[i])
+    end.record(stream)
+    torch.cuda.synchronize()
+    if int(st.err.item()) != 0:
+        raise RuntimeError(f"device error bits {int(st.err.item())} on the hash-storage leg")
+    return dict(index_capacity=cap, pool_rows=pool_rows, rows_in_use=int(num_rows.item()),
+                ms_per_step=start.elapsed_time(end) / n,
+                find_or_insert_ms=float(np.mean([a.elapsed_time(b) for a, b in ev])))
 
 
 def cpu_baseline(name, S):
@@ -389,6 +451,7 @@ def main():
         "roofline": head["roofline"],
         "early_weighted_sum": head["early_sum"],
         "pull": head["pull"],
+        "hash_storage": head.get("hash_storage"),
         "other_workloads": others,
     }
     if not args.no_cpu_baseline:

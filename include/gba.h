@@ -50,7 +50,8 @@ enum {
   GBA_DERR_ID_RANGE = 1,      /* an embedding ID outside [0, R)                    */
   GBA_DERR_FUTURE_TOKEN = 2,  /* a token newer than the step being applied         */
   GBA_DERR_OFFSETS = 4,       /* contribution offsets not 0 .. N and non-decreasing */
-  GBA_DERR_ROW_RANGE = 8      /* a row index passed to a sparse apply outside [0, R) */
+  GBA_DERR_ROW_RANGE = 8,     /* a row index passed to a sparse apply outside [0, R) */
+  GBA_DERR_TABLE_FULL = 16    /* the ID index or the row pool has no room left      */
 };
 
 /* How embedding gradients are decayed (Alg. 2). */
@@ -255,6 +256,53 @@ gba_status gba_pull_workspace_size(int64_t n, int64_t R, size_t* bytes /* host o
 gba_status gba_pull_rows(const int64_t* ids, int64_t n, int64_t R, const float* table, int32_t D,
                          int64_t* unique_ids, int32_t* inverse, float* rows, int64_t* num_unique,
                          void* workspace, size_t workspace_bytes, int32_t* err, hipStream_t stream);
+
+/*
+ * Embedding storage keyed by 64-bit IDs (the paper's PS keeps embeddings in
+ * expandable hash tables keyed by feature ID; Sec. 4.1 setting).  An
+ * open-addressing index maps an ID to a row of a row pool; the push and pull
+ * paths then run on row numbers (pass them as `ids`, with R = the pool size).
+ *   slot_ids   [capacity] int64, the ID held by each slot (GBA_EMPTY_ID: free).
+ *   slot_rows  [capacity] int32, the row of the ID in that slot.
+ *   capacity   a power of two, <= 2^31; keep the load below about 0.7 and grow
+ *              with gba_hash_rehash.
+ * The ID value GBA_EMPTY_ID is reserved.  IDs are never removed.
+ *
+ * gba_hash_clear: every slot free (a fill kernel; no memset is recorded).
+ *
+ * gba_hash_find_or_insert: rows_out[i] = the row of ids[i]; an ID not yet in
+ * the index gets a slot and the next free row of the pool.  The rows handed
+ * out by one call are [old *num_rows, new *num_rows), in no particular order
+ * of IDs; the caller initialises them (values and optimiser state) before the
+ * step reads them.
+ *   num_rows   one int64 on the device: rows in use (read and advanced).
+ *   max_rows   size of the row pool (<= 2^31 - 1).
+ *   row_ids    [max_rows] int64 out, row -> ID for the new rows; may be NULL.
+ *   num_new    one int64 out on the device: IDs inserted by this call; may be NULL.
+ *   workspace  gba_hash_workspace_size(n) bytes.
+ *   err        GBA_DERR_ID_RANGE for an ID equal to GBA_EMPTY_ID,
+ *              GBA_DERR_TABLE_FULL when the index or the pool is full (those
+ *              positions get row -1).
+ * Which slot and which row an ID gets depends on the order in which threads
+ * win their races; every other output is deterministic.
+ *
+ * gba_hash_rehash: build the index again at new_capacity (cleared here) from
+ * the old one; rows do not move, so rows_out of later calls is unchanged.
+ */
+#define GBA_EMPTY_ID (-1)
+
+gba_status gba_hash_clear(int64_t* slot_ids, int32_t* slot_rows, int64_t capacity, hipStream_t stream);
+
+gba_status gba_hash_workspace_size(int64_t n, size_t* bytes /* host out */);
+
+gba_status gba_hash_find_or_insert(int64_t* slot_ids, int32_t* slot_rows, int64_t capacity,
+                                   const int64_t* ids, int64_t n, int64_t* rows_out, int64_t* num_rows,
+                                   int64_t max_rows, int64_t* row_ids, int64_t* num_new, void* workspace,
+                                   size_t workspace_bytes, int32_t* err, hipStream_t stream);
+
+gba_status gba_hash_rehash(const int64_t* old_slot_ids, const int32_t* old_slot_rows, int64_t old_capacity,
+                           int64_t* new_slot_ids, int32_t* new_slot_rows, int64_t new_capacity, int32_t* err,
+                           hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -18,7 +18,8 @@ __all__ = [
     "gba_aggregate_sparse_workspace_size", "gba_apply_adagrad", "gba_apply_adam",
     "gba_aggregate_apply_dense_adagrad", "gba_aggregate_apply_dense_adam", "gba_accumulate_dense",
     "gba_finalize_dense", "gba_finalize_apply_dense_adagrad", "gba_finalize_apply_dense_adam",
-    "gba_token_of_batch", "gba_pull_workspace_size", "gba_pull_rows",
+    "gba_token_of_batch", "gba_pull_workspace_size", "gba_pull_rows", "gba_hash_clear",
+    "gba_hash_workspace_size", "gba_hash_find_or_insert", "gba_hash_rehash", "EMPTY_ID", "DERR_TABLE_FULL",
     "pointer_table", "DECAY_TOKEN", "DECAY_ID_TAG", "NORM_PER_ID_COUNT", "NORM_BY_K",
     "DERR_ID_RANGE", "DERR_FUTURE_TOKEN", "DERR_OFFSETS", "DERR_ROW_RANGE", "MAX_K", "MAX_D",
     "LIB_PATH",
@@ -31,7 +32,8 @@ LIB_PATH = os.environ.get("GBA_LIBRARY") or os.path.join(os.path.dirname(os.path
 
 DECAY_TOKEN, DECAY_ID_TAG = 0, 1
 NORM_PER_ID_COUNT, NORM_BY_K = 0, 1
-DERR_ID_RANGE, DERR_FUTURE_TOKEN, DERR_OFFSETS, DERR_ROW_RANGE = 1, 2, 4, 8
+DERR_ID_RANGE, DERR_FUTURE_TOKEN, DERR_OFFSETS, DERR_ROW_RANGE, DERR_TABLE_FULL = 1, 2, 4, 8, 16
+EMPTY_ID = -1
 MAX_K, MAX_D = 4096, 256
 
 _P = ctypes.c_void_p
@@ -57,6 +59,10 @@ _SIGNATURES = {
     "gba_token_of_batch": ([_I64, _I32], _I64),
     "gba_pull_workspace_size": ([_I64, _I64, ctypes.POINTER(ctypes.c_size_t)], _I32),
     "gba_pull_rows": ([_P, _I64, _I64, _P, _I32, _P, _P, _P, _P, _P, ctypes.c_size_t, _P, _P], _I32),
+    "gba_hash_clear": ([_P, _P, _I64, _P], _I32),
+    "gba_hash_workspace_size": ([_I64, ctypes.POINTER(ctypes.c_size_t)], _I32),
+    "gba_hash_find_or_insert": ([_P, _P, _I64, _P, _I64, _P, _P, _I64, _P, _P, _P, ctypes.c_size_t, _P, _P], _I32),
+    "gba_hash_rehash": ([_P, _P, _I64, _P, _P, _I64, _P, _P], _I32),
     "gba_apply_adagrad": ([_P, _P, _P, _P, _P, _P, _I64, _I32, _I64, _F64, _F64, _P, _P], _I32),
     "gba_apply_adam": ([_P, _P, _P, _P, _P, _P, _P, _I64, _I32, _I64, _F64, _F64, _F64, _F64, _I64,
                         _P, _P], _I32),
@@ -225,6 +231,45 @@ def gba_pull_rows(ids, table, unique_ids, inverse, rows, num_unique, workspace, 
     _need(err, torch.int32, "err", 1)
     _check(lib().gba_pull_rows(_ptr(ids), n, int(R), _ptr(table), int(D), _ptr(unique_ids), _ptr(inverse), _ptr(rows),
                                _ptr(num_unique), _ptr(workspace), workspace.numel(), _ptr(err), _stream(stream)))
+
+
+def gba_hash_clear(slot_ids, slot_rows, stream=None):
+    _need(slot_ids, torch.int64, "slot_ids")
+    _need(slot_rows, torch.int32, "slot_rows", slot_ids.numel())
+    _check(lib().gba_hash_clear(_ptr(slot_ids), _ptr(slot_rows), slot_ids.numel(), _stream(stream)))
+
+
+def gba_hash_workspace_size(n) -> int:
+    b = ctypes.c_size_t(0)
+    _check(lib().gba_hash_workspace_size(int(n), ctypes.byref(b)))
+    return int(b.value)
+
+
+def gba_hash_find_or_insert(slot_ids, slot_rows, ids, rows_out, num_rows, max_rows, workspace, row_ids=None,
+                            num_new=None, err=None, stream=None):
+    """rows_out[i] = row of ids[i] in the pool; new IDs get the next rows."""
+    n = ids.numel()
+    _need(slot_ids, torch.int64, "slot_ids")
+    _need(slot_rows, torch.int32, "slot_rows", slot_ids.numel())
+    _need(ids, torch.int64, "ids")
+    _need(rows_out, torch.int64, "rows_out", n)
+    _need(num_rows, torch.int64, "num_rows", 1)
+    _need(row_ids, torch.int64, "row_ids", max_rows if row_ids is not None else None)
+    _need(num_new, torch.int64, "num_new", 1)
+    _need(workspace, torch.uint8, "workspace")
+    _need(err, torch.int32, "err", 1)
+    _check(lib().gba_hash_find_or_insert(_ptr(slot_ids), _ptr(slot_rows), slot_ids.numel(), _ptr(ids), n,
+                                         _ptr(rows_out), _ptr(num_rows), int(max_rows), _ptr(row_ids), _ptr(num_new),
+                                         _ptr(workspace), workspace.numel(), _ptr(err), _stream(stream)))
+
+
+def gba_hash_rehash(old_ids, old_rows, new_ids, new_rows, err=None, stream=None):
+    for name, x, dt in (("old_ids", old_ids, torch.int64), ("old_rows", old_rows, torch.int32),
+                        ("new_ids", new_ids, torch.int64), ("new_rows", new_rows, torch.int32)):
+        _need(x, dt, name)
+    _need(err, torch.int32, "err", 1)
+    _check(lib().gba_hash_rehash(_ptr(old_ids), _ptr(old_rows), old_ids.numel(), _ptr(new_ids), _ptr(new_rows),
+                                 new_ids.numel(), _ptr(err), _stream(stream)))
 
 
 def gba_aggregate_sparse_workspace_size(N, K, D, R) -> int:

@@ -237,6 +237,43 @@ gba_status gba_pull_rows(const int64_t* ids, int64_t n, int64_t R, const float* 
   return from_hip(launch_pull(a, ws + align_up(plan.bytes), stream));
 }
 
+static bool pow2_capacity(int64_t c) { return c >= 1 && c <= (int64_t(1) << 31) && (c & (c - 1)) == 0; }
+
+gba_status gba_hash_clear(int64_t* slot_ids, int32_t* slot_rows, int64_t capacity, hipStream_t stream) {
+  if (!pow2_capacity(capacity)) return GBA_ERR_INVALID_ARG;
+  if (!slot_ids || !slot_rows) return GBA_ERR_NULL;
+  return from_hip(launch_hash_clear(slot_ids, slot_rows, capacity, stream));
+}
+
+gba_status gba_hash_workspace_size(int64_t n, size_t* bytes) {
+  if (!bytes) return GBA_ERR_NULL;
+  if (n < 0 || n > kMaxN) return GBA_ERR_INVALID_ARG;
+  *bytes = hash_workspace_bytes(n);
+  return GBA_OK;
+}
+
+gba_status gba_hash_find_or_insert(int64_t* slot_ids, int32_t* slot_rows, int64_t capacity, const int64_t* ids,
+                                   int64_t n, int64_t* rows_out, int64_t* num_rows, int64_t max_rows,
+                                   int64_t* row_ids, int64_t* num_new, void* workspace, size_t workspace_bytes,
+                                   int32_t* err, hipStream_t stream) {
+  if (!pow2_capacity(capacity) || n < 0 || n > kMaxN || max_rows < 1 || max_rows > INT32_MAX)
+    return GBA_ERR_INVALID_ARG;
+  if (!slot_ids || !slot_rows || !num_rows || !workspace) return GBA_ERR_NULL;
+  if (n > 0 && (!ids || !rows_out)) return GBA_ERR_NULL;
+  if (workspace_bytes < hash_workspace_bytes(n)) return GBA_ERR_WORKSPACE;
+  return from_hip(launch_hash_find_or_insert(slot_ids, slot_rows, capacity, ids, n, rows_out, num_rows, max_rows,
+                                             row_ids, num_new, workspace, err, stream));
+}
+
+gba_status gba_hash_rehash(const int64_t* old_slot_ids, const int32_t* old_slot_rows, int64_t old_capacity,
+                           int64_t* new_slot_ids, int32_t* new_slot_rows, int64_t new_capacity, int32_t* err,
+                           hipStream_t stream) {
+  if (!pow2_capacity(old_capacity) || !pow2_capacity(new_capacity)) return GBA_ERR_INVALID_ARG;
+  if (!old_slot_ids || !old_slot_rows || !new_slot_ids || !new_slot_rows) return GBA_ERR_NULL;
+  return from_hip(launch_hash_rehash(old_slot_ids, old_slot_rows, old_capacity, new_slot_ids, new_slot_rows,
+                                     new_capacity, err, stream));
+}
+
 gba_status gba_apply_adagrad(float* param, float* accum, const float* grad, const int64_t* rows,
                              const int32_t* active, const int64_t* num_rows, int64_t n, int32_t D,
                              int64_t R, double lr, double eps, int32_t* err, hipStream_t stream) {

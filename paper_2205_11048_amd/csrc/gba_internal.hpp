@@ -117,4 +117,14 @@ struct PullArgs {
 size_t pull_workspace_bytes(int64_t n);
 hipError_t launch_pull(const PullArgs& a, void* ws, hipStream_t stream);
 
+// ---- storage keyed by 64-bit IDs: open-addressing index (ID -> row) + row pool
+size_t hash_workspace_bytes(int64_t n);
+hipError_t launch_hash_clear(int64_t* slot_ids, int32_t* slot_rows, int64_t capacity, hipStream_t stream);
+hipError_t launch_hash_find_or_insert(int64_t* slot_ids, int32_t* slot_rows, int64_t capacity, const int64_t* ids,
+                                      int64_t n, int64_t* rows_out, int64_t* num_rows, int64_t max_rows,
+                                      int64_t* row_ids, int64_t* num_new, void* ws, int32_t* err,
+                                      hipStream_t stream);
+hipError_t launch_hash_rehash(const int64_t* old_ids, const int32_t* old_rows, int64_t old_capacity, int64_t* new_ids,
+                              int32_t* new_rows, int64_t new_capacity, int32_t* err, hipStream_t stream);
+
 }  // namespace gba

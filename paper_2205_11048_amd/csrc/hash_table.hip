@@ -1,0 +1,234 @@
+// Embedding storage keyed by 64-bit IDs (the paper's PS keeps embeddings in
+// expandable hash tables keyed by feature ID, Sec. 4.1 / Table 1 setting): an
+// open-addressing index from ID to row, and a row pool that grows from a
+// device counter.  The push and pull paths run unchanged on the row numbers;
+// growing the index (rehash) re-inserts (ID, row) pairs and never moves rows.
+//
+// find-or-insert is three launches, so no thread ever waits for another's
+// write: (1) every position claims or finds its ID's slot (compare-and-swap on
+// the slot's ID; IDs are never removed, so a non-empty slot never changes) and
+// the slots it claimed are appended to a list, one atomic per wave; (2) the
+// claimed slots get the next rows of the pool, in list order; (3) every
+// position reads its slot's row.
+#include "gba_device.hpp"
+#include "gba_internal.hpp"
+
+namespace gba {
+
+constexpr int kHashBlock = 256;
+constexpr int64_t kHashMaxBlocks = 8192;
+
+static inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+static inline size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
+
+struct HashLayout {
+  size_t off_slot, off_claimed, off_count, bytes;
+};
+
+static HashLayout hash_layout(int64_t n) {
+  HashLayout L{};
+  const size_t m = (size_t)(n > 0 ? n : 1);
+  size_t o = 0;
+  L.off_slot = o;    o += align_up(m * 4);    // slot of each position
+  L.off_claimed = o; o += align_up(m * 4);    // slots claimed by this call
+  L.off_count = o;   o += 256;                // number of claimed slots
+  L.bytes = o;
+  return L;
+}
+
+size_t hash_workspace_bytes(int64_t n) { return hash_layout(n).bytes; }
+
+// 64-bit finaliser of MurmurHash3 (Appleby): spreads consecutive or strided
+// IDs over the whole index.
+__device__ __forceinline__ uint64_t mix64(uint64_t h) {
+  h ^= h >> 33;
+  h *= 0xff51afd7ed558ccdull;
+  h ^= h >> 33;
+  h *= 0xc4ceb9fe1a85ec53ull;
+  h ^= h >> 33;
+  return h;
+}
+
+__global__ void hash_count_reset_kernel(uint32_t* __restrict__ claimed_count) { *claimed_count = 0u; }
+
+__global__ void __launch_bounds__(kHashBlock)
+hash_clear_kernel(int64_t* __restrict__ slot_ids, int32_t* __restrict__ slot_rows, int64_t capacity) {
+  const int64_t stride = (int64_t)gridDim.x * kHashBlock;
+  for (int64_t s = (int64_t)blockIdx.x * kHashBlock + threadIdx.x; s < capacity; s += stride) {
+    slot_ids[s] = GBA_EMPTY_ID;
+    slot_rows[s] = -1;
+  }
+}
+
+// Linear probing from the ID's home slot.  Returns the slot that holds `id`
+// (claimed here when *claimed), or -1 when every slot holds another ID.
+__device__ __forceinline__ int64_t claim_or_find(int64_t* slot_ids, int64_t mask, int64_t id, bool* claimed) {
+  int64_t s = (int64_t)(mix64((uint64_t)id) & (uint64_t)mask);
+  *claimed = false;
+  for (int64_t probe = 0; probe <= mask; ++probe) {
+    // a plain load may be stale only while the slot is empty: a filled slot
+    // never changes, and the swap below decides every race for an empty one
+    const int64_t cur = slot_ids[s];
+    if (cur == id) return s;
+    if (cur == GBA_EMPTY_ID) {
+      const unsigned long long prev =
+          atomicCAS(reinterpret_cast<unsigned long long*>(slot_ids + s), (unsigned long long)GBA_EMPTY_ID,
+                    (unsigned long long)id);
+      if ((int64_t)prev == GBA_EMPTY_ID) {
+        *claimed = true;
+        return s;
+      }
+      if ((int64_t)prev == id) return s;
+    }
+    s = (s + 1) & mask;
+  }
+  return -1;
+}
+
+__global__ void __launch_bounds__(kHashBlock)
+hash_claim_kernel(int64_t* __restrict__ slot_ids, int64_t mask, const int64_t* __restrict__ ids, int64_t n,
+                  int32_t* __restrict__ slot_of, int32_t* __restrict__ claimed_slots,
+                  uint32_t* __restrict__ claimed_count, int32_t* __restrict__ err) {
+  const int64_t stride = (int64_t)gridDim.x * kHashBlock;
+  const uint64_t lt = lanemask_lt();
+  // every lane of a wave runs the same number of rounds, so the ballots below
+  // see the whole wave
+  for (int64_t base = (int64_t)blockIdx.x * kHashBlock + (threadIdx.x & ~(kWave - 1)); base < n; base += stride) {
+    const int64_t i = base + lane_id();
+    bool claimed = false;
+    int64_t s = -1;
+    if (i < n) {
+      const int64_t id = ids[i];
+      if (id == GBA_EMPTY_ID) {
+        raise_error(err, GBA_DERR_ID_RANGE);
+      } else {
+        s = claim_or_find(slot_ids, mask, id, &claimed);
+        if (s < 0) raise_error(err, GBA_DERR_TABLE_FULL);
+      }
+      slot_of[i] = (int32_t)s;
+    }
+    const uint64_t m = __ballot(claimed);
+    if (m) {
+      uint32_t at = 0;
+      if (lane_id() == __ffsll((unsigned long long)m) - 1) at = atomicAdd(claimed_count, (uint32_t)__popcll(m));
+      at = __shfl(at, __ffsll((unsigned long long)m) - 1, kWave);
+      if (claimed) claimed_slots[at + __popcll(m & lt)] = (int32_t)s;
+    }
+  }
+}
+
+// Rows [num_rows, num_rows + claimed) go to the claimed slots, in list order.
+__global__ void __launch_bounds__(kHashBlock)
+hash_assign_kernel(const int64_t* __restrict__ slot_ids, int32_t* __restrict__ slot_rows,
+                   const int32_t* __restrict__ claimed_slots, const uint32_t* __restrict__ claimed_count,
+                   const int64_t* __restrict__ num_rows, int64_t max_rows, int64_t* __restrict__ row_ids,
+                   int32_t* __restrict__ err) {
+  const int64_t c = *claimed_count;
+  const int64_t r0 = *num_rows;
+  const int64_t stride = (int64_t)gridDim.x * kHashBlock;
+  for (int64_t j = (int64_t)blockIdx.x * kHashBlock + threadIdx.x; j < c; j += stride) {
+    const int64_t s = claimed_slots[j];
+    const int64_t r = r0 + j;
+    if (r >= max_rows) {   // the pool is full: the slot keeps no row
+      raise_error(err, GBA_DERR_TABLE_FULL);
+      continue;
+    }
+    slot_rows[s] = (int32_t)r;
+    if (row_ids) row_ids[r] = slot_ids[s];
+  }
+}
+
+__global__ void hash_count_kernel(const uint32_t* __restrict__ claimed_count, int64_t max_rows,
+                                  int64_t* __restrict__ num_rows, int64_t* __restrict__ num_new) {
+  const int64_t c = *claimed_count;
+  int64_t r = *num_rows + c;
+  *num_rows = r < max_rows ? r : max_rows;
+  if (num_new) *num_new = c;
+}
+
+__global__ void __launch_bounds__(kHashBlock)
+hash_rows_kernel(const int32_t* __restrict__ slot_rows, const int32_t* __restrict__ slot_of, int64_t n,
+                 int64_t* __restrict__ rows_out) {
+  const int64_t stride = (int64_t)gridDim.x * kHashBlock;
+  for (int64_t i = (int64_t)blockIdx.x * kHashBlock + threadIdx.x; i < n; i += stride) {
+    const int32_t s = slot_of[i];
+    rows_out[i] = s < 0 ? -1 : (int64_t)slot_rows[s];
+  }
+}
+
+// Re-insert every (ID, row) of the old index into the new one; each ID is
+// present once, so every claim succeeds without a race on its row.
+__global__ void __launch_bounds__(kHashBlock)
+hash_rehash_kernel(const int64_t* __restrict__ old_ids, const int32_t* __restrict__ old_rows, int64_t old_capacity,
+                   int64_t* __restrict__ new_ids, int32_t* __restrict__ new_rows, int64_t new_mask,
+                   int32_t* __restrict__ err) {
+  const int64_t stride = (int64_t)gridDim.x * kHashBlock;
+  for (int64_t s = (int64_t)blockIdx.x * kHashBlock + threadIdx.x; s < old_capacity; s += stride) {
+    const int64_t id = old_ids[s];
+    if (id == GBA_EMPTY_ID) continue;
+    bool claimed = false;
+    const int64_t t = claim_or_find(new_ids, new_mask, id, &claimed);
+    if (t < 0) {
+      raise_error(err, GBA_DERR_TABLE_FULL);
+      continue;
+    }
+    new_rows[t] = old_rows[s];
+  }
+}
+
+static dim3 grid_for(int64_t n) {
+  int64_t b = ceil_div(n > 0 ? n : 1, kHashBlock);
+  if (b > kHashMaxBlocks) b = kHashMaxBlocks;
+  return dim3((unsigned)b);
+}
+
+hipError_t launch_hash_clear(int64_t* slot_ids, int32_t* slot_rows, int64_t capacity, hipStream_t stream) {
+  hipLaunchKernelGGL(hash_clear_kernel, grid_for(capacity), dim3(kHashBlock), 0, stream, slot_ids, slot_rows,
+                     capacity);
+  return hipGetLastError();
+}
+
+hipError_t launch_hash_find_or_insert(int64_t* slot_ids, int32_t* slot_rows, int64_t capacity, const int64_t* ids,
+                                      int64_t n, int64_t* rows_out, int64_t* num_rows, int64_t max_rows,
+                                      int64_t* row_ids, int64_t* num_new, void* ws, int32_t* err,
+                                      hipStream_t stream) {
+  const HashLayout L = hash_layout(n);
+  char* base = static_cast<char*>(ws);
+  int32_t* slot_of = reinterpret_cast<int32_t*>(base + L.off_slot);
+  int32_t* claimed = reinterpret_cast<int32_t*>(base + L.off_claimed);
+  uint32_t* count = reinterpret_cast<uint32_t*>(base + L.off_count);
+  // the counter is cleared by a kernel, not a memset, so the sequence can be
+  // captured in a graph
+  hipLaunchKernelGGL(hash_count_reset_kernel, dim3(1), dim3(1), 0, stream, count);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (n > 0) {
+    hipLaunchKernelGGL(hash_claim_kernel, grid_for(n), dim3(kHashBlock), 0, stream, slot_ids, capacity - 1, ids, n,
+                       slot_of, claimed, count, err);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(hash_assign_kernel, grid_for(n), dim3(kHashBlock), 0, stream, (const int64_t*)slot_ids,
+                       slot_rows, (const int32_t*)claimed, (const uint32_t*)count, (const int64_t*)num_rows, max_rows,
+                       row_ids, err);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(hash_count_kernel, dim3(1), dim3(1), 0, stream, (const uint32_t*)count, max_rows, num_rows,
+                     num_new);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (n > 0) {
+    hipLaunchKernelGGL(hash_rows_kernel, grid_for(n), dim3(kHashBlock), 0, stream, (const int32_t*)slot_rows,
+                       (const int32_t*)slot_of, n, rows_out);
+    e = hipGetLastError();
+  }
+  return e;
+}
+
+hipError_t launch_hash_rehash(const int64_t* old_ids, const int32_t* old_rows, int64_t old_capacity, int64_t* new_ids,
+                              int32_t* new_rows, int64_t new_capacity, int32_t* err, hipStream_t stream) {
+  hipError_t e = launch_hash_clear(new_ids, new_rows, new_capacity, stream);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(hash_rehash_kernel, grid_for(old_capacity), dim3(kHashBlock), 0, stream, old_ids, old_rows,
+                     old_capacity, new_ids, new_rows, new_capacity - 1, err);
+  return hipGetLastError();
+}
+
+}  // namespace gba

@@ -620,3 +620,137 @@ def test_pull_rows_host_checks():
                            nu.data_ptr(), ws.data_ptr(), ws.numel(), None, st) == 1
     assert L.gba_pull_rows(ids.data_ptr(), 4, 10, t.data_ptr(), 4, t.data_ptr(), t.data_ptr(), t.data_ptr(),
                            nu.data_ptr(), ws.data_ptr(), 16, None, st) == 4
+
+
+# ------------------------------------------------ storage keyed by 64-bit IDs
+class _HashStore:
+    def __init__(self, capacity, max_rows, n_max):
+        self.slot_ids = torch.empty(capacity, dtype=torch.int64, device=DEV)
+        self.slot_rows = torch.empty(capacity, dtype=torch.int32, device=DEV)
+        gba.gba_hash_clear(self.slot_ids, self.slot_rows)
+        self.max_rows = max_rows
+        self.num_rows = torch.zeros(1, dtype=torch.int64, device=DEV)
+        self.row_ids = torch.full((max_rows,), -7, dtype=torch.int64, device=DEV)
+        self.ws = torch.empty(gba.gba_hash_workspace_size(n_max), dtype=torch.uint8, device=DEV)
+        self.err = torch.zeros(1, dtype=torch.int32, device=DEV)
+
+    def rows_of(self, ids):
+        out = torch.full((max(ids.size, 1),), -9, dtype=torch.int64, device=DEV)
+        nn = torch.full((1,), -9, dtype=torch.int64, device=DEV)
+        gba.gba_hash_find_or_insert(self.slot_ids, self.slot_rows, dev(ids) if ids.size else out[:0], out,
+                                    self.num_rows, self.max_rows, self.ws, row_ids=self.row_ids, num_new=nn,
+                                    err=self.err)
+        return host(out)[:ids.size], int(host(nn)[0])
+
+
+def _ids64(rng, n, distinct):
+    pool = rng.integers(-(2 ** 62), 2 ** 62, distinct, dtype=np.int64) * 2 + 1   # spread over all 64 bits
+    pool[pool == gba.EMPTY_ID] = 5                                               # the reserved value
+    pool = np.unique(pool)
+    hot = rng.random(n) < 0.3
+    ids = np.where(hot, pool[0], pool[rng.integers(0, pool.size, n)])
+    return ids.astype(np.int64)
+
+
+@pytest.mark.parametrize("capacity,n,distinct", [(1 << 10, 700, 300), (1 << 16, 50_000, 20_000),
+                                                 (1 << 21, 400_000, 700_000)])
+def test_hash_find_or_insert(capacity, n, distinct):
+    rng = np.random.default_rng(capacity + n)
+    ids = _ids64(rng, n, distinct)
+    st = _HashStore(capacity, max_rows=n + 10, n_max=2 * n)
+    rows, nn = st.rows_of(ids)
+    assert int(host(st.err)[0]) == 0
+    U = np.unique(ids).size
+    assert nn == U and int(host(st.num_rows)[0]) == U
+    # one row per distinct ID, rows 0..U-1, and the reverse map agrees
+    pairs = np.unique(np.stack([ids, rows]), axis=1)
+    assert pairs.shape[1] == U and np.unique(pairs[1]).size == U
+    assert rows.min() == 0 and rows.max() == U - 1
+    assert_exact(host(st.row_ids)[rows], ids, "row -> ID")
+    sid, srow = host(st.slot_ids), host(st.slot_rows)
+    assert int((sid != gba.EMPTY_ID).sum()) == U and np.all(srow[sid != gba.EMPTY_ID] >= 0)
+    # a second call with old and new IDs: old IDs keep their rows, new ones get the next rows
+    more = np.concatenate([ids[: n // 2], rng.integers(2 ** 40, 2 ** 41, n // 3).astype(np.int64)])
+    rows2, nn2 = st.rows_of(more)
+    assert int(host(st.err)[0]) == 0
+    assert_exact(rows2[: n // 2], rows[: n // 2], "rows of known IDs")
+    new_ids = np.setdiff1d(more, ids)
+    assert nn2 == new_ids.size
+    fresh = rows2[np.isin(more, new_ids)]
+    assert fresh.min() == U and fresh.max() == U + new_ids.size - 1
+
+
+def test_hash_full_index_full_pool_and_reserved_id():
+    st = _HashStore(16, max_rows=100, n_max=64)
+    st.rows_of(np.arange(20, dtype=np.int64) * 7 + 3)
+    assert int(host(st.err)[0]) & gba.DERR_TABLE_FULL
+    st = _HashStore(64, max_rows=10, n_max=64)
+    rows, _ = st.rows_of(np.arange(20, dtype=np.int64) + 100)
+    assert int(host(st.err)[0]) & gba.DERR_TABLE_FULL
+    assert int(host(st.num_rows)[0]) == 10 and (rows == -1).sum() == 10
+    st = _HashStore(64, max_rows=10, n_max=64)
+    st.rows_of(np.array([4, gba.EMPTY_ID, 4], np.int64))
+    assert int(host(st.err)[0]) & gba.DERR_ID_RANGE
+
+
+def test_hash_rehash_keeps_every_row():
+    rng = np.random.default_rng(5)
+    ids = _ids64(rng, 3000, 1500)
+    st = _HashStore(1 << 12, max_rows=4000, n_max=3000)
+    rows, _ = st.rows_of(ids)
+    big_ids = torch.empty(1 << 14, dtype=torch.int64, device=DEV)
+    big_rows = torch.empty(1 << 14, dtype=torch.int32, device=DEV)
+    gba.gba_hash_rehash(st.slot_ids, st.slot_rows, big_ids, big_rows, err=st.err)
+    st.slot_ids, st.slot_rows = big_ids, big_rows
+    rows2, nn = st.rows_of(ids[::-1].copy())
+    assert int(host(st.err)[0]) == 0 and nn == 0
+    assert_exact(rows2[::-1], rows, "rows after rehash")
+
+
+@pytest.mark.parametrize("opt", ["adagrad", "adam"])
+def test_hash_backed_push_step(opt):
+    """A push step on storage keyed by 64-bit IDs: IDs -> rows, the sparse call
+    and the row apply on the pool give, per ID, the oracle's row-indexed step."""
+    c = BY_NAME["c0"].scaled(optimizer=opt, lr=0.01 if opt == "adagrad" else 1e-3)
+    hs = workload.host_step(c)
+    scramble = lambda r: (r.astype(np.uint64) * np.uint64(0x9E3779B97F4A7C15) + np.uint64(12345)).view(np.int64)  # noqa: E731
+    ids64 = scramble(hs.ids)
+    st = _HashStore(1 << 16, max_rows=c.R, n_max=c.N)
+    rows, U = st.rows_of(ids64)
+    assert int(host(st.err)[0]) == 0
+    uniq = np.unique(hs.ids)
+    # the caller initialises the new rows: the values the row-indexed table holds for those IDs
+    orig_of_row = np.empty(U, np.int64)
+    orig_of_row[rows] = hs.ids
+    pool = dev(hs.table[orig_of_row])
+    pslots = [dev(s_[orig_of_row]) for s_ in hs.table_slots]
+    w, _, _ = oracle.token_weights(hs.tokens, hs.step, c.iota)
+    K, N, D = c.K, c.N, c.D
+    out_u = torch.empty(N, dtype=torch.int64, device=DEV)
+    so = torch.empty(N + 1, dtype=torch.int64, device=DEV)
+    cc = torch.empty(N, dtype=torch.int32, device=DEV)
+    ww = torch.empty(N, dtype=torch.int32, device=DEV)
+    agg = torch.empty((N, D), device=DEV)
+    nu = torch.zeros(1, dtype=torch.int64, device=DEV)
+    ws = torch.empty(gba.gba_aggregate_sparse_workspace_size(N, K, D, U), dtype=torch.uint8, device=DEV)
+    gba.gba_aggregate_sparse(dev(rows), dev(hs.rows), dev(hs.offsets), U, dev(w), dev(hs.tokens), hs.step, c.iota,
+                             None, gba.DECAY_TOKEN, gba.NORM_PER_ID_COUNT, out_u, so, cc, ww, agg, nu, ws, st.err)
+    if opt == "adagrad":
+        gba.gba_apply_adagrad(pool, pslots[0], agg, c.lr, c.eps, rows=out_u, active=ww, num_rows=nu, R=U, err=st.err)
+    else:
+        gba.gba_apply_adam(pool, pslots[0], pslots[1], agg, c.lr, c.beta1, c.beta2, c.eps, c.adam_t, rows=out_u,
+                           active=ww, num_rows=nu, R=U, err=st.err)
+    assert int(host(st.err)[0]) == 0
+    Ud = int(host(nu)[0])
+    assert Ud == uniq.size
+    # the distinct rows name exactly the request's distinct IDs
+    assert_exact(np.sort(host(st.row_ids)[host(out_u)[:Ud]]), np.sort(scramble(uniq)), "distinct IDs")
+    hp = dict(lr=c.lr, eps=c.eps, beta1=c.beta1, beta2=c.beta2)
+    ref = oracle.gba_step(hs.tokens, hs.step, c.iota, hs.grads, hs.ids, hs.rows, hs.offsets, hs.param,
+                          hs.dense_slots, lambda r: hs.table[r], lambda k, r: hs.table_slots[k][r], opt, hp,
+                          t=c.adam_t)
+    row_of_orig = dict(zip(orig_of_row.tolist(), range(U)))
+    act_rows = np.array([row_of_orig[r] for r in ref["active_ids"]])
+    assert_rule_t(host(pool)[act_rows], ref["table_rows"], None, "rows")
+    for k, s_ in enumerate(ref["table_slot_rows"]):
+        assert_rule_t(host(pslots[k])[act_rows], s_, None, f"slot {k}")
