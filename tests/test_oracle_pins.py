@@ -423,3 +423,32 @@ def test_pull_rows_reconstructs_the_request(n, R):
     assert np.array_equal(u[inv], ids)
     assert np.array_equal(rows[inv], table[ids])
     assert set(u.tolist()) == set(ids.tolist())
+
+
+# ---------------------------------------------- storage keyed by 64-bit IDs
+@pytest.mark.parametrize("decay", ["token", "id_tag"])
+def test_results_follow_the_id_not_its_value(decay):
+    """Renaming the IDs by any injective map (as an ID -> row index does)
+    renames the outputs and changes nothing else: per-ID sums, c_r, W_r and
+    tags travel with the ID."""
+    rng = np.random.default_rng(11)
+    K, R, D = 5, 300, 4
+    sizes = rng.integers(0, 60, K)
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    N = int(off[-1])
+    ids = rng.integers(0, R, N).astype(np.int64)
+    rows = counter.values_range(4, counter.STREAM_ROWS, 0, N * D, counter.KIND_DYADIC).reshape(N, D)
+    tokens = 40 - rng.integers(0, 5, K)
+    w, _, _ = oracle.token_weights(tokens, 40, 2)
+    tag = rng.integers(-1, 40, R).astype(np.int64)
+    perm = rng.permutation(R)          # the renaming: ID r becomes perm[r]
+    tag2 = np.empty(R, np.int64)
+    tag2[perm] = tag
+    a = oracle.aggregate_sparse(ids, rows, off, w, tokens, 40, 2, tag.copy(), decay)
+    b = oracle.aggregate_sparse(perm[ids], rows, off, w, tokens, 40, 2, tag2.copy(), decay)
+    order = np.argsort(perm[a["unique_ids"]])
+    assert np.array_equal(b["unique_ids"], perm[a["unique_ids"]][order])
+    for k in ("contrib_count", "active_count", "agg"):
+        assert np.array_equal(b[k], a[k][order]), k
+    if decay == "id_tag":
+        assert np.array_equal(b["new_tag"][perm], a["new_tag"])
