@@ -12,7 +12,11 @@ headline workload (c4: K=256 contributions of 256 x 1000 Zipf IDs over a
 500M x 32 table, 16M dense parameters, Adagrad); embedding-grad rows/s and
 the achieved algorithmic HBM bandwidth against the 8 TB/s peak are reported
 beside it, and the same figures for the dense-heavy workload c3 under
-`other_workloads`.
+`other_workloads`.  The dense sum and the dense optimiser run as one fused
+call (`--separate-dense` for two).  Beside the step, each workload also
+reports the step with the dense sum taken early as contributions arrive
+(`early_weighted_sum`), one worker's pull request looked up once per distinct
+ID (`pull`), and the step on storage keyed by 64-bit IDs (`hash_storage`).
 """
 from __future__ import annotations
 
@@ -405,7 +409,7 @@ def cpu_baseline(name, S):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one GPU: this build holds one PS shard per GPU and has no multi-GPU "
+        print("bench.py measures one GPU: the library runs one PS shard per GPU and has no multi-GPU "
               "path (run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
     import torch
