@@ -57,6 +57,8 @@ def parse():
                          "contributions folded per call ('' for none)")
     ap.add_argument("--no-hash-storage", dest="hash_storage", action="store_false",
                     help="skip the leg that runs the step on storage keyed by 64-bit IDs")
+    ap.add_argument("--step-only", action="store_true",
+                    help="time the step only: no early-sum, pull or hash-storage legs (for kernel profiles)")
     ap.add_argument("--cpu-sample", type=int, default=4, help="1/S of the workload for the oracle timing")
     return ap.parse_args()
 
@@ -236,11 +238,11 @@ def run_workload(name, args, torch, gba_step_mod, sdev, gba):
     if args.separate_dense:
         dense_kernel_bytes = K_eff * w.P * 4 + w.P * 4
         dk_ms = breakdown["aggregate_dense"]
-        kname = "aggregate_dense_kernel<0>"
+        kname = "aggregate_dense_kernel<0, false>"
     else:
         dense_kernel_bytes = K_eff * w.P * 4 + (2 + 2 * S) * w.P * 4
         dk_ms = breakdown["aggregate_apply_dense"]
-        kname = f"aggregate_dense_kernel<{S}>"
+        kname = f"aggregate_dense_kernel<{S}, false>"
     dk_gbs = dense_kernel_bytes / (dk_ms * 1e-3) / 1e9
     traffic = measured_traffic(kname, name)
     res = dict(
@@ -278,6 +280,12 @@ def run_workload(name, args, torch, gba_step_mod, sdev, gba):
 
     # pull side: one worker's request (the IDs of one contribution), rows looked
     # up once per distinct ID
+    if args.step_only:
+        if int(st.err.item()) != 0:
+            raise RuntimeError(f"device error bits {int(st.err.item())}")
+        del ds, st
+        torch.cuda.empty_cache()
+        return res
     n_req = int(ds.offsets_host[1] - ds.offsets_host[0])
     req = ds.ids[:n_req]
     pu = torch.empty(n_req, dtype=torch.int64, device="cuda")
@@ -408,6 +416,8 @@ def cpu_baseline(name, S):
 
 def main():
     args = parse()
+    if args.step_only:
+        args.early_sum, args.hash_storage = "", False
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: the library runs one PS shard per GPU and has no multi-GPU "
               "path (run with --gpus 1)", file=sys.stderr)
@@ -454,7 +464,7 @@ def main():
         "realised": {k: head[k] for k in ("K_eff", "N", "N_act", "U", "U_act", "step_alg_bytes")},
         "roofline": head["roofline"],
         "early_weighted_sum": head["early_sum"],
-        "pull": head["pull"],
+        "pull": head.get("pull"),
         "hash_storage": head.get("hash_storage"),
         "other_workloads": others,
     }
