@@ -142,3 +142,93 @@ def test_full_size(name, decay):
     print(f"{name}/{decay}: K={K} N={w.N} U={U} hottest segment {int(counts[order[0]])} occurrences")
     del ds, st
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("name", ["c3", "c4"])
+def test_full_size_early_sum(name):
+    """The dense sum taken early (J = 16 arriving contributions per call, as the
+    benchmark times it) gives bitwise the one-shot fused result at full size;
+    the one-shot result is checked against the oracle in test_full_size."""
+    w = BY_NAME[name]
+    ds = sdev.make_device_step(w)
+    st = GBAStep(w.K, w.N, w.D, w.R, w.P)
+    gba.gba_token_weights(ds.tokens, ds.step, w.iota, st.w, err=st.err)
+    p1, s1 = ds.param.clone(), [x.clone() for x in ds.dense_slots]
+    out1, out2 = torch.empty(w.P, device=ds.param.device), torch.empty(w.P, device=ds.param.device)
+    run = torch.zeros(w.P, dtype=torch.float64, device=ds.param.device)
+    for lo in range(0, w.K, 16):
+        gba.gba_accumulate_dense(gba.pointer_table(ds.grads[lo:lo + 16]), st.w[lo:lo + 16], w.P, run)
+    if w.optimizer == "adagrad":
+        gba.gba_aggregate_apply_dense_adagrad(st.grad_table(ds.grads), st.w, w.P, p1, s1[0], w.lr, w.eps, out=out1)
+        gba.gba_finalize_apply_dense_adagrad(run, w.K, w.P, ds.param, ds.dense_slots[0], w.lr, w.eps, out=out2)
+    else:
+        gba.gba_aggregate_apply_dense_adam(st.grad_table(ds.grads), st.w, w.P, p1, s1[0], s1[1], w.lr, w.beta1,
+                                           w.beta2, w.eps, w.adam_t, out=out1)
+        gba.gba_finalize_apply_dense_adam(run, w.K, w.P, ds.param, ds.dense_slots[0], ds.dense_slots[1], w.lr,
+                                          w.beta1, w.beta2, w.eps, w.adam_t, out=out2)
+    torch.cuda.synchronize()
+    assert int(st.err.item()) == 0
+    assert torch.equal(out1, out2), "g_bar"
+    assert torch.equal(p1, ds.param), "param"
+    for a, b in zip(s1, ds.dense_slots):
+        assert torch.equal(a, b), "state"
+    assert int(torch.count_nonzero(run).item()) == 0, "reset"
+    del ds, st
+    torch.cuda.empty_cache()
+
+
+def test_full_size_hash_storage():
+    """c4 on storage keyed by 64-bit IDs, launched as the benchmark's hash leg
+    (index of 2^25 slots, pool of 2^24 rows): per ID, the updated row and
+    accumulator equal the row-indexed step's (checked against the oracle in
+    test_full_size) to float rounding."""
+    w = BY_NAME["c4"]
+    ds = sdev.make_device_step(w)
+    dev_ = ds.table.device
+    st = GBAStep(w.K, w.N, w.D, w.R, w.P)
+    gba.gba_token_weights(ds.tokens, ds.step, w.iota, st.w, err=st.err)
+    ids64 = ds.ids * (1 << 32) + 7                      # injective for IDs < 2^31, never the reserved value
+    cap, pool_rows = 1 << 25, 1 << 24
+    slot_ids = torch.empty(cap, dtype=torch.int64, device=dev_)
+    slot_rows = torch.empty(cap, dtype=torch.int32, device=dev_)
+    gba.gba_hash_clear(slot_ids, slot_rows)
+    num_rows = torch.zeros(1, dtype=torch.int64, device=dev_)
+    row_ids = torch.full((pool_rows,), -1, dtype=torch.int64, device=dev_)
+    rows_of = torch.empty(w.N, dtype=torch.int64, device=dev_)
+    hws = torch.empty(gba.gba_hash_workspace_size(w.N), dtype=torch.uint8, device=dev_)
+    gba.gba_hash_find_or_insert(slot_ids, slot_rows, ids64, rows_of, num_rows, pool_rows, hws, row_ids=row_ids,
+                                err=st.err)
+    torch.cuda.synchronize()
+    U = int(num_rows.item())
+    orig = (row_ids[:U] - 7) >> 32
+    pool = torch.zeros((pool_rows, w.D), device=dev_)
+    pacc = torch.zeros((pool_rows, w.D), device=dev_)
+    pool[:U] = ds.table[orig]                           # the caller initialises the new rows
+    pacc[:U] = ds.table_slots[0][orig]
+    sws = torch.empty(gba.gba_aggregate_sparse_workspace_size(w.N, w.K, w.D, pool_rows), dtype=torch.uint8,
+                      device=dev_)
+    gba.gba_aggregate_sparse(rows_of, ds.rows, ds.offsets, pool_rows, st.w, ds.tokens, ds.step, w.iota, None,
+                             gba.DECAY_TOKEN, gba.NORM_PER_ID_COUNT, st.unique_ids, st.seg_offsets, st.contrib_count,
+                             st.active_count, st.agg, st.num_unique, sws, st.err)
+    gba.gba_apply_adagrad(pool, pacc, st.agg, w.lr, w.eps, rows=st.unique_ids, active=st.active_count,
+                          num_rows=st.num_unique, R=pool_rows, err=st.err)
+    torch.cuda.synchronize()
+    assert int(st.err.item()) == 0
+    assert int(st.num_unique.item()) == U
+    # the row-indexed step on the same inputs
+    gba.gba_aggregate_sparse(ds.ids, ds.rows, ds.offsets, w.R, st.w, ds.tokens, ds.step, w.iota, None,
+                             gba.DECAY_TOKEN, gba.NORM_PER_ID_COUNT, st.unique_ids, st.seg_offsets, st.contrib_count,
+                             st.active_count, st.agg, st.num_unique, st.workspace, st.err)
+    gba.gba_apply_adagrad(ds.table, ds.table_slots[0], st.agg, w.lr, w.eps, rows=st.unique_ids,
+                          active=st.active_count, num_rows=st.num_unique, R=w.R, err=st.err)
+    torch.cuda.synchronize()
+    assert int(st.err.item()) == 0
+    assert int(st.num_unique.item()) == U
+    a, b = pool[:U], ds.table[orig]
+    rel = ((a - b).abs() / b.abs().clamp_min(1e-30)).max().item()
+    assert rel <= 1e-5, rel
+    assert torch.allclose(pacc[:U], ds.table_slots[0][orig], rtol=1e-5, atol=0)
+    same = torch.eq(a, b).float().mean().item()
+    print(f"hash storage: U={U}, rows bitwise equal: {same:.4%}, max relative difference {rel:.2e}")
+    del ds, st, pool, pacc, slot_ids, slot_rows
+    torch.cuda.empty_cache()
