@@ -57,6 +57,8 @@ def parse():
                          "contributions folded per call ('' for none)")
     ap.add_argument("--no-hash-storage", dest="hash_storage", action="store_false",
                     help="skip the leg that runs the step on storage keyed by 64-bit IDs")
+    ap.add_argument("--no-graph", dest="graph", action="store_false",
+                    help="skip the leg that replays the step from a captured HIP graph")
     ap.add_argument("--step-only", action="store_true",
                     help="time the step only: no early-sum, pull or hash-storage legs (for kernel profiles)")
     ap.add_argument("--cpu-sample", type=int, default=4, help="1/S of the workload for the oracle timing")
@@ -128,9 +130,9 @@ def run_workload(name, args, torch, gba_step_mod, sdev, gba):
             gba.gba_finalize_apply_dense_adam(run, w.K, w.P, ds.param, ds.dense_slots[0], ds.dense_slots[1], w.lr,
                                               w.beta1, w.beta2, w.eps, w.adam_t, **dkw)
 
-    def one_step(ev=None, early_J=0):
-        kw = dict(stream=stream)
-        dkw = dict(stream=dstream)
+    def one_step(ev=None, early_J=0, on=None):
+        kw = dict(stream=on or stream)
+        dkw = dict(stream=on or dstream)
         if ev is not None:
             ev["t0"].record(stream)
         gba.gba_token_weights(ds.tokens, ds.step, w.iota, st.w, st.staleness, st.num_excluded, st.err, **kw)
@@ -273,6 +275,31 @@ def run_workload(name, args, torch, gba_step_mod, sdev, gba):
             J=J, calls_per_step=-(-w.K // J) + 1, ms_per_step=start.elapsed_time(end) / n,
             dense_ms=float(np.mean([e["d0"].elapsed_time(e["d1"]) for e in evs])),
             running_sum_bytes=w.P * 8, buffered_gradient_bytes_saved=w.K * w.P * 4 - w.P * 8))
+    # the same step captured once in a HIP graph and replayed (no per-launch
+    # host work); every library call is capturable: no allocation, memset or
+    # synchronisation inside
+    if args.graph and not args.overlap:
+        g = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            one_step(on=side)               # warm the pointer tables outside the capture
+            torch.cuda.synchronize()
+            with torch.cuda.graph(g, stream=side):
+                one_step(on=side)
+        torch.cuda.synchronize()
+        for _ in range(2):
+            g.replay()
+        torch.cuda.synchronize()
+        n = max(3, args.steps)
+        start.record(stream)
+        for _ in range(n):
+            g.replay()
+        end.record(stream)
+        torch.cuda.synchronize()
+        res["graph"] = dict(ms_per_step=start.elapsed_time(end) / n)
+        del g
+
     # storage keyed by 64-bit IDs: the same step with the IDs scrambled over the
     # whole 64-bit range and mapped to rows of a pool by the hash index first
     if args.hash_storage:
@@ -303,10 +330,29 @@ def run_workload(name, args, torch, gba_step_mod, sdev, gba):
     end.record(stream)
     torch.cuda.synchronize()
     pull_ms = start.elapsed_time(end) / n_pull
+    # the same request replayed from a captured HIP graph: the 18 small launches
+    # of one request then cost no host work
+    pg = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(stream)
+    with torch.cuda.graph(pg, stream=side):
+        gba.gba_pull_rows(req, ds.table, pu, pinv, prows, pnu, pws, st.err, stream=side)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        pg.replay()
+    torch.cuda.synchronize()
+    start.record(stream)
+    for _ in range(n_pull):
+        pg.replay()
+    end.record(stream)
+    torch.cuda.synchronize()
+    pull_graph_ms = start.elapsed_time(end) / n_pull
+    del pg
     U_req = int(pnu.item())
     pull_bytes = n_req * 8 + U_req * w.D * 4 * 2 + U_req * 8 + n_req * 4
     res["pull"] = dict(ids_per_request=n_req, distinct=U_req, us_per_request=pull_ms * 1e3,
-                       requests_per_s=1e3 / pull_ms, alg_gbs=pull_bytes / (pull_ms * 1e-3) / 1e9)
+                       requests_per_s=1e3 / pull_ms, alg_gbs=pull_bytes / (pull_ms * 1e-3) / 1e9,
+                       us_per_request_graph=pull_graph_ms * 1e3)
     del pu, pinv, prows, pws
     if int(st.err.item()) != 0:
         raise RuntimeError(f"device error bits {int(st.err.item())}")
@@ -417,7 +463,7 @@ def cpu_baseline(name, S):
 def main():
     args = parse()
     if args.step_only:
-        args.early_sum, args.hash_storage = "", False
+        args.early_sum, args.hash_storage, args.graph = "", False, False
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: the library runs one PS shard per GPU and has no multi-GPU "
               "path (run with --gpus 1)", file=sys.stderr)
@@ -466,6 +512,7 @@ def main():
         "early_weighted_sum": head["early_sum"],
         "pull": head.get("pull"),
         "hash_storage": head.get("hash_storage"),
+        "graph": head.get("graph"),
         "other_workloads": others,
     }
     if not args.no_cpu_baseline:

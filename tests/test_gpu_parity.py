@@ -754,3 +754,80 @@ def test_hash_backed_push_step(opt):
     assert_rule_t(host(pool)[act_rows], ref["table_rows"], None, "rows")
     for k, s_ in enumerate(ref["table_slot_rows"]):
         assert_rule_t(host(pslots[k])[act_rows], s_, None, f"slot {k}")
+
+
+# ------------------------------------------------ capture in a HIP graph
+@pytest.mark.parametrize("decay", ["token", "id_tag"])
+def test_graph_replays_of_a_step_match_eager_steps(decay):
+    """Every call of the step is capturable (no allocation, memset or sync
+    inside): three replays of a captured step, with eager steps on a twin
+    state and synchronisations between them, give bitwise the eager results."""
+    c = BY_NAME["c0"].scaled(optimizer="adam", lr=1e-3)
+    hs = workload.host_step(c)
+    dec = gba.DECAY_ID_TAG if decay == "id_tag" else gba.DECAY_TOKEN
+
+    def state():
+        return dict(param=dev(hs.param), dense_slots=[dev(x) for x in hs.dense_slots], table=dev(hs.table),
+                    table_slots=[dev(x) for x in hs.table_slots], tag=dev(hs.tags))
+    inputs = dict(tokens=dev(hs.tokens), step=hs.step, iota=c.iota, grads=[dev(g) for g in hs.grads],
+                  ids=dev(hs.ids), rows=dev(hs.rows), offsets=dev(hs.offsets), optimizer="adam", lr=c.lr,
+                  eps=c.eps, t=c.adam_t, decay=dec)
+    A, B = state(), state()
+    sa, sb = GBAStep(c.K, c.N, c.D, c.R, c.P), GBAStep(c.K, c.N, c.D, c.R, c.P)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        sb.run(**inputs, **B, stream=side)             # first use: pointer table and buffers outside the capture
+    sa.run(**inputs, **A)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        sb.run(**inputs, **B, stream=side)
+    torch.cuda.synchronize()
+    for i in range(3):
+        sa.run(**inputs, **A)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        U = int(host(sa.num_unique)[0])
+        assert int(host(sb.num_unique)[0]) == U
+        for name in ("param", "table", "tag"):
+            assert torch.equal(A[name], B[name]), (i, name)
+        for k in range(2):
+            assert torch.equal(A["dense_slots"][k], B["dense_slots"][k]), (i, k)
+            assert torch.equal(A["table_slots"][k], B["table_slots"][k]), (i, k)
+        assert torch.equal(sa.g_bar, sb.g_bar) and torch.equal(sa.agg[:U], sb.agg[:U]), i
+        assert int(host(sa.err)[0]) == 0 and int(host(sb.err)[0]) == 0
+
+
+def test_graph_replays_of_a_pull_match_eager_pulls():
+    R, D, n = 50_000, 32, 30_000
+    rng = np.random.default_rng(2)
+    ids = dev(rng.integers(0, R, n).astype(np.int64))
+    table = dev(counter.values_range(3, counter.STREAM_TABLE, 0, R * D, counter.KIND_PARAM).reshape(R, D))
+    ws = torch.empty(gba.gba_pull_workspace_size(n, R), dtype=torch.uint8, device=DEV)
+    outs = [dict(u=torch.empty(n, dtype=torch.int64, device=DEV), inv=torch.empty(n, dtype=torch.int32, device=DEV),
+                 rows=torch.empty((n, D), device=DEV), nu=torch.zeros(1, dtype=torch.int64, device=DEV))
+            for _ in range(2)]
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+
+    def pull(o, stream=None):
+        gba.gba_pull_rows(ids, table, o["u"], o["inv"], o["rows"], o["nu"], ws, err, stream=stream)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        pull(outs[1], stream=side)
+    torch.cuda.synchronize()
+    for i in range(3):
+        for v in outs[1].values():
+            v.fill_(-3)
+        pull(outs[0])
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        U = int(host(outs[0]["nu"])[0])
+        assert int(host(outs[1]["nu"])[0]) == U
+        assert torch.equal(outs[0]["u"][:U], outs[1]["u"][:U]) and torch.equal(outs[0]["inv"], outs[1]["inv"])
+        assert torch.equal(outs[0]["rows"][:U], outs[1]["rows"][:U]), i
+    assert int(host(err)[0]) == 0
