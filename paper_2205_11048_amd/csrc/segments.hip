@@ -28,8 +28,8 @@ namespace gba {
 
 constexpr int kSegBlock = 256;
 constexpr int kSegWaves = kSegBlock / kWave;                 // 4
-constexpr int kRounds = 4;                                   // positions per lane in seg_meta
-constexpr int64_t kMetaTile = (int64_t)kSegBlock * kRounds;  // 1024 positions
+constexpr int kRounds = 4;                                   // 16-byte loads per lane in seg_heads
+constexpr int64_t kMetaTile = (int64_t)kSegBlock * kRounds;  // 1024 positions: 4 per thread of a block
 static_assert(kMetaTile == kRunTile, "run-head tiles are the per-position tiles");
 constexpr int kGroupSpan = 128;                              // positions per lane group in seg_rows
 constexpr int kBatch = 8;                                    // row gathers in flight per group
@@ -256,8 +256,12 @@ __global__ void seg_finish_kernel(const uint32_t* __restrict__ total, int64_t N,
 }
 
 // Per-position pass: numbering, segment IDs and starts, packed words.
-// kMetaTilesPerBlock consecutive 1024-position tiles per block.
+// kMetaTilesPerBlock consecutive 1024-position tiles per block; in a tile each
+// lane takes 4 consecutive positions (16-byte loads and stores), and the
+// segment numbers come from a scan of the lanes' head counts.
 constexpr int kMetaTilesPerBlock = 4;
+constexpr int kMetaPer = 4;   // consecutive positions per lane
+static_assert(kSegBlock * kMetaPer == kMetaTile, "a block covers one tile per pass");
 __global__ void __launch_bounds__(kSegBlock)
 seg_meta_kernel(SegmentArgs a, const uint32_t* __restrict__ tile_seg_base,
                 const int32_t* __restrict__ buckets, int q, int nbuckets, int64_t num_tiles,
@@ -275,82 +279,90 @@ seg_meta_kernel(SegmentArgs a, const uint32_t* __restrict__ tile_seg_base,
 
   const int w = threadIdx.x / kWave;
   const int lane = lane_id();
-  const uint64_t lt = lanemask_lt();
   for (int kt = 0; kt < kMetaTilesPerBlock; ++kt) {
-  const int64_t tile = (int64_t)blockIdx.x * kMetaTilesPerBlock + kt;
-  if (tile >= num_tiles) break;
-  const uint32_t seg_base = tile_seg_base[tile];
-  const int64_t pw = tile * kMetaTile + (int64_t)w * (kRounds * kWave);
-  uint32_t carry_key = 0;
-  int carry_m = -1;
-  bool carry_ok = false;
-  if (pw > 0 && pw < N) {
-    carry_key = a.keys[pw - 1];
-    const uint32_t jp = a.vals[pw - 1];
-    carry_m = (int64_t)jp < N ? contribution_of(s_off, s_bucket, q, K, jp) : 0;
-    carry_ok = true;
-  }
-  uint64_t hm[kRounds];
-  uint32_t keyr[kRounds];
+    const int64_t tile = (int64_t)blockIdx.x * kMetaTilesPerBlock + kt;
+    if (tile >= num_tiles) break;
+    const int64_t p0 = tile * kMetaTile + (int64_t)threadIdx.x * kMetaPer;
+    uint32_t key[kMetaPer] = {0u, 0u, 0u, 0u}, jv[kMetaPer] = {0u, 0u, 0u, 0u};
+    if (p0 + kMetaPer - 1 < N) {
+      const u32x4 kv = *reinterpret_cast<const u32x4*>(a.keys + p0);
+      const u32x4 vv = *reinterpret_cast<const u32x4*>(a.vals + p0);
+      key[0] = kv.x; key[1] = kv.y; key[2] = kv.z; key[3] = kv.w;
+      jv[0] = vv.x; jv[1] = vv.y; jv[2] = vv.z; jv[3] = vv.w;
+    } else {
 #pragma unroll
-  for (int r = 0; r < kRounds; ++r) {
-    const int64_t p = pw + r * kWave + lane;
-    const bool valid = p < N;
-    const uint32_t key = valid ? a.keys[p] : 0u;
-    const uint32_t jv = valid ? a.vals[p] : 0u;
-    const int m = (valid && (int64_t)jv < N) ? contribution_of(s_off, s_bucket, q, K, jv) : 0;
-    uint32_t kp = __shfl_up(key, 1, kWave);
-    int mp = __shfl_up(m, 1, kWave);
+      for (int e = 0; e < kMetaPer; ++e)
+        if (p0 + e < N) {
+          key[e] = a.keys[p0 + e];
+          jv[e] = a.vals[p0 + e];
+        }
+    }
+    int m[kMetaPer];
+#pragma unroll
+    for (int e = 0; e < kMetaPer; ++e)
+      m[e] = (p0 + e < N && (int64_t)jv[e] < N) ? contribution_of(s_off, s_bucket, q, K, jv[e]) : 0;
+    // the position before this lane's first: the previous lane's last, or
+    // (first lane of a wave) read directly
+    uint32_t kp = __shfl_up(key[kMetaPer - 1], 1, kWave);
+    int mp = __shfl_up(m[kMetaPer - 1], 1, kWave);
     bool prev_ok = true;
     if (lane == 0) {
-      kp = carry_key;
-      mp = carry_m;
-      prev_ok = carry_ok;
-    }
-    const bool head = valid && (!prev_ok || key != kp);
-    const bool newc = valid && (head || m != mp);
-    float wt = 0.0f;
-    if (valid) {
-      if (a.decay == GBA_DECAY_TOKEN) {
-        wt = s_w[m];
-      } else {
-        const int64_t tg = ((int64_t)key < a.R) ? (int64_t)a.tag[key] : -1;
-        int64_t s = tg - a.step + (int64_t)s_sm[m] + 1;
-        s = s < 0 ? 0 : s;
-        wt = (s <= a.iota) ? 1.0f : 0.0f;
-      }
-      packed[p] = (jv & kIndexMask) | (head ? kHead : 0u) | (newc ? kNewC : 0u) |
-                  (wt == 0.0f ? kZeroW : 0u) | ((wt != 0.0f && wt != 1.0f) ? kNonUnit : 0u);
-    }
-    hm[r] = __ballot(head);
-    keyr[r] = key;
-    carry_key = __shfl(key, kWave - 1, kWave);
-    carry_m = __shfl(m, kWave - 1, kWave);
-    carry_ok = (pw + r * kWave + kWave - 1) < N;
-  }
-  uint32_t wave_heads = 0;
-#pragma unroll
-  for (int r = 0; r < kRounds; ++r) wave_heads += (uint32_t)__popcll(hm[r]);
-  if (lane == 0) s_wave_heads[w] = wave_heads;
-  __syncthreads();
-  uint32_t before = seg_base;
-  for (int k = 0; k < w; ++k) before += s_wave_heads[k];
-#pragma unroll
-  for (int r = 0; r < kRounds; ++r) {
-    const int64_t p = pw + r * kWave + lane;
-    const uint32_t below = (uint32_t)__popcll(hm[r] & lt);
-    if ((hm[r] >> lane) & 1ull) {
-      const int64_t seg = (int64_t)before + below;
-      if (seg < N) {
-        a.unique_ids[seg] = (int64_t)keyr[r];
-        a.seg_offsets[seg] = p;
+      prev_ok = p0 > 0 && p0 - 1 < N;
+      if (prev_ok) {
+        kp = a.keys[p0 - 1];
+        const uint32_t jp = a.vals[p0 - 1];
+        mp = (int64_t)jp < N ? contribution_of(s_off, s_bucket, q, K, jp) : 0;
       }
     }
+    uint32_t word[kMetaPer];
+    uint32_t heads = 0, head_bits = 0;
+#pragma unroll
+    for (int e = 0; e < kMetaPer; ++e) {
+      const bool valid = p0 + e < N;
+      const bool head = valid && (e == 0 ? (!prev_ok || key[0] != kp) : key[e] != key[e - 1]);
+      const bool newc = valid && (head || m[e] != (e == 0 ? mp : m[e - 1]));
+      float wt = 0.0f;
+      if (valid) {
+        if (a.decay == GBA_DECAY_TOKEN) {
+          wt = s_w[m[e]];
+        } else {
+          const int64_t tg = ((int64_t)key[e] < a.R) ? (int64_t)a.tag[key[e]] : -1;
+          int64_t st = tg - a.step + (int64_t)s_sm[m[e]] + 1;
+          st = st < 0 ? 0 : st;
+          wt = (st <= a.iota) ? 1.0f : 0.0f;
+        }
+      }
+      word[e] = (jv[e] & kIndexMask) | (head ? kHead : 0u) | (newc ? kNewC : 0u) |
+                (wt == 0.0f ? kZeroW : 0u) | ((wt != 0.0f && wt != 1.0f) ? kNonUnit : 0u);
+      heads += head ? 1u : 0u;
+      head_bits |= head ? (1u << e) : 0u;
+    }
+    if (p0 + kMetaPer - 1 < N) {
+      *reinterpret_cast<u32x4*>(packed + p0) = u32x4{word[0], word[1], word[2], word[3]};
+    } else {
+#pragma unroll
+      for (int e = 0; e < kMetaPer; ++e)
+        if (p0 + e < N) packed[p0 + e] = word[e];
+    }
+    // segment numbers: the tile's base, the waves before, the lanes before
+    const uint32_t incl = wave_inclusive_scan(heads);
+    if (lane == kWave - 1) s_wave_heads[w] = incl;
+    __syncthreads();
+    uint32_t before = tile_seg_base[tile] + incl - heads;
+    for (int k = 0; k < w; ++k) before += s_wave_heads[k];
     // segments that start before each group-aligned position
-    if ((p & (kGroupSpan - 1)) == 0 && p < N) base32[p / kGroupSpan] = before + below;
-    before += (uint32_t)__popcll(hm[r]);
-  }
-  __syncthreads();   // s_wave_heads is rewritten by the next tile
+    if ((p0 & (kGroupSpan - 1)) == 0 && p0 < N) base32[p0 / kGroupSpan] = before;
+#pragma unroll
+    for (int e = 0; e < kMetaPer; ++e) {
+      if ((head_bits >> e) & 1u) {
+        if ((int64_t)before < N) {   // always true when the numbering is consistent
+          a.unique_ids[before] = (int64_t)key[e];
+          a.seg_offsets[before] = p0 + e;
+        }
+        ++before;
+      }
+    }
+    __syncthreads();   // s_wave_heads is rewritten by the next tile
   }
 }
 
