@@ -6,8 +6,8 @@
  * recommendation models", arXiv 2205.11048.  Sec. 3.1 defines the token
  * mechanism and the tolerance function (Eq. 1); Alg. 2 (PS workflow, push
  * responder) pops the K buffered gradients of one global batch, decays them,
- * takes the weighted sums (dense: divided by N_a; embeddings: divided by the
- * number of workers that encountered the ID) and applies them.  K here is the
+ * takes the weighted sums (dense: divided by N_a; embeddings: divided by how
+ * many workers sent the ID) and applies them.  K here is the
  * paper's M = N_a, the number of local-batch gradients aggregated per step.
  *
  * Conventions shared by every call:
@@ -191,8 +191,8 @@ gba_status gba_aggregate_apply_dense_adam(const float* const* grads, const float
                                           int64_t t, hipStream_t stream);
 
 /*
- * Early weighted sum of the dense gradients (App. B, with Alg. 2: the weighted
- * sum can be taken over some gradients in advance, from their tokens).  The
+ * Early weighted sum of the dense gradients (App. B, with Alg. 2: the PS may
+ * sum part of the buffer ahead of time, weighted by the tokens).  The
  * weight of a contribution depends only on its token and the step it will be
  * applied at, both known when it arrives, so it can be folded into a running
  * sum right away and the buffer holds P doubles instead of K gradients.

@@ -15,9 +15,9 @@ recommendation models" (arXiv 2205.11048).
   them, update each ID's tag of last appearance, decay dense gradients by the
   token, decay embedding gradients by the ID tag and the token, sum the dense
   gradients with the weights and divide by N_a, sum the embedding gradients
-  with the weights and divide by the number of workers that encountered the ID.
-* App. B (workflows of GBA): the weighted sum may be taken over some
-  gradients in advance, from their tokens (the early weighted sum).
+  with the weights and divide by how many workers sent the ID.
+* App. B (workflows of GBA): part of the weighted sum may be taken ahead of
+  time, from the tokens (the early weighted sum).
 * Table 1 (Sec. 4.1): GBA runs with Adam; the asynchronous baseline with
   Adagrad.  The update rules are the textbook ones (Duchi, Hazan and Singer,
   JMLR 2011; Kingma and Ba, ICLR 2015), since the paper names them only.
@@ -116,9 +116,9 @@ def aggregate_dense_magnitude(grads, w):
 # --------------------------------------------------------------------------
 def accumulate_dense(run, grads, w):
     """Fold arriving contributions into the float64 running sum, in arrival
-    order: run += w_j * g_j for every j with w_j != 0 (App. B notes that the
-    weighted sum may be taken over some gradients in advance, from their
-    tokens; a weight depends only on the token and the step it is applied at).
+    order: run += w_j * g_j for every j with w_j != 0 (App. B allows part of
+    the weighted sum to be taken ahead of time; a weight depends only on the
+    token and the step it is applied at).
     ``run`` is updated in place and returned."""
     for j in range(len(grads)):
         if w[j] != 0:                               # excluded: never read (R2)

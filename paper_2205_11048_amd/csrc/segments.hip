@@ -1,7 +1,7 @@
 // Embedding gradients by ID (Alg. 2, push responder): after the occurrences
 // are sorted by ID, every run of equal IDs is one segment.  For each segment
 // this computes its ID and start (dedup), c_r (number of contributions that
-// hold the ID: the divisor "number of workers that encountered the ID"),
+// hold the ID: the divisor of Alg. 2, the count of workers that sent the ID),
 // W_r (contributions whose weight for the ID is non-zero), and the weighted
 // sum of the rows divided by c_r (or by K).  The weight of a contribution for
 // a row is its token weight, or in per-ID mode [max(0, tag[r] - tau_m + 1) <=

@@ -831,3 +831,11 @@ def test_graph_replays_of_a_pull_match_eager_pulls():
         assert torch.equal(outs[0]["u"][:U], outs[1]["u"][:U]) and torch.equal(outs[0]["inv"], outs[1]["inv"])
         assert torch.equal(outs[0]["rows"][:U], outs[1]["rows"][:U]), i
     assert int(host(err)[0]) == 0
+
+
+def test_hash_find_or_insert_empty_request():
+    st = _HashStore(64, max_rows=10, n_max=1)
+    st.rows_of(np.array([3, 9], np.int64))
+    rows, nn = st.rows_of(np.zeros(0, np.int64))
+    assert rows.size == 0 and nn == 0
+    assert int(host(st.num_rows)[0]) == 2 and int(host(st.err)[0]) == 0
