@@ -839,3 +839,76 @@ def test_hash_find_or_insert_empty_request():
     rows, nn = st.rows_of(np.zeros(0, np.int64))
     assert rows.size == 0 and nn == 0
     assert int(host(st.num_rows)[0]) == 2 and int(host(st.err)[0]) == 0
+
+
+# ------------------------------------------------ randomised shapes (hypothesis)
+from hypothesis import HealthCheck, given, settings, strategies as hst   # noqa: E402
+
+
+@settings(max_examples=60, deadline=None, derandomize=True,
+          suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large])
+@given(K=hst.integers(1, 12), n_max=hst.integers(0, 3000), R=hst.sampled_from([1, 2, 17, 1000, 70_000, 1 << 20]),
+       D=hst.sampled_from([4, 8, 12, 32, 64, 256]), decay=hst.sampled_from(["token", "id_tag"]),
+       norm=hst.sampled_from(["per_id_count", "by_k"]), seed=hst.integers(0, 2 ** 31 - 1),
+       dyadic=hst.booleans(), zipf_s=hst.sampled_from([0.6, 1.1, 2.0]))
+def test_sparse_random_shapes(K, n_max, R, D, decay, norm, seed, dyadic, zipf_s):
+    """Random shapes, empty contributions, tiny and large tables, hot and
+    spread IDs: the GPU equals the oracle (exactly on dyadic values)."""
+    rng = np.random.default_rng(seed)
+    sizes = rng.integers(0, n_max + 1, K)
+    sizes[rng.random(K) < 0.2] = 0
+    kind = counter.KIND_DYADIC if dyadic else counter.KIND_GRAD
+    ids, rows, off, tokens, tag = _case(K, sizes, R, D, seed % 100_000, zipf_s=zipf_s, kind=kind, stale_hi=4)
+    w, _, _ = oracle.token_weights(tokens, 1000, 2)
+    res = _run_sparse(ids, rows, off, w, tokens, 1000, 2, R, tag if decay == "id_tag" else None, decay, norm)
+    _check_sparse(res, ids, rows, off, w, tokens, 1000, 2, tag if decay == "id_tag" else None, decay, norm,
+                  expect_exact=dyadic)
+
+
+@settings(max_examples=40, deadline=None, derandomize=True, suppress_health_check=[HealthCheck.too_slow])
+@given(K=hst.integers(1, 70), P=hst.integers(1, 150_000), offset=hst.sampled_from([0, 0, 1, 3]),
+       frac=hst.booleans(), seed=hst.integers(0, 2 ** 31 - 1), J=hst.integers(1, 9),
+       opt=hst.sampled_from(["adagrad", "adam"]))
+def test_dense_random_shapes(K, P, offset, frac, seed, J, opt):
+    """Random K, P, alignment and weights (0/1 or fractional): the one-shot sum
+    equals the oracle bitwise; the fused call and the early sum folded J at a
+    time give bitwise the same parameters and state as the two separate calls."""
+    rng = np.random.default_rng(seed)
+    host_g = [counter.values_range(seed % 1000, 400 + m, 0, P, counter.KIND_GRAD, counter.grad_scale(1e-2))
+              for m in range(K)]
+    w = (rng.random(K) < 0.8).astype(np.float32)
+    if frac:
+        w *= rng.choice(np.array([0.25, 0.5, 1.0, 2.0], np.float32), K)
+    grads = [dev_at(g if w[m] != 0 else np.full(P, np.nan, np.float32), offset) for m, g in enumerate(host_g)]
+    table, w_d = gba.pointer_table(grads), dev(w)
+    g_bar = torch.empty(P, device=DEV)
+    gba.gba_aggregate_dense(table, w_d, P, g_bar)
+    assert_exact(host(g_bar), oracle.aggregate_dense(host_g, w), "g_bar")
+    p0 = counter.values_range(seed % 1000, 1, 0, P, counter.KIND_PARAM)
+    kinds = workload.state_kinds(opt)
+    s0 = [counter.values_range(seed % 1000, 2 + k, 0, P, kind) for k, (_, _, kind) in enumerate(kinds)]
+    runs = []
+    for mode in ("separate", "fused", "early"):
+        p, s_ = dev_at(p0, offset), [dev(x) for x in s0]
+        if mode == "separate":
+            if opt == "adagrad":
+                gba.gba_apply_adagrad(p, s_[0], g_bar, 0.01, 1e-8)
+            else:
+                gba.gba_apply_adam(p, s_[0], s_[1], g_bar, 1e-3, 0.9, 0.999, 1e-8, 7)
+        elif mode == "fused":
+            if opt == "adagrad":
+                gba.gba_aggregate_apply_dense_adagrad(table, w_d, P, p, s_[0], 0.01, 1e-8)
+            else:
+                gba.gba_aggregate_apply_dense_adam(table, w_d, P, p, s_[0], s_[1], 1e-3, 0.9, 0.999, 1e-8, 7)
+        else:
+            run = torch.zeros(P, dtype=torch.float64, device=DEV)
+            for lo in range(0, K, J):
+                gba.gba_accumulate_dense(gba.pointer_table(grads[lo:lo + J]), w_d[lo:lo + J], P, run)
+            if opt == "adagrad":
+                gba.gba_finalize_apply_dense_adagrad(run, K, P, p, s_[0], 0.01, 1e-8)
+            else:
+                gba.gba_finalize_apply_dense_adam(run, K, P, p, s_[0], s_[1], 1e-3, 0.9, 0.999, 1e-8, 7)
+        runs.append([host(p)] + [host(x) for x in s_])
+    for other in runs[1:]:
+        for a, b in zip(runs[0], other):
+            assert_exact(b, a, "fused / early vs separate")
