@@ -214,6 +214,23 @@ def test_sparse_all_distinct():
     assert ref["num_unique"] == 9999 and np.all(ref["contrib_count"] == 1)
 
 
+# ID ranges whose key widths select every plan of the ID sort: one to four
+# 8-bit digit passes with a first (narrowest) digit of 1, 2, 5 or 8 bits
+# (R = 200: 8; 1000: 2+8; 5000: 5+8; 70,000: 1+8+8; 2^21: 5+8+8; 2^26:
+# 2+8+8+8; 2^29 - 3: 5+8+8+8; 2^31 + 5: 8+8+8+8).  18,411 occurrences span
+# several sort tiles and a ragged last one; dyadic rows make every sum exact,
+# so any misplaced key shows.
+@pytest.mark.parametrize("R", [200, 1000, 5000, 70_000, 1 << 21, 1 << 26, (1 << 29) - 3, (1 << 31) + 5])
+def test_sparse_sort_digit_plans(R):
+    K, D = 3, 4
+    sizes = np.array([7000, 5000, 6411])
+    ids, rows, off, tokens, _ = _case(K, sizes, R, D, seed=R % 997, zipf_s=1.05, kind=counter.KIND_DYADIC)
+    assert ids.max() >= R // 2   # the top digit is exercised
+    w, _, _ = oracle.token_weights(tokens, 1000, 3)
+    res = _run_sparse(ids, rows, off, w, tokens, 1000, 3, R)
+    _check_sparse(res, ids, rows, off, w, tokens, 1000, 3, expect_exact=True)
+
+
 def test_sparse_empty():
     K, D = 3, 8
     off = np.zeros(K + 1, np.int64)
