@@ -3,12 +3,12 @@
 // push-step can deduplicate them and reduce their rows (Alg. 2: gradients of
 // the embedding parameters are processed by ID).
 //
-// Each digit takes three launches: digit counts per tile (1 KB per tile,
-// tile-major) and per chunk of four tiles; an exclusive scan of every digit's
-// chunk counts, one block per digit; and a scatter in which each tile adds up
-// its own offsets (digit start + chunk prefix + the tiles before it in its
-// chunk), ranks its keys stably in LDS and writes runs of equal digits
-// together.
+// Each digit takes three launches: digit counts per chunk of four tiles, and
+// per tile the counts of the earlier tiles of its chunk (1 KB per tile,
+// tile-major); an exclusive scan of every digit's chunk counts, one block per
+// digit; and a scatter in which each tile adds up its own offsets (digit
+// start + chunk prefix + the tiles before it in its chunk), ranks its keys
+// stably in LDS and writes runs of equal digits together.
 // Ranks inside a wave come from ballots that match lanes holding the same
 // digit, so skewed (Zipf) keys cost no LDS atomics on hot bins in the scatter.
 #include "gba_device.hpp"
@@ -80,7 +80,7 @@ __device__ __forceinline__ uint32_t load_key(const void* src, int64_t i, int64_t
   return static_cast<const uint32_t*>(src)[i];
 }
 
-// Digit counts of one tile, one 1 KB row per tile.  One wave takes a whole
+// Digit counts of the four tiles of one chunk.  One wave takes a whole
 // tile (4 ITEMS keys per lane, loaded as 16-byte vectors, so many bytes are in
 // flight per wave) and adds one count per run of equal digits among each
 // lane's 4 consecutive keys.
@@ -160,16 +160,20 @@ sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n, int64_t tiles
         if (len) atomicAdd(&h[w][cur], len);
       }
     }
-    __builtin_amdgcn_wave_barrier();
-    for (int d = lane; d < kRadix; d += kWave) hist[tile * kRadix + d] = h[w][d];
   }
   __syncthreads();
-  // the block's tiles form one chunk
+  // the block's tiles form one chunk: each tile's row holds the counts of the
+  // chunk's earlier tiles (so the scatter needs one row, not a loop over
+  // rows), and the chunk row holds the chunk's counts
   {
     const int d = threadIdx.x;
+    const int64_t t0 = (int64_t)blockIdx.x * kSortWaves;
     uint32_t s = 0;
 #pragma unroll
-    for (int k = 0; k < kSortWaves; ++k) s += h[k][d];
+    for (int k = 0; k < kSortWaves; ++k) {
+      if (t0 + k < tiles) hist[(t0 + k) * kRadix + d] = s;
+      s += h[k][d];
+    }
     chunk[(int64_t)blockIdx.x * kRadix + d] = s;
   }
   if (FIRST && bad) raise_error(err, GBA_DERR_ID_RANGE);
@@ -234,18 +238,13 @@ sort_scatter_kernel(const void* __restrict__ keys_in, const uint32_t* __restrict
   __shared__ uint32_t s_vals[kTile];
   for (int i = threadIdx.x; i < kSortWaves * kRadix; i += kSortBlock) (&cnt[0][0])[i] = 0;
   const int64_t tile = xcd_tile(blockIdx.x, gridDim.x);   // the grid has one block per tile
-  {
-    // global position of the tile's first key of each digit value: where the
-    // digit starts, plus its count in earlier chunks, plus in earlier tiles of
-    // this tile's chunk
-    const int d = threadIdx.x;
-    const int64_t c = tile / kChunk;
-    uint32_t off = chunk[c * kRadix + d];
-    for (int64_t t = c * kChunk; t < tile; ++t) off += hist[t * kRadix + d];
-    uint32_t all;
-    const uint32_t start = block_exclusive_scan<kSortBlock>(total[d], tmp, &all);   // also publishes cnt = 0
-    global_base[d] = start + off;
-  }
+  // global position of the tile's first key of each digit value: where the
+  // digit starts, plus its count in earlier chunks, plus in earlier tiles of
+  // this tile's chunk.  Its loads are issued first and the tile's keys right
+  // after them, so the keys are in flight during the scan of the digit starts.
+  const int d = threadIdx.x;
+  const uint32_t off = chunk[(tile / kChunk) * kRadix + d] + hist[tile * kRadix + d];
+  const uint32_t tot = total[d];
   const int w = threadIdx.x / kWave;
   const int64_t tile0 = tile * kTile;
   const int64_t base = tile0 + (int64_t)w * (kWave * ITEMS) + lane_id();
@@ -260,6 +259,11 @@ sort_scatter_kernel(const void* __restrict__ keys_in, const uint32_t* __restrict
     const bool active = i < n;
     key[r] = active ? load_key<FIRST>(keys_in, i, R, &bad) : 0u;
     val[r] = active ? (FIRST ? (uint32_t)i : vals_in[i]) : 0u;
+  }
+  {
+    uint32_t all;
+    const uint32_t start = block_exclusive_scan<kSortBlock>(tot, tmp, &all);   // also publishes cnt = 0
+    global_base[d] = start + off;
   }
   (void)bad;   // range errors are reported by the histogram launch
   // Stable rank within (wave, digit): rounds in index order, lanes in order.
@@ -279,7 +283,6 @@ sort_scatter_kernel(const void* __restrict__ keys_in, const uint32_t* __restrict
   }
   __syncthreads();
   {
-    const int d = threadIdx.x;
     uint32_t c[kSortWaves];
     uint32_t s = 0;
 #pragma unroll
