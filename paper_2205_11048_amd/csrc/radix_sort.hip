@@ -67,15 +67,15 @@ __device__ __forceinline__ uint64_t match_digit(uint32_t digit, int bits, bool a
 
 // Key of position i: from the int64 IDs on the first pass (checked against
 // [0, R); an ID outside it is reported and sorted as 0), else the u32 keys.
+// The check is a select, not a branch, so a lane's loads are all issued
+// before the first one is waited for.
 template <bool FIRST>
 __device__ __forceinline__ uint32_t load_key(const void* src, int64_t i, int64_t R, bool* bad) {
   if (FIRST) {
     const int64_t id = static_cast<const int64_t*>(src)[i];
-    if (id < 0 || id >= R) {
-      *bad = true;
-      return 0u;
-    }
-    return (uint32_t)id;
+    const bool out = id < 0 || id >= R;
+    *bad |= out;
+    return out ? 0u : (uint32_t)id;
   }
   return static_cast<const uint32_t*>(src)[i];
 }
@@ -223,25 +223,53 @@ __device__ __forceinline__ int64_t xcd_tile(int64_t b, int64_t tiles) {
   return x * q + (x < r ? x : r) + i;
 }
 
+// Exclusive scans of x and of y over the block, behind one barrier: every
+// thread adds up the totals of the waves before its own.  `tmp` holds
+// 2 * kSortWaves words.
+__device__ __forceinline__ void block_exclusive_scan2(uint32_t x, uint32_t y, uint32_t* tmp, uint32_t* ex_x,
+                                                      uint32_t* ex_y) {
+  const int w = threadIdx.x / kWave;
+  const uint32_t ix = wave_inclusive_scan(x), iy = wave_inclusive_scan(y);
+  if (lane_id() == kWave - 1) {
+    tmp[w] = ix;
+    tmp[kSortWaves + w] = iy;
+  }
+  __syncthreads();
+  uint32_t bx = 0, by = 0;
+#pragma unroll
+  for (int k = 0; k < kSortWaves; ++k) {
+    if (k < w) {
+      bx += tmp[k];
+      by += tmp[kSortWaves + k];
+    }
+  }
+  *ex_x = bx + ix - x;
+  *ex_y = by + iy - y;
+}
+
 template <bool FIRST, int ITEMS>
 __global__ void __launch_bounds__(kSortBlock)
 sort_scatter_kernel(const void* __restrict__ keys_in, const uint32_t* __restrict__ vals_in,
                     uint32_t* __restrict__ keys_out, uint32_t* __restrict__ vals_out, int64_t n,
                     int shift, int bits, int64_t R, const uint32_t* __restrict__ hist,
                     const uint32_t* __restrict__ chunk, const uint32_t* __restrict__ total) {
+  // per (wave, digit): the wave's count, then the tile position of the wave's
+  // first key of that digit
   __shared__ uint32_t cnt[kSortWaves][kRadix];
-  __shared__ uint32_t digit_start[kRadix];
-  __shared__ uint32_t global_base[kRadix];
-  __shared__ uint32_t tmp[kSortBlock / kWave + 1];
+  // per digit: the output position minus the tile position of its keys
+  // (first the chunk and tile offset alone), and the digit total
+  __shared__ uint32_t gshift[kRadix];
+  __shared__ uint32_t s_tot[kRadix];
+  __shared__ uint32_t tmp[2 * kSortWaves];
   constexpr int64_t kTile = tile_keys<ITEMS>();
   __shared__ uint32_t s_keys[kTile];
   __shared__ uint32_t s_vals[kTile];
-  for (int i = threadIdx.x; i < kSortWaves * kRadix; i += kSortBlock) (&cnt[0][0])[i] = 0;
   const int64_t tile = xcd_tile(blockIdx.x, gridDim.x);   // the grid has one block per tile
-  // global position of the tile's first key of each digit value: where the
-  // digit starts, plus its count in earlier chunks, plus in earlier tiles of
-  // this tile's chunk.  Its loads are issued first and the tile's keys right
-  // after them, so the keys are in flight during the scan of the digit starts.
+  // Where the tile's keys of digit d go: where the digit starts (scan of the
+  // digit totals), plus its count in earlier chunks, plus in earlier tiles of
+  // this tile's chunk.  The loads are issued with the keys' and used only
+  // after the ranking, where one scan finds both the digit starts and the
+  // tile's own digit offsets.
   const int d = threadIdx.x;
   const uint32_t off = chunk[(tile / kChunk) * kRadix + d] + hist[tile * kRadix + d];
   const uint32_t tot = total[d];
@@ -252,20 +280,34 @@ sort_scatter_kernel(const void* __restrict__ keys_in, const uint32_t* __restrict
   const uint64_t lt = lanemask_lt();
 
   uint32_t key[ITEMS], val[ITEMS], rank[ITEMS];
-  bool bad = false;
-#pragma unroll
-  for (int r = 0; r < ITEMS; ++r) {
-    const int64_t i = base + (int64_t)r * kWave;
-    const bool active = i < n;
-    key[r] = active ? load_key<FIRST>(keys_in, i, R, &bad) : 0u;
-    val[r] = active ? (FIRST ? (uint32_t)i : vals_in[i]) : 0u;
-  }
+  // Every lane loads (lanes past the end re-read the last key, n > 0), so no
+  // branch waits on a load and all of a lane's loads are in flight at once.
+  // An ID outside [0, R) is sorted as 0 (the histogram launch reports it);
+  // the first pass's values are the positions themselves, formed when stored.
   {
-    uint32_t all;
-    const uint32_t start = block_exclusive_scan<kSortBlock>(tot, tmp, &all);   // also publishes cnt = 0
-    global_base[d] = start + off;
+    uint64_t raw[FIRST ? ITEMS : 1];
+#pragma unroll
+    for (int r = 0; r < ITEMS; ++r) {
+      const int64_t i = base + (int64_t)r * kWave;
+      const int64_t ic = i < n ? i : n - 1;
+      if (FIRST) {
+        raw[r] = static_cast<const uint64_t*>(keys_in)[ic];
+      } else {
+        key[r] = static_cast<const uint32_t*>(keys_in)[ic];
+        val[r] = vals_in[ic];
+      }
+    }
+    if (FIRST) {
+#pragma unroll
+      for (int r = 0; r < ITEMS; ++r) key[r] = raw[r] < (uint64_t)R ? (uint32_t)raw[r] : 0u;
+    }
   }
-  (void)bad;   // range errors are reported by the histogram launch
+  // parked in LDS during the ranking (registers are what limit residency)
+  gshift[d] = off;
+  s_tot[d] = tot;
+  // each wave counts in its own row
+  for (int i = lane_id(); i < kRadix; i += kWave) cnt[w][i] = 0u;
+  __builtin_amdgcn_wave_barrier();
   // Stable rank within (wave, digit): rounds in index order, lanes in order.
 #pragma unroll
   for (int r = 0; r < ITEMS; ++r) {
@@ -283,6 +325,7 @@ sort_scatter_kernel(const void* __restrict__ keys_in, const uint32_t* __restrict
   }
   __syncthreads();
   {
+    // thread d alone reads and rewrites column d of cnt and entry d of gshift
     uint32_t c[kSortWaves];
     uint32_t s = 0;
 #pragma unroll
@@ -290,9 +333,9 @@ sort_scatter_kernel(const void* __restrict__ keys_in, const uint32_t* __restrict
       c[k] = cnt[k][d];
       s += c[k];
     }
-    uint32_t total;
-    const uint32_t ex = block_exclusive_scan<kSortBlock>(s, tmp, &total);
-    digit_start[d] = ex;
+    uint32_t ex, start;
+    block_exclusive_scan2(s, s_tot[d], tmp, &ex, &start);
+    gshift[d] = start + gshift[d] - ex;   // modulo 2^32
     uint32_t run = ex;
 #pragma unroll
     for (int k = 0; k < kSortWaves; ++k) {
@@ -308,15 +351,14 @@ sort_scatter_kernel(const void* __restrict__ keys_in, const uint32_t* __restrict
       const uint32_t digit = (key[r] >> shift) & mask;
       const uint32_t pos = cnt[w][digit] + rank[r];
       s_keys[pos] = key[r];
-      s_vals[pos] = val[r];
+      s_vals[pos] = FIRST ? (uint32_t)i : val[r];
     }
   }
   __syncthreads();
   const int64_t tile_n = (n - tile0) < kTile ? (n - tile0) : kTile;
   for (int i = threadIdx.x; i < tile_n; i += kSortBlock) {
     const uint32_t k = s_keys[i];
-    const uint32_t digit = (k >> shift) & mask;
-    const uint32_t g = global_base[digit] + ((uint32_t)i - digit_start[digit]);
+    const uint32_t g = gshift[(k >> shift) & mask] + (uint32_t)i;
     if ((int64_t)g < n) {   // always true when the counts are consistent
       keys_out[g] = k;
       vals_out[g] = s_vals[i];
