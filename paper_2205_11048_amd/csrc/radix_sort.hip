@@ -80,10 +80,80 @@ __device__ __forceinline__ uint32_t load_key(const void* src, int64_t i, int64_t
   return static_cast<const uint32_t*>(src)[i];
 }
 
-// Digit counts of the four tiles of one chunk.  One wave takes a whole
-// tile (4 ITEMS keys per lane, loaded as 16-byte vectors, so many bytes are in
-// flight per wave) and adds one count per run of equal digits among each
-// lane's 4 consecutive keys.
+// Digit counts of one tile into the wave's LDS row h_row.  Lane l holds keys
+// tile0 + 4 * (l + 64 * c) + e, c < ITEMS, e < 4: each vector load of the
+// wave covers 1 KB of consecutive keys.  FULL (every key of the tile exists)
+// drops the bounds checks, so no branch waits on a load and a phase's loads
+// are in flight together; only the last tile of a pass can be partial.
+// Returns whether an ID outside [0, R) was seen (first pass).
+template <bool FIRST, int ITEMS, bool FULL>
+__device__ __forceinline__ bool count_tile(const void* __restrict__ keys_in, int64_t n, int64_t tile0, int shift,
+                                           uint32_t mask, int64_t R, uint32_t* h_row, int lane) {
+  constexpr int kHistKeys = 4 * ITEMS;   // keys per lane
+  // eight vectors (32 keys) per lane per phase, all in flight together
+  constexpr int kVecs = 8;
+  static_assert(kHistKeys % (4 * kVecs) == 0, "whole phases per tile");
+  bool bad = false;
+#pragma unroll
+  for (int ph = 0; ph < kHistKeys / 4 / kVecs; ++ph) {
+    uint32_t digit[4 * kVecs];
+#pragma unroll
+    for (int cc = 0; cc < kVecs; ++cc) {
+      const int c = ph * kVecs + cc;
+      const int64_t i0 = tile0 + 4 * ((int64_t)lane + (int64_t)kWave * c);
+      if (FULL || i0 + 3 < n) {
+        uint32_t k4[4];
+        if (FIRST) {
+          const int64_t* ids = static_cast<const int64_t*>(keys_in);
+          typedef int64_t i64x2 __attribute__((ext_vector_type(2)));
+          const i64x2 a = *reinterpret_cast<const i64x2*>(ids + i0);
+          const i64x2 b = *reinterpret_cast<const i64x2*>(ids + i0 + 2);
+          const int64_t v[4] = {a.x, a.y, b.x, b.y};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const bool out = v[e] < 0 || v[e] >= R;
+            bad |= out;
+            k4[e] = out ? 0u : (uint32_t)v[e];
+          }
+        } else {
+          const u32x4 v = *reinterpret_cast<const u32x4*>(static_cast<const uint32_t*>(keys_in) + i0);
+          k4[0] = v.x; k4[1] = v.y; k4[2] = v.z; k4[3] = v.w;
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) digit[4 * cc + e] = (k4[e] >> shift) & mask;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          digit[4 * cc + e] = (i0 + e < n) ? (load_key<FIRST>(keys_in, i0 + e, R, &bad) >> shift) & mask : 0u;
+      }
+    }
+    // one LDS add per run of equal digits among each lane's 4 consecutive keys
+#pragma unroll
+    for (int cc = 0; cc < kVecs; ++cc) {
+      const int c = ph * kVecs + cc;
+      const int64_t i0 = tile0 + 4 * ((int64_t)lane + (int64_t)kWave * c);
+      uint32_t cur = digit[4 * cc];
+      uint32_t len = (FULL || i0 < n) ? 1u : 0u;
+#pragma unroll
+      for (int e = 1; e < 4; ++e) {
+        if (FULL || i0 + e < n) {
+          if (digit[4 * cc + e] == cur) {
+            ++len;
+          } else {
+            atomicAdd(&h_row[cur], len);
+            cur = digit[4 * cc + e];
+            len = 1;
+          }
+        }
+      }
+      if (len) atomicAdd(&h_row[cur], len);
+    }
+  }
+  return bad;
+}
+
+// Digit counts of the four tiles of one chunk, one wave per tile; each adds
+// one count per run of equal digits among each lane's 4 consecutive keys.
 template <bool FIRST, int ITEMS>
 __global__ void __launch_bounds__(kSortBlock)
 sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n, int64_t tiles, int shift, int bits,
@@ -97,69 +167,12 @@ sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n, int64_t tiles
   const int64_t tile = (int64_t)blockIdx.x * kSortWaves + w;
   bool bad = false;
   if (tile < tiles) {
-    constexpr int kHistKeys = 4 * ITEMS;   // keys per lane
     const uint32_t mask = (1u << bits) - 1u;
-    // lane l holds keys tile0 + 4 * (l + 64 * c) + e, c < ITEMS, e < 4: each
-    // vector load of the wave covers 1 KB of consecutive keys
     const int64_t tile0 = tile * tile_keys<ITEMS>();
-    // four vectors (16 keys) per lane per phase: few registers, so eight waves
-    // per SIMD keep loads in flight while others count
-    constexpr int kVecs = 4;
-#pragma unroll
-    for (int ph = 0; ph < kHistKeys / 4 / kVecs; ++ph) {
-      uint32_t digit[4 * kVecs];
-#pragma unroll
-      for (int cc = 0; cc < kVecs; ++cc) {
-        const int c = ph * kVecs + cc;
-        const int64_t i0 = tile0 + 4 * ((int64_t)lane + (int64_t)kWave * c);
-        if (i0 + 3 < n) {
-          uint32_t k4[4];
-          if (FIRST) {
-            const int64_t* ids = static_cast<const int64_t*>(keys_in);
-            typedef int64_t i64x2 __attribute__((ext_vector_type(2)));
-            const i64x2 a = *reinterpret_cast<const i64x2*>(ids + i0);
-            const i64x2 b = *reinterpret_cast<const i64x2*>(ids + i0 + 2);
-            const int64_t v[4] = {a.x, a.y, b.x, b.y};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const bool out = v[e] < 0 || v[e] >= R;
-              bad |= out;
-              k4[e] = out ? 0u : (uint32_t)v[e];
-            }
-          } else {
-            const u32x4 v = *reinterpret_cast<const u32x4*>(static_cast<const uint32_t*>(keys_in) + i0);
-            k4[0] = v.x; k4[1] = v.y; k4[2] = v.z; k4[3] = v.w;
-          }
-#pragma unroll
-          for (int e = 0; e < 4; ++e) digit[4 * cc + e] = (k4[e] >> shift) & mask;
-        } else {
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            digit[4 * cc + e] = (i0 + e < n) ? (load_key<FIRST>(keys_in, i0 + e, R, &bad) >> shift) & mask : 0u;
-        }
-      }
-      // one LDS add per run of equal digits among each lane's 4 consecutive keys
-#pragma unroll
-      for (int cc = 0; cc < kVecs; ++cc) {
-        const int c = ph * kVecs + cc;
-        const int64_t i0 = tile0 + 4 * ((int64_t)lane + (int64_t)kWave * c);
-        uint32_t cur = digit[4 * cc];
-        uint32_t len = i0 < n ? 1u : 0u;
-#pragma unroll
-        for (int e = 1; e < 4; ++e) {
-          if (i0 + e < n) {
-            if (digit[4 * cc + e] == cur) {
-              ++len;
-            } else {
-              atomicAdd(&h[w][cur], len);
-              cur = digit[4 * cc + e];
-              len = 1;
-            }
-          }
-        }
-        if (len) atomicAdd(&h[w][cur], len);
-      }
-    }
+    if (tile0 + tile_keys<ITEMS>() <= n)
+      bad = count_tile<FIRST, ITEMS, true>(keys_in, n, tile0, shift, mask, R, h[w], lane);
+    else
+      bad = count_tile<FIRST, ITEMS, false>(keys_in, n, tile0, shift, mask, R, h[w], lane);
   }
   __syncthreads();
   // the block's tiles form one chunk: each tile's row holds the counts of the

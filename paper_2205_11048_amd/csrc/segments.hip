@@ -408,14 +408,22 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
       const u32x4 wa = wp[0], wb = wp[1];
       const uint32_t word[kBatch] = {wa.x, wa.y, wa.z, wa.w, wb.x, wb.y, wb.z, wb.w};
       if (i0 == 0) first_open = !(word[0] & kHead);
+      // Every lane issues all eight gathers: one whose row is not needed
+      // (past the group, a zero weight, a lane past D) reads the first 16
+      // bytes of the rows, which stay in cache, and is zeroed after.  With no
+      // load inside a branch, the compiler can count the loads in flight and
+      // never waits for all of them at once.
       f32x4 rv[kBatch];
+      bool use[kBatch];
 #pragma unroll
       for (int u = 0; u < kBatch; ++u) {
-        rv[u] = f32x4{0.f, 0.f, 0.f, 0.f};
         const uint32_t jv = word[u] & kIndexMask;
-        if (i0 + u < nvalid && !(word[u] & kZeroW) && lane_on && (int64_t)jv < N)
-          rv[u] = *reinterpret_cast<const f32x4*>(a.rows + (int64_t)jv * D + gl * 4);
+        use[u] = i0 + u < nvalid && !(word[u] & kZeroW) && lane_on && (int64_t)jv < N;
+        rv[u] = *reinterpret_cast<const f32x4*>(a.rows + (use[u] ? (int64_t)jv * D + gl * 4 : 0));
       }
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u)
+        if (!use[u]) rv[u] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int u = 0; u < kBatch; ++u) {
         const int i = i0 + u;
