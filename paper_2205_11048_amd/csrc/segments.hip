@@ -43,7 +43,6 @@ constexpr uint32_t kNewC = 1u << 30;              // first occurrence of a contr
 constexpr uint32_t kZeroW = 1u << 31;             // weight 0: the row is never read
 
 enum : uint32_t { kValid = 1, kOpen = 2, kPass = 4 };            // group flags
-enum : uint32_t { kHasFirst = 1, kHasLast = 2, kBlockPass = 4 }; // tile flags
 
 static inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 static inline size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
@@ -70,14 +69,15 @@ struct SegPartials {
   int32_t* first_ww;
   int32_t* last_cc;
   int32_t* last_ww;
-  uint32_t* last_seg;
-  uint32_t* flags;
+  u32x4* fix_list;       // per tile whose last chain continues into the next
+                         // tile: (tile, segment, last tile of the segment, 0)
+  uint32_t* fix_count;   // entries of fix_list (cleared before the row pass)
 };
 
 struct SegLayout {
   int64_t meta_tiles, row_tiles;
-  size_t off_heads, off_total, off_scan, off_buckets, off_packed, off_base32, off_flags, off_last_seg,
-      off_cnt, off_first_acc, off_last_acc, bytes;
+  size_t off_heads, off_total, off_scan, off_buckets, off_packed, off_base32,
+      off_cnt, off_first_acc, off_last_acc, off_fix, bytes;
 };
 
 static SegLayout seg_layout(int64_t N, int32_t D) {
@@ -93,9 +93,8 @@ static SegLayout seg_layout(int64_t N, int32_t D) {
   L.off_buckets = o;   o += align_up(kMaxBuckets * 4);
   L.off_packed = o;    o += align_up((n + kGroupSpan) * 4);   // padded: whole-group vector loads stay inside
   L.off_base32 = o;    o += align_up((n / kGroupSpan + 2) * 4);
-  L.off_flags = o;     o += align_up(rt * 4);
-  L.off_last_seg = o;  o += align_up(rt * 4);
   L.off_cnt = o;       o += align_up(rt * 16);
+  L.off_fix = o;       o += 256 + align_up(rt * 16);  // count, then the list
   L.off_first_acc = o; o += align_up(rt * (size_t)D * 8);
   L.off_last_acc = o;  o += align_up(rt * (size_t)D * 8);
   L.bytes = o;
@@ -180,6 +179,56 @@ __device__ __forceinline__ void load_contrib_tables(const SegmentArgs& a, const 
   for (int i = threadIdx.x; i < nb; i += kSegBlock) s_bucket[i] = buckets[i];
 }
 
+// The same tables in two halves, for K < 2 * kSegBlock: issue() loads a
+// thread's entries into registers with clamped indices (no branch, so the
+// caller can issue more loads before any is waited for) and store() writes
+// them to LDS.
+struct ContribTableRegs {
+  static constexpr int kR = 2;                            // K + 1 <= 2 * kSegBlock entries
+  static constexpr int kB = kMaxBuckets / kSegBlock;      // bucket entries per thread
+  int64_t off[kR], tok[kR];
+  float w[kR];
+  int32_t bucket[kB];
+
+  __device__ __forceinline__ void issue(const SegmentArgs& a, const int32_t* buckets, int nb) {
+#pragma unroll
+    for (int r = 0; r < kR; ++r) {
+      const int i = threadIdx.x + r * kSegBlock;
+      off[r] = a.offsets[i <= a.K ? i : a.K];
+      w[r] = a.w[i < a.K ? i : a.K - 1];
+      tok[r] = a.tokens[i < a.K ? i : a.K - 1];
+    }
+#pragma unroll
+    for (int r = 0; r < kB; ++r) {
+      const int i = threadIdx.x + r * kSegBlock;
+      bucket[r] = buckets[i < nb ? i : nb - 1];
+    }
+  }
+  __device__ __forceinline__ void store(const SegmentArgs& a, int nb, int32_t* s_off, float* s_w, int32_t* s_sm,
+                                        int32_t* s_bucket) const {
+#pragma unroll
+    for (int r = 0; r < kR; ++r) {
+      const int i = threadIdx.x + r * kSegBlock;
+      if (i <= a.K) {
+        const int64_t o = off[r] < 0 ? 0 : (off[r] > a.N ? a.N : off[r]);
+        s_off[i] = (int32_t)o;
+      }
+      if (i < a.K) {
+        s_w[i] = w[r];
+        int64_t sm = a.step - tok[r];
+        sm = sm < -(1 << 30) ? -(1 << 30) : (sm > (1 << 30) ? (1 << 30) : sm);
+        s_sm[i] = (int32_t)sm;
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < kB; ++r) {
+      const int i = threadIdx.x + r * kSegBlock;
+      if (i < nb) s_bucket[i] = bucket[r];
+    }
+  }
+};
+static_assert(kMaxBuckets % kSegBlock == 0, "whole bucket rounds");
+
 // ------------------------------------------------------------------ kernels
 __global__ void check_offsets_kernel(const int64_t* __restrict__ off, int K, int64_t N,
                                      int32_t* __restrict__ err) {
@@ -249,10 +298,12 @@ seg_heads_kernel(const uint32_t* __restrict__ keys, int64_t N, int64_t tiles, ui
 }
 
 __global__ void seg_finish_kernel(const uint32_t* __restrict__ total, int64_t N,
-                                  int64_t* __restrict__ num_unique, int64_t* __restrict__ seg_offsets) {
+                                  int64_t* __restrict__ num_unique, int64_t* __restrict__ seg_offsets,
+                                  uint32_t* __restrict__ fix_count) {
   const uint32_t U = *total;
   *num_unique = (int64_t)U;
   seg_offsets[U] = N;
+  *fix_count = 0u;   // the row pass appends to the fixup list
 }
 
 // Per-position pass: numbering, segment IDs and starts, packed words.
@@ -274,44 +325,62 @@ seg_meta_kernel(SegmentArgs a, const uint32_t* __restrict__ tile_seg_base,
   float* s_w = reinterpret_cast<float*>(s_dyn + K + 1);
   int32_t* s_sm = s_dyn + 2 * K + 1;
   int32_t* s_bucket = s_dyn + 3 * K + 1;
-  load_contrib_tables(a, buckets, nbuckets, s_off, s_w, s_sm, s_bucket);
+  // The lookup tables' loads are issued first (branch-free when K is below
+  // 512), then, when every position of the block exists, all loads of its
+  // tiles, so that the tables are waited for while the tiles are in flight.
+  const int64_t blk0 = (int64_t)blockIdx.x * kMetaTilesPerBlock * kMetaTile;
+  const bool full = blk0 + kMetaTilesPerBlock * kMetaTile <= N;
+  const bool small_k = K < ContribTableRegs::kR * kSegBlock;
+  ContribTableRegs tables;
+  if (small_k) tables.issue(a, buckets, nbuckets);
+  // Loaded unconditionally (a branch would make the compiler wait for them
+  // where its paths join): a block that is not full clamps its indices into
+  // the arrays (the key and value arrays are padded to 64 entries, so a
+  // 16-byte load at the last multiple of 4 below N stays inside them) and
+  // uses none of these values.
+  u32x4 kv[kMetaTilesPerBlock], vv[kMetaTilesPerBlock];
+  uint32_t kpv[kMetaTilesPerBlock], jpv[kMetaTilesPerBlock], sb[kMetaTilesPerBlock];
+  {
+    const int64_t last4 = (N - 1) & ~int64_t(kMetaPer - 1);
+#pragma unroll
+    for (int kt = 0; kt < kMetaTilesPerBlock; ++kt) {
+      int64_t p0 = blk0 + kt * kMetaTile + (int64_t)threadIdx.x * kMetaPer;
+      p0 = p0 < last4 ? p0 : last4;
+      kv[kt] = *reinterpret_cast<const u32x4*>(a.keys + p0);
+      vv[kt] = *reinterpret_cast<const u32x4*>(a.vals + p0);
+      const int64_t pp = p0 > 0 ? p0 - 1 : 0;   // used by lane 0 only, when p0 > 0
+      kpv[kt] = a.keys[pp];
+      jpv[kt] = a.vals[pp];
+      int64_t t = (int64_t)blockIdx.x * kMetaTilesPerBlock + kt;
+      sb[kt] = tile_seg_base[t < num_tiles ? t : num_tiles - 1];
+    }
+  }
+  if (small_k)
+    tables.store(a, nbuckets, s_off, s_w, s_sm, s_bucket);
+  else
+    load_contrib_tables(a, buckets, nbuckets, s_off, s_w, s_sm, s_bucket);
   __syncthreads();
 
   const int w = threadIdx.x / kWave;
   const int lane = lane_id();
-  for (int kt = 0; kt < kMetaTilesPerBlock; ++kt) {
-    const int64_t tile = (int64_t)blockIdx.x * kMetaTilesPerBlock + kt;
-    if (tile >= num_tiles) break;
-    const int64_t p0 = tile * kMetaTile + (int64_t)threadIdx.x * kMetaPer;
-    uint32_t key[kMetaPer] = {0u, 0u, 0u, 0u}, jv[kMetaPer] = {0u, 0u, 0u, 0u};
-    if (p0 + kMetaPer - 1 < N) {
-      const u32x4 kv = *reinterpret_cast<const u32x4*>(a.keys + p0);
-      const u32x4 vv = *reinterpret_cast<const u32x4*>(a.vals + p0);
-      key[0] = kv.x; key[1] = kv.y; key[2] = kv.z; key[3] = kv.w;
-      jv[0] = vv.x; jv[1] = vv.y; jv[2] = vv.z; jv[3] = vv.w;
-    } else {
-#pragma unroll
-      for (int e = 0; e < kMetaPer; ++e)
-        if (p0 + e < N) {
-          key[e] = a.keys[p0 + e];
-          jv[e] = a.vals[p0 + e];
-        }
-    }
+  // One tile: key/jv are this lane's 4 positions from p0, kprev/jprev the
+  // position before p0 (when p0 > 0), seg_base the segments before the tile.
+  auto tile_body = [&](int64_t tile, int64_t p0, const uint32_t* key, const uint32_t* jv, uint32_t kprev,
+                       uint32_t jprev, uint32_t seg_base) {
     int m[kMetaPer];
 #pragma unroll
     for (int e = 0; e < kMetaPer; ++e)
       m[e] = (p0 + e < N && (int64_t)jv[e] < N) ? contribution_of(s_off, s_bucket, q, K, jv[e]) : 0;
     // the position before this lane's first: the previous lane's last, or
-    // (first lane of a wave) read directly
+    // (first lane of a wave) the one loaded for it
     uint32_t kp = __shfl_up(key[kMetaPer - 1], 1, kWave);
     int mp = __shfl_up(m[kMetaPer - 1], 1, kWave);
     bool prev_ok = true;
     if (lane == 0) {
       prev_ok = p0 > 0 && p0 - 1 < N;
       if (prev_ok) {
-        kp = a.keys[p0 - 1];
-        const uint32_t jp = a.vals[p0 - 1];
-        mp = (int64_t)jp < N ? contribution_of(s_off, s_bucket, q, K, jp) : 0;
+        kp = kprev;
+        mp = (int64_t)jprev < N ? contribution_of(s_off, s_bucket, q, K, jprev) : 0;
       }
     }
     uint32_t word[kMetaPer];
@@ -348,7 +417,7 @@ seg_meta_kernel(SegmentArgs a, const uint32_t* __restrict__ tile_seg_base,
     const uint32_t incl = wave_inclusive_scan(heads);
     if (lane == kWave - 1) s_wave_heads[w] = incl;
     __syncthreads();
-    uint32_t before = tile_seg_base[tile] + incl - heads;
+    uint32_t before = seg_base + incl - heads;
     for (int k = 0; k < w; ++k) before += s_wave_heads[k];
     // segments that start before each group-aligned position
     if ((p0 & (kGroupSpan - 1)) == 0 && p0 < N) base32[p0 / kGroupSpan] = before;
@@ -363,6 +432,35 @@ seg_meta_kernel(SegmentArgs a, const uint32_t* __restrict__ tile_seg_base,
       }
     }
     __syncthreads();   // s_wave_heads is rewritten by the next tile
+  };
+
+  if (full) {
+#pragma unroll
+    for (int kt = 0; kt < kMetaTilesPerBlock; ++kt) {
+      const int64_t p0 = blk0 + kt * kMetaTile + (int64_t)threadIdx.x * kMetaPer;
+      const uint32_t key[kMetaPer] = {kv[kt].x, kv[kt].y, kv[kt].z, kv[kt].w};
+      const uint32_t jv[kMetaPer] = {vv[kt].x, vv[kt].y, vv[kt].z, vv[kt].w};
+      tile_body((int64_t)blockIdx.x * kMetaTilesPerBlock + kt, p0, key, jv, kpv[kt], jpv[kt], sb[kt]);
+    }
+    return;
+  }
+  for (int kt = 0; kt < kMetaTilesPerBlock; ++kt) {
+    const int64_t tile = (int64_t)blockIdx.x * kMetaTilesPerBlock + kt;
+    if (tile >= num_tiles) break;
+    const int64_t p0 = tile * kMetaTile + (int64_t)threadIdx.x * kMetaPer;
+    uint32_t key[kMetaPer] = {0u, 0u, 0u, 0u}, jv[kMetaPer] = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int e = 0; e < kMetaPer; ++e)
+      if (p0 + e < N) {
+        key[e] = a.keys[p0 + e];
+        jv[e] = a.vals[p0 + e];
+      }
+    uint32_t kprev = 0, jprev = 0;
+    if (p0 > 0 && p0 - 1 < N) {
+      kprev = a.keys[p0 - 1];
+      jprev = a.vals[p0 - 1];
+    }
+    tile_body(tile, p0, key, jv, kprev, jprev, tile_seg_base[tile]);
   }
 }
 
@@ -377,7 +475,6 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
   __shared__ f64x4 s_acc[kSegBlock];
   __shared__ int32_t s_cc[G], s_ww[G];
   __shared__ uint32_t s_seg[G], s_flags[G];
-  __shared__ uint32_t s_bflags;
 
   const int64_t N = a.N;
   const int D = a.D;
@@ -390,7 +487,6 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
 
   {
     const int64_t tile = blockIdx.x;
-    if (threadIdx.x == 0) s_bflags = 0;
     const int64_t p0 = tile * TILE + (int64_t)grp * kGroupSpan;
     const int nvalid = (N - p0) >= kGroupSpan ? kGroupSpan : (N - p0 > 0 ? (int)(N - p0) : 0);
     const uint32_t gbase = nvalid > 0 ? base32[p0 / kGroupSpan] : 0u;
@@ -497,7 +593,6 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
         if (gl == 0) {
           part.first_cc[tile] = tcc;
           part.first_ww[tile] = tww;
-          atomicOr(&s_bflags, kHasFirst);
         }
       } else {
         finalize_segment(a, (int64_t)gbase - 1, tot, tcc, tww, gl, lane_on);
@@ -519,69 +614,74 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
         if (gl == 0) {
           part.first_cc[tile] = tcc;
           part.first_ww[tile] = tww;
-          atomicOr(&s_bflags, kHasFirst | kBlockPass);
         }
       } else {
         if (lane_on) *reinterpret_cast<f64x4*>(part.last_acc + tile * D + gl * 4) = tot;
         if (gl == 0) {
           part.last_cc[tile] = tcc;
           part.last_ww[tile] = tww;
-          part.last_seg[tile] = s_seg[G - 1];
-          atomicOr(&s_bflags, kHasLast);
+          // one lane per tile: the fixup pass takes the tiles from this list,
+          // with the segment and the last tile it covers
+          const uint32_t seg = s_seg[G - 1];
+          int64_t end = (int64_t)seg + 1 <= N ? a.seg_offsets[seg + 1] : N;   // written by the position pass
+          end = end < 1 ? 1 : (end > N ? N : end);
+          part.fix_list[atomicAdd(part.fix_count, 1u)] =
+              u32x4{(uint32_t)tile, seg, (uint32_t)((end - 1) / TILE), 0u};
         }
       }
     }
-    __syncthreads();
-    if (threadIdx.x == 0) part.flags[tile] = s_bflags;
   }
 }
 
 // Joins, for each segment that runs past the end of the tile holding its
-// head, the partial sums of every later tile it covers.  1024 threads per
-// block, so the longest chain (the hottest ID) is summed 1024/LPR ways.
-constexpr int kFixBlock = 1024;
+// head, the partial sums of every later tile it covers.  Only the tiles the
+// row pass listed are visited (about a third of them for Zipf IDs), spread
+// over a fixed grid; 256/LPR groups with eight loads in flight each sum the
+// longest chain (the hottest ID: some 1700 tiles at 65M positions).
+constexpr int kFixBlock = 256;
+constexpr int64_t kFixGrid = 2048;
 template <int LPR>
 __global__ void __launch_bounds__(kFixBlock)
 seg_fixup_kernel(SegmentArgs a, SegPartials part) {
   constexpr int G = kFixBlock / LPR;
-  constexpr int64_t TILE = (int64_t)kSegWaves * (kWave / LPR) * kGroupSpan;
   __shared__ f64x4 s_acc[kFixBlock];
   __shared__ int32_t s_cc[G], s_ww[G];
-  const int64_t b = blockIdx.x;
-  if (!(part.flags[b] & kHasLast)) return;
   const int lane = threadIdx.x % LPR;
   const int grp = threadIdx.x / LPR;
   const bool lane_on = lane * 4 < a.D;
   const int D = a.D;
-  const int64_t seg = (int64_t)part.last_seg[b];
-  if (seg + 1 > a.N) return;   // unreachable when the numbering is consistent
-  int64_t end = a.seg_offsets[seg + 1];
-  end = end < 1 ? 1 : (end > a.N ? a.N : end);
-  const int64_t b_end = (end - 1) / TILE;
-  f64x4 acc = {0.0, 0.0, 0.0, 0.0};
-  int cc = 0, ww = 0;
-#pragma unroll 4
-  for (int64_t bb = b + 1 + grp; bb <= b_end; bb += G) {
-    if (lane_on) acc += *reinterpret_cast<const f64x4*>(part.first_acc + bb * D + lane * 4);
-    cc += part.first_cc[bb];
-    ww += part.first_ww[bb];
-  }
-  s_acc[threadIdx.x] = acc;
-  if (lane == 0) {
-    s_cc[grp] = cc;
-    s_ww[grp] = ww;
-  }
-  __syncthreads();
-  if (grp == 0) {
-    f64x4 tot = lane_on ? *reinterpret_cast<const f64x4*>(part.last_acc + b * D + lane * 4)
-                        : f64x4{0.0, 0.0, 0.0, 0.0};
-    int tcc = part.last_cc[b], tww = part.last_ww[b];
-    for (int g = 0; g < G; ++g) {
-      tot += s_acc[g * LPR + lane];
-      tcc += s_cc[g];
-      tww += s_ww[g];
+  const uint32_t count = *part.fix_count;
+  // the listed tiles in any order: each one's sum is taken in a fixed order
+  for (uint32_t k = blockIdx.x; k < count; k += gridDim.x) {
+    const u32x4 rec = part.fix_list[k];
+    const int64_t b = rec.x, seg = rec.y, b_end = rec.z;
+    if (seg >= a.N) continue;   // unreachable when the numbering is consistent (block-uniform)
+    f64x4 acc = {0.0, 0.0, 0.0, 0.0};
+    int cc = 0, ww = 0;
+#pragma unroll 8
+    for (int64_t bb = b + 1 + grp; bb <= b_end; bb += G) {
+      if (lane_on) acc += *reinterpret_cast<const f64x4*>(part.first_acc + bb * D + lane * 4);
+      cc += part.first_cc[bb];
+      ww += part.first_ww[bb];
     }
-    finalize_segment(a, seg, tot, tcc, tww, lane, lane_on);
+    s_acc[threadIdx.x] = acc;
+    if (lane == 0) {
+      s_cc[grp] = cc;
+      s_ww[grp] = ww;
+    }
+    __syncthreads();
+    if (grp == 0) {
+      f64x4 tot = lane_on ? *reinterpret_cast<const f64x4*>(part.last_acc + b * D + lane * 4)
+                          : f64x4{0.0, 0.0, 0.0, 0.0};
+      int tcc = part.last_cc[b], tww = part.last_ww[b];
+      for (int g = 0; g < G; ++g) {
+        tot += s_acc[g * LPR + lane];
+        tcc += s_cc[g];
+        tww += s_ww[g];
+      }
+      finalize_segment(a, seg, tot, tcc, tww, lane, lane_on);
+    }
+    __syncthreads();   // s_acc is rewritten for the next listed tile
   }
 }
 
@@ -618,7 +718,9 @@ static hipError_t launch_rows(const SegmentArgs& a, const uint32_t* packed, cons
                      base32, part);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(seg_fixup_kernel<LPR>, dim3((unsigned)tiles), dim3(kFixBlock), 0, stream, a, part);
+  // the listed tiles (at most all of them) are spread over a fixed grid
+  const int64_t fix_blocks = tiles < kFixGrid ? tiles : kFixGrid;
+  hipLaunchKernelGGL(seg_fixup_kernel<LPR>, dim3((unsigned)fix_blocks), dim3(kFixBlock), 0, stream, a, part);
   return hipGetLastError();
 }
 
@@ -632,8 +734,6 @@ hipError_t launch_segments(const SegmentArgs& a, void* ws, hipStream_t stream) {
   uint32_t* packed = reinterpret_cast<uint32_t*>(base + L.off_packed);
   uint32_t* base32 = reinterpret_cast<uint32_t*>(base + L.off_base32);
   SegPartials part;
-  part.flags = reinterpret_cast<uint32_t*>(base + L.off_flags);
-  part.last_seg = reinterpret_cast<uint32_t*>(base + L.off_last_seg);
   int32_t* cnt = reinterpret_cast<int32_t*>(base + L.off_cnt);
   part.first_cc = cnt;
   part.first_ww = cnt + L.row_tiles;
@@ -641,6 +741,8 @@ hipError_t launch_segments(const SegmentArgs& a, void* ws, hipStream_t stream) {
   part.last_ww = cnt + 3 * L.row_tiles;
   part.first_acc = reinterpret_cast<double*>(base + L.off_first_acc);
   part.last_acc = reinterpret_cast<double*>(base + L.off_last_acc);
+  part.fix_count = reinterpret_cast<uint32_t*>(base + L.off_fix);
+  part.fix_list = reinterpret_cast<u32x4*>(base + L.off_fix + 256);
 
   hipLaunchKernelGGL(check_offsets_kernel, dim3(1), dim3(256), 0, stream, a.offsets, a.K, a.N, a.err);
   hipError_t e = hipGetLastError();
@@ -648,7 +750,7 @@ hipError_t launch_segments(const SegmentArgs& a, void* ws, hipStream_t stream) {
   e = launch_run_heads(a.keys, a.N, heads, total, scan_ws, stream);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(seg_finish_kernel, dim3(1), dim3(1), 0, stream, (const uint32_t*)total, a.N,
-                     a.num_unique, a.seg_offsets);
+                     a.num_unique, a.seg_offsets, part.fix_count);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (a.N <= 0) return hipSuccess;
 
