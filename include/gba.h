@@ -228,6 +228,32 @@ gba_status gba_finalize_apply_dense_adam(double* run, int32_t K, int64_t P, floa
                                          double eps, int64_t t, int32_t reset, hipStream_t stream);
 
 /*
+ * Grouping of embedding IDs by value -- the dedup step of gba_aggregate_sparse
+ * (Alg. 2 handles embedding gradients per ID), on its own: a stable sort of
+ * the IDs, keeping each one's occurrence index.
+ *   ids        [n] int64 IDs in [0, R) (16-byte aligned).
+ *   keys_out   [n] uint32 out, the IDs ascending.
+ *   index_out  [n] uint32 out, the occurrence index of each sorted entry;
+ *              equal IDs keep their input order.
+ *   plan       GBA_SORT_AUTO, GBA_SORT_PLAIN or GBA_SORT_HOT: whether the
+ *              frequent IDs found in a sample of the input are placed in the
+ *              first pass so that only the others are sorted further (AUTO
+ *              does so for large inputs).  The output does not depend on it.
+ *   workspace  gba_sort_ids_workspace_size(n, R, plan) bytes.
+ *   err        GBA_DERR_ID_RANGE for an ID outside [0, R) (sorted as 0).
+ * Limits: 0 <= n < 2^28, 1 <= R <= 2^32.
+ */
+#define GBA_SORT_AUTO (-1)
+#define GBA_SORT_PLAIN 0
+#define GBA_SORT_HOT 1
+
+gba_status gba_sort_ids_workspace_size(int64_t n, int64_t R, int32_t plan, size_t* bytes /* host out */);
+
+gba_status gba_sort_ids(const int64_t* ids, int64_t n, int64_t R, int32_t plan, uint32_t* keys_out,
+                        uint32_t* index_out, void* workspace, size_t workspace_bytes, int32_t* err,
+                        hipStream_t stream);
+
+/*
  * Pull side (Sec. 3.1 token list; Alg. 2, pull responder).
  *
  * gba_token_of_batch (host function, no device work): the token handed out

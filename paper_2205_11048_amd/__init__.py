@@ -20,6 +20,7 @@ __all__ = [
     "gba_finalize_dense", "gba_finalize_apply_dense_adagrad", "gba_finalize_apply_dense_adam",
     "gba_token_of_batch", "gba_pull_workspace_size", "gba_pull_rows", "gba_hash_clear",
     "gba_hash_workspace_size", "gba_hash_find_or_insert", "gba_hash_rehash", "EMPTY_ID", "DERR_TABLE_FULL",
+    "gba_sort_ids_workspace_size", "gba_sort_ids", "SORT_AUTO", "SORT_PLAIN", "SORT_HOT",
     "pointer_table", "DECAY_TOKEN", "DECAY_ID_TAG", "NORM_PER_ID_COUNT", "NORM_BY_K",
     "DERR_ID_RANGE", "DERR_FUTURE_TOKEN", "DERR_OFFSETS", "DERR_ROW_RANGE", "MAX_K", "MAX_D",
     "LIB_PATH",
@@ -34,6 +35,7 @@ DECAY_TOKEN, DECAY_ID_TAG = 0, 1
 NORM_PER_ID_COUNT, NORM_BY_K = 0, 1
 DERR_ID_RANGE, DERR_FUTURE_TOKEN, DERR_OFFSETS, DERR_ROW_RANGE, DERR_TABLE_FULL = 1, 2, 4, 8, 16
 EMPTY_ID = -1
+SORT_AUTO, SORT_PLAIN, SORT_HOT = -1, 0, 1
 MAX_K, MAX_D = 4096, 256
 
 _P = ctypes.c_void_p
@@ -59,6 +61,8 @@ _SIGNATURES = {
     "gba_token_of_batch": ([_I64, _I32], _I64),
     "gba_pull_workspace_size": ([_I64, _I64, ctypes.POINTER(ctypes.c_size_t)], _I32),
     "gba_pull_rows": ([_P, _I64, _I64, _P, _I32, _P, _P, _P, _P, _P, ctypes.c_size_t, _P, _P], _I32),
+    "gba_sort_ids_workspace_size": ([_I64, _I64, _I32, ctypes.POINTER(ctypes.c_size_t)], _I32),
+    "gba_sort_ids": ([_P, _I64, _I64, _I32, _P, _P, _P, ctypes.c_size_t, _P, _P], _I32),
     "gba_hash_clear": ([_P, _P, _I64, _P], _I32),
     "gba_hash_workspace_size": ([_I64, ctypes.POINTER(ctypes.c_size_t)], _I32),
     "gba_hash_find_or_insert": ([_P, _P, _I64, _P, _I64, _P, _P, _I64, _P, _P, _P, ctypes.c_size_t, _P, _P], _I32),
@@ -231,6 +235,25 @@ def gba_pull_rows(ids, table, unique_ids, inverse, rows, num_unique, workspace, 
     _need(err, torch.int32, "err", 1)
     _check(lib().gba_pull_rows(_ptr(ids), n, int(R), _ptr(table), int(D), _ptr(unique_ids), _ptr(inverse), _ptr(rows),
                                _ptr(num_unique), _ptr(workspace), workspace.numel(), _ptr(err), _stream(stream)))
+
+
+def gba_sort_ids_workspace_size(n, R, plan=SORT_AUTO) -> int:
+    b = ctypes.c_size_t(0)
+    _check(lib().gba_sort_ids_workspace_size(int(n), int(R), int(plan), ctypes.byref(b)))
+    return int(b.value)
+
+
+def gba_sort_ids(ids, R, keys_out, index_out, workspace, plan=SORT_AUTO, err=None, stream=None):
+    """Stable sort of the IDs: keys_out = the IDs ascending (uint32 stored in
+    int32), index_out = each sorted entry's occurrence index."""
+    n = ids.numel()
+    _need(ids, torch.int64, "ids")
+    _need(keys_out, torch.int32, "keys_out", n)
+    _need(index_out, torch.int32, "index_out", n)
+    _need(workspace, torch.uint8, "workspace")
+    _need(err, torch.int32, "err", 1)
+    _check(lib().gba_sort_ids(_ptr(ids), n, int(R), int(plan), _ptr(keys_out), _ptr(index_out), _ptr(workspace),
+                              workspace.numel(), _ptr(err), _stream(stream)))
 
 
 def gba_hash_clear(slot_ids, slot_rows, stream=None):

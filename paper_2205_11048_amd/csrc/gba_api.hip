@@ -194,6 +194,32 @@ gba_status gba_aggregate_sparse(const int64_t* ids, const float* rows, const int
   return from_hip(launch_segments(a, ws + align_up(plan.bytes), stream));
 }
 
+gba_status gba_sort_ids_workspace_size(int64_t n, int64_t R, int32_t plan, size_t* bytes) {
+  if (!bytes) return GBA_ERR_NULL;
+  if (n < 0 || n > kMaxN || R < 1 || R > (int64_t(1) << 32) || plan < -1 || plan > 1) return GBA_ERR_INVALID_ARG;
+  *bytes = align_up(plan_sort(n, R, plan).bytes);
+  return GBA_OK;
+}
+
+gba_status gba_sort_ids(const int64_t* ids, int64_t n, int64_t R, int32_t plan, uint32_t* keys_out,
+                        uint32_t* index_out, void* workspace, size_t workspace_bytes, int32_t* err,
+                        hipStream_t stream) {
+  if (n < 0 || n > kMaxN || R < 1 || R > (int64_t(1) << 32) || plan < -1 || plan > 1) return GBA_ERR_INVALID_ARG;
+  if (!workspace) return GBA_ERR_NULL;
+  if (n > 0 && (!ids || !keys_out || !index_out)) return GBA_ERR_NULL;
+  if ((ids && !aligned16(ids)) || !aligned16(workspace)) return GBA_ERR_INVALID_ARG;
+  const SortPlan p = plan_sort(n, R, plan);
+  if (workspace_bytes < align_up(p.bytes)) return GBA_ERR_WORKSPACE;
+  if (n == 0) return GBA_OK;
+  const uint32_t* keys = nullptr;
+  const uint32_t* vals = nullptr;
+  hipError_t e = launch_sort_ids(ids, n, R, p, workspace, &keys, &vals, err, stream);
+  if (e != hipSuccess) return GBA_ERR_HIP;
+  e = hipMemcpyAsync(keys_out, keys, (size_t)n * 4, hipMemcpyDeviceToDevice, stream);
+  if (e == hipSuccess) e = hipMemcpyAsync(index_out, vals, (size_t)n * 4, hipMemcpyDeviceToDevice, stream);
+  return from_hip(e);
+}
+
 int64_t gba_token_of_batch(int64_t i, int32_t M) {
   if (i < 0 || M < 1) return -1;
   return i / M;

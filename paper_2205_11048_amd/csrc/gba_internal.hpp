@@ -61,10 +61,15 @@ struct SortPlan {
   int64_t n;
   int key_bits;          // significant key bits (>= 1)
   int passes;
+  int first_bits;        // cold digit bits of the first pass (the later passes take 8)
+  bool hot;              // hot-key plan: frequent IDs placed by the first pass
+  int hot_cap;           // most hot IDs (hot plan)
   int64_t blocks;        // tiles of the first pass (the most of any pass)
   size_t bytes;          // workspace bytes
 };
-SortPlan plan_sort(int64_t n, int64_t R);
+// hot_mode: -1 picks the hot-key plan for large inputs whose key width leaves
+// room for it, 0 never, 1 whenever the key width allows.
+SortPlan plan_sort(int64_t n, int64_t R, int hot_mode = -1);
 // Sorts ids (int64 [n], each checked against [0, R)) by value, stably.  The
 // sorted keys and original occurrence indices are returned through
 // *keys_out / *vals_out, which point into `ws`.

@@ -11,6 +11,18 @@
 // stably in LDS and writes runs of equal digits together.
 // Ranks inside a wave come from ballots that match lanes holding the same
 // digit, so skewed (Zipf) keys cost no LDS atomics on hot bins in the scatter.
+//
+// Hot keys.  Embedding IDs are Zipf-skewed (the paper's Insight 2: a few IDs
+// appear in most batches), so a few hundred IDs can hold half of all
+// occurrences.  With the hot-key plan, one block first picks the IDs that are
+// frequent in an evenly spaced sample of the input.  The first pass gives
+// each of them a bin of its own next to the cold digit bins, counts the cold
+// keys that fall between consecutive hot IDs, and writes every hot occurrence
+// straight to its final position: the cold keys below it, plus the hot
+// occurrences of smaller hot IDs, plus its stable rank in its bin.  The later
+// passes sort only the cold keys, and the last one leaves a gap for the hot
+// runs below each key.  The result is the same stable sort, element for
+// element; which IDs are hot changes only the time it takes.
 #include "gba_device.hpp"
 #include "gba_internal.hpp"
 
@@ -24,34 +36,87 @@ constexpr int kSortWaves = kSortBlock / kWave;
 // the latency of the 8-byte ID loads better.
 constexpr int kItemsFirst = 8;
 constexpr int kItemsRest = 16;
+constexpr int kItemsHotFirst = 8;   // the first pass of the hot-key plan
 template <int ITEMS>
 constexpr int64_t tile_keys() { return (int64_t)kSortBlock * ITEMS; }
 constexpr int kRadix = 256;
 constexpr int kXcds = 8;   // MI355X: 8 accelerator dies, each with its own L2
 constexpr int kChunk = kSortWaves;                     // tiles per chunk: one hist block
 
+// Hot-key plan.
+constexpr int kHotSample = 16384;      // sampled positions (one block sorts them in LDS)
+constexpr int kHotBlock = 1024;
+constexpr int kHotCap = 254;           // most hot IDs (one bin each; the lookup reads one entry past H)
+constexpr int kHotBuckets = 1024;      // lookup buckets over the top 10 key bits
+constexpr uint32_t kHotMinCount = 4;   // a sampled ID must occur this often to be hot
+constexpr int64_t kHotMinKeys = int64_t(1) << 22;   // below this the plain sort is used
+
+// Pass kinds.
+enum : int {
+  kPlain = 0,      // n keys from the launch arguments
+  kHotFirst = 1,   // first pass with hot bins: cold keys to the work arrays, hot ones to the final arrays
+  kCold = 2,       // a middle pass over the cold keys (their count read on the device)
+  kColdLast = 3    // the last pass over the cold keys, into the final arrays, past the hot runs
+};
+
 __host__ __device__ static inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 static inline size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
 
+// Device tables of the hot-key plan (inside the workspace).
+struct HotTables {
+  uint32_t* ids;        // [256] hot IDs, ascending (the first H are used)
+  uint16_t* bucket;     // [kHotBuckets] hot IDs whose top bits are below the bucket index
+  uint32_t* prefix;     // [256] hot occurrences of the hot IDs before hot ID h ([H]: all of them)
+  uint32_t* meta;       // [0] H, [1] number of cold keys
+  uint32_t* iv_chunk;   // [chunks][256] cold keys per chunk by the number of hot IDs below them
+  uint32_t* iv_total;   // [256] the same over all chunks
+  uint8_t* digit;       // [n] first-pass digit of every key (written by the histogram launch)
+  int bshift;           // key >> bshift is the key's bucket
+};
+
 struct SortLayout {
-  size_t arr, off_keys0, off_keys1, off_vals0, off_vals1, off_hist, off_chunk, off_total, bytes;
+  size_t arr, off_keys0, off_keys1, off_vals0, off_vals1, off_keys2, off_vals2, off_hist, off_chunk, off_total,
+      off_iv, off_iv_total, off_hot, off_digit, bytes;
 };
 
 // tiles: the largest tile count of any pass (the first pass's)
-static SortLayout sort_layout(int64_t n, int64_t tiles) {
+static SortLayout sort_layout(int64_t n, int64_t tiles, bool hot) {
   SortLayout L{};
   L.arr = align_up((size_t)(n > 0 ? n : 1) * sizeof(uint32_t));
   const size_t nt = (size_t)(tiles > 0 ? tiles : 1);
+  const size_t chunk_bytes = align_up((size_t)ceil_div((int64_t)nt, kChunk) * kRadix * 4);
   size_t o = 0;
   L.off_keys0 = o; o += L.arr;
   L.off_keys1 = o; o += L.arr;
   L.off_vals0 = o; o += L.arr;
   L.off_vals1 = o; o += L.arr;
   L.off_hist = o;  o += align_up(nt * kRadix * 4);                       // [tile][digit]
-  L.off_chunk = o; o += align_up((size_t)ceil_div((int64_t)nt, kChunk) * kRadix * 4);   // [chunk][digit]
+  L.off_chunk = o; o += chunk_bytes;                                     // [chunk][digit]
   L.off_total = o; o += align_up(kRadix * 4);
+  if (hot) {
+    L.off_keys2 = o; o += L.arr;
+    L.off_vals2 = o; o += L.arr;
+    L.off_iv = o;    o += chunk_bytes;                                   // [chunk][hot IDs below]
+    L.off_iv_total = o; o += align_up(kRadix * 4);
+    L.off_hot = o;   o += 4096 + 256;                                    // ids, bucket, prefix, meta
+    L.off_digit = o; o += align_up((size_t)(n > 0 ? n : 1) + 64);       // + a vector's overrun
+  }
   L.bytes = o;
   return L;
+}
+
+static HotTables hot_tables(char* ws, const SortLayout& L, int key_bits) {
+  HotTables t;
+  char* h = ws + L.off_hot;
+  t.ids = reinterpret_cast<uint32_t*>(h);              // 1 KB
+  t.bucket = reinterpret_cast<uint16_t*>(h + 1024);    // 2 KB
+  t.prefix = reinterpret_cast<uint32_t*>(h + 3072);    // 1 KB
+  t.meta = reinterpret_cast<uint32_t*>(h + 4096);
+  t.iv_chunk = reinterpret_cast<uint32_t*>(ws + L.off_iv);
+  t.iv_total = reinterpret_cast<uint32_t*>(ws + L.off_iv_total);
+  t.digit = reinterpret_cast<uint8_t*>(ws + L.off_digit);
+  t.bshift = key_bits > 10 ? key_bits - 10 : 0;
+  return t;
 }
 
 // Mask of the active lanes whose digit equals this lane's digit.
@@ -63,6 +128,159 @@ __device__ __forceinline__ uint64_t match_digit(uint32_t digit, int bits, bool a
     m &= bit ? bal : ~bal;
   }
   return active ? m : 0ull;
+}
+
+// Number of hot IDs below `key`, and whether `key` is one of them.  The bucket
+// table narrows the search to the hot IDs that share the key's top bits: the
+// first two are compared without a branch (no loop, so the lookups of a
+// lane's keys overlap), the rare rest in a loop.
+struct HotLookup {
+  const uint16_t* bucket;   // LDS [kHotBuckets]
+  const uint32_t* ids;      // LDS [>= H + 1]
+  uint32_t H;
+  int bshift;
+  __device__ __forceinline__ uint32_t rank(uint32_t key, bool* hot) const {
+    const uint32_t t = key >> bshift;
+    const uint32_t lo = bucket[t];
+    const uint32_t hi = t + 1 < (uint32_t)kHotBuckets ? (uint32_t)bucket[t + 1] : H;
+    const uint32_t a0 = ids[lo], a1 = ids[lo + 1];   // lo + 1 <= H <= kHotCap: inside the table
+    const bool in0 = lo < hi, in1 = lo + 1 < hi;
+    uint32_t r = lo + ((in0 && a0 < key) ? 1u : 0u) + ((in1 && a1 < key) ? 1u : 0u);
+    bool h = (in0 && a0 == key) || (in1 && a1 == key);
+    for (uint32_t i = lo + 2; i < hi; ++i) {   // a bucket with three or more hot IDs
+      const uint32_t a = ids[i];
+      r += a < key ? 1u : 0u;
+      h = h || a == key;
+    }
+    *hot = h;
+    return r;
+  }
+};
+
+// Copies the hot tables into LDS (every thread of the block takes part; the
+// caller puts a barrier after).
+__device__ __forceinline__ void load_hot_tables(const HotTables& t, uint16_t* s_bucket, uint32_t* s_ids) {
+  const uint32_t* b32 = reinterpret_cast<const uint32_t*>(t.bucket);
+  uint32_t* s32 = reinterpret_cast<uint32_t*>(s_bucket);
+  for (int i = threadIdx.x; i < kHotBuckets / 2; i += blockDim.x) s32[i] = b32[i];
+  for (int i = threadIdx.x; i < 256; i += blockDim.x) s_ids[i] = t.ids[i];
+}
+
+// Picks the hot IDs: counts the IDs of kHotSample / 64 evenly spaced runs of
+// 64 consecutive positions (one coalesced load per wave; single scattered
+// positions would each cost a page walk) in an LDS hash table, keeps those seen at least kHotMinCount times (raising
+// the bar until at most `cap` remain), sorts them and builds the bucket
+// table.  Each wave first sorts its 64 samples of a round in registers, so an
+// ID is added once per run (the hottest ones would otherwise serialise on
+// their counter).  Only the first kHotInsertRounds rounds insert new IDs; the
+// later ones only count IDs already in the table (an ID frequent enough to
+// matter is there by then), which keeps the table sparse and the probes
+// short.  A sampled ID that finds no free slot within kHotProbe steps is not
+// counted; the choice of hot IDs changes only the speed of the sort.
+constexpr int kHotTable = 16384;   // slots (a power of two)
+constexpr int kHotProbe = 64;
+constexpr int kHotInsertRounds = 4;   // of kHotSample / kHotBlock
+__global__ void __launch_bounds__(kHotBlock)
+hot_select_kernel(const int64_t* __restrict__ ids, int64_t n, int64_t R, int cap, HotTables t) {
+  __shared__ uint32_t s_key[kHotTable];
+  __shared__ uint32_t s_cnt[kHotTable];
+  __shared__ uint32_t s_tmp[kHotBlock / kWave + 1];
+  __shared__ uint32_t s_list[256];
+  __shared__ uint32_t s_hot[256];
+  __shared__ uint32_t s_nlist;
+  const int tid = threadIdx.x;
+  constexpr uint32_t kNone = 0xffffffffu;   // not a valid key (keys are below 2^31 here)
+  constexpr int kPer = kHotSample / kHotBlock;
+  constexpr int kRuns = kHotSample / kWave;
+  const int lane = lane_id();
+  uint32_t smp[kPer];
+#pragma unroll
+  for (int e = 0; e < kPer; ++e) {
+    const int run = tid / kWave + e * (kHotBlock / kWave);   // wave w takes runs w, w + 16, ...
+    int64_t p0 = ((2 * (int64_t)run + 1) * n) / (2 * (int64_t)kRuns) - kWave / 2;
+    p0 = p0 < n - kWave ? p0 : n - kWave;
+    p0 = p0 > 0 ? p0 : 0;
+    int64_t p = p0 + lane;
+    p = p < n ? p : n - 1;
+    const int64_t id = ids[p];
+    smp[e] = (id >= 0 && id < R) ? (uint32_t)id : kNone;
+  }
+  for (int i = tid; i < kHotTable; i += kHotBlock) {
+    s_key[i] = kNone;
+    s_cnt[i] = 0u;
+  }
+  if (tid == 0) s_nlist = 0u;
+  __syncthreads();
+#pragma unroll
+  for (int e = 0; e < kPer; ++e) {
+    if (e == kHotInsertRounds) __syncthreads();   // every insertion is done
+    // bitonic sort of the wave's 64 samples, ascending by lane
+    uint32_t k = smp[e];
+#pragma unroll
+    for (int kk = 2; kk <= kWave; kk <<= 1) {
+#pragma unroll
+      for (int j = kk >> 1; j > 0; j >>= 1) {
+        const uint32_t o = __shfl_xor(k, j, kWave);
+        const bool keep_min = ((lane & j) == 0) == ((lane & kk) == 0);
+        k = keep_min ? (k < o ? k : o) : (k < o ? o : k);
+      }
+    }
+    const uint32_t prev = __shfl_up(k, 1, kWave);
+    const uint64_t starts = __ballot(lane == 0 || k != prev);
+    const uint64_t above = lane == kWave - 1 ? 0ull : starts & (~0ull << (lane + 1));
+    const uint32_t len = (above ? (uint32_t)__builtin_ctzll(above) : (uint32_t)kWave) - (uint32_t)lane;
+    if (k == kNone || !((starts >> lane) & 1ull)) continue;
+    uint32_t h = (k * 2654435761u) >> (32 - 14);   // Fibonacci hashing onto 2^14 slots
+    for (int probe = 0; probe < kHotProbe; ++probe) {
+      uint32_t cur = s_key[h];
+      if (cur == kNone) {
+        if (e >= kHotInsertRounds) break;   // not in the table: not counted
+        cur = atomicCAS(&s_key[h], kNone, k);
+      }
+      if (cur == kNone || cur == k) {
+        atomicAdd(&s_cnt[h], len);
+        break;
+      }
+      h = (h + 1) & (kHotTable - 1);
+    }
+  }
+  static_assert(kHotTable == 1 << 14, "hash width");
+  __syncthreads();
+  uint32_t T = kHotMinCount;
+  for (;;) {
+    uint32_t c = 0;
+    for (int i = tid; i < kHotTable; i += kHotBlock) c += s_cnt[i] >= T ? 1u : 0u;
+    uint32_t tot;
+    (void)block_exclusive_scan<kHotBlock>(c, s_tmp, &tot);
+    if (tot <= (uint32_t)cap) break;
+    T += 1 + T / 8;
+  }
+  for (int i = tid; i < kHotTable; i += kHotBlock)
+    if (s_cnt[i] >= T) s_list[atomicAdd(&s_nlist, 1u)] = s_key[i];
+  __syncthreads();
+  const uint32_t H = s_nlist;
+  if ((uint32_t)tid < H) {
+    // rank among the chosen IDs (distinct), so they come out ascending
+    const uint32_t k = s_list[tid];
+    uint32_t r = 0;
+    for (uint32_t j = 0; j < H; ++j) r += s_list[j] < k ? 1u : 0u;
+    s_hot[r] = k;
+  }
+  __syncthreads();
+  const int bshift = t.bshift;
+  for (int b = tid; b < kHotBuckets; b += kHotBlock) {
+    // hot IDs whose top bits are below b: the first index with id >= b << bshift
+    const uint32_t lim = (uint32_t)b << bshift;
+    uint32_t lo = 0, hi = H;
+    while (lo < hi) {
+      const uint32_t mid = (lo + hi) >> 1;
+      if (s_hot[mid] < lim) lo = mid + 1;
+      else hi = mid;
+    }
+    t.bucket[b] = (uint16_t)lo;
+  }
+  if (tid < 256) t.ids[tid] = (uint32_t)tid < H ? s_hot[tid] : kNone;
+  if (tid == 0) t.meta[0] = H;
 }
 
 // Key of position i: from the int64 IDs on the first pass (checked against
@@ -80,18 +298,30 @@ __device__ __forceinline__ uint32_t load_key(const void* src, int64_t i, int64_t
   return static_cast<const uint32_t*>(src)[i];
 }
 
+// Digit of a key on a hot-key first pass: a hot ID's own bin past the cold
+// bins, else its low bits.  Cold keys are also counted by the hot IDs below
+// them (iv, LDS).
+__device__ __forceinline__ uint32_t hot_first_digit(uint32_t key, uint32_t mask, uint32_t cold_bins,
+                                                    const HotLookup& hl, bool* hot, uint32_t* below) {
+  *below = hl.rank(key, hot);
+  return *hot ? cold_bins + *below : (key & mask);
+}
+
 // Digit counts of one tile into the wave's LDS row h_row.  Lane l holds keys
 // tile0 + 4 * (l + 64 * c) + e, c < ITEMS, e < 4: each vector load of the
 // wave covers 1 KB of consecutive keys.  FULL (every key of the tile exists)
 // drops the bounds checks, so no branch waits on a load and a phase's loads
 // are in flight together; only the last tile of a pass can be partial.
 // Returns whether an ID outside [0, R) was seen (first pass).
-template <bool FIRST, int ITEMS, bool FULL>
+template <bool FIRST, int ITEMS, bool FULL, bool HOT>
 __device__ __forceinline__ bool count_tile(const void* __restrict__ keys_in, int64_t n, int64_t tile0, int shift,
-                                           uint32_t mask, int64_t R, uint32_t* h_row, int lane) {
+                                           uint32_t mask, int64_t R, uint32_t* h_row, int lane,
+                                           const HotLookup& hl, uint32_t cold_bins, uint32_t* iv,
+                                           uint8_t* __restrict__ dig_out) {
   constexpr int kHistKeys = 4 * ITEMS;   // keys per lane
-  // eight vectors (32 keys) per lane per phase, all in flight together
-  constexpr int kVecs = 8;
+  // eight vectors (32 keys) per lane per phase, all in flight together (four
+  // with the hot lookup, whose registers would otherwise halve residency)
+  constexpr int kVecs = HOT ? 4 : 8;
   static_assert(kHistKeys % (4 * kVecs) == 0, "whole phases per tile");
   bool bad = false;
 #pragma unroll
@@ -101,8 +331,8 @@ __device__ __forceinline__ bool count_tile(const void* __restrict__ keys_in, int
     for (int cc = 0; cc < kVecs; ++cc) {
       const int c = ph * kVecs + cc;
       const int64_t i0 = tile0 + 4 * ((int64_t)lane + (int64_t)kWave * c);
+      uint32_t k4[4];
       if (FULL || i0 + 3 < n) {
-        uint32_t k4[4];
         if (FIRST) {
           const int64_t* ids = static_cast<const int64_t*>(keys_in);
           typedef int64_t i64x2 __attribute__((ext_vector_type(2)));
@@ -119,12 +349,30 @@ __device__ __forceinline__ bool count_tile(const void* __restrict__ keys_in, int
           const u32x4 v = *reinterpret_cast<const u32x4*>(static_cast<const uint32_t*>(keys_in) + i0);
           k4[0] = v.x; k4[1] = v.y; k4[2] = v.z; k4[3] = v.w;
         }
-#pragma unroll
-        for (int e = 0; e < 4; ++e) digit[4 * cc + e] = (k4[e] >> shift) & mask;
       } else {
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          digit[4 * cc + e] = (i0 + e < n) ? (load_key<FIRST>(keys_in, i0 + e, R, &bad) >> shift) & mask : 0u;
+        for (int e = 0; e < 4; ++e) k4[e] = (i0 + e < n) ? load_key<FIRST>(keys_in, i0 + e, R, &bad) : 0u;
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if (HOT) {
+          bool hot;
+          uint32_t below;
+          digit[4 * cc + e] = hot_first_digit(k4[e], mask, cold_bins, hl, &hot, &below);
+          if (!hot && (FULL || i0 + e < n)) atomicAdd(&iv[below], 1u);
+        } else {
+          digit[4 * cc + e] = (k4[e] >> shift) & mask;
+        }
+      }
+      if (HOT) {   // the scatter reads the digits instead of looking the keys up again
+        if (FULL || i0 + 3 < n) {
+          *reinterpret_cast<uint32_t*>(dig_out + i0) = digit[4 * cc] | (digit[4 * cc + 1] << 8) |
+                                                        (digit[4 * cc + 2] << 16) | (digit[4 * cc + 3] << 24);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (i0 + e < n) dig_out[i0 + e] = (uint8_t)digit[4 * cc + e];
+        }
       }
     }
     // one LDS add per run of equal digits among each lane's 4 consecutive keys
@@ -154,25 +402,46 @@ __device__ __forceinline__ bool count_tile(const void* __restrict__ keys_in, int
 
 // Digit counts of the four tiles of one chunk, one wave per tile; each adds
 // one count per run of equal digits among each lane's 4 consecutive keys.
-template <bool FIRST, int ITEMS>
+// kCold reads the key count from n_dev; kHotFirst also writes the chunk's
+// counts of cold keys by the number of hot IDs below them.
+template <bool FIRST, int ITEMS, int MODE>
 __global__ void __launch_bounds__(kSortBlock)
-sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n, int64_t tiles, int shift, int bits,
-                      int64_t R, uint32_t* __restrict__ hist, uint32_t* __restrict__ chunk,
-                      int32_t* __restrict__ err) {
+sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n_arg, const uint32_t* __restrict__ n_dev,
+                      int shift, int bits, int64_t R, uint32_t* __restrict__ hist, uint32_t* __restrict__ chunk,
+                      HotTables ht, int32_t* __restrict__ err) {
+  constexpr bool HOT = MODE == kHotFirst;
   __shared__ uint32_t h[kSortWaves][kRadix];
+  __shared__ uint32_t s_bucket_w[HOT ? kHotBuckets / 2 : 1];   // uint16 entries
+  __shared__ uint32_t s_ids[HOT ? 256 : 1];
+  __shared__ uint32_t s_iv[HOT ? kRadix : 1];
+  uint16_t* s_bucket = reinterpret_cast<uint16_t*>(s_bucket_w);
+  const int64_t n = MODE == kCold ? (int64_t)*n_dev : n_arg;
+  const int64_t tiles = ceil_div(n, tile_keys<ITEMS>());
   const int w = threadIdx.x / kWave;
   const int lane = lane_id();
   for (int i = lane; i < kRadix; i += kWave) h[w][i] = 0u;
-  __builtin_amdgcn_wave_barrier();
+  HotLookup hl{s_bucket, s_ids, 0u, ht.bshift};
+  uint32_t cold_bins = 0;
+  if (HOT) {
+    load_hot_tables(ht, s_bucket, s_ids);
+    s_iv[threadIdx.x] = 0u;
+    hl.H = ht.meta[0];
+    cold_bins = 1u << bits;
+    __syncthreads();
+  } else {
+    __builtin_amdgcn_wave_barrier();
+  }
   const int64_t tile = (int64_t)blockIdx.x * kSortWaves + w;
   bool bad = false;
   if (tile < tiles) {
     const uint32_t mask = (1u << bits) - 1u;
     const int64_t tile0 = tile * tile_keys<ITEMS>();
     if (tile0 + tile_keys<ITEMS>() <= n)
-      bad = count_tile<FIRST, ITEMS, true>(keys_in, n, tile0, shift, mask, R, h[w], lane);
+      bad = count_tile<FIRST, ITEMS, true, HOT>(keys_in, n, tile0, shift, mask, R, h[w], lane, hl, cold_bins, s_iv,
+                                                ht.digit);
     else
-      bad = count_tile<FIRST, ITEMS, false>(keys_in, n, tile0, shift, mask, R, h[w], lane);
+      bad = count_tile<FIRST, ITEMS, false, HOT>(keys_in, n, tile0, shift, mask, R, h[w], lane, hl, cold_bins,
+                                                 s_iv, ht.digit);
   }
   __syncthreads();
   // the block's tiles form one chunk: each tile's row holds the counts of the
@@ -188,6 +457,7 @@ sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n, int64_t tiles
       s += h[k][d];
     }
     chunk[(int64_t)blockIdx.x * kRadix + d] = s;
+    if (HOT) ht.iv_chunk[(int64_t)blockIdx.x * kRadix + d] = s_iv[d];
   }
   if (FIRST && bad) raise_error(err, GBA_DERR_ID_RANGE);
 }
@@ -195,12 +465,17 @@ sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n, int64_t tiles
 // One block per digit value: exclusive prefix of the digit's chunk counts, in
 // place, and the digit's total.  Blocks of one XCD (block b runs on XCD b % 8)
 // take 32 consecutive digits, so each 128-byte line of a chunk row is read by
-// one XCD only.
+// one XCD only.  With a second array (iv), blocks kRadix.. add up its columns
+// into iv_total (no prefix).
 constexpr int kDigitScanBatch = 8;
 __global__ void __launch_bounds__(kSortBlock)
-sort_digit_scan_kernel(uint32_t* __restrict__ chunk, int64_t nchunks, uint32_t* __restrict__ total) {
+sort_digit_scan_kernel(uint32_t* __restrict__ chunk, int64_t nchunks, uint32_t* __restrict__ total,
+                       const uint32_t* __restrict__ iv, uint32_t* __restrict__ iv_total) {
   __shared__ uint32_t tmp[kSortBlock / kWave + 1];
-  const int d = (int)(blockIdx.x % kXcds) * (kRadix / kXcds) + (int)(blockIdx.x / kXcds);
+  const bool second = blockIdx.x >= kRadix;
+  const int b = second ? blockIdx.x - kRadix : blockIdx.x;
+  const int d = (int)(b % kXcds) * (kRadix / kXcds) + (int)(b / kXcds);
+  const uint32_t* src = second ? iv : chunk;
   const int64_t per = ceil_div(nchunks, kSortBlock);
   const int64_t c_lo = (int64_t)threadIdx.x * per;
   const int64_t c_hi = (c_lo + per < nchunks) ? c_lo + per : nchunks;
@@ -208,12 +483,16 @@ sort_digit_scan_kernel(uint32_t* __restrict__ chunk, int64_t nchunks, uint32_t* 
   for (int64_t c0 = c_lo; c0 < c_hi; c0 += kDigitScanBatch) {
     uint32_t v[kDigitScanBatch];
 #pragma unroll
-    for (int k = 0; k < kDigitScanBatch; ++k) v[k] = (c0 + k < c_hi) ? chunk[(c0 + k) * kRadix + d] : 0u;
+    for (int k = 0; k < kDigitScanBatch; ++k) v[k] = (c0 + k < c_hi) ? src[(c0 + k) * kRadix + d] : 0u;
 #pragma unroll
     for (int k = 0; k < kDigitScanBatch; ++k) s += v[k];
   }
   uint32_t all;
   uint32_t run = block_exclusive_scan<kSortBlock>(s, tmp, &all);
+  if (second) {
+    if (threadIdx.x == 0) iv_total[d] = all;
+    return;
+  }
   for (int64_t c0 = c_lo; c0 < c_hi; c0 += kDigitScanBatch) {
     uint32_t v[kDigitScanBatch];
 #pragma unroll
@@ -236,48 +515,65 @@ __device__ __forceinline__ int64_t xcd_tile(int64_t b, int64_t tiles) {
   return x * q + (x < r ? x : r) + i;
 }
 
-// Exclusive scans of x and of y over the block, behind one barrier: every
+// Exclusive scans of V values over the block, behind one barrier: every
 // thread adds up the totals of the waves before its own.  `tmp` holds
-// 2 * kSortWaves words.
-__device__ __forceinline__ void block_exclusive_scan2(uint32_t x, uint32_t y, uint32_t* tmp, uint32_t* ex_x,
-                                                      uint32_t* ex_y) {
+// V * kSortWaves words.
+template <int V>
+__device__ __forceinline__ void block_exclusive_scan_v(const uint32_t (&x)[V], uint32_t* tmp, uint32_t (&ex)[V],
+                                                       uint32_t (&all)[V]) {
   const int w = threadIdx.x / kWave;
-  const uint32_t ix = wave_inclusive_scan(x), iy = wave_inclusive_scan(y);
+  uint32_t inc[V];
+#pragma unroll
+  for (int v = 0; v < V; ++v) inc[v] = wave_inclusive_scan(x[v]);
   if (lane_id() == kWave - 1) {
-    tmp[w] = ix;
-    tmp[kSortWaves + w] = iy;
+#pragma unroll
+    for (int v = 0; v < V; ++v) tmp[v * kSortWaves + w] = inc[v];
   }
   __syncthreads();
-  uint32_t bx = 0, by = 0;
 #pragma unroll
-  for (int k = 0; k < kSortWaves; ++k) {
-    if (k < w) {
-      bx += tmp[k];
-      by += tmp[kSortWaves + k];
+  for (int v = 0; v < V; ++v) {
+    uint32_t b = 0, t = 0;
+#pragma unroll
+    for (int k = 0; k < kSortWaves; ++k) {
+      const uint32_t u = tmp[v * kSortWaves + k];
+      if (k < w) b += u;
+      t += u;
     }
+    ex[v] = b + inc[v] - x[v];
+    all[v] = t;
   }
-  *ex_x = bx + ix - x;
-  *ex_y = by + iy - y;
 }
 
-template <bool FIRST, int ITEMS>
-__global__ void __launch_bounds__(kSortBlock)
-sort_scatter_kernel(const void* __restrict__ keys_in, const uint32_t* __restrict__ vals_in,
-                    uint32_t* __restrict__ keys_out, uint32_t* __restrict__ vals_out, int64_t n,
-                    int shift, int bits, int64_t R, const uint32_t* __restrict__ hist,
-                    const uint32_t* __restrict__ chunk, const uint32_t* __restrict__ total) {
+// Scatter of one tile.  kHotFirst writes cold keys to keys_out/vals_out and
+// hot ones to their final places in keys_fin/vals_fin; kColdLast writes the
+// cold keys to keys_out/vals_out (the final arrays), each past the hot runs of
+// the hot IDs below it.  n_total bounds the final arrays.
+template <bool FIRST, int ITEMS, int MODE>
+__device__ __forceinline__ void
+scatter_tile(const void* __restrict__ keys_in, const uint32_t* __restrict__ vals_in,
+             uint32_t* __restrict__ keys_out, uint32_t* __restrict__ vals_out,
+             uint32_t* __restrict__ keys_fin, uint32_t* __restrict__ vals_fin, int64_t n_arg,
+             const uint32_t* __restrict__ n_dev, int64_t n_total, int shift, int bits, int64_t R,
+             const uint32_t* __restrict__ hist, const uint32_t* __restrict__ chunk,
+             const uint32_t* __restrict__ total, const HotTables& ht) {
+  constexpr bool HOT = MODE == kHotFirst;
+  constexpr bool DYN = MODE == kCold || MODE == kColdLast;
+  constexpr bool GAP = MODE == kColdLast;
   // per (wave, digit): the wave's count, then the tile position of the wave's
-  // first key of that digit
+  // first key of that digit (kColdLast: then the hot tables)
   __shared__ uint32_t cnt[kSortWaves][kRadix];
   // per digit: the output position minus the tile position of its keys
   // (first the chunk and tile offset alone), and the digit total
   __shared__ uint32_t gshift[kRadix];
   __shared__ uint32_t s_tot[kRadix];
-  __shared__ uint32_t tmp[2 * kSortWaves];
+  __shared__ uint32_t tmp[4 * kSortWaves];
   constexpr int64_t kTile = tile_keys<ITEMS>();
   __shared__ uint32_t s_keys[kTile];
   __shared__ uint32_t s_vals[kTile];
-  const int64_t tile = xcd_tile(blockIdx.x, gridDim.x);   // the grid has one block per tile
+  const int64_t n = DYN ? (int64_t)*n_dev : n_arg;
+  const int64_t tiles = DYN ? ceil_div(n, kTile) : (int64_t)gridDim.x;
+  if (DYN && (int64_t)blockIdx.x >= tiles) return;   // the grid is sized for every key
+  const int64_t tile = xcd_tile(blockIdx.x, tiles);
   // Where the tile's keys of digit d go: where the digit starts (scan of the
   // digit totals), plus its count in earlier chunks, plus in earlier tiles of
   // this tile's chunk.  The loads are issued with the keys' and used only
@@ -286,13 +582,31 @@ sort_scatter_kernel(const void* __restrict__ keys_in, const uint32_t* __restrict
   const int d = threadIdx.x;
   const uint32_t off = chunk[(tile / kChunk) * kRadix + d] + hist[tile * kRadix + d];
   const uint32_t tot = total[d];
+  // hot bin d (ID d - cold_bins) starts after the cold keys with at most
+  // d - cold_bins hot IDs below them: thread d takes column d - cold_bins
+  uint32_t iv_tot = 0;
+  if (HOT && d >= (1 << bits)) iv_tot = ht.iv_total[d - (1 << bits)];
+  // kColdLast: this thread's share of the hot tables, parked in registers
+  // until the ranking is done with cnt
+  uint32_t g_prefix = 0, g_id = 0, g_bucket0 = 0, g_bucket1 = 0, g_H = 0;
+  if (GAP) {
+    g_prefix = ht.prefix[d];
+    g_id = ht.ids[d];
+    const uint32_t* b32 = reinterpret_cast<const uint32_t*>(ht.bucket);
+    g_bucket0 = b32[d];
+    g_bucket1 = b32[d + kSortBlock];
+    g_H = ht.meta[0];
+  }
   const int w = threadIdx.x / kWave;
   const int64_t tile0 = tile * kTile;
   const int64_t base = tile0 + (int64_t)w * (kWave * ITEMS) + lane_id();
   const uint32_t mask = (1u << bits) - 1u;
   const uint64_t lt = lanemask_lt();
+  const int bshift = ht.bshift;
 
   uint32_t key[ITEMS], val[ITEMS], rank[ITEMS];
+  // kHotFirst: each key's digit (8 bits, from the histogram launch), four to a register
+  uint32_t dig_hot[HOT ? (ITEMS + 3) / 4 : 1] = {};
   // Every lane loads (lanes past the end re-read the last key, n > 0), so no
   // branch waits on a load and all of a lane's loads are in flight at once.
   // An ID outside [0, R) is sorted as 0 (the histogram launch reports it);
@@ -305,6 +619,7 @@ sort_scatter_kernel(const void* __restrict__ keys_in, const uint32_t* __restrict
       const int64_t ic = i < n ? i : n - 1;
       if (FIRST) {
         raw[r] = static_cast<const uint64_t*>(keys_in)[ic];
+        if (HOT) dig_hot[r / 4] |= (uint32_t)ht.digit[ic] << (8 * (r % 4));
       } else {
         key[r] = static_cast<const uint32_t*>(keys_in)[ic];
         val[r] = vals_in[ic];
@@ -320,14 +635,21 @@ sort_scatter_kernel(const void* __restrict__ keys_in, const uint32_t* __restrict
   s_tot[d] = tot;
   // each wave counts in its own row
   for (int i = lane_id(); i < kRadix; i += kWave) cnt[w][i] = 0u;
+  const uint32_t cold_bins = HOT ? (1u << bits) : 0u;
+  uint32_t H = 0;
+  if (HOT) H = ht.meta[0];
   __builtin_amdgcn_wave_barrier();
+  auto dig = [&](int r) -> uint32_t {
+    return HOT ? (dig_hot[r / 4] >> (8 * (r % 4))) & 0xffu : (key[r] >> shift) & mask;
+  };
   // Stable rank within (wave, digit): rounds in index order, lanes in order.
+  const int match_bits = HOT ? 8 : bits;
 #pragma unroll
   for (int r = 0; r < ITEMS; ++r) {
     const int64_t i = base + (int64_t)r * kWave;
     const bool active = i < n;
-    const uint32_t digit = (key[r] >> shift) & mask;
-    const uint64_t m = match_digit(digit, bits, active);
+    const uint32_t digit = dig(r);
+    const uint64_t m = match_digit(digit, match_bits, active);
     uint32_t before = 0;
     if (active) before = cnt[w][digit];
     // every lane of the wave has read the counter before the leader updates it
@@ -347,7 +669,31 @@ sort_scatter_kernel(const void* __restrict__ keys_in, const uint32_t* __restrict
       s += c[k];
     }
     uint32_t ex, start;
-    block_exclusive_scan2(s, s_tot[d], tmp, &ex, &start);
+    if (HOT) {
+      // cold bins start where the cold keys before them end; hot bin h starts
+      // after every cold key below hot ID h (iv columns 0..h) and every hot
+      // occurrence of the hot IDs before it
+      const bool cold = (uint32_t)d < cold_bins;
+      const uint32_t x[4] = {s, cold ? s_tot[d] : 0u, cold ? 0u : s_tot[d], iv_tot};
+      uint32_t e4[4], a4[4];
+      block_exclusive_scan_v<4>(x, tmp, e4, a4);
+      ex = e4[0];
+      start = cold ? e4[1] : e4[2] + e4[3] + x[3];
+      if (blockIdx.x == 0) {
+        // for the later passes: hot occurrences below each hot ID, cold keys
+        if (!cold) ht.prefix[d - cold_bins] = e4[2];
+        if (d == 0) {
+          ht.prefix[H] = a4[2];
+          ht.meta[1] = a4[1];
+        }
+      }
+    } else {
+      const uint32_t x[2] = {s, s_tot[d]};
+      uint32_t e2[2], a2[2];
+      block_exclusive_scan_v<2>(x, tmp, e2, a2);
+      ex = e2[0];
+      start = e2[1];
+    }
     gshift[d] = start + gshift[d] - ex;   // modulo 2^32
     uint32_t run = ex;
 #pragma unroll
@@ -361,79 +707,189 @@ sort_scatter_kernel(const void* __restrict__ keys_in, const uint32_t* __restrict
   for (int r = 0; r < ITEMS; ++r) {
     const int64_t i = base + (int64_t)r * kWave;
     if (i < n) {
-      const uint32_t digit = (key[r] >> shift) & mask;
-      const uint32_t pos = cnt[w][digit] + rank[r];
+      const uint32_t pos = cnt[w][dig(r)] + rank[r];
       s_keys[pos] = key[r];
-      s_vals[pos] = FIRST ? (uint32_t)i : val[r];
+      // kHotFirst: the digit beside the key's place in the tile
+      s_vals[pos] = HOT ? (uint32_t)(i - tile0) | (dig(r) << 16) : (FIRST ? (uint32_t)i : val[r]);
     }
   }
   __syncthreads();
   const int64_t tile_n = (n - tile0) < kTile ? (n - tile0) : kTile;
+  if (GAP) {
+    // cnt is free now: the hot prefix [0, 256), hot IDs [256, 512), buckets [512, 1024)
+    uint32_t* c32 = &cnt[0][0];
+    c32[d] = g_prefix;
+    c32[256 + d] = g_id;
+    c32[512 + d] = g_bucket0;
+    c32[512 + kSortBlock + d] = g_bucket1;
+    __syncthreads();
+    const HotLookup gl{reinterpret_cast<const uint16_t*>(c32 + 512), c32 + 256, g_H, bshift};
+    const uint32_t* prefix = c32;
+    auto put = [&](int64_t i) {
+      const uint32_t k = s_keys[i];
+      bool hot;
+      const uint32_t below = gl.rank(k, &hot);
+      const uint32_t g = gshift[(k >> shift) & mask] + (uint32_t)i + prefix[below];
+      if ((int64_t)g < n_total) {   // always true when the counts are consistent
+        keys_out[g] = k;
+        vals_out[g] = s_vals[i];
+      }
+    };
+    if (tile_n == kTile) {
+#pragma unroll
+      for (int r = 0; r < ITEMS; ++r) put(threadIdx.x + (int64_t)r * kSortBlock);
+    } else {
+      for (int64_t i = threadIdx.x; i < tile_n; i += kSortBlock) put(i);
+    }
+    return;
+  }
   for (int i = threadIdx.x; i < tile_n; i += kSortBlock) {
     const uint32_t k = s_keys[i];
-    const uint32_t g = gshift[(k >> shift) & mask] + (uint32_t)i;
+    const uint32_t v = s_vals[i];
+    const uint32_t digit = HOT ? v >> 16 : (k >> shift) & mask;
+    const uint32_t val_out = HOT ? (uint32_t)tile0 + (v & 0xffffu) : v;
+    const uint32_t g = gshift[digit] + (uint32_t)i;
+    uint32_t* ko = keys_out;
+    uint32_t* vo = vals_out;
+    if (HOT && digit >= cold_bins) {   // a hot ID: straight to its final place
+      ko = keys_fin;
+      vo = vals_fin;
+    }
     if ((int64_t)g < n) {   // always true when the counts are consistent
-      keys_out[g] = k;
-      vals_out[g] = s_vals[i];
+      ko[g] = k;
+      vo[g] = val_out;
     }
   }
 }
 
-SortPlan plan_sort(int64_t n, int64_t R) {
+#define GBA_SCATTER_PARAMS                                                                              \
+  const void* __restrict__ keys_in, const uint32_t* __restrict__ vals_in, uint32_t* __restrict__ keys_out,  \
+      uint32_t* __restrict__ vals_out, uint32_t* __restrict__ keys_fin, uint32_t* __restrict__ vals_fin,   \
+      int64_t n_arg, const uint32_t* __restrict__ n_dev, int64_t n_total, int shift, int bits, int64_t R,   \
+      const uint32_t* __restrict__ hist, const uint32_t* __restrict__ chunk,                               \
+      const uint32_t* __restrict__ total, HotTables ht
+#define GBA_SCATTER_ARGS \
+  keys_in, vals_in, keys_out, vals_out, keys_fin, vals_fin, n_arg, n_dev, n_total, shift, bits, R, hist, chunk, total, ht
+
+template <bool FIRST, int ITEMS, int MODE>
+__global__ void __launch_bounds__(kSortBlock) sort_scatter_kernel(GBA_SCATTER_PARAMS) {
+  scatter_tile<FIRST, ITEMS, MODE>(GBA_SCATTER_ARGS);
+}
+
+// The hot-key first pass.
+__global__ void __launch_bounds__(kSortBlock) sort_scatter_hot_first_kernel(GBA_SCATTER_PARAMS) {
+  scatter_tile<true, kItemsHotFirst, kHotFirst>(GBA_SCATTER_ARGS);
+}
+
+SortPlan plan_sort(int64_t n, int64_t R, int hot_mode) {
   SortPlan p{};
   p.n = n;
   int bits = 1;
   while (bits < 32 && ((int64_t)1 << bits) < R) ++bits;
   p.key_bits = bits;
   p.passes = (bits + 7) / 8;
+  p.first_bits = bits - 8 * (p.passes - 1);
+  // The hot plan needs room for hot bins beside the first pass's cold bins; a
+  // key whose width is a whole number of bytes gets a first pass of hot bins
+  // only (one cold bin), which pays when it saves a full pass of cold keys.
+  bool hot = bits >= 9 && bits <= 31 && n > 0;
+  int hot_passes = p.passes, hot_first = p.first_bits;
+  if (p.first_bits == 8) {
+    hot_passes = p.passes + 1;
+    hot_first = 0;
+    hot = hot && p.passes >= 3;
+  }
+  if (hot_mode == 0) hot = false;
+  if (hot_mode < 0) hot = hot && n >= kHotMinKeys;
+  p.hot = hot;
+  if (hot) {
+    p.passes = hot_passes;
+    p.first_bits = hot_first;
+    const int cold_bins = 1 << hot_first;
+    p.hot_cap = kRadix - cold_bins < kHotCap ? kRadix - cold_bins : kHotCap;
+  }
   p.blocks = n > 0 ? ceil_div(n, tile_keys<kItemsFirst>()) : 0;
-  p.bytes = sort_layout(n, p.blocks).bytes;
+  p.bytes = sort_layout(n, p.blocks, p.hot).bytes;
   return p;
 }
 
 hipError_t launch_sort_ids(const int64_t* ids, int64_t n, int64_t R, const SortPlan& plan, void* ws,
                            const uint32_t** keys_out, const uint32_t** vals_out, int32_t* err,
                            hipStream_t stream) {
-  const SortLayout L = sort_layout(n, plan.blocks);
+  const SortLayout L = sort_layout(n, plan.blocks, plan.hot);
   char* p = static_cast<char*>(ws);
-  uint32_t* keys[2] = {reinterpret_cast<uint32_t*>(p + L.off_keys0), reinterpret_cast<uint32_t*>(p + L.off_keys1)};
-  uint32_t* vals[2] = {reinterpret_cast<uint32_t*>(p + L.off_vals0), reinterpret_cast<uint32_t*>(p + L.off_vals1)};
+  uint32_t* keys[3] = {reinterpret_cast<uint32_t*>(p + L.off_keys0), reinterpret_cast<uint32_t*>(p + L.off_keys1),
+                       plan.hot ? reinterpret_cast<uint32_t*>(p + L.off_keys2) : nullptr};
+  uint32_t* vals[3] = {reinterpret_cast<uint32_t*>(p + L.off_vals0), reinterpret_cast<uint32_t*>(p + L.off_vals1),
+                       plan.hot ? reinterpret_cast<uint32_t*>(p + L.off_vals2) : nullptr};
   uint32_t* hist = reinterpret_cast<uint32_t*>(p + L.off_hist);
   uint32_t* chunk = reinterpret_cast<uint32_t*>(p + L.off_chunk);
   uint32_t* total = reinterpret_cast<uint32_t*>(p + L.off_total);
-  *keys_out = keys[0];
-  *vals_out = vals[0];
+  HotTables ht{};
+  if (plan.hot) ht = hot_tables(p, L, plan.key_bits);
+  *keys_out = keys[plan.hot ? 2 : 0];
+  *vals_out = vals[plan.hot ? 2 : 0];
   if (n <= 0) return hipSuccess;
   hipError_t e;
+  const dim3 block(kSortBlock);
+  if (plan.hot) {
+    hipLaunchKernelGGL(hot_select_kernel, dim3(1), dim3(kHotBlock), 0, stream, ids, n, R, plan.hot_cap, ht);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
   int cur = 0;
   // the narrowest digit goes first: the first pass sees keys in arrival order,
   // and fewer bins there mean longer runs of equal digits to write
-  const int first_bits = plan.key_bits - 8 * (plan.passes - 1);
+  const int first_bits = plan.first_bits;
+  const uint32_t* n_cold = plan.hot ? ht.meta + 1 : nullptr;
   for (int pass = 0; pass < plan.passes; ++pass) {
     const int shift = pass == 0 ? 0 : first_bits + 8 * (pass - 1);
     const int bits = pass == 0 ? first_bits : 8;
-    const int out = pass == 0 ? 0 : 1 - cur;
+    const bool last = pass == plan.passes - 1;
+    const int out = pass == 0 ? 0 : ((plan.hot && last) ? 2 : 1 - cur);
     const void* kin = pass == 0 ? (const void*)ids : (const void*)keys[cur];
-    const int64_t tiles = ceil_div(n, pass == 0 ? tile_keys<kItemsFirst>() : tile_keys<kItemsRest>());
+    const int64_t tiles = ceil_div(n, pass > 0 ? tile_keys<kItemsRest>()
+                                               : (plan.hot ? tile_keys<kItemsHotFirst>() : tile_keys<kItemsFirst>()));
     const int64_t nchunks = ceil_div(tiles, kChunk);
-    const dim3 grid((unsigned)tiles), block(kSortBlock);
-    if (pass == 0)
-      hipLaunchKernelGGL((sort_tile_hist_kernel<true, kItemsFirst>), dim3((unsigned)nchunks), block, 0, stream,
-                         kin, n, tiles, shift, bits, R, hist, chunk, err);
+    const dim3 grid((unsigned)tiles);
+    if (pass == 0 && plan.hot)
+      hipLaunchKernelGGL((sort_tile_hist_kernel<true, kItemsHotFirst, kHotFirst>), dim3((unsigned)nchunks), block, 0,
+                         stream, kin, n, (const uint32_t*)nullptr, shift, bits, R, hist, chunk, ht, err);
+    else if (pass == 0)
+      hipLaunchKernelGGL((sort_tile_hist_kernel<true, kItemsFirst, kPlain>), dim3((unsigned)nchunks), block, 0,
+                         stream, kin, n, (const uint32_t*)nullptr, shift, bits, R, hist, chunk, ht, err);
+    else if (plan.hot)
+      hipLaunchKernelGGL((sort_tile_hist_kernel<false, kItemsRest, kCold>), dim3((unsigned)nchunks), block, 0,
+                         stream, kin, n, n_cold, shift, bits, R, hist, chunk, ht, err);
     else
-      hipLaunchKernelGGL((sort_tile_hist_kernel<false, kItemsRest>), dim3((unsigned)nchunks), block, 0, stream,
-                         kin, n, tiles, shift, bits, R, hist, chunk, err);
+      hipLaunchKernelGGL((sort_tile_hist_kernel<false, kItemsRest, kPlain>), dim3((unsigned)nchunks), block, 0,
+                         stream, kin, n, (const uint32_t*)nullptr, shift, bits, R, hist, chunk, ht, err);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(sort_digit_scan_kernel, dim3(kRadix), block, 0, stream, chunk, nchunks, total);
+    const bool with_iv = pass == 0 && plan.hot;
+    hipLaunchKernelGGL(sort_digit_scan_kernel, dim3(with_iv ? 2 * kRadix : kRadix), block, 0, stream, chunk,
+                       nchunks, total, (const uint32_t*)ht.iv_chunk, ht.iv_total);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    if (pass == 0)
-      hipLaunchKernelGGL((sort_scatter_kernel<true, kItemsFirst>), grid, block, 0, stream, kin,
-                         (const uint32_t*)nullptr, keys[out], vals[out], n, shift, bits, R, (const uint32_t*)hist,
-                         (const uint32_t*)chunk, (const uint32_t*)total);
+    const uint32_t* vin = pass == 0 ? (const uint32_t*)nullptr : (const uint32_t*)vals[cur];
+    if (pass == 0 && plan.hot)
+      hipLaunchKernelGGL(sort_scatter_hot_first_kernel, grid, block, 0, stream, kin, vin,
+                         keys[0], vals[0], keys[2], vals[2], n, (const uint32_t*)nullptr, n, shift, bits, R,
+                         (const uint32_t*)hist, (const uint32_t*)chunk, (const uint32_t*)total, ht);
+    else if (pass == 0)
+      hipLaunchKernelGGL((sort_scatter_kernel<true, kItemsFirst, kPlain>), grid, block, 0, stream, kin, vin,
+                         keys[0], vals[0], (uint32_t*)nullptr, (uint32_t*)nullptr, n, (const uint32_t*)nullptr, n,
+                         shift, bits, R, (const uint32_t*)hist, (const uint32_t*)chunk, (const uint32_t*)total, ht);
+    else if (plan.hot && last)
+      hipLaunchKernelGGL((sort_scatter_kernel<false, kItemsRest, kColdLast>), grid, block, 0, stream, kin, vin,
+                         keys[out], vals[out], (uint32_t*)nullptr, (uint32_t*)nullptr, n, n_cold, n, shift, bits,
+                         R, (const uint32_t*)hist, (const uint32_t*)chunk, (const uint32_t*)total, ht);
+    else if (plan.hot)
+      hipLaunchKernelGGL((sort_scatter_kernel<false, kItemsRest, kCold>), grid, block, 0, stream, kin, vin,
+                         keys[out], vals[out], (uint32_t*)nullptr, (uint32_t*)nullptr, n, n_cold, n, shift, bits,
+                         R, (const uint32_t*)hist, (const uint32_t*)chunk, (const uint32_t*)total, ht);
     else
-      hipLaunchKernelGGL((sort_scatter_kernel<false, kItemsRest>), grid, block, 0, stream, kin,
-                         (const uint32_t*)vals[cur], keys[out], vals[out], n, shift, bits, R,
-                         (const uint32_t*)hist, (const uint32_t*)chunk, (const uint32_t*)total);
+      hipLaunchKernelGGL((sort_scatter_kernel<false, kItemsRest, kPlain>), grid, block, 0, stream, kin, vin,
+                         keys[out], vals[out], (uint32_t*)nullptr, (uint32_t*)nullptr, n, (const uint32_t*)nullptr,
+                         n, shift, bits, R, (const uint32_t*)hist, (const uint32_t*)chunk, (const uint32_t*)total,
+                         ht);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     cur = out;
   }

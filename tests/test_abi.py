@@ -67,3 +67,23 @@ def test_token_of_batch_host_function():
         for i in (0, 1, M - 1, M, 5 * M + 2):
             assert gba.gba_token_of_batch(i, M) == oracle.token_of_batch(i, M)
     assert gba.gba_token_of_batch(-1, 4) == -1 and gba.gba_token_of_batch(3, 0) == -1
+
+
+def test_sort_workspace_query_and_host_checks():
+    L = gba.lib()
+    # the hot-key plan needs a third key/index array pair; where the key width
+    # leaves it no room (8-bit or 32-bit keys) it is the plain plan
+    n = 5_000_000
+    plain = gba.gba_sort_ids_workspace_size(n, 500_000_000, gba.SORT_PLAIN)
+    hot = gba.gba_sort_ids_workspace_size(n, 500_000_000, gba.SORT_HOT)
+    assert hot >= plain + 8 * n
+    assert gba.gba_sort_ids_workspace_size(n, 500_000_000, gba.SORT_AUTO) == hot
+    assert gba.gba_sort_ids_workspace_size(1000, 500_000_000, gba.SORT_AUTO) == \
+        gba.gba_sort_ids_workspace_size(1000, 500_000_000, gba.SORT_PLAIN)
+    for R in (200, 1 << 32):
+        assert gba.gba_sort_ids_workspace_size(n, R, gba.SORT_HOT) == gba.gba_sort_ids_workspace_size(n, R, 0)
+    for bad in [(-1, 10, 0), (10, 0, 0), (10, (1 << 32) + 1, 0), (10, 10, 2), (10, 10, -2)]:
+        with pytest.raises(gba.GBAError):
+            gba.gba_sort_ids_workspace_size(*bad)
+    assert L.gba_sort_ids(None, 10, 100, 0, None, None, None, 0, None, None) == 1
+    assert L.gba_sort_ids(None, 10, 100, 5, None, None, None, 0, None, None) == 2
