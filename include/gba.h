@@ -254,6 +254,26 @@ gba_status gba_sort_ids(const int64_t* ids, int64_t n, int64_t R, int32_t plan, 
                         hipStream_t stream);
 
 /*
+ * gba_aggregate_sparse with the sort plan chosen by the caller (GBA_SORT_AUTO,
+ * GBA_SORT_PLAIN or GBA_SORT_HOT, as for gba_sort_ids); gba_aggregate_sparse
+ * is this call with GBA_SORT_AUTO.  With the hot-key plan the frequent IDs
+ * are also reduced apart from the others; every output is the same either way
+ * (the sums to within their float64 rounding, taken in a fixed order).  The
+ * workspace size depends on the plan.
+ */
+gba_status gba_aggregate_sparse_plan_workspace_size(int64_t N, int32_t K, int32_t D, int64_t R, int32_t plan,
+                                                    size_t* bytes /* host out */);
+
+gba_status gba_aggregate_sparse_plan(const int64_t* ids, const float* rows,
+                                     const int64_t* contrib_offsets, int32_t K, int64_t N, int32_t D,
+                                     int64_t R, const float* w, const int64_t* tokens, int64_t step,
+                                     int64_t iota, int32_t* tag, gba_decay decay, gba_norm norm,
+                                     int64_t* unique_ids, int64_t* seg_offsets, int32_t* contrib_count,
+                                     int32_t* active_count, float* agg, int64_t* num_unique,
+                                     void* workspace, size_t workspace_bytes, int32_t plan, int32_t* err,
+                                     hipStream_t stream);
+
+/*
  * Pull side (Sec. 3.1 token list; Alg. 2, pull responder).
  *
  * gba_token_of_batch (host function, no device work): the token handed out

@@ -21,6 +21,7 @@ __all__ = [
     "gba_token_of_batch", "gba_pull_workspace_size", "gba_pull_rows", "gba_hash_clear",
     "gba_hash_workspace_size", "gba_hash_find_or_insert", "gba_hash_rehash", "EMPTY_ID", "DERR_TABLE_FULL",
     "gba_sort_ids_workspace_size", "gba_sort_ids", "SORT_AUTO", "SORT_PLAIN", "SORT_HOT",
+    "gba_aggregate_sparse_plan_workspace_size", "gba_aggregate_sparse_plan",
     "pointer_table", "DECAY_TOKEN", "DECAY_ID_TAG", "NORM_PER_ID_COUNT", "NORM_BY_K",
     "DERR_ID_RANGE", "DERR_FUTURE_TOKEN", "DERR_OFFSETS", "DERR_ROW_RANGE", "MAX_K", "MAX_D",
     "LIB_PATH",
@@ -50,6 +51,10 @@ _SIGNATURES = {
     "gba_aggregate_sparse_workspace_size": ([_I64, _I32, _I32, _I64, ctypes.POINTER(ctypes.c_size_t)], _I32),
     "gba_aggregate_sparse": ([_P, _P, _P, _I32, _I64, _I32, _I64, _P, _P, _I64, _I64, _P, _I32, _I32,
                               _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P, _P], _I32),
+    "gba_aggregate_sparse_plan_workspace_size": ([_I64, _I32, _I32, _I64, _I32, ctypes.POINTER(ctypes.c_size_t)],
+                                                 _I32),
+    "gba_aggregate_sparse_plan": ([_P, _P, _P, _I32, _I64, _I32, _I64, _P, _P, _I64, _I64, _P, _I32, _I32,
+                                   _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _I32, _P, _P], _I32),
     "gba_aggregate_apply_dense_adagrad": ([_P, _P, _I32, _I64, _P, _P, _P, _F64, _F64, _P], _I32),
     "gba_aggregate_apply_dense_adam": ([_P, _P, _I32, _I64, _P, _P, _P, _P, _F64, _F64, _F64, _F64, _I64, _P],
                                        _I32),
@@ -301,9 +306,15 @@ def gba_aggregate_sparse_workspace_size(N, K, D, R) -> int:
     return int(n.value)
 
 
-def gba_aggregate_sparse(ids, rows, contrib_offsets, R, w, tokens, step, iota, tag, decay, norm,
-                         unique_ids, seg_offsets, contrib_count, active_count, agg, num_unique,
-                         workspace, err=None, stream=None):
+def gba_aggregate_sparse_plan_workspace_size(N, K, D, R, plan) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib().gba_aggregate_sparse_plan_workspace_size(int(N), int(K), int(D), int(R), int(plan),
+                                                          ctypes.byref(n)))
+    return int(n.value)
+
+
+def _sparse_args(ids, rows, contrib_offsets, R, w, tokens, tag, unique_ids, seg_offsets, contrib_count,
+                 active_count, agg, num_unique, workspace, err):
     N = ids.numel()
     K = contrib_offsets.numel() - 1
     D = rows.shape[-1]
@@ -321,11 +332,32 @@ def gba_aggregate_sparse(ids, rows, contrib_offsets, R, w, tokens, step, iota, t
     _need(num_unique, torch.int64, "num_unique", 1)
     _need(workspace, torch.uint8, "workspace")
     _need(err, torch.int32, "err", 1)
+    return N, K, D
+
+
+def gba_aggregate_sparse(ids, rows, contrib_offsets, R, w, tokens, step, iota, tag, decay, norm,
+                         unique_ids, seg_offsets, contrib_count, active_count, agg, num_unique,
+                         workspace, err=None, stream=None):
+    N, K, D = _sparse_args(ids, rows, contrib_offsets, R, w, tokens, tag, unique_ids, seg_offsets, contrib_count,
+                           active_count, agg, num_unique, workspace, err)
     _check(lib().gba_aggregate_sparse(
         _ptr(ids), _ptr(rows), _ptr(contrib_offsets), K, N, D, int(R), _ptr(w), _ptr(tokens), int(step),
         int(iota), _ptr(tag), int(decay), int(norm), _ptr(unique_ids), _ptr(seg_offsets),
         _ptr(contrib_count), _ptr(active_count), _ptr(agg), _ptr(num_unique), _ptr(workspace),
         workspace.numel(), _ptr(err), _stream(stream)))
+
+
+def gba_aggregate_sparse_plan(ids, rows, contrib_offsets, R, w, tokens, step, iota, tag, decay, norm,
+                              unique_ids, seg_offsets, contrib_count, active_count, agg, num_unique,
+                              workspace, plan, err=None, stream=None):
+    """gba_aggregate_sparse with the sort plan chosen by the caller (SORT_AUTO, SORT_PLAIN, SORT_HOT)."""
+    N, K, D = _sparse_args(ids, rows, contrib_offsets, R, w, tokens, tag, unique_ids, seg_offsets, contrib_count,
+                           active_count, agg, num_unique, workspace, err)
+    _check(lib().gba_aggregate_sparse_plan(
+        _ptr(ids), _ptr(rows), _ptr(contrib_offsets), K, N, D, int(R), _ptr(w), _ptr(tokens), int(step),
+        int(iota), _ptr(tag), int(decay), int(norm), _ptr(unique_ids), _ptr(seg_offsets),
+        _ptr(contrib_count), _ptr(active_count), _ptr(agg), _ptr(num_unique), _ptr(workspace),
+        workspace.numel(), int(plan), _ptr(err), _stream(stream)))
 
 
 def gba_apply_adagrad(param, accum, grad, lr, eps, rows=None, active=None, num_rows=None, R=0,

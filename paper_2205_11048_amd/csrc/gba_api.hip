@@ -18,8 +18,8 @@ inline gba_status from_hip(hipError_t e) { return e == hipSuccess ? GBA_OK : GBA
 
 bool width_ok(int32_t D) { return D >= 4 && D <= GBA_MAX_D && D % 4 == 0; }
 
-size_t sparse_bytes(int64_t N, int32_t D, int64_t R, SortPlan* plan_out) {
-  const SortPlan plan = plan_sort(N, R);
+size_t sparse_bytes(int64_t N, int32_t D, int64_t R, int32_t sort_plan, SortPlan* plan_out) {
+  const SortPlan plan = plan_sort(N, R, sort_plan);
   if (plan_out) *plan_out = plan;
   return align_up(plan.bytes) + align_up(segments_workspace_bytes(N, D));
 }
@@ -125,14 +125,19 @@ gba_status gba_finalize_apply_dense_adam(double* run, int32_t K, int64_t P, floa
                                                    adam_params(lr, beta1, beta2, eps, t), reset != 0, stream));
 }
 
-gba_status gba_aggregate_sparse_workspace_size(int64_t N, int32_t K, int32_t D, int64_t R,
-                                               size_t* bytes) {
+gba_status gba_aggregate_sparse_plan_workspace_size(int64_t N, int32_t K, int32_t D, int64_t R, int32_t plan,
+                                                    size_t* bytes) {
   if (!bytes) return GBA_ERR_NULL;
-  if (K < 1 || K > GBA_MAX_K || N < 0 || N > kMaxN || R < 1 || R > (int64_t(1) << 32))
+  if (K < 1 || K > GBA_MAX_K || N < 0 || N > kMaxN || R < 1 || R > (int64_t(1) << 32) || plan < -1 || plan > 1)
     return GBA_ERR_INVALID_ARG;
   if (!width_ok(D)) return GBA_ERR_UNSUPPORTED;
-  *bytes = sparse_bytes(N, D, R, nullptr);
+  *bytes = sparse_bytes(N, D, R, plan, nullptr);
   return GBA_OK;
+}
+
+gba_status gba_aggregate_sparse_workspace_size(int64_t N, int32_t K, int32_t D, int64_t R,
+                                               size_t* bytes) {
+  return gba_aggregate_sparse_plan_workspace_size(N, K, D, R, GBA_SORT_AUTO, bytes);
 }
 
 gba_status gba_aggregate_sparse(const int64_t* ids, const float* rows, const int64_t* contrib_offsets,
@@ -142,8 +147,21 @@ gba_status gba_aggregate_sparse(const int64_t* ids, const float* rows, const int
                                 int64_t* seg_offsets, int32_t* contrib_count, int32_t* active_count,
                                 float* agg, int64_t* num_unique, void* workspace,
                                 size_t workspace_bytes, int32_t* err, hipStream_t stream) {
+  return gba_aggregate_sparse_plan(ids, rows, contrib_offsets, K, N, D, R, w, tokens, step, iota, tag, decay, norm,
+                                   unique_ids, seg_offsets, contrib_count, active_count, agg, num_unique, workspace,
+                                   workspace_bytes, GBA_SORT_AUTO, err, stream);
+}
+
+gba_status gba_aggregate_sparse_plan(const int64_t* ids, const float* rows, const int64_t* contrib_offsets,
+                                     int32_t K, int64_t N, int32_t D, int64_t R, const float* w,
+                                     const int64_t* tokens, int64_t step, int64_t iota, int32_t* tag,
+                                     gba_decay decay, gba_norm norm, int64_t* unique_ids,
+                                     int64_t* seg_offsets, int32_t* contrib_count, int32_t* active_count,
+                                     float* agg, int64_t* num_unique, void* workspace,
+                                     size_t workspace_bytes, int32_t sort_plan, int32_t* err, hipStream_t stream) {
   if (K < 1 || K > GBA_MAX_K || N < 0 || N > kMaxN || R < 1 || R > (int64_t(1) << 32))
     return GBA_ERR_INVALID_ARG;
+  if (sort_plan < -1 || sort_plan > 1) return GBA_ERR_INVALID_ARG;
   if (decay != GBA_DECAY_TOKEN && decay != GBA_DECAY_ID_TAG) return GBA_ERR_INVALID_ARG;
   if (norm != GBA_NORM_PER_ID_COUNT && norm != GBA_NORM_BY_K) return GBA_ERR_INVALID_ARG;
   if (!width_ok(D)) return GBA_ERR_UNSUPPORTED;
@@ -159,16 +177,22 @@ gba_status gba_aggregate_sparse(const int64_t* ids, const float* rows, const int
       !aligned16(workspace))
     return GBA_ERR_INVALID_ARG;
   SortPlan plan;
-  const size_t need = sparse_bytes(N, D, R, &plan);
+  const size_t need = sparse_bytes(N, D, R, sort_plan, &plan);
   if (workspace_bytes < need) return GBA_ERR_WORKSPACE;
 
   char* ws = static_cast<char*>(workspace);
   const uint32_t* keys = nullptr;
   const uint32_t* vals = nullptr;
-  hipError_t e = launch_sort_ids(ids, N, R, plan, ws, &keys, &vals, err, stream);
+  // with the hot-key plan the frequent IDs are reduced apart from the rest
+  SortHot hot;
+  hipError_t e = launch_sort_ids(ids, N, R, plan, ws, &keys, &vals, err, stream, plan.hot ? &hot : nullptr);
   if (e != hipSuccess) return GBA_ERR_HIP;
 
   SegmentArgs a;
+  if (plan.hot) {
+    a.n_dev = hot.n_cold;
+    a.hot = hot;
+  }
   a.keys = keys;
   a.vals = vals;
   a.rows = rows;

@@ -70,12 +70,27 @@ struct SortPlan {
 // hot_mode: -1 picks the hot-key plan for large inputs whose key width leaves
 // room for it, 0 never, 1 whenever the key width allows.
 SortPlan plan_sort(int64_t n, int64_t R, int hot_mode = -1);
+// With the hot-key plan the sort can also hand over its two parts apart
+// ("split"): the cold keys sorted in [0, *n_cold) of *keys_out / *vals_out,
+// and the occurrence indices of the hot IDs grouped by hot ID (ascending
+// within each).  Every hot ID occurs at least once (it was seen in the sample).
+struct SortHot {
+  const uint32_t* n_cold = nullptr;     // device word: number of cold keys (null: no hot plan)
+  const uint32_t* hot_vals = nullptr;   // [n - n_cold] occurrence indices of the hot IDs
+  const uint32_t* ids = nullptr;        // [256] hot IDs, ascending ([0, H) used)
+  const uint16_t* bucket = nullptr;     // [1024] hot IDs whose key >> bshift is below the index
+  const uint32_t* prefix = nullptr;     // [256] hot occurrences of the hot IDs before h; [H] = all
+  const uint32_t* meta = nullptr;       // [0] = H
+  const uint32_t* iv_total = nullptr;   // [256] cold keys with exactly h hot IDs below them
+  int bshift = 0;
+};
 // Sorts ids (int64 [n], each checked against [0, R)) by value, stably.  The
 // sorted keys and original occurrence indices are returned through
-// *keys_out / *vals_out, which point into `ws`.
+// *keys_out / *vals_out, which point into `ws`.  With `split` non-null and
+// the hot-key plan, the output is split as described above.
 hipError_t launch_sort_ids(const int64_t* ids, int64_t n, int64_t R, const SortPlan& plan, void* ws,
                            const uint32_t** keys_out, const uint32_t** vals_out, int32_t* err,
-                           hipStream_t stream);
+                           hipStream_t stream, SortHot* split = nullptr);
 
 // ---- segments over the sorted keys: dedup, counts, decayed weighted sums
 struct SegmentArgs {
@@ -96,6 +111,11 @@ struct SegmentArgs {
   float* agg;
   int64_t* num_unique;
   int32_t* err;
+  // Split hot-key plan: keys/vals hold only the cold keys, *n_dev of them,
+  // and the hot IDs (hot) are reduced apart; the outputs interleave both in
+  // ID order.  Null n_dev: keys/vals hold all N occurrences.
+  const uint32_t* n_dev = nullptr;
+  SortHot hot;
 };
 size_t segments_workspace_bytes(int64_t N, int32_t D);
 hipError_t launch_segments(const SegmentArgs& a, void* ws, hipStream_t stream);
@@ -104,8 +124,9 @@ hipError_t launch_segments(const SegmentArgs& a, void* ws, hipStream_t stream);
 // of runs that start before it (tile_base[ceil(N/1024)]); *total = number of runs
 constexpr int64_t kRunTile = 1024;
 size_t run_heads_workspace_bytes(int64_t N);
+// n_dev (optional): the number of keys, on the device (at most N)
 hipError_t launch_run_heads(const uint32_t* keys, int64_t N, uint32_t* tile_base, uint32_t* total, void* scan_ws,
-                            hipStream_t stream);
+                            hipStream_t stream, const uint32_t* n_dev = nullptr);
 
 // ---- pull side: distinct IDs of a worker's request, the inverse map, the rows
 struct PullArgs {

@@ -72,6 +72,7 @@ struct HotTables {
   uint32_t* iv_total;   // [256] the same over all chunks
   uint8_t* digit;       // [n] first-pass digit of every key (written by the histogram launch)
   int bshift;           // key >> bshift is the key's bucket
+  int split;            // hot occurrences go to their own array, grouped by hot ID (not among the cold keys)
 };
 
 struct SortLayout {
@@ -545,7 +546,8 @@ __device__ __forceinline__ void block_exclusive_scan_v(const uint32_t (&x)[V], u
 }
 
 // Scatter of one tile.  kHotFirst writes cold keys to keys_out/vals_out and
-// hot ones to their final places in keys_fin/vals_fin; kColdLast writes the
+// hot ones to their final places in keys_fin/vals_fin (split: grouped by hot
+// ID, from 0, with no cold keys between them); kColdLast writes the
 // cold keys to keys_out/vals_out (the final arrays), each past the hot runs of
 // the hot IDs below it.  n_total bounds the final arrays.
 template <bool FIRST, int ITEMS, int MODE>
@@ -678,7 +680,7 @@ scatter_tile(const void* __restrict__ keys_in, const uint32_t* __restrict__ vals
       uint32_t e4[4], a4[4];
       block_exclusive_scan_v<4>(x, tmp, e4, a4);
       ex = e4[0];
-      start = cold ? e4[1] : e4[2] + e4[3] + x[3];
+      start = cold ? e4[1] : (ht.split ? e4[2] : e4[2] + e4[3] + x[3]);
       if (blockIdx.x == 0) {
         // for the later passes: hot occurrences below each hot ID, cold keys
         if (!cold) ht.prefix[d - cold_bins] = e4[2];
@@ -815,7 +817,7 @@ SortPlan plan_sort(int64_t n, int64_t R, int hot_mode) {
 
 hipError_t launch_sort_ids(const int64_t* ids, int64_t n, int64_t R, const SortPlan& plan, void* ws,
                            const uint32_t** keys_out, const uint32_t** vals_out, int32_t* err,
-                           hipStream_t stream) {
+                           hipStream_t stream, SortHot* split) {
   const SortLayout L = sort_layout(n, plan.blocks, plan.hot);
   char* p = static_cast<char*>(ws);
   uint32_t* keys[3] = {reinterpret_cast<uint32_t*>(p + L.off_keys0), reinterpret_cast<uint32_t*>(p + L.off_keys1),
@@ -827,8 +829,22 @@ hipError_t launch_sort_ids(const int64_t* ids, int64_t n, int64_t R, const SortP
   uint32_t* total = reinterpret_cast<uint32_t*>(p + L.off_total);
   HotTables ht{};
   if (plan.hot) ht = hot_tables(p, L, plan.key_bits);
-  *keys_out = keys[plan.hot ? 2 : 0];
-  *vals_out = vals[plan.hot ? 2 : 0];
+  ht.split = (plan.hot && split) ? 1 : 0;
+  *keys_out = keys[plan.hot && !split ? 2 : 0];
+  *vals_out = vals[plan.hot && !split ? 2 : 0];
+  if (split) {
+    *split = SortHot{};
+    if (plan.hot) {
+      split->n_cold = ht.meta + 1;
+      split->hot_vals = vals[2];
+      split->ids = ht.ids;
+      split->bucket = ht.bucket;
+      split->prefix = ht.prefix;
+      split->meta = ht.meta;
+      split->iv_total = ht.iv_total;
+      split->bshift = ht.bshift;
+    }
+  }
   if (n <= 0) return hipSuccess;
   hipError_t e;
   const dim3 block(kSortBlock);
@@ -845,7 +861,8 @@ hipError_t launch_sort_ids(const int64_t* ids, int64_t n, int64_t R, const SortP
     const int shift = pass == 0 ? 0 : first_bits + 8 * (pass - 1);
     const int bits = pass == 0 ? first_bits : 8;
     const bool last = pass == plan.passes - 1;
-    const int out = pass == 0 ? 0 : ((plan.hot && last) ? 2 : 1 - cur);
+    const bool gap = plan.hot && last && !ht.split;   // merged output: the cold keys make room for the hot runs
+    const int out = pass == 0 ? 0 : (gap ? 2 : 1 - cur);
     const void* kin = pass == 0 ? (const void*)ids : (const void*)keys[cur];
     const int64_t tiles = ceil_div(n, pass > 0 ? tile_keys<kItemsRest>()
                                                : (plan.hot ? tile_keys<kItemsHotFirst>() : tile_keys<kItemsFirst>()));
@@ -877,7 +894,7 @@ hipError_t launch_sort_ids(const int64_t* ids, int64_t n, int64_t R, const SortP
       hipLaunchKernelGGL((sort_scatter_kernel<true, kItemsFirst, kPlain>), grid, block, 0, stream, kin, vin,
                          keys[0], vals[0], (uint32_t*)nullptr, (uint32_t*)nullptr, n, (const uint32_t*)nullptr, n,
                          shift, bits, R, (const uint32_t*)hist, (const uint32_t*)chunk, (const uint32_t*)total, ht);
-    else if (plan.hot && last)
+    else if (gap)
       hipLaunchKernelGGL((sort_scatter_kernel<false, kItemsRest, kColdLast>), grid, block, 0, stream, kin, vin,
                          keys[out], vals[out], (uint32_t*)nullptr, (uint32_t*)nullptr, n, n_cold, n, shift, bits,
                          R, (const uint32_t*)hist, (const uint32_t*)chunk, (const uint32_t*)total, ht);

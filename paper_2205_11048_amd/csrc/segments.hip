@@ -21,6 +21,13 @@
 //    boundaries are joined in LDS; runs that cross tile boundaries leave one
 //    partial per tile end, joined by seg_fixup in a fixed order, so results
 //    are deterministic.
+//
+// With the split hot-key plan the sort hands over the cold keys and, apart,
+// the occurrences of each hot ID (a few hundred IDs holding about half of all
+// occurrences under Zipf skew).  The passes above then run over the cold keys
+// only and write each segment at its place among all IDs; each hot ID is one
+// long segment, summed by hot_rows (per 4096-occurrence chunk, no per-position
+// segment logic) and finished by hot_finish, both in a fixed order.
 #include "gba_device.hpp"
 #include "gba_internal.hpp"
 
@@ -32,7 +39,8 @@ constexpr int kRounds = 4;                                   // 16-byte loads pe
 constexpr int64_t kMetaTile = (int64_t)kSegBlock * kRounds;  // 1024 positions: 4 per thread of a block
 static_assert(kMetaTile == kRunTile, "run-head tiles are the per-position tiles");
 constexpr int kGroupSpan = 128;                              // positions per lane group in seg_rows
-constexpr int kBatch = 8;                                    // row gathers in flight per group
+constexpr int kBatch = 8;                                    // row gathers per batch of a group
+constexpr bool kPipelined = false;                           // next batch's gathers issued before this one is summed
 constexpr int kMaxBuckets = 1024;                            // contribution lookup buckets
 
 // packed word of a sorted position
@@ -74,10 +82,12 @@ struct SegPartials {
   uint32_t* fix_count;   // entries of fix_list (cleared before the row pass)
 };
 
+constexpr int kHotSlots = 256;   // at least the sort's largest number of hot IDs (+1)
+
 struct SegLayout {
-  int64_t meta_tiles, row_tiles;
+  int64_t meta_tiles, row_tiles, hot_chunks;
   size_t off_heads, off_total, off_scan, off_buckets, off_packed, off_base32,
-      off_cnt, off_first_acc, off_last_acc, off_fix, bytes;
+      off_cnt, off_first_acc, off_last_acc, off_fix, off_start, off_cnum, off_hot_acc, off_hot_cnt, bytes;
 };
 
 static SegLayout seg_layout(int64_t N, int32_t D) {
@@ -91,12 +101,20 @@ static SegLayout seg_layout(int64_t N, int32_t D) {
   L.off_total = o;     o += 256;                     // head total
   L.off_scan = o;      o += align_up(run_heads_workspace_bytes(N));
   L.off_buckets = o;   o += align_up(kMaxBuckets * 4);
-  L.off_packed = o;    o += align_up((n + kGroupSpan) * 4);   // padded: whole-group vector loads stay inside
+  L.off_packed = o;    o += align_up((n + 2 * kGroupSpan) * 4);   // padded: whole-group vector loads stay inside
   L.off_base32 = o;    o += align_up((n / kGroupSpan + 2) * 4);
   L.off_cnt = o;       o += align_up(rt * 16);
   L.off_fix = o;       o += 256 + align_up(rt * 16);  // count, then the list
   L.off_first_acc = o; o += align_up(rt * (size_t)D * 8);
   L.off_last_acc = o;  o += align_up(rt * (size_t)D * 8);
+  // the position where each (cold) segment starts, and its end
+  L.off_start = o;     o += align_up((n + 1) * 4);
+  // per hot ID: the cold segments below it, then the chunk prefix of its run
+  L.off_cnum = o;      o += align_up(2 * (kHotSlots + 1) * 4);
+  // per chunk of a hot run: float64 sums and (contributions, active, first and last contribution)
+  L.hot_chunks = rt + kHotSlots;
+  L.off_hot_acc = o;   o += align_up((size_t)L.hot_chunks * D * 8);
+  L.off_hot_cnt = o;   o += align_up((size_t)L.hot_chunks * 16);
   L.bytes = o;
   return L;
 }
@@ -116,6 +134,30 @@ __device__ __forceinline__ int count_le(const int32_t* off, int lo, int hi, uint
       len = half;
     }
   }
+  return lo;
+}
+
+// Entries of the ascending s[0, n) that are at most x (n <= 256): a fixed
+// sequence of halving steps, with no loop for the compiler to keep registers
+// live across.
+__device__ __forceinline__ uint32_t count_at_most(const uint32_t* s, uint32_t n, int64_t x) {
+  uint32_t pos = 0;
+#pragma unroll
+  for (uint32_t step = 128; step >= 1; step >>= 1) {
+    const uint32_t next = pos + step;
+    if (next <= n && (int64_t)s[next - 1] <= x) pos = next;
+  }
+  return pos;
+}
+
+// Hot IDs below `key` (split plan): the sort's bucket table narrows the
+// search to the hot IDs that share the key's top bits.
+__device__ __forceinline__ uint32_t hot_below(uint32_t key, const uint16_t* bucket, const uint32_t* ids, uint32_t H,
+                                              int bshift) {
+  const uint32_t t = key >> bshift;
+  uint32_t lo = bucket[t];
+  const uint32_t hi = t + 1 < 1024u ? (uint32_t)bucket[t + 1] : H;
+  while (lo < hi && ids[lo] < key) ++lo;
   return lo;
 }
 
@@ -148,6 +190,7 @@ __device__ __forceinline__ int contribution_global(const int64_t* off, int K, ui
   return m < 0 ? 0 : (m < K ? m : K - 1);
 }
 
+// out: the segment's place among all distinct IDs
 __device__ __forceinline__ void finalize_segment(const SegmentArgs& a, int64_t seg, f64x4 acc,
                                                  int cc, int ww, int lane, bool lane_on) {
   if (seg < 0 || seg >= a.N) return;   // unreachable when the numbering is consistent
@@ -265,11 +308,17 @@ __global__ void contrib_buckets_kernel(const int64_t* __restrict__ off, int K, i
 // covers 1 KB of consecutive keys, and the key before a lane's first one is
 // the last key of the lane before it.
 __global__ void __launch_bounds__(kSegBlock)
-seg_heads_kernel(const uint32_t* __restrict__ keys, int64_t N, int64_t tiles, uint32_t* __restrict__ heads) {
+seg_heads_kernel(const uint32_t* __restrict__ keys, int64_t N_arg, const uint32_t* __restrict__ n_dev, int64_t tiles,
+                 uint32_t* __restrict__ heads) {
   const int lane = lane_id();
   const int64_t tile = (int64_t)blockIdx.x * kSegWaves + threadIdx.x / kWave;
   if (tile >= tiles) return;   // whole waves leave; no block-wide barrier follows
+  const int64_t N = n_dev ? (int64_t)*n_dev : N_arg;
   const int64_t t0 = tile * kMetaTile;
+  if (t0 >= N) {   // past the keys on the device (a grid sized for the most keys)
+    if (lane == 0) heads[tile] = 0u;
+    return;
+  }
   uint32_t carry = t0 > 0 ? keys[t0 - 1] : 0u;   // position 0 is always a head
   uint32_t cnt = 0;
 #pragma unroll
@@ -297,13 +346,22 @@ seg_heads_kernel(const uint32_t* __restrict__ keys, int64_t N, int64_t tiles, ui
   if (lane == 0) heads[tile] = total;
 }
 
-__global__ void seg_finish_kernel(const uint32_t* __restrict__ total, int64_t N,
-                                  int64_t* __restrict__ num_unique, int64_t* __restrict__ seg_offsets,
-                                  uint32_t* __restrict__ fix_count) {
+// U, the end of the last segment, and (split plan) the defaults of the hot
+// IDs' places: above every cold segment, until the position pass finds a
+// cold segment above them.
+__global__ void __launch_bounds__(kSegBlock)
+seg_finish_kernel(const SegmentArgs a, const uint32_t* __restrict__ total, uint32_t* __restrict__ seg_start,
+                  uint32_t* __restrict__ cnum, uint32_t* __restrict__ fix_count) {
   const uint32_t U = *total;
-  *num_unique = (int64_t)U;
-  seg_offsets[U] = N;
-  *fix_count = 0u;   // the row pass appends to the fixup list
+  const uint32_t H = a.n_dev ? *a.hot.meta : 0u;
+  const int64_t n = a.n_dev ? (int64_t)*a.n_dev : a.N;
+  if (threadIdx.x == 0) {
+    *a.num_unique = (int64_t)U + H;
+    a.seg_offsets[U + H] = a.N;
+    seg_start[U] = (uint32_t)n;
+    *fix_count = 0u;   // the row pass appends to the fixup list
+  }
+  for (uint32_t h = threadIdx.x; h < H; h += kSegBlock) cnum[h] = U;
 }
 
 // Per-position pass: numbering, segment IDs and starts, packed words.
@@ -316,11 +374,18 @@ static_assert(kSegBlock * kMetaPer == kMetaTile, "a block covers one tile per pa
 __global__ void __launch_bounds__(kSegBlock)
 seg_meta_kernel(SegmentArgs a, const uint32_t* __restrict__ tile_seg_base,
                 const int32_t* __restrict__ buckets, int q, int nbuckets, int64_t num_tiles,
-                uint32_t* __restrict__ packed, uint32_t* __restrict__ base32) {
+                uint32_t* __restrict__ packed, uint32_t* __restrict__ base32, uint32_t* __restrict__ seg_start,
+                uint32_t* __restrict__ cnum) {
   extern __shared__ int32_t s_dyn[];
   __shared__ uint32_t s_wave_heads[kSegWaves];
+  // split plan: the hot IDs, their buckets and the hot occurrences below each
+  __shared__ uint32_t s_hbucket[512];
+  __shared__ uint32_t s_hids[kHotSlots];
+  __shared__ uint32_t s_hprefix[kHotSlots];
   const int K = a.K;
-  const int64_t N = a.N;
+  const int64_t N = a.N;                                        // occurrences
+  const int64_t n = a.n_dev ? (int64_t)*a.n_dev : a.N;          // sorted positions (the cold ones when split)
+  const bool split = a.n_dev != nullptr;
   int32_t* s_off = s_dyn;
   float* s_w = reinterpret_cast<float*>(s_dyn + K + 1);
   int32_t* s_sm = s_dyn + 2 * K + 1;
@@ -329,7 +394,17 @@ seg_meta_kernel(SegmentArgs a, const uint32_t* __restrict__ tile_seg_base,
   // 512), then, when every position of the block exists, all loads of its
   // tiles, so that the tables are waited for while the tiles are in flight.
   const int64_t blk0 = (int64_t)blockIdx.x * kMetaTilesPerBlock * kMetaTile;
-  const bool full = blk0 + kMetaTilesPerBlock * kMetaTile <= N;
+  if (blk0 >= n) return;   // the grid is sized for every occurrence
+  const bool full = blk0 + kMetaTilesPerBlock * kMetaTile <= n;
+  uint32_t H = 0;
+  if (split) {
+    H = *a.hot.meta;
+    const uint32_t* b32 = reinterpret_cast<const uint32_t*>(a.hot.bucket);
+    for (int i = threadIdx.x; i < 512; i += kSegBlock) s_hbucket[i] = b32[i];
+    s_hids[threadIdx.x] = a.hot.ids[threadIdx.x];
+    s_hprefix[threadIdx.x] = a.hot.prefix[threadIdx.x];
+  }
+  const uint16_t* hbucket = reinterpret_cast<const uint16_t*>(s_hbucket);
   const bool small_k = K < ContribTableRegs::kR * kSegBlock;
   ContribTableRegs tables;
   if (small_k) tables.issue(a, buckets, nbuckets);
@@ -341,7 +416,7 @@ seg_meta_kernel(SegmentArgs a, const uint32_t* __restrict__ tile_seg_base,
   u32x4 kv[kMetaTilesPerBlock], vv[kMetaTilesPerBlock];
   uint32_t kpv[kMetaTilesPerBlock], jpv[kMetaTilesPerBlock], sb[kMetaTilesPerBlock];
   {
-    const int64_t last4 = (N - 1) & ~int64_t(kMetaPer - 1);
+    const int64_t last4 = (n - 1) & ~int64_t(kMetaPer - 1);
 #pragma unroll
     for (int kt = 0; kt < kMetaTilesPerBlock; ++kt) {
       int64_t p0 = blk0 + kt * kMetaTile + (int64_t)threadIdx.x * kMetaPer;
@@ -370,14 +445,14 @@ seg_meta_kernel(SegmentArgs a, const uint32_t* __restrict__ tile_seg_base,
     int m[kMetaPer];
 #pragma unroll
     for (int e = 0; e < kMetaPer; ++e)
-      m[e] = (p0 + e < N && (int64_t)jv[e] < N) ? contribution_of(s_off, s_bucket, q, K, jv[e]) : 0;
+      m[e] = (p0 + e < n && (int64_t)jv[e] < N) ? contribution_of(s_off, s_bucket, q, K, jv[e]) : 0;
     // the position before this lane's first: the previous lane's last, or
     // (first lane of a wave) the one loaded for it
     uint32_t kp = __shfl_up(key[kMetaPer - 1], 1, kWave);
     int mp = __shfl_up(m[kMetaPer - 1], 1, kWave);
     bool prev_ok = true;
     if (lane == 0) {
-      prev_ok = p0 > 0 && p0 - 1 < N;
+      prev_ok = p0 > 0 && p0 - 1 < n;
       if (prev_ok) {
         kp = kprev;
         mp = (int64_t)jprev < N ? contribution_of(s_off, s_bucket, q, K, jprev) : 0;
@@ -387,7 +462,7 @@ seg_meta_kernel(SegmentArgs a, const uint32_t* __restrict__ tile_seg_base,
     uint32_t heads = 0, head_bits = 0;
 #pragma unroll
     for (int e = 0; e < kMetaPer; ++e) {
-      const bool valid = p0 + e < N;
+      const bool valid = p0 + e < n;
       const bool head = valid && (e == 0 ? (!prev_ok || key[0] != kp) : key[e] != key[e - 1]);
       const bool newc = valid && (head || m[e] != (e == 0 ? mp : m[e - 1]));
       float wt = 0.0f;
@@ -406,12 +481,12 @@ seg_meta_kernel(SegmentArgs a, const uint32_t* __restrict__ tile_seg_base,
       heads += head ? 1u : 0u;
       head_bits |= head ? (1u << e) : 0u;
     }
-    if (p0 + kMetaPer - 1 < N) {
+    if (p0 + kMetaPer - 1 < n) {
       *reinterpret_cast<u32x4*>(packed + p0) = u32x4{word[0], word[1], word[2], word[3]};
     } else {
 #pragma unroll
       for (int e = 0; e < kMetaPer; ++e)
-        if (p0 + e < N) packed[p0 + e] = word[e];
+        if (p0 + e < n) packed[p0 + e] = word[e];
     }
     // segment numbers: the tile's base, the waves before, the lanes before
     const uint32_t incl = wave_inclusive_scan(heads);
@@ -420,13 +495,25 @@ seg_meta_kernel(SegmentArgs a, const uint32_t* __restrict__ tile_seg_base,
     uint32_t before = seg_base + incl - heads;
     for (int k = 0; k < w; ++k) before += s_wave_heads[k];
     // segments that start before each group-aligned position
-    if ((p0 & (kGroupSpan - 1)) == 0 && p0 < N) base32[p0 / kGroupSpan] = before;
+    if ((p0 & (kGroupSpan - 1)) == 0 && p0 < n) base32[p0 / kGroupSpan] = before;
 #pragma unroll
     for (int e = 0; e < kMetaPer; ++e) {
       if ((head_bits >> e) & 1u) {
-        if ((int64_t)before < N) {   // always true when the numbering is consistent
-          a.unique_ids[before] = (int64_t)key[e];
-          a.seg_offsets[before] = p0 + e;
+        // split plan: the hot IDs below this key come before it among all IDs
+        // (and their occurrences before its start); those above the key
+        // before it (none for position 0) lie between the two segments
+        uint32_t below = 0;
+        if (split) {
+          below = hot_below(key[e], hbucket, s_hids, H, a.hot.bshift);
+          const uint32_t kprev = e == 0 ? kp : key[e - 1];
+          const uint32_t from = (p0 + e > 0) ? hot_below(kprev, hbucket, s_hids, H, a.hot.bshift) : 0u;
+          for (uint32_t h = from; h < below; ++h) cnum[h] = before;
+        }
+        const int64_t out = (int64_t)before + below;
+        if (out < N) {   // always true when the numbering is consistent
+          a.unique_ids[out] = (int64_t)key[e];
+          a.seg_offsets[out] = p0 + e + (split ? (int64_t)s_hprefix[below] : 0);
+          seg_start[before] = (uint32_t)(p0 + e);
         }
         ++before;
       }
@@ -451,12 +538,12 @@ seg_meta_kernel(SegmentArgs a, const uint32_t* __restrict__ tile_seg_base,
     uint32_t key[kMetaPer] = {0u, 0u, 0u, 0u}, jv[kMetaPer] = {0u, 0u, 0u, 0u};
 #pragma unroll
     for (int e = 0; e < kMetaPer; ++e)
-      if (p0 + e < N) {
+      if (p0 + e < n) {
         key[e] = a.keys[p0 + e];
         jv[e] = a.vals[p0 + e];
       }
     uint32_t kprev = 0, jprev = 0;
-    if (p0 > 0 && p0 - 1 < N) {
+    if (p0 > 0 && p0 - 1 < n) {
       kprev = a.keys[p0 - 1];
       jprev = a.vals[p0 - 1];
     }
@@ -468,16 +555,24 @@ seg_meta_kernel(SegmentArgs a, const uint32_t* __restrict__ tile_seg_base,
 template <int LPR>
 __global__ void __launch_bounds__(kSegBlock)
 seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32_t* __restrict__ base32,
-                SegPartials part) {
+                SegPartials part, const uint32_t* __restrict__ seg_start, const uint32_t* __restrict__ cnum) {
   constexpr int GW = kWave / LPR;            // groups per wave
   constexpr int G = kSegWaves * GW;          // groups per block
   constexpr int64_t TILE = (int64_t)G * kGroupSpan;
   __shared__ f64x4 s_acc[kSegBlock];
   __shared__ int32_t s_cc[G], s_ww[G];
   __shared__ uint32_t s_seg[G], s_flags[G];
+  __shared__ uint32_t s_cnum[kHotSlots];
 
-  const int64_t N = a.N;
+  const int64_t N = a.N;                                   // occurrences
+  const int64_t n = a.n_dev ? (int64_t)*a.n_dev : a.N;     // sorted positions
   const int D = a.D;
+  if ((int64_t)blockIdx.x * TILE >= n) return;   // the grid is sized for every occurrence
+  // split plan: hot ID h comes before cold segment s among all IDs when
+  // cnum[h] <= s (cnum ascending)
+  const uint32_t H = a.n_dev ? *a.hot.meta : 0u;
+  if (threadIdx.x < H) s_cnum[threadIdx.x] = cnum[threadIdx.x];
+  __syncthreads();
 
   const int w = threadIdx.x / kWave;
   const int lane = lane_id();
@@ -488,43 +583,53 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
   {
     const int64_t tile = blockIdx.x;
     const int64_t p0 = tile * TILE + (int64_t)grp * kGroupSpan;
-    const int nvalid = (N - p0) >= kGroupSpan ? kGroupSpan : (N - p0 > 0 ? (int)(N - p0) : 0);
+    const int nvalid = (n - p0) >= kGroupSpan ? kGroupSpan : (n - p0 > 0 ? (int)(n - p0) : 0);
     const uint32_t gbase = nvalid > 0 ? base32[p0 / kGroupSpan] : 0u;
     f64x4 acc = {0.0, 0.0, 0.0, 0.0};
     int cc = 0, ww = 0;
     int64_t seg = (int64_t)gbase - 1;
+    // hot IDs before segment seg among all IDs (its output is seg + hb)
+    uint32_t hb = H ? count_at_most(s_cnum, H, seg) : 0u;
+    const uint32_t hb0 = hb;
     bool first_open = false;
     bool in_first = true;
     f64x4 facc = {0.0, 0.0, 0.0, 0.0};
     int fcc = 0, fww = 0;
     bool owner = false;
-    for (int i0 = 0; i0 < nvalid; i0 += kBatch) {
-      // the packed array is padded by a group span: whole vectors stay in bounds
+    // Words of the batch at i0 (the packed array is padded by two group spans,
+    // so whole vectors stay in bounds past the group's end).
+    auto load_words = [&](int i0, uint32_t (&word)[kBatch]) {
       const u32x4* wp = reinterpret_cast<const u32x4*>(packed + p0 + i0);
-      const u32x4 wa = wp[0], wb = wp[1];
-      const uint32_t word[kBatch] = {wa.x, wa.y, wa.z, wa.w, wb.x, wb.y, wb.z, wb.w};
-      if (i0 == 0) first_open = !(word[0] & kHead);
-      // Every lane issues all eight gathers: one whose row is not needed
-      // (past the group, a zero weight, a lane past D) reads the first 16
-      // bytes of the rows, which stay in cache, and is zeroed after.  With no
-      // load inside a branch, the compiler can count the loads in flight and
-      // never waits for all of them at once.
-      f32x4 rv[kBatch];
-      bool use[kBatch];
+#pragma unroll
+      for (int v = 0; v < kBatch / 4; ++v) {
+        const u32x4 x = wp[v];
+        word[4 * v] = x.x; word[4 * v + 1] = x.y; word[4 * v + 2] = x.z; word[4 * v + 3] = x.w;
+      }
+    };
+    // Every lane issues all of a batch's gathers: one whose row is not needed
+    // (past the group, a zero weight, a lane past D) reads the first 16
+    // bytes of the rows, which stay in cache, and is zeroed when summed.  With
+    // no load inside a branch, the compiler can count the loads in flight and
+    // never waits for all of them at once.
+    auto gather = [&](int i0, const uint32_t (&word)[kBatch], f32x4 (&rv)[kBatch], uint32_t& use) {
+      use = 0;
 #pragma unroll
       for (int u = 0; u < kBatch; ++u) {
         const uint32_t jv = word[u] & kIndexMask;
-        use[u] = i0 + u < nvalid && !(word[u] & kZeroW) && lane_on && (int64_t)jv < N;
-        rv[u] = *reinterpret_cast<const f32x4*>(a.rows + (use[u] ? (int64_t)jv * D + gl * 4 : 0));
+        const bool on = i0 + u < nvalid && !(word[u] & kZeroW) && lane_on && (int64_t)jv < N;
+        use |= on ? (1u << u) : 0u;
+        rv[u] = *reinterpret_cast<const f32x4*>(a.rows + (on ? (int64_t)jv * D + gl * 4 : 0));
       }
+    };
+    auto sum_batch = [&](int i0, const uint32_t (&word)[kBatch], f32x4 (&rv)[kBatch], uint32_t use) {
 #pragma unroll
       for (int u = 0; u < kBatch; ++u)
-        if (!use[u]) rv[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (!((use >> u) & 1u)) rv[u] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int u = 0; u < kBatch; ++u) {
         const int i = i0 + u;
-        // keep each row's float64 widening next to its use: hoisting all eight
-        // costs 64 registers and halves the waves that keep gathers in flight
+        // keep each row's float64 widening next to its use: hoisting all of
+        // them costs registers and the waves that keep gathers in flight
         __builtin_amdgcn_sched_barrier(0);
         if (i < nvalid) {
           if (word[u] & kHead) {
@@ -532,11 +637,12 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
               if (in_first && first_open) {
                 facc = acc; fcc = cc; fww = ww; owner = true;
               } else {
-                finalize_segment(a, seg, acc, cc, ww, gl, lane_on);
+                finalize_segment(a, seg + hb, acc, cc, ww, gl, lane_on);
               }
               in_first = false;
             }
             ++seg;
+            while (hb < H && (int64_t)s_cnum[hb] <= seg) ++hb;
             acc = f64x4{0.0, 0.0, 0.0, 0.0};
             cc = ww = 0;
           }
@@ -552,11 +658,48 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
           ww += (nc && !zero) ? 1 : 0;
         }
       }
+    };
+    if (kPipelined) {
+      // words two batches ahead, rows one batch ahead of the batch being summed
+      uint32_t w0[kBatch], w1[kBatch];
+      f32x4 r0[kBatch];
+      uint32_t u0 = 0;
+      if (nvalid > 0) {
+        load_words(0, w0);
+        load_words(kBatch, w1);
+        first_open = !(w0[0] & kHead);
+        gather(0, w0, r0, u0);
+      }
+      for (int i0 = 0; i0 < nvalid; i0 += kBatch) {
+        uint32_t w2[kBatch];
+        f32x4 r1[kBatch];
+        uint32_t u1;
+        load_words(i0 + 2 * kBatch, w2);
+        gather(i0 + kBatch, w1, r1, u1);
+        sum_batch(i0, w0, r0, u0);
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+          w0[u] = w1[u];
+          w1[u] = w2[u];
+          r0[u] = r1[u];
+        }
+        u0 = u1;
+      }
+    } else {
+      for (int i0 = 0; i0 < nvalid; i0 += kBatch) {
+        uint32_t word[kBatch];
+        load_words(i0, word);
+        if (i0 == 0) first_open = !(word[0] & kHead);
+        f32x4 rv[kBatch];
+        uint32_t use;
+        gather(i0, word, rv, use);
+        sum_batch(i0, word, rv, use);
+      }
     }
 
     bool last_open = false, pass = false;
     if (nvalid > 0) {
-      last_open = nvalid == kGroupSpan && (p0 + kGroupSpan) < N && !(packed[p0 + kGroupSpan] & kHead);
+      last_open = nvalid == kGroupSpan && (p0 + kGroupSpan) < n && !(packed[p0 + kGroupSpan] & kHead);
       if (last_open) {
         pass = in_first && first_open;
         s_acc[threadIdx.x] = acc;
@@ -568,7 +711,7 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
       } else if (in_first && first_open) {
         facc = acc; fcc = cc; fww = ww; owner = true;
       } else {
-        finalize_segment(a, seg, acc, cc, ww, gl, lane_on);
+        finalize_segment(a, seg + hb, acc, cc, ww, gl, lane_on);
       }
     }
     if (gl == 0) s_flags[grp] = (nvalid > 0 ? kValid : 0u) | (last_open ? kOpen : 0u) | (pass ? kPass : 0u);
@@ -595,7 +738,7 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
           part.first_ww[tile] = tww;
         }
       } else {
-        finalize_segment(a, (int64_t)gbase - 1, tot, tcc, tww, gl, lane_on);
+        finalize_segment(a, (int64_t)gbase - 1 + hb0, tot, tcc, tww, gl, lane_on);
       }
     }
     // the chain that runs into the next tile
@@ -623,10 +766,10 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
           // one lane per tile: the fixup pass takes the tiles from this list,
           // with the segment and the last tile it covers
           const uint32_t seg = s_seg[G - 1];
-          int64_t end = (int64_t)seg + 1 <= N ? a.seg_offsets[seg + 1] : N;   // written by the position pass
-          end = end < 1 ? 1 : (end > N ? N : end);
+          int64_t end = (int64_t)seg + 1 <= n ? (int64_t)seg_start[seg + 1] : n;   // written by the position pass
+          end = end < 1 ? 1 : (end > n ? n : end);
           part.fix_list[atomicAdd(part.fix_count, 1u)] =
-              u32x4{(uint32_t)tile, seg, (uint32_t)((end - 1) / TILE), 0u};
+              u32x4{(uint32_t)tile, seg, (uint32_t)((end - 1) / TILE), hb};
         }
       }
     }
@@ -654,7 +797,7 @@ seg_fixup_kernel(SegmentArgs a, SegPartials part) {
   // the listed tiles in any order: each one's sum is taken in a fixed order
   for (uint32_t k = blockIdx.x; k < count; k += gridDim.x) {
     const u32x4 rec = part.fix_list[k];
-    const int64_t b = rec.x, seg = rec.y, b_end = rec.z;
+    const int64_t b = rec.x, seg = rec.y, b_end = rec.z, hb = rec.w;   // hb: hot IDs before it (split plan)
     if (seg >= a.N) continue;   // unreachable when the numbering is consistent (block-uniform)
     f64x4 acc = {0.0, 0.0, 0.0, 0.0};
     int cc = 0, ww = 0;
@@ -679,9 +822,220 @@ seg_fixup_kernel(SegmentArgs a, SegPartials part) {
         tcc += s_cc[g];
         tww += s_ww[g];
       }
-      finalize_segment(a, seg, tot, tcc, tww, lane, lane_on);
+      finalize_segment(a, seg + hb, tot, tcc, tww, lane, lane_on);
     }
     __syncthreads();   // s_acc is rewritten for the next listed tile
+  }
+}
+
+// ------------------------------------------------------------ hot IDs (split plan)
+// Each hot ID's occurrences are one segment, split into chunks of kGroupSpan
+// occurrences per lane group, TILE per block.  The chunk prefix of the runs is
+// rebuilt by every block from the hot occurrence counts.
+struct HotPartials {
+  double* acc;     // [chunks][D] float64 sums of the weighted rows
+  int32_t* cnt;    // [chunks][4]: contributions, active contributions, first and last contribution
+  uint32_t* cp;    // [H + 1] first chunk of each hot ID's run (written by block 0 of hot_rows)
+};
+
+// Weight of contribution m for the row with tag `tg` (per-ID mode) or its
+// token weight, from the LDS tables.
+__device__ __forceinline__ float row_weight(const SegmentArgs& a, const float* s_w, const int32_t* s_sm, int m,
+                                           int64_t tg) {
+  if (a.decay == GBA_DECAY_TOKEN) return s_w[m];
+  int64_t st = tg - a.step + (int64_t)s_sm[m] + 1;
+  st = st < 0 ? 0 : st;
+  return st <= a.iota ? 1.0f : 0.0f;
+}
+
+template <int LPR>
+__global__ void __launch_bounds__(kSegBlock)
+hot_rows_kernel(SegmentArgs a, const int32_t* __restrict__ buckets, int q, int nbuckets, HotPartials hp) {
+  constexpr int GW = kWave / LPR;            // groups per wave
+  constexpr int G = kSegWaves * GW;          // groups per block
+  constexpr int64_t TILE = (int64_t)G * kGroupSpan;
+  extern __shared__ int32_t s_dyn[];
+  __shared__ uint32_t s_cp[kHotSlots + 1];
+  __shared__ uint32_t s_tmp[kSegWaves + 1];
+  __shared__ f64x4 s_acc[kSegBlock];
+  __shared__ int32_t s_c[G], s_a[G], s_first[G], s_last[G];
+  const int K = a.K;
+  const int D = a.D;
+  int32_t* s_off = s_dyn;
+  float* s_w = reinterpret_cast<float*>(s_dyn + K + 1);
+  int32_t* s_sm = s_dyn + 2 * K + 1;
+  int32_t* s_bucket = s_dyn + 3 * K + 1;
+  const uint32_t H = *a.hot.meta;
+  const int t = threadIdx.x;
+  // chunks of every hot ID's run, and their prefix
+  uint32_t nch = 0;
+  if ((uint32_t)t < H) nch = (uint32_t)((a.hot.prefix[t + 1] - a.hot.prefix[t] + TILE - 1) / TILE);
+  uint32_t total;
+  const uint32_t ex = block_exclusive_scan<kSegBlock>(nch, s_tmp, &total);
+  if ((uint32_t)t < H) s_cp[t] = ex;
+  if (t == 0) s_cp[H] = total;
+  if (blockIdx.x == 0) {
+    if ((uint32_t)t < H) hp.cp[t] = ex;
+    if (t == 0) hp.cp[H] = total;
+  }
+  const uint32_t b = blockIdx.x;
+  if (b >= total) return;   // block-uniform; the grid is sized for the most chunks
+  load_contrib_tables(a, buckets, nbuckets, s_off, s_w, s_sm, s_bucket);
+  __syncthreads();
+  // the run holding chunk b: the last h with s_cp[h] <= b
+  uint32_t h = count_at_most(s_cp, H, (int64_t)b) - 1;
+  const int64_t run_end = a.hot.prefix[h + 1];
+  const int64_t c0 = (int64_t)a.hot.prefix[h] + (int64_t)(b - s_cp[h]) * TILE;
+  const int64_t key = a.hot.ids[h];
+  const int64_t tg = (a.decay == GBA_DECAY_ID_TAG && key < a.R) ? (int64_t)a.tag[key] : -1;
+
+  const int w = t / kWave;
+  const int lane = lane_id();
+  const int gl = lane % LPR;
+  const int grp = w * GW + lane / LPR;
+  const bool lane_on = gl * 4 < D;
+  const int64_t p0 = c0 + (int64_t)grp * kGroupSpan;
+  const int64_t left = (p0 < run_end) ? run_end - p0 : 0;
+  const int nvalid = left >= kGroupSpan ? kGroupSpan : (int)left;
+  f64x4 acc = {0.0, 0.0, 0.0, 0.0};
+  int cg = 0, ag = 0, first = -1, last = -1;
+  for (int i0 = 0; i0 < nvalid; i0 += kBatch) {
+    // the lanes of a group read the same indices (clamped into the run)
+    uint32_t j[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int64_t pi = p0 + i0 + u;
+      j[u] = a.hot.hot_vals[pi < run_end ? pi : run_end - 1];
+    }
+    int m[kBatch];
+    float wt[kBatch];
+    f32x4 rv[kBatch];
+    uint32_t use = 0;
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const bool valid = i0 + u < nvalid && (int64_t)j[u] < a.N;
+      m[u] = valid ? contribution_of(s_off, s_bucket, q, K, j[u]) : 0;
+      wt[u] = valid ? row_weight(a, s_w, s_sm, m[u], tg) : 0.0f;
+      const bool on = valid && wt[u] != 0.0f && lane_on;
+      use |= on ? (1u << u) : 0u;
+      rv[u] = *reinterpret_cast<const f32x4*>(a.rows + (on ? (int64_t)j[u] * D + gl * 4 : 0));
+    }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      __builtin_amdgcn_sched_barrier(0);
+      if (i0 + u < nvalid) {
+        if ((use >> u) & 1u) acc += (double)wt[u] * widen(rv[u]);
+        const bool newc = m[u] != last;   // occurrences of one contribution are consecutive
+        cg += newc ? 1 : 0;
+        ag += (newc && wt[u] != 0.0f) ? 1 : 0;
+        if (first < 0) first = m[u];
+        last = m[u];
+      }
+    }
+  }
+  s_acc[t] = acc;
+  if (gl == 0) {
+    s_c[grp] = cg;
+    s_a[grp] = ag;
+    s_first[grp] = first;
+    s_last[grp] = last;
+  }
+  __syncthreads();
+  if (grp == 0) {
+    // groups in order; a contribution that runs across two groups counts once
+    f64x4 tot = {0.0, 0.0, 0.0, 0.0};
+    int C = 0, A = 0, f = -1, l = -1;
+    for (int g = 0; g < G; ++g) {
+      if (s_first[g] < 0) continue;   // an empty group (past the end of the run)
+      tot += s_acc[g * LPR + gl];
+      C += s_c[g];
+      A += s_a[g];
+      if (s_first[g] == l) {
+        C -= 1;
+        if (row_weight(a, s_w, s_sm, l, tg) != 0.0f) A -= 1;
+      }
+      if (f < 0) f = s_first[g];
+      l = s_last[g];
+    }
+    if (lane_on) *reinterpret_cast<f64x4*>(hp.acc + (int64_t)b * D + gl * 4) = tot;
+    if (gl == 0) {
+      int32_t* c = hp.cnt + (int64_t)b * 4;
+      c[0] = C;
+      c[1] = A;
+      c[2] = f;
+      c[3] = l;
+    }
+  }
+}
+
+// One block per hot ID: joins the chunks of its run in a fixed order and
+// writes its place among all IDs (after the cold segments below it, cnum),
+// its start (the cold occurrences below it plus the hot ones before it), c_r,
+// W_r and the weighted sum divided by c_r (or K).
+template <int LPR>
+__global__ void __launch_bounds__(kFixBlock)
+hot_finish_kernel(SegmentArgs a, HotPartials hp, const uint32_t* __restrict__ cnum) {
+  constexpr int G = kFixBlock / LPR;
+  __shared__ f64x4 s_acc[kFixBlock];
+  __shared__ int32_t s_c[G], s_a[G];
+  __shared__ uint32_t s_tmp[kFixBlock / kWave + 1];
+  const uint32_t H = *a.hot.meta;
+  const uint32_t h = blockIdx.x;
+  if (h >= H) return;
+  const int D = a.D;
+  const int t = threadIdx.x;
+  const int lane = t % LPR;
+  const int grp = t / LPR;
+  const bool lane_on = lane * 4 < D;
+  const int64_t key = a.hot.ids[h];
+  const int64_t tg = (a.decay == GBA_DECAY_ID_TAG && key < a.R) ? (int64_t)a.tag[key] : -1;
+  // cold occurrences below the hot ID: cold keys with at most h hot IDs below them
+  uint32_t below_all;
+  (void)block_exclusive_scan<kFixBlock>((uint32_t)t <= h ? a.hot.iv_total[t] : 0u, s_tmp, &below_all);
+  const uint32_t b0 = hp.cp[h], b1 = hp.cp[h + 1];
+  f64x4 acc = {0.0, 0.0, 0.0, 0.0};
+  int C = 0, A = 0;
+  for (uint32_t bb = b0 + grp; bb < b1; bb += G) {
+    if (lane_on) acc += *reinterpret_cast<const f64x4*>(hp.acc + (int64_t)bb * D + lane * 4);
+    const int32_t* c = hp.cnt + (int64_t)bb * 4;
+    C += c[0];
+    A += c[1];
+    if (bb > b0 && c[2] == hp.cnt[(int64_t)(bb - 1) * 4 + 3]) {   // a contribution across two chunks
+      C -= 1;
+      const int m = c[2];
+      float wm;
+      if (a.decay == GBA_DECAY_TOKEN) {
+        wm = a.w[m];
+      } else {
+        int64_t st = tg - a.tokens[m] + 1;
+        st = st < 0 ? 0 : st;
+        wm = st <= a.iota ? 1.0f : 0.0f;
+      }
+      if (wm != 0.0f) A -= 1;
+    }
+  }
+  s_acc[t] = acc;
+  if (lane == 0) {
+    s_c[grp] = C;
+    s_a[grp] = A;
+  }
+  __syncthreads();
+  if (grp == 0) {
+    f64x4 tot = {0.0, 0.0, 0.0, 0.0};
+    int tc = 0, ta = 0;
+    for (int g = 0; g < G; ++g) {
+      tot += s_acc[g * LPR + lane];
+      tc += s_c[g];
+      ta += s_a[g];
+    }
+    const int64_t out = (int64_t)h + cnum[h];
+    if (out < a.N) {   // always true when the numbering is consistent
+      finalize_segment(a, out, tot, tc, ta, lane, lane_on);
+      if (lane == 0) {
+        a.unique_ids[out] = key;
+        a.seg_offsets[out] = (int64_t)below_all + a.hot.prefix[h];
+      }
+    }
   }
 }
 
@@ -700,11 +1054,11 @@ size_t run_heads_workspace_bytes(int64_t N) {
 }
 
 hipError_t launch_run_heads(const uint32_t* keys, int64_t N, uint32_t* tile_base, uint32_t* total, void* scan_ws,
-                            hipStream_t stream) {
+                            hipStream_t stream, const uint32_t* n_dev) {
   const int64_t tiles = N > 0 ? ceil_div(N, kMetaTile) : 0;
   if (N > 0) {
     hipLaunchKernelGGL(seg_heads_kernel, dim3((unsigned)ceil_div(tiles, kSegWaves)), dim3(kSegBlock), 0, stream,
-                       keys, N, tiles, tile_base);
+                       keys, N, n_dev, tiles, tile_base);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -713,15 +1067,26 @@ hipError_t launch_run_heads(const uint32_t* keys, int64_t N, uint32_t* tile_base
 
 template <int LPR>
 static hipError_t launch_rows(const SegmentArgs& a, const uint32_t* packed, const uint32_t* base32,
-                              SegPartials part, int64_t tiles, hipStream_t stream) {
+                              SegPartials part, const uint32_t* seg_start, const uint32_t* cnum, HotPartials hp,
+                              const int32_t* buckets, int q, int nb, const SegLayout& L, hipStream_t stream) {
+  const int64_t tiles = L.row_tiles;
   hipLaunchKernelGGL(seg_rows_kernel<LPR>, dim3((unsigned)tiles), dim3(kSegBlock), 0, stream, a, packed,
-                     base32, part);
+                     base32, part, seg_start, cnum);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // the listed tiles (at most all of them) are spread over a fixed grid
   const int64_t fix_blocks = tiles < kFixGrid ? tiles : kFixGrid;
   hipLaunchKernelGGL(seg_fixup_kernel<LPR>, dim3((unsigned)fix_blocks), dim3(kFixBlock), 0, stream, a, part);
-  return hipGetLastError();
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (a.n_dev) {
+    const size_t lds = (size_t)(3 * a.K + 1 + nb) * sizeof(int32_t);
+    hipLaunchKernelGGL(hot_rows_kernel<LPR>, dim3((unsigned)L.hot_chunks), dim3(kSegBlock), lds, stream, a, buckets,
+                       q, nb, hp);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL(hot_finish_kernel<LPR>, dim3(kHotSlots), dim3(kFixBlock), 0, stream, a, hp, cnum);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_segments(const SegmentArgs& a, void* ws, hipStream_t stream) {
@@ -743,14 +1108,20 @@ hipError_t launch_segments(const SegmentArgs& a, void* ws, hipStream_t stream) {
   part.last_acc = reinterpret_cast<double*>(base + L.off_last_acc);
   part.fix_count = reinterpret_cast<uint32_t*>(base + L.off_fix);
   part.fix_list = reinterpret_cast<u32x4*>(base + L.off_fix + 256);
+  uint32_t* seg_start = reinterpret_cast<uint32_t*>(base + L.off_start);
+  uint32_t* cnum = reinterpret_cast<uint32_t*>(base + L.off_cnum);
+  HotPartials hp;
+  hp.acc = reinterpret_cast<double*>(base + L.off_hot_acc);
+  hp.cnt = reinterpret_cast<int32_t*>(base + L.off_hot_cnt);
+  hp.cp = cnum + kHotSlots + 1;
 
   hipLaunchKernelGGL(check_offsets_kernel, dim3(1), dim3(256), 0, stream, a.offsets, a.K, a.N, a.err);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  e = launch_run_heads(a.keys, a.N, heads, total, scan_ws, stream);
+  e = launch_run_heads(a.keys, a.N, heads, total, scan_ws, stream, a.n_dev);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(seg_finish_kernel, dim3(1), dim3(1), 0, stream, (const uint32_t*)total, a.N,
-                     a.num_unique, a.seg_offsets, part.fix_count);
+  hipLaunchKernelGGL(seg_finish_kernel, dim3(1), dim3(kSegBlock), 0, stream, a, (const uint32_t*)total, seg_start,
+                     cnum, part.fix_count);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (a.N <= 0) return hipSuccess;
 
@@ -762,16 +1133,16 @@ hipError_t launch_segments(const SegmentArgs& a, void* ws, hipStream_t stream) {
   const size_t lds = (size_t)(3 * a.K + 1 + nb) * sizeof(int32_t);
   hipLaunchKernelGGL(seg_meta_kernel, dim3((unsigned)ceil_div(L.meta_tiles, kMetaTilesPerBlock)),
                      dim3(kSegBlock), lds, stream, a, (const uint32_t*)heads, (const int32_t*)buckets, q, nb,
-                     L.meta_tiles, packed, base32);
+                     L.meta_tiles, packed, base32, seg_start, cnum);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   switch (lanes_per_row(a.D)) {
-    case 1: e = launch_rows<1>(a, packed, base32, part, L.row_tiles, stream); break;
-    case 2: e = launch_rows<2>(a, packed, base32, part, L.row_tiles, stream); break;
-    case 4: e = launch_rows<4>(a, packed, base32, part, L.row_tiles, stream); break;
-    case 8: e = launch_rows<8>(a, packed, base32, part, L.row_tiles, stream); break;
-    case 16: e = launch_rows<16>(a, packed, base32, part, L.row_tiles, stream); break;
-    case 32: e = launch_rows<32>(a, packed, base32, part, L.row_tiles, stream); break;
-    case 64: e = launch_rows<64>(a, packed, base32, part, L.row_tiles, stream); break;
+    case 1: e = launch_rows<1>(a, packed, base32, part, seg_start, cnum, hp, buckets, q, nb, L, stream); break;
+    case 2: e = launch_rows<2>(a, packed, base32, part, seg_start, cnum, hp, buckets, q, nb, L, stream); break;
+    case 4: e = launch_rows<4>(a, packed, base32, part, seg_start, cnum, hp, buckets, q, nb, L, stream); break;
+    case 8: e = launch_rows<8>(a, packed, base32, part, seg_start, cnum, hp, buckets, q, nb, L, stream); break;
+    case 16: e = launch_rows<16>(a, packed, base32, part, seg_start, cnum, hp, buckets, q, nb, L, stream); break;
+    case 32: e = launch_rows<32>(a, packed, base32, part, seg_start, cnum, hp, buckets, q, nb, L, stream); break;
+    case 64: e = launch_rows<64>(a, packed, base32, part, seg_start, cnum, hp, buckets, q, nb, L, stream); break;
     default: return hipErrorInvalidValue;
   }
   if (e != hipSuccess) return e;

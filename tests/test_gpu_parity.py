@@ -92,7 +92,10 @@ def test_aggregate_dense_all_excluded():
 
 
 # ----------------------------------------------------------- sparse, Alg. 2
-def _run_sparse(ids, rows, offsets, w, tokens, step, iota, R, tag=None, decay="token", norm="per_id_count"):
+def _run_sparse(ids, rows, offsets, w, tokens, step, iota, R, tag=None, decay="token", norm="per_id_count",
+                plan=None):
+    """plan: None calls gba_aggregate_sparse (automatic sort plan), else
+    gba_aggregate_sparse_plan with that plan."""
     N, D = rows.shape
     K = len(offsets) - 1
     cap = max(N, 1)
@@ -102,15 +105,21 @@ def _run_sparse(ids, rows, offsets, w, tokens, step, iota, R, tag=None, decay="t
                active_count=torch.full((cap,), -5, dtype=torch.int32, device=DEV),
                agg=torch.full((cap, D), float("nan"), dtype=torch.float32, device=DEV),
                num_unique=torch.full((1,), -5, dtype=torch.int64, device=DEV))
-    ws = torch.empty(gba.gba_aggregate_sparse_workspace_size(N, K, D, R), dtype=torch.uint8, device=DEV)
+    wsb = (gba.gba_aggregate_sparse_workspace_size(N, K, D, R) if plan is None
+           else gba.gba_aggregate_sparse_plan_workspace_size(N, K, D, R, plan))
+    ws = torch.empty(wsb, dtype=torch.uint8, device=DEV)
     err = torch.zeros(1, dtype=torch.int32, device=DEV)
     tag_d = dev(tag) if tag is not None else None
-    gba.gba_aggregate_sparse(dev(ids), dev(rows.reshape(N, D)) if N else torch.empty((0, D), device=DEV),
-                             dev(offsets), R, dev(w), dev(tokens), step, iota, tag_d,
-                             gba.DECAY_ID_TAG if decay == "id_tag" else gba.DECAY_TOKEN,
-                             gba.NORM_BY_K if norm == "by_k" else gba.NORM_PER_ID_COUNT,
-                             out["unique_ids"], out["seg_offsets"], out["contrib_count"],
-                             out["active_count"], out["agg"], out["num_unique"], ws, err)
+    args = (dev(ids), dev(rows.reshape(N, D)) if N else torch.empty((0, D), device=DEV),
+            dev(offsets), R, dev(w), dev(tokens), step, iota, tag_d,
+            gba.DECAY_ID_TAG if decay == "id_tag" else gba.DECAY_TOKEN,
+            gba.NORM_BY_K if norm == "by_k" else gba.NORM_PER_ID_COUNT,
+            out["unique_ids"], out["seg_offsets"], out["contrib_count"],
+            out["active_count"], out["agg"], out["num_unique"], ws)
+    if plan is None:
+        gba.gba_aggregate_sparse(*args, err)
+    else:
+        gba.gba_aggregate_sparse_plan(*args, plan, err)
     res = {k: host(v) for k, v in out.items()}
     res["err"] = int(host(err)[0])
     res["tag"] = host(tag_d) if tag_d is not None else None
@@ -149,30 +158,34 @@ def _case(K, sizes, R, D, seed, zipf_s=1.1, kind=counter.KIND_GRAD, step=1000, s
     return ids.astype(np.int64), rows, off, tokens, tag
 
 
+@pytest.mark.parametrize("plan", [None, gba.SORT_HOT])
 @pytest.mark.parametrize("D", [4, 8, 12, 16, 20, 32, 64, 128, 256])
 @pytest.mark.parametrize("decay", ["token", "id_tag"])
-def test_sparse_widths(D, decay):
+def test_sparse_widths(D, decay, plan):
     K = 7
     sizes = np.array([900, 0, 1733, 17, 1200, 0, 611])
     ids, rows, off, tokens, tag = _case(K, sizes, 3000, D, seed=D)
     w, _, _ = oracle.token_weights(tokens, 1000, 2)
-    res = _run_sparse(ids, rows, off, w, tokens, 1000, 2, 3000, tag, decay)
+    res = _run_sparse(ids, rows, off, w, tokens, 1000, 2, 3000, tag, decay, plan=plan)
     _check_sparse(res, ids, rows, off, w, tokens, 1000, 2, tag, decay)
 
 
+@pytest.mark.parametrize("plan", [None, gba.SORT_HOT])
 @pytest.mark.parametrize("norm", ["per_id_count", "by_k"])
 @pytest.mark.parametrize("decay", ["token", "id_tag"])
-def test_sparse_c0_full_size(norm, decay):
+def test_sparse_c0_full_size(norm, decay, plan):
     c = BY_NAME["c0"]
     hs = workload.host_step(c, value_kind=counter.KIND_DYADIC)
     w, _, _ = oracle.token_weights(hs.tokens, hs.step, c.iota)
-    res = _run_sparse(hs.ids, hs.rows, hs.offsets, w, hs.tokens, hs.step, c.iota, c.R, hs.tags, decay, norm)
+    res = _run_sparse(hs.ids, hs.rows, hs.offsets, w, hs.tokens, hs.step, c.iota, c.R, hs.tags, decay, norm,
+                      plan=plan)
     _check_sparse(res, hs.ids, hs.rows, hs.offsets, w, hs.tokens, hs.step, c.iota, hs.tags, decay, norm,
                   expect_exact=True)
 
 
+@pytest.mark.parametrize("plan", [None, gba.SORT_HOT])
 @pytest.mark.parametrize("D", [4, 32, 256])
-def test_sparse_one_hot_id_spans_many_blocks(D):
+def test_sparse_one_hot_id_spans_many_blocks(D, plan):
     """One ID holds most occurrences, so its segment crosses many blocks and
     the per-block partial sums must be joined."""
     K, n = 6, 40_000
@@ -184,23 +197,27 @@ def test_sparse_one_hot_id_spans_many_blocks(D):
     rows = counter.values_range(9, counter.STREAM_ROWS, 0, N * D, counter.KIND_DYADIC).reshape(N, D)
     tokens = 100 - np.array([0, 1, 4, 0, 2, 7])
     w, _, _ = oracle.token_weights(tokens, 100, 3)
-    res = _run_sparse(ids, rows, off, w, tokens, 100, 3, 10_000)
+    res = _run_sparse(ids, rows, off, w, tokens, 100, 3, 10_000, plan=plan)
     _check_sparse(res, ids, rows, off, w, tokens, 100, 3, expect_exact=True)
 
 
-def test_sparse_single_id_everywhere():
+@pytest.mark.parametrize("plan", [None, gba.SORT_HOT])
+def test_sparse_single_id_everywhere(plan):
+    """Every occurrence holds one ID (with the hot-key plan: no cold key at all)."""
     K, n, D = 3, 50_000, 16
     ids = np.full(K * n, 7, np.int64)
     off = np.arange(K + 1, dtype=np.int64) * n
     rows = counter.values_range(4, counter.STREAM_ROWS, 0, K * n * D, counter.KIND_DYADIC).reshape(-1, D)
     tokens = np.array([10, 10, 3])
     w, _, _ = oracle.token_weights(tokens, 10, 2)
-    res = _run_sparse(ids, rows, off, w, tokens, 10, 2, 8)
+    res = _run_sparse(ids, rows, off, w, tokens, 10, 2, 8, plan=plan)
     ref = _check_sparse(res, ids, rows, off, w, tokens, 10, 2, expect_exact=True)
     assert ref["num_unique"] == 1 and list(ref["contrib_count"]) == [3] and list(ref["active_count"]) == [2]
 
 
-def test_sparse_all_distinct():
+@pytest.mark.parametrize("plan", [None, gba.SORT_HOT])
+def test_sparse_all_distinct(plan):
+    """All IDs distinct (with the hot-key plan: no hot ID at all)."""
     K, D, R = 4, 32, 1 << 20
     rng = np.random.default_rng(1)
     ids = rng.permutation(R)[:9999].astype(np.int64)
@@ -209,7 +226,7 @@ def test_sparse_all_distinct():
                                 counter.grad_scale(1e-2)).reshape(-1, D)
     tokens = np.array([9, 9, 8, 1])
     w, _, _ = oracle.token_weights(tokens, 9, 3)
-    res = _run_sparse(ids, rows, off, w, tokens, 9, 3, R)
+    res = _run_sparse(ids, rows, off, w, tokens, 9, 3, R, plan=plan)
     ref = _check_sparse(res, ids, rows, off, w, tokens, 9, 3)
     assert ref["num_unique"] == 9999 and np.all(ref["contrib_count"] == 1)
 
@@ -220,14 +237,15 @@ def test_sparse_all_distinct():
 # 2+8+8+8; 2^29 - 3: 5+8+8+8; 2^31 + 5: 8+8+8+8).  18,411 occurrences span
 # several sort tiles and a ragged last one; dyadic rows make every sum exact,
 # so any misplaced key shows.
+@pytest.mark.parametrize("plan", [None, gba.SORT_HOT])
 @pytest.mark.parametrize("R", [200, 1000, 5000, 70_000, 1 << 21, 1 << 26, (1 << 29) - 3, (1 << 31) + 5])
-def test_sparse_sort_digit_plans(R):
+def test_sparse_sort_digit_plans(R, plan):
     K, D = 3, 4
     sizes = np.array([7000, 5000, 6411])
     ids, rows, off, tokens, _ = _case(K, sizes, R, D, seed=R % 997, zipf_s=1.05, kind=counter.KIND_DYADIC)
     assert ids.max() >= R // 2   # the top digit is exercised
     w, _, _ = oracle.token_weights(tokens, 1000, 3)
-    res = _run_sparse(ids, rows, off, w, tokens, 1000, 3, R)
+    res = _run_sparse(ids, rows, off, w, tokens, 1000, 3, R, plan=plan)
     _check_sparse(res, ids, rows, off, w, tokens, 1000, 3, expect_exact=True)
 
 
@@ -239,13 +257,14 @@ def test_sparse_empty():
     assert int(res["num_unique"][0]) == 0 and int(res["seg_offsets"][0]) == 0 and res["err"] == 0
 
 
-def test_sparse_all_excluded():
+@pytest.mark.parametrize("plan", [None, gba.SORT_HOT])
+def test_sparse_all_excluded(plan):
     K, sizes, R, D = 5, np.array([300, 200, 0, 50, 450]), 500, 16
     ids, rows, off, tokens, tag = _case(K, sizes, R, D, seed=77, stale_hi=0)
     tokens = tokens - 10                                     # every contribution too stale
     w, _, nex = oracle.token_weights(tokens, 1000, 2)
     assert nex == K
-    res = _run_sparse(ids, rows, off, w, tokens, 1000, 2, R)
+    res = _run_sparse(ids, rows, off, w, tokens, 1000, 2, R, plan=plan)
     ref = _check_sparse(res, ids, rows, off, w, tokens, 1000, 2)
     assert np.all(ref["active_count"] == 0) and np.all(res["agg"][:ref["num_unique"]] == 0)
 
@@ -266,14 +285,17 @@ def test_sparse_table_of_one_row_and_full_32bit_ids():
     _check_sparse(res, ids, rows, off, w, tokens, 4, 0, expect_exact=True)
 
 
-def test_sparse_many_small_contributions():
+@pytest.mark.parametrize("plan", [None, gba.SORT_HOT])
+def test_sparse_many_small_contributions(plan):
+    """4096 tiny contributions: hot IDs run through many of them, and their
+    contributions cross the chunks of the hot-key plan."""
     K, D, R = 4096, 8, 5000
     rng = np.random.default_rng(3)
     sizes = rng.integers(0, 6, K)
     ids, rows, off, tokens, tag = _case(K, sizes, R, D, seed=3)
     w, _, _ = oracle.token_weights(tokens, 1000, 3)
     for decay in ("token", "id_tag"):
-        res = _run_sparse(ids, rows, off, w, tokens, 1000, 3, R, tag, decay)
+        res = _run_sparse(ids, rows, off, w, tokens, 1000, 3, R, tag, decay, plan=plan)
         _check_sparse(res, ids, rows, off, w, tokens, 1000, 3, tag, decay)
 
 
@@ -437,15 +459,16 @@ def test_full_step_small(decay, opt, fused_dense):
         assert_exact(host(tag), ref["sparse"]["new_tag"], "tag")
 
 
+@pytest.mark.parametrize("plan", [None, gba.SORT_HOT])
 @pytest.mark.parametrize("D", [8, 32])
-def test_sparse_fractional_token_weights(D):
+def test_sparse_fractional_token_weights(D, plan):
     """Weights other than 0 and 1 (other decay strategies than Eq. 1's) scale
     the rows they weigh; a zero weight still excludes."""
     K = 5
     sizes = np.array([700, 300, 0, 900, 450])
     ids, rows, off, tokens, tag = _case(K, sizes, 800, D, seed=41, kind=counter.KIND_DYADIC)
     w = np.array([1.0, 0.5, 0.0, 0.25, 0.0], np.float32)
-    res = _run_sparse(ids, rows, off, w, tokens, 1000, 2, 800)
+    res = _run_sparse(ids, rows, off, w, tokens, 1000, 2, 800, plan=plan)
     _check_sparse(res, ids, rows, off, w, tokens, 1000, 2, expect_exact=True)
 
 
@@ -867,8 +890,9 @@ from hypothesis import HealthCheck, given, settings, strategies as hst   # noqa:
 @given(K=hst.integers(1, 12), n_max=hst.integers(0, 3000), R=hst.sampled_from([1, 2, 17, 1000, 70_000, 1 << 20]),
        D=hst.sampled_from([4, 8, 12, 32, 64, 256]), decay=hst.sampled_from(["token", "id_tag"]),
        norm=hst.sampled_from(["per_id_count", "by_k"]), seed=hst.integers(0, 2 ** 31 - 1),
-       dyadic=hst.booleans(), zipf_s=hst.sampled_from([0.6, 1.1, 2.0]))
-def test_sparse_random_shapes(K, n_max, R, D, decay, norm, seed, dyadic, zipf_s):
+       dyadic=hst.booleans(), zipf_s=hst.sampled_from([0.6, 1.1, 2.0]),
+       plan=hst.sampled_from([None, gba.SORT_HOT]))
+def test_sparse_random_shapes(K, n_max, R, D, decay, norm, seed, dyadic, zipf_s, plan):
     """Random shapes, empty contributions, tiny and large tables, hot and
     spread IDs: the GPU equals the oracle (exactly on dyadic values)."""
     rng = np.random.default_rng(seed)
@@ -877,7 +901,8 @@ def test_sparse_random_shapes(K, n_max, R, D, decay, norm, seed, dyadic, zipf_s)
     kind = counter.KIND_DYADIC if dyadic else counter.KIND_GRAD
     ids, rows, off, tokens, tag = _case(K, sizes, R, D, seed % 100_000, zipf_s=zipf_s, kind=kind, stale_hi=4)
     w, _, _ = oracle.token_weights(tokens, 1000, 2)
-    res = _run_sparse(ids, rows, off, w, tokens, 1000, 2, R, tag if decay == "id_tag" else None, decay, norm)
+    res = _run_sparse(ids, rows, off, w, tokens, 1000, 2, R, tag if decay == "id_tag" else None, decay, norm,
+                      plan=plan)
     _check_sparse(res, ids, rows, off, w, tokens, 1000, 2, tag if decay == "id_tag" else None, decay, norm,
                   expect_exact=dyadic)
 
