@@ -171,9 +171,7 @@ __device__ __forceinline__ void load_hot_tables(const HotTables& t, uint16_t* s_
 // 64 consecutive positions (one coalesced load per wave; single scattered
 // positions would each cost a page walk) in an LDS hash table, keeps those seen at least kHotMinCount times (raising
 // the bar until at most `cap` remain), sorts them and builds the bucket
-// table.  Each wave first sorts its 64 samples of a round in registers, so an
-// ID is added once per run (the hottest ones would otherwise serialise on
-// their counter).  Only the first kHotInsertRounds rounds insert new IDs; the
+// table.  Only the first kHotInsertRounds rounds insert new IDs; the
 // later ones only count IDs already in the table (an ID frequent enough to
 // matter is there by then), which keeps the table sparse and the probes
 // short.  A sampled ID that finds no free slot within kHotProbe steps is not
@@ -215,22 +213,8 @@ hot_select_kernel(const int64_t* __restrict__ ids, int64_t n, int64_t R, int cap
 #pragma unroll
   for (int e = 0; e < kPer; ++e) {
     if (e == kHotInsertRounds) __syncthreads();   // every insertion is done
-    // bitonic sort of the wave's 64 samples, ascending by lane
-    uint32_t k = smp[e];
-#pragma unroll
-    for (int kk = 2; kk <= kWave; kk <<= 1) {
-#pragma unroll
-      for (int j = kk >> 1; j > 0; j >>= 1) {
-        const uint32_t o = __shfl_xor(k, j, kWave);
-        const bool keep_min = ((lane & j) == 0) == ((lane & kk) == 0);
-        k = keep_min ? (k < o ? k : o) : (k < o ? o : k);
-      }
-    }
-    const uint32_t prev = __shfl_up(k, 1, kWave);
-    const uint64_t starts = __ballot(lane == 0 || k != prev);
-    const uint64_t above = lane == kWave - 1 ? 0ull : starts & (~0ull << (lane + 1));
-    const uint32_t len = (above ? (uint32_t)__builtin_ctzll(above) : (uint32_t)kWave) - (uint32_t)lane;
-    if (k == kNone || !((starts >> lane) & 1ull)) continue;
+    const uint32_t k = smp[e];
+    if (k == kNone) continue;
     uint32_t h = (k * 2654435761u) >> (32 - 14);   // Fibonacci hashing onto 2^14 slots
     for (int probe = 0; probe < kHotProbe; ++probe) {
       uint32_t cur = s_key[h];
@@ -239,7 +223,7 @@ hot_select_kernel(const int64_t* __restrict__ ids, int64_t n, int64_t R, int cap
         cur = atomicCAS(&s_key[h], kNone, k);
       }
       if (cur == kNone || cur == k) {
-        atomicAdd(&s_cnt[h], len);
+        atomicAdd(&s_cnt[h], 1u);
         break;
       }
       h = (h + 1) & (kHotTable - 1);
@@ -753,12 +737,14 @@ scatter_tile(const void* __restrict__ keys_in, const uint32_t* __restrict__ vals
     const uint32_t g = gshift[digit] + (uint32_t)i;
     uint32_t* ko = keys_out;
     uint32_t* vo = vals_out;
+    bool store_key = true;
     if (HOT && digit >= cold_bins) {   // a hot ID: straight to its final place
       ko = keys_fin;
       vo = vals_fin;
+      store_key = !ht.split;           // split: only the occurrence indices are read
     }
     if ((int64_t)g < n) {   // always true when the counts are consistent
-      ko[g] = k;
+      if (store_key) ko[g] = k;
       vo[g] = val_out;
     }
   }

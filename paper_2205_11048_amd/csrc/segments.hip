@@ -995,23 +995,43 @@ hot_finish_kernel(SegmentArgs a, HotPartials hp, const uint32_t* __restrict__ cn
   const uint32_t b0 = hp.cp[h], b1 = hp.cp[h + 1];
   f64x4 acc = {0.0, 0.0, 0.0, 0.0};
   int C = 0, A = 0;
-  for (uint32_t bb = b0 + grp; bb < b1; bb += G) {
-    if (lane_on) acc += *reinterpret_cast<const f64x4*>(hp.acc + (int64_t)bb * D + lane * 4);
-    const int32_t* c = hp.cnt + (int64_t)bb * 4;
-    C += c[0];
-    A += c[1];
-    if (bb > b0 && c[2] == hp.cnt[(int64_t)(bb - 1) * 4 + 3]) {   // a contribution across two chunks
-      C -= 1;
-      const int m = c[2];
-      float wm;
-      if (a.decay == GBA_DECAY_TOKEN) {
-        wm = a.w[m];
-      } else {
-        int64_t st = tg - a.tokens[m] + 1;
-        st = st < 0 ? 0 : st;
-        wm = st <= a.iota ? 1.0f : 0.0f;
+  // group grp takes chunks b0 + grp, b0 + grp + G, ... in that order, eight
+  // loads in flight at a time
+  constexpr int kFin = 8;
+  for (uint32_t base = b0 + grp; base < b1; base += kFin * G) {
+    f64x4 v[kFin];
+    int32_t c0[kFin], c1[kFin], c2[kFin], prev_last[kFin];
+#pragma unroll
+    for (int u = 0; u < kFin; ++u) {
+      const uint32_t bb = base + u * G;
+      const uint32_t bc = bb < b1 ? bb : b1 - 1;   // clamped: read, then ignored
+      v[u] = lane_on ? *reinterpret_cast<const f64x4*>(hp.acc + (int64_t)bc * D + lane * 4)
+                     : f64x4{0.0, 0.0, 0.0, 0.0};
+      const int32_t* c = hp.cnt + (int64_t)bc * 4;
+      c0[u] = c[0];
+      c1[u] = c[1];
+      c2[u] = c[2];
+      prev_last[u] = bc > b0 ? hp.cnt[(int64_t)(bc - 1) * 4 + 3] : -1;
+    }
+#pragma unroll
+    for (int u = 0; u < kFin; ++u) {
+      if (base + u * G >= b1) break;
+      acc += v[u];
+      C += c0[u];
+      A += c1[u];
+      if (c2[u] == prev_last[u]) {   // a contribution across two chunks counts once
+        C -= 1;
+        const int m = c2[u];
+        float wm;
+        if (a.decay == GBA_DECAY_TOKEN) {
+          wm = a.w[m];
+        } else {
+          int64_t st = tg - a.tokens[m] + 1;
+          st = st < 0 ? 0 : st;
+          wm = st <= a.iota ? 1.0f : 0.0f;
+        }
+        if (wm != 0.0f) A -= 1;
       }
-      if (wm != 0.0f) A -= 1;
     }
   }
   s_acc[t] = acc;
