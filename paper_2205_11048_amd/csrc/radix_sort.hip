@@ -132,9 +132,10 @@ __device__ __forceinline__ uint64_t match_digit(uint32_t digit, int bits, bool a
 }
 
 // Number of hot IDs below `key`, and whether `key` is one of them.  The bucket
-// table narrows the search to the hot IDs that share the key's top bits: the
-// first two are compared without a branch (no loop, so the lookups of a
-// lane's keys overlap), the rare rest in a loop.
+// table narrows the search to the hot IDs that share the key's top bits: up
+// to two are compared without a branch (no loop, so the lookups of a lane's
+// keys overlap); a crowded bucket (hot IDs that are close in value, such as
+// rows numbered in order of first appearance) is searched by halving.
 struct HotLookup {
   const uint16_t* bucket;   // LDS [kHotBuckets]
   const uint32_t* ids;      // LDS [>= H + 1]
@@ -148,10 +149,15 @@ struct HotLookup {
     const bool in0 = lo < hi, in1 = lo + 1 < hi;
     uint32_t r = lo + ((in0 && a0 < key) ? 1u : 0u) + ((in1 && a1 < key) ? 1u : 0u);
     bool h = (in0 && a0 == key) || (in1 && a1 == key);
-    for (uint32_t i = lo + 2; i < hi; ++i) {   // a bucket with three or more hot IDs
-      const uint32_t a = ids[i];
-      r += a < key ? 1u : 0u;
-      h = h || a == key;
+    if (hi > lo + 2) {   // three or more hot IDs in the bucket
+      uint32_t l = lo, u = hi;
+      while (l < u) {
+        const uint32_t mid = (l + u) >> 1;
+        if (ids[mid] < key) l = mid + 1;
+        else u = mid;
+      }
+      r = l;
+      h = l < hi && ids[l] == key;
     }
     *hot = h;
     return r;

@@ -151,13 +151,17 @@ __device__ __forceinline__ uint32_t count_at_most(const uint32_t* s, uint32_t n,
 }
 
 // Hot IDs below `key` (split plan): the sort's bucket table narrows the
-// search to the hot IDs that share the key's top bits.
+// search to the hot IDs that share the key's top bits, then halving.
 __device__ __forceinline__ uint32_t hot_below(uint32_t key, const uint16_t* bucket, const uint32_t* ids, uint32_t H,
                                               int bshift) {
   const uint32_t t = key >> bshift;
   uint32_t lo = bucket[t];
-  const uint32_t hi = t + 1 < 1024u ? (uint32_t)bucket[t + 1] : H;
-  while (lo < hi && ids[lo] < key) ++lo;
+  uint32_t hi = t + 1 < 1024u ? (uint32_t)bucket[t + 1] : H;
+  while (lo < hi) {
+    const uint32_t mid = (lo + hi) >> 1;
+    if (ids[mid] < key) lo = mid + 1;
+    else hi = mid;
+  }
   return lo;
 }
 

@@ -249,6 +249,27 @@ def test_sparse_sort_digit_plans(R, plan):
     _check_sparse(res, ids, rows, off, w, tokens, 1000, 3, expect_exact=True)
 
 
+@pytest.mark.parametrize("decay", ["token", "id_tag"])
+def test_sparse_hot_ids_crowded_in_one_bucket(decay):
+    """The hot-key plan with the hot IDs close together in value (rows numbered
+    in order of first appearance), so they share one lookup bucket."""
+    K, D, R = 6, 16, 1 << 24
+    rng = np.random.default_rng(12)
+    sizes = np.array([40_000, 0, 25_000, 33_000, 1, 20_000])
+    N = int(sizes.sum())
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    ids = rng.integers(0, R, N)
+    hot = rng.random(N) < 0.6
+    ids[hot] = rng.integers(0, 200, int(hot.sum()))
+    ids = ids.astype(np.int64)
+    rows = counter.values_range(12, counter.STREAM_ROWS, 0, N * D, counter.KIND_DYADIC).reshape(N, D)
+    tokens = 1000 - rng.integers(0, 5, K)
+    tag = workload.tag_values(12, np.arange(R), 1000)
+    w, _, _ = oracle.token_weights(tokens, 1000, 2)
+    res = _run_sparse(ids, rows, off, w, tokens, 1000, 2, R, tag, decay, plan=gba.SORT_HOT)
+    _check_sparse(res, ids, rows, off, w, tokens, 1000, 2, tag, decay, expect_exact=True)
+
+
 def test_sparse_empty():
     K, D = 3, 8
     off = np.zeros(K + 1, np.int64)

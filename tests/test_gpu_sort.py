@@ -104,3 +104,15 @@ def test_sort_plan_is_plain_where_the_key_width_leaves_no_room():
 def test_sort_empty():
     keys, idx, err = run_sort(np.zeros(0, np.int64), 100, gba.SORT_HOT)
     assert keys.size == 0 and idx.size == 0 and err == 0
+
+
+@pytest.mark.parametrize("R", [1 << 24, 500_000_000])
+def test_sort_hot_ids_crowded_in_one_bucket(R):
+    """Hot IDs close together in value (rows numbered in order of first
+    appearance): they share one lookup bucket, searched by halving."""
+    rng = np.random.default_rng(8)
+    n = 400_000
+    ids = rng.integers(0, R, n)
+    hot = rng.random(n) < 0.7
+    ids[hot] = rng.integers(0, 240, int(hot.sum()))        # 240 hot IDs, all in the first bucket
+    check(ids.astype(np.int64), R, gba.SORT_HOT)
