@@ -40,7 +40,6 @@ constexpr int64_t kMetaTile = (int64_t)kSegBlock * kRounds;  // 1024 positions: 
 static_assert(kMetaTile == kRunTile, "run-head tiles are the per-position tiles");
 constexpr int kGroupSpan = 128;                              // positions per lane group in seg_rows
 constexpr int kBatch = 8;                                    // row gathers per batch of a group
-constexpr bool kPipelined = false;                           // next batch's gathers issued before this one is summed
 constexpr int kMaxBuckets = 1024;                            // contribution lookup buckets
 
 // packed word of a sorted position
@@ -101,7 +100,7 @@ static SegLayout seg_layout(int64_t N, int32_t D) {
   L.off_total = o;     o += 256;                     // head total
   L.off_scan = o;      o += align_up(run_heads_workspace_bytes(N));
   L.off_buckets = o;   o += align_up(kMaxBuckets * 4);
-  L.off_packed = o;    o += align_up((n + 2 * kGroupSpan) * 4);   // padded: whole-group vector loads stay inside
+  L.off_packed = o;    o += align_up((n + kGroupSpan) * 4);   // padded: whole-group vector loads stay inside
   L.off_base32 = o;    o += align_up((n / kGroupSpan + 2) * 4);
   L.off_cnt = o;       o += align_up(rt * 16);
   L.off_fix = o;       o += 256 + align_up(rt * 16);  // count, then the list
@@ -563,7 +562,26 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
   constexpr int GW = kWave / LPR;            // groups per wave
   constexpr int G = kSegWaves * GW;          // groups per block
   constexpr int64_t TILE = (int64_t)G * kGroupSpan;
-  __shared__ f64x4 s_acc[kSegBlock];
+  // With one lane per 16 bytes of a 32-float row (eight groups of eight lanes
+  // per wave), a segment that closes inside a batch is parked in LDS (its
+  // row, place and counts, one slot per group and batch position) and the
+  // wave writes the batch's parked segments together afterwards, eight rows
+  // per store with every lane busy, instead of each group storing as its
+  // segments close while the other groups' lanes idle.
+  constexpr bool kPark = LPR == 8 && GW == kBatch;
+  constexpr int kSlots = GW * kBatch;
+  __shared__ f32x4 s_park[kPark ? kSegWaves : 1][kPark ? kSlots : 1][LPR];
+  __shared__ uint32_t s_park_out[kPark ? kSegWaves : 1][kSlots];
+  __shared__ uint32_t s_park_cw[kPark ? kSegWaves : 1][kSlots];
+  __shared__ uint32_t s_park_list[kPark ? kSegWaves : 1][kSlots];
+  // per-lane chain sums at the end of the groups: in the parking area of the
+  // lane's own wave when parking (free by then), else their own array
+  static_assert(!kPark || sizeof(s_park[0]) >= kWave * sizeof(f64x4), "chain sums fit a wave's parking area");
+  __shared__ f64x4 s_acc_own[kPark ? 1 : kSegBlock];
+  auto s_acc_at = [&](int t) -> f64x4& {
+    if (kPark) return reinterpret_cast<f64x4*>(&s_park[t / kWave][0][0])[t % kWave];
+    return s_acc_own[t];
+  };
   __shared__ int32_t s_cc[G], s_ww[G];
   __shared__ uint32_t s_seg[G], s_flags[G];
   __shared__ uint32_t s_cnum[kHotSlots];
@@ -600,10 +618,12 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
     f64x4 facc = {0.0, 0.0, 0.0, 0.0};
     int fcc = 0, fww = 0;
     bool owner = false;
-    // Words of the batch at i0 (the packed array is padded by two group spans,
-    // so whole vectors stay in bounds past the group's end).
+    uint32_t parked = 0;   // batch positions at which a segment of this group was parked
+    // Words of the batch at i0 (the packed array is padded by a group span, so
+    // whole vectors stay in bounds past the group's end).
     auto load_words = [&](int i0, uint32_t (&word)[kBatch]) {
-      const u32x4* wp = reinterpret_cast<const u32x4*>(packed + p0 + i0);
+      // a group past its positions (waves loop to their longest group) reads the first words, ignored
+      const u32x4* wp = reinterpret_cast<const u32x4*>(packed + (i0 < nvalid ? p0 + i0 : 0));
 #pragma unroll
       for (int v = 0; v < kBatch / 4; ++v) {
         const u32x4 x = wp[v];
@@ -640,6 +660,15 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
             if (i > 0) {
               if (in_first && first_open) {
                 facc = acc; fcc = cc; fww = ww; owner = true;
+              } else if (kPark) {
+                const int slot = (lane / LPR) * kBatch + u;
+                const double div = (a.norm == GBA_NORM_BY_K) ? (double)a.K : (double)cc;
+                if (lane_on) s_park[w][slot][gl] = narrow(acc / div);
+                if (gl == 0) {
+                  s_park_out[w][slot] = (uint32_t)(seg + hb);
+                  s_park_cw[w][slot] = (uint32_t)cc | ((uint32_t)ww << 16);
+                }
+                parked |= 1u << u;
               } else {
                 finalize_segment(a, seg + hb, acc, cc, ww, gl, lane_on);
               }
@@ -663,42 +692,51 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
         }
       }
     };
-    if (kPipelined) {
-      // words two batches ahead, rows one batch ahead of the batch being summed
-      uint32_t w0[kBatch], w1[kBatch];
-      f32x4 r0[kBatch];
-      uint32_t u0 = 0;
-      if (nvalid > 0) {
-        load_words(0, w0);
-        load_words(kBatch, w1);
-        first_open = !(w0[0] & kHead);
-        gather(0, w0, r0, u0);
-      }
-      for (int i0 = 0; i0 < nvalid; i0 += kBatch) {
-        uint32_t w2[kBatch];
-        f32x4 r1[kBatch];
-        uint32_t u1;
-        load_words(i0 + 2 * kBatch, w2);
-        gather(i0 + kBatch, w1, r1, u1);
-        sum_batch(i0, w0, r0, u0);
-#pragma unroll
-        for (int u = 0; u < kBatch; ++u) {
-          w0[u] = w1[u];
-          w1[u] = w2[u];
-          r0[u] = r1[u];
+    // The parked segments of a batch, written by the whole wave: lane L
+    // stands for slot L (group L / 8, batch position L % 8).
+    auto flush = [&]() {
+      const bool mine = (parked >> gl) & 1u;
+      const uint64_t m = __ballot(mine);
+      if (mine) s_park_list[w][__popcll(m & lanemask_lt())] = (uint32_t)lane;
+      __builtin_amdgcn_wave_barrier();
+      const int E = __popcll(m);
+      for (int b = 0; b < E; b += GW) {
+        const int e = b + lane / LPR;
+        if (e < E) {
+          const uint32_t slot = s_park_list[w][e];
+          const int64_t out = s_park_out[w][slot];
+          if (out < N) {   // always true when the numbering is consistent
+            if (lane_on) store_stream(reinterpret_cast<f32x4*>(a.agg + out * D + gl * 4), s_park[w][slot][gl]);
+            if (gl == 0) {
+              const uint32_t v = s_park_cw[w][slot];
+              a.contrib_count[out] = (int32_t)(v & 0xffffu);
+              a.active_count[out] = (int32_t)(v >> 16);
+            }
+          }
         }
-        u0 = u1;
       }
-    } else {
-      for (int i0 = 0; i0 < nvalid; i0 += kBatch) {
-        uint32_t word[kBatch];
-        load_words(i0, word);
-        if (i0 == 0) first_open = !(word[0] & kHead);
-        f32x4 rv[kBatch];
-        uint32_t use;
-        gather(i0, word, rv, use);
-        sum_batch(i0, word, rv, use);
+      __builtin_amdgcn_wave_barrier();   // the next batch reuses the slots
+      parked = 0;
+    };
+    // every group of a wave runs the wave's longest group's batches, so the
+    // flush sees the whole wave
+    int iters = nvalid;
+    if (kPark) {
+#pragma unroll
+      for (int off = kWave / 2; off > 0; off >>= 1) {
+        const int o = __shfl_xor(iters, off, kWave);
+        iters = o > iters ? o : iters;
       }
+    }
+    for (int i0 = 0; i0 < iters; i0 += kBatch) {
+      uint32_t word[kBatch];
+      load_words(i0, word);
+      if (i0 == 0) first_open = !(word[0] & kHead);
+      f32x4 rv[kBatch];
+      uint32_t use;
+      gather(i0, word, rv, use);
+      sum_batch(i0, word, rv, use);
+      if (kPark) flush();
     }
 
     bool last_open = false, pass = false;
@@ -706,7 +744,7 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
       last_open = nvalid == kGroupSpan && (p0 + kGroupSpan) < n && !(packed[p0 + kGroupSpan] & kHead);
       if (last_open) {
         pass = in_first && first_open;
-        s_acc[threadIdx.x] = acc;
+        s_acc_at(threadIdx.x) = acc;
         if (gl == 0) {
           s_cc[grp] = cc;
           s_ww[grp] = ww;
@@ -727,7 +765,7 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
       int tcc = fcc, tww = fww;
       bool from_prev_tile = true;
       for (int gg = grp - 1; gg >= 0; --gg) {
-        tot += s_acc[gg * LPR + gl];
+        tot += s_acc_at(gg * LPR + gl);
         tcc += s_cc[gg];
         tww += s_ww[gg];
         if (!(s_flags[gg] & kPass)) {
@@ -747,12 +785,12 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
     }
     // the chain that runs into the next tile
     if (grp == G - 1 && (s_flags[G - 1] & kOpen)) {
-      f64x4 tot = s_acc[(G - 1) * LPR + gl];
+      f64x4 tot = s_acc_at((G - 1) * LPR + gl);
       int tcc = s_cc[G - 1], tww = s_ww[G - 1];
       int gg = G - 1;
       while (gg > 0 && (s_flags[gg] & kPass)) {
         --gg;
-        tot += s_acc[gg * LPR + gl];
+        tot += s_acc_at(gg * LPR + gl);
         tcc += s_cc[gg];
         tww += s_ww[gg];
       }
