@@ -320,16 +320,17 @@ def test_sparse_many_small_contributions(plan):
         _check_sparse(res, ids, rows, off, w, tokens, 1000, 3, tag, decay)
 
 
-def test_sparse_device_errors():
-    K, D, R = 2, 4, 100
+@pytest.mark.parametrize("plan", [None, gba.SORT_HOT])
+def test_sparse_device_errors(plan):
+    K, D, R = 2, 4, 1000
     off = np.array([0, 3, 6], np.int64)
     rows = np.ones((6, D), np.float32)
-    ids = np.array([1, 2, 300, 4, 5, 6], np.int64)          # 300 is outside [0, R)
-    res = _run_sparse(ids, rows, off, np.ones(K, np.float32), np.array([1, 1]), 1, 0, R)
+    ids = np.array([1, 2, 3000, 4, 5, 6], np.int64)         # 3000 is outside [0, R)
+    res = _run_sparse(ids, rows, off, np.ones(K, np.float32), np.array([1, 1]), 1, 0, R, plan=plan)
     assert res["err"] & gba.DERR_ID_RANGE
     ids = np.array([1, 2, 3, 4, 5, 6], np.int64)
     res = _run_sparse(ids, rows, np.array([0, 4, 3], np.int64), np.ones(K, np.float32),
-                      np.array([1, 1]), 1, 0, R)
+                      np.array([1, 1]), 1, 0, R, plan=plan)
     assert res["err"] & gba.DERR_OFFSETS
 
 
