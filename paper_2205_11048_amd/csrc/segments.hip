@@ -649,6 +649,13 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
 #pragma unroll
       for (int u = 0; u < kBatch; ++u)
         if (!((use >> u) & 1u)) rv[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+      // weights other than 0 and 1 are rare: unless some position of the
+      // wave's batch has one, rows are added without a multiply (a weight-0
+      // row was zeroed above), a branch the whole wave takes together
+      bool nonunit = false;
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) nonunit |= i0 + u < nvalid && (word[u] & kNonUnit);
+      const bool weighted = __ballot(nonunit) != 0ull;
 #pragma unroll
       for (int u = 0; u < kBatch; ++u) {
         const int i = i0 + u;
@@ -680,7 +687,9 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
             cc = ww = 0;
           }
           const bool zero = word[u] & kZeroW;
-          if (!zero) {
+          if (!weighted) {
+            acc += widen(rv[u]);
+          } else if (!zero) {
             double wd = 1.0;
             if (word[u] & kNonUnit)   // a weight other than 0 or 1: look up its contribution
               wd = (double)a.w[contribution_global(a.offsets, a.K, word[u] & kIndexMask)];
