@@ -3,11 +3,13 @@
 // back.  Rows without a non-zero-weight contribution are skipped (they are
 // not updated at this global step; Alg. 2 updates embeddings by ID).
 //
-// A group of LPR lanes owns one row at a time and moves it as 16-byte
-// non-temporal vectors (every row, state and gradient is touched once, so the
-// L2 is left to the kernels that reuse lines); the grid is persistent and
-// reads the row count from device memory, so no host round trip sits between
-// the aggregation and the apply.
+// A group of LPR lanes owns kRowBatch consecutive rows at a time and moves
+// them as 16-byte non-temporal vectors (every row, state and gradient is
+// touched once, so the L2 is left to the kernels that reuse lines); all of a
+// batch's loads are issued before the first is used (a skipped row reads row
+// 0 and is not written), so a group keeps kRowBatch rows in flight.  The grid
+// is persistent and reads the row count from device memory, so no host round
+// trip sits between the aggregation and the apply.
 #include "gba_device.hpp"
 #include "gba_internal.hpp"
 #include "optim.hpp"
@@ -16,6 +18,7 @@ namespace gba {
 
 constexpr int kRowsBlock = 256;
 constexpr int64_t kRowsMaxBlocks = 4096;
+constexpr int kRowBatch = 4;
 
 static inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
@@ -32,34 +35,52 @@ rows_apply_kernel(float* __restrict__ p, float* __restrict__ s1, float* __restri
   int64_t count = *num_rows;
   if (count > n) count = n;
   bool bad = false;
-  const int64_t stride = (int64_t)gridDim.x * G;
-  for (int64_t i = (int64_t)blockIdx.x * G + grp; i < count; i += stride) {
-    if (active && active[i] <= 0) continue;
-    const int64_t r = rows[i];
-    if (r < 0 || r >= R) {
-      bad = true;
-      continue;
+  const int64_t stride = (int64_t)gridDim.x * G * kRowBatch;
+  for (int64_t i0 = ((int64_t)blockIdx.x * G + grp) * kRowBatch; i0 < count; i0 += stride) {
+    int64_t r[kRowBatch];
+    bool on[kRowBatch];
+#pragma unroll
+    for (int k = 0; k < kRowBatch; ++k) {
+      const int64_t i = i0 + k;
+      const int64_t ic = i < count ? i : count - 1;
+      const int64_t rk = rows[ic];
+      const bool act = i < count && (!active || active[ic] > 0);
+      const bool in_range = rk >= 0 && rk < R;
+      bad |= act && !in_range;
+      on[k] = act && in_range;
+      r[k] = on[k] ? rk : 0;
     }
     for (int c = lane * 4; c < D; c += LPR * 4) {
-      const int64_t at = r * (int64_t)D + c;
-      const f32x4 pv = load_stream(reinterpret_cast<const f32x4*>(p + at));
-      const f32x4 av = load_stream(reinterpret_cast<const f32x4*>(s1 + at));
-      const f32x4 gv = load_stream(reinterpret_cast<const f32x4*>(g + i * (int64_t)D + c));
-      float pe[4] = {pv.x, pv.y, pv.z, pv.w};
-      float ae[4] = {av.x, av.y, av.z, av.w};
-      const float ge[4] = {gv.x, gv.y, gv.z, gv.w};
-      if (ADAM) {
-        const f32x4 vv = load_stream(reinterpret_cast<const f32x4*>(s2 + at));
-        float ve[4] = {vv.x, vv.y, vv.z, vv.w};
+      f32x4 pv[kRowBatch], av[kRowBatch], gv[kRowBatch], vv[ADAM ? kRowBatch : 1];
 #pragma unroll
-        for (int k = 0; k < 4; ++k) adam_update(pe[k], ae[k], ve[k], ge[k], lr, b1, b2, eps, bc1, bc2);
-        store_stream(reinterpret_cast<f32x4*>(s2 + at), f32x4{ve[0], ve[1], ve[2], ve[3]});
-      } else {
-#pragma unroll
-        for (int k = 0; k < 4; ++k) adagrad_update(pe[k], ae[k], ge[k], lr, eps);
+      for (int k = 0; k < kRowBatch; ++k) {
+        const int64_t at = r[k] * (int64_t)D + c;
+        const int64_t gi = on[k] ? i0 + k : 0;
+        pv[k] = load_stream(reinterpret_cast<const f32x4*>(p + at));
+        av[k] = load_stream(reinterpret_cast<const f32x4*>(s1 + at));
+        if (ADAM) vv[ADAM ? k : 0] = load_stream(reinterpret_cast<const f32x4*>(s2 + at));
+        gv[k] = load_stream(reinterpret_cast<const f32x4*>(g + gi * (int64_t)D + c));
       }
-      store_stream(reinterpret_cast<f32x4*>(p + at), f32x4{pe[0], pe[1], pe[2], pe[3]});
-      store_stream(reinterpret_cast<f32x4*>(s1 + at), f32x4{ae[0], ae[1], ae[2], ae[3]});
+#pragma unroll
+      for (int k = 0; k < kRowBatch; ++k) {
+        if (!on[k]) continue;
+        const int64_t at = r[k] * (int64_t)D + c;
+        float pe[4] = {pv[k].x, pv[k].y, pv[k].z, pv[k].w};
+        float ae[4] = {av[k].x, av[k].y, av[k].z, av[k].w};
+        const float ge[4] = {gv[k].x, gv[k].y, gv[k].z, gv[k].w};
+        if (ADAM) {
+          const f32x4 vk = vv[ADAM ? k : 0];
+          float ve[4] = {vk.x, vk.y, vk.z, vk.w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) adam_update(pe[e], ae[e], ve[e], ge[e], lr, b1, b2, eps, bc1, bc2);
+          store_stream(reinterpret_cast<f32x4*>(s2 + at), f32x4{ve[0], ve[1], ve[2], ve[3]});
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) adagrad_update(pe[e], ae[e], ge[e], lr, eps);
+        }
+        store_stream(reinterpret_cast<f32x4*>(p + at), f32x4{pe[0], pe[1], pe[2], pe[3]});
+        store_stream(reinterpret_cast<f32x4*>(s1 + at), f32x4{ae[0], ae[1], ae[2], ae[3]});
+      }
     }
   }
   if (bad) raise_error(err, GBA_DERR_ROW_RANGE);
@@ -74,7 +95,7 @@ static hipError_t launch_rows(float* p, float* s1, float* s2, const float* g, co
   int lpr = 1;
   while (lpr < 64 && lpr * 4 < D) lpr <<= 1;
   const int G = kRowsBlock / lpr;
-  int64_t blocks = ceil_div(n, G);
+  int64_t blocks = ceil_div(n, (int64_t)G * kRowBatch);
   if (blocks > kRowsMaxBlocks) blocks = kRowsMaxBlocks;
   const dim3 grid((unsigned)blocks), block(kRowsBlock);
 #define GBA_ROWS_CASE(L)                                                                          \
