@@ -78,4 +78,24 @@ __device__ __forceinline__ f32x4 narrow(f64x4 v) {
   return f32x4{(float)v.x, (float)v.y, (float)v.z, (float)v.w};
 }
 
+// acc / d for each element, rounded once, as a float64 division rounds it,
+// at one division per vector instead of four: with y the rounded reciprocal
+// of d and q = acc * y rounded (within an ulp of the quotient), the residual
+// acc - q * d is exact in one fma and q + residual * y, rounded, is the
+// rounded quotient (Markstein's theorem; Muller et al., Handbook of
+// Floating-Point Arithmetic, the chapter on division by iteration).  It holds
+// away from the float64 underflow and overflow ranges, far from sums of
+// float32 values divided by a count.
+__device__ __forceinline__ f64x4 div_rounded(f64x4 acc, double d) {
+  const double y = 1.0 / d;
+  f64x4 q;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const double q0 = acc[e] * y;
+    const double r = __builtin_fma(-q0, d, acc[e]);
+    q[e] = __builtin_fma(r, y, q0);
+  }
+  return q;
+}
+
 }  // namespace gba

@@ -199,7 +199,7 @@ __device__ __forceinline__ void finalize_segment(const SegmentArgs& a, int64_t s
   if (seg < 0 || seg >= a.N) return;   // unreachable when the numbering is consistent
   const double div = (a.norm == GBA_NORM_BY_K) ? (double)a.K : (double)cc;
   if (lane_on)
-    store_stream(reinterpret_cast<f32x4*>(a.agg + seg * (int64_t)a.D + lane * 4), narrow(acc / div));   // read once, by the apply
+    store_stream(reinterpret_cast<f32x4*>(a.agg + seg * (int64_t)a.D + lane * 4), narrow(div_rounded(acc, div)));   // read once, by the apply
   if (lane == 0) {
     a.contrib_count[seg] = cc;
     a.active_count[seg] = ww;
@@ -670,7 +670,7 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
               } else if (kPark) {
                 const int slot = (lane / LPR) * kBatch + u;
                 const double div = (a.norm == GBA_NORM_BY_K) ? (double)a.K : (double)cc;
-                if (lane_on) s_park[w][slot][gl] = narrow(acc / div);
+                if (lane_on) s_park[w][slot][gl] = narrow(div_rounded(acc, div));
                 if (gl == 0) {
                   s_park_out[w][slot] = (uint32_t)(seg + hb);
                   s_park_cw[w][slot] = (uint32_t)cc | ((uint32_t)ww << 16);
