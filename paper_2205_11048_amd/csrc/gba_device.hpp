@@ -85,9 +85,8 @@ __device__ __forceinline__ f32x4 narrow(f64x4 v) {
 // rounded quotient (Markstein's theorem; Muller et al., Handbook of
 // Floating-Point Arithmetic, the chapter on division by iteration).  It holds
 // away from the float64 underflow and overflow ranges, far from sums of
-// float32 values divided by a count.
-__device__ __forceinline__ f64x4 div_rounded(f64x4 acc, double d) {
-  const double y = 1.0 / d;
+// float32 values divided by a count.  y must be the rounded 1 / d.
+__device__ __forceinline__ f64x4 div_rounded(f64x4 acc, double d, double y) {
   f64x4 q;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
@@ -97,5 +96,6 @@ __device__ __forceinline__ f64x4 div_rounded(f64x4 acc, double d) {
   }
   return q;
 }
+__device__ __forceinline__ f64x4 div_rounded(f64x4 acc, double d) { return div_rounded(acc, d, 1.0 / d); }
 
 }  // namespace gba

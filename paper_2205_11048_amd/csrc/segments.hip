@@ -82,6 +82,7 @@ struct SegPartials {
 };
 
 constexpr int kHotSlots = 256;   // at least the sort's largest number of hot IDs (+1)
+constexpr int kRecipMax = 256;   // divisors with a reciprocal in the row pass's table
 
 struct SegLayout {
   int64_t meta_tiles, row_tiles, hot_chunks;
@@ -585,6 +586,8 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
   __shared__ int32_t s_cc[G], s_ww[G];
   __shared__ uint32_t s_seg[G], s_flags[G];
   __shared__ uint32_t s_cnum[kHotSlots];
+  // rounded reciprocals of the small divisors (a segment's contribution count)
+  __shared__ double s_recip[kRecipMax + 1];
 
   const int64_t N = a.N;                                   // occurrences
   const int64_t n = a.n_dev ? (int64_t)*a.n_dev : a.N;     // sorted positions
@@ -594,7 +597,11 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
   // cnum[h] <= s (cnum ascending)
   const uint32_t H = a.n_dev ? *a.hot.meta : 0u;
   if (threadIdx.x < H) s_cnum[threadIdx.x] = cnum[threadIdx.x];
+  for (int i = threadIdx.x; i <= kRecipMax; i += kSegBlock) s_recip[i] = 1.0 / (double)i;
   __syncthreads();
+  const bool by_k = a.norm == GBA_NORM_BY_K;
+  const double recip_k = 1.0 / (double)a.K;
+  const bool small_k = a.K <= kRecipMax;
 
   const int w = threadIdx.x / kWave;
   const int lane = lane_id();
@@ -613,6 +620,8 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
     // hot IDs before segment seg among all IDs (its output is seg + hb)
     uint32_t hb = H ? count_at_most(s_cnum, H, seg) : 0u;
     const uint32_t hb0 = hb;
+    // the first segment number that has hot ID hb before it
+    uint32_t hnext = hb < H ? s_cnum[hb] : 0xffffffffu;   // positions (and segments) stay below 2^32 - 1
     bool first_open = false;
     bool in_first = true;
     f64x4 facc = {0.0, 0.0, 0.0, 0.0};
@@ -669,8 +678,10 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
                 facc = acc; fcc = cc; fww = ww; owner = true;
               } else if (kPark) {
                 const int slot = (lane / LPR) * kBatch + u;
-                const double div = (a.norm == GBA_NORM_BY_K) ? (double)a.K : (double)cc;
-                if (lane_on) s_park[w][slot][gl] = narrow(div_rounded(acc, div));
+                const double div = by_k ? (double)a.K : (double)cc;
+                // a segment has at most K contributions: the table covers every count when K is small
+                const double y = by_k ? recip_k : (small_k ? s_recip[cc] : 1.0 / div);
+                if (lane_on) s_park[w][slot][gl] = narrow(div_rounded(acc, div, y));
                 if (gl == 0) {
                   s_park_out[w][slot] = (uint32_t)(seg + hb);
                   s_park_cw[w][slot] = (uint32_t)cc | ((uint32_t)ww << 16);
@@ -682,7 +693,10 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
               in_first = false;
             }
             ++seg;
-            while (hb < H && (int64_t)s_cnum[hb] <= seg) ++hb;
+            if ((uint32_t)seg >= hnext) {
+              do ++hb; while (hb < H && (int64_t)s_cnum[hb] <= seg);
+              hnext = hb < H ? s_cnum[hb] : 0xffffffffu;
+            }
             acc = f64x4{0.0, 0.0, 0.0, 0.0};
             cc = ww = 0;
           }
