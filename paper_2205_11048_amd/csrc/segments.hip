@@ -563,22 +563,25 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
   constexpr int GW = kWave / LPR;            // groups per wave
   constexpr int G = kSegWaves * GW;          // groups per block
   constexpr int64_t TILE = (int64_t)G * kGroupSpan;
-  // With one lane per 16 bytes of a 32-float row (eight groups of eight lanes
-  // per wave), a segment that closes inside a batch is parked in LDS (its
-  // row, place and counts, one slot per group and batch position) and the
-  // wave writes the batch's parked segments together afterwards, eight rows
-  // per store with every lane busy, instead of each group storing as its
-  // segments close while the other groups' lanes idle.
-  constexpr bool kPark = LPR == 8 && GW == kBatch;
-  constexpr int kSlots = GW * kBatch;
-  __shared__ f32x4 s_park[kPark ? kSegWaves : 1][kPark ? kSlots : 1][LPR];
-  __shared__ uint32_t s_park_out[kPark ? kSegWaves : 1][kSlots];
-  __shared__ uint32_t s_park_cw[kPark ? kSegWaves : 1][kSlots];
-  __shared__ uint32_t s_park_list[kPark ? kSegWaves : 1][kSlots];
+  // With several groups per wave, a segment that closes is parked in LDS
+  // (its float64 sums, place and counts) in the wave's next free slot, and
+  // when the slots run low the wave finishes the parked segments together:
+  // the division, the narrowing and the row stores run with every lane busy,
+  // GW rows per store, instead of in each group as its segments close while
+  // the other groups' lanes idle.
+  constexpr bool kPark = LPR == 8;
+  constexpr int kParkCap = 3 * GW;   // slots per wave
+  __shared__ f64x4 s_park[kPark ? kSegWaves : 1][kPark ? kParkCap : 1][LPR];
+  __shared__ uint32_t s_park_out[kPark ? kSegWaves : 1][kParkCap];
+  __shared__ uint32_t s_park_cw[kPark ? kSegWaves : 1][kParkCap];
   // per-lane chain sums at the end of the groups: in the parking area of the
   // lane's own wave when parking (free by then), else their own array
   static_assert(!kPark || sizeof(s_park[0]) >= kWave * sizeof(f64x4), "chain sums fit a wave's parking area");
   __shared__ f64x4 s_acc_own[kPark ? 1 : kSegBlock];
+  // the sums of the segment each group began inside, held until the chain of
+  // groups before it is known
+  __shared__ f64x4 s_first[kSegBlock];
+  __shared__ int32_t s_fcc[G], s_fww[G];
   auto s_acc_at = [&](int t) -> f64x4& {
     if (kPark) return reinterpret_cast<f64x4*>(&s_park[t / kWave][0][0])[t % kWave];
     return s_acc_own[t];
@@ -624,10 +627,43 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
     uint32_t hnext = hb < H ? s_cnum[hb] : 0xffffffffu;   // positions (and segments) stay below 2^32 - 1
     bool first_open = false;
     bool in_first = true;
-    f64x4 facc = {0.0, 0.0, 0.0, 0.0};
-    int fcc = 0, fww = 0;
     bool owner = false;
-    uint32_t parked = 0;   // batch positions at which a segment of this group was parked
+    int pbase = 0;   // parked segments of the wave (the same in every lane)
+    auto hold_first = [&]() {
+      if (lane_on) s_first[threadIdx.x] = acc;
+      if (gl == 0) {
+        s_fcc[grp] = cc;
+        s_fww[grp] = ww;
+      }
+      owner = true;
+    };
+    // The wave's parked segments: each group finishes one per round.
+    auto flush = [&]() {
+      __builtin_amdgcn_wave_barrier();
+      for (int b = 0; b < pbase; b += GW) {
+        const int e = b + lane / LPR;
+        if (e < pbase) {
+          const int64_t out = s_park_out[w][e];
+          const uint32_t v = s_park_cw[w][e];
+          const int c = (int)(v & 0xffffu);
+          if (out < N) {   // always true when the numbering is consistent
+            if (lane_on) {
+              const double div = by_k ? (double)a.K : (double)c;
+              // a segment has at most K contributions: the table covers every count when K is small
+              const double y = by_k ? recip_k : (small_k ? s_recip[c < kRecipMax ? c : kRecipMax] : 1.0 / div);
+              store_stream(reinterpret_cast<f32x4*>(a.agg + out * D + gl * 4),
+                           narrow(div_rounded(s_park[w][e][gl], div, y)));
+            }
+            if (gl == 0) {
+              a.contrib_count[out] = c;
+              a.active_count[out] = (int32_t)(v >> 16);
+            }
+          }
+        }
+      }
+      __builtin_amdgcn_wave_barrier();   // the slots are reused
+      pbase = 0;
+    };
     // Words of the batch at i0 (the packed array is padded by a group span, so
     // whole vectors stay in bounds past the group's end).
     auto load_words = [&](int i0, uint32_t (&word)[kBatch]) {
@@ -671,22 +707,25 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
         // keep each row's float64 widening next to its use: hoisting all of
         // them costs registers and the waves that keep gathers in flight
         __builtin_amdgcn_sched_barrier(0);
+        // parking: a free slot for every group, the groups' slots numbered in
+        // group order (both wave-wide, so outside the branches below)
+        uint64_t pm = 0;
+        if (kPark) {
+          if (pbase + GW > kParkCap) flush();
+          pm = __ballot(i < nvalid && (word[u] & kHead) && i > 0 && !(in_first && first_open));
+        }
         if (i < nvalid) {
           if (word[u] & kHead) {
             if (i > 0) {
               if (in_first && first_open) {
-                facc = acc; fcc = cc; fww = ww; owner = true;
+                hold_first();
               } else if (kPark) {
-                const int slot = (lane / LPR) * kBatch + u;
-                const double div = by_k ? (double)a.K : (double)cc;
-                // a segment has at most K contributions: the table covers every count when K is small
-                const double y = by_k ? recip_k : (small_k ? s_recip[cc] : 1.0 / div);
-                if (lane_on) s_park[w][slot][gl] = narrow(div_rounded(acc, div, y));
+                const int slot = pbase + (__popcll(pm & lanemask_lt()) / LPR);
+                if (lane_on) s_park[w][slot][gl] = acc;
                 if (gl == 0) {
                   s_park_out[w][slot] = (uint32_t)(seg + hb);
                   s_park_cw[w][slot] = (uint32_t)cc | ((uint32_t)ww << 16);
                 }
-                parked |= 1u << u;
               } else {
                 finalize_segment(a, seg + hb, acc, cc, ww, gl, lane_on);
               }
@@ -713,36 +752,11 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
           cc += nc;
           ww += (nc && !zero) ? 1 : 0;
         }
+        if (kPark) pbase += __popcll(pm) / LPR;
       }
-    };
-    // The parked segments of a batch, written by the whole wave: lane L
-    // stands for slot L (group L / 8, batch position L % 8).
-    auto flush = [&]() {
-      const bool mine = (parked >> gl) & 1u;
-      const uint64_t m = __ballot(mine);
-      if (mine) s_park_list[w][__popcll(m & lanemask_lt())] = (uint32_t)lane;
-      __builtin_amdgcn_wave_barrier();
-      const int E = __popcll(m);
-      for (int b = 0; b < E; b += GW) {
-        const int e = b + lane / LPR;
-        if (e < E) {
-          const uint32_t slot = s_park_list[w][e];
-          const int64_t out = s_park_out[w][slot];
-          if (out < N) {   // always true when the numbering is consistent
-            if (lane_on) store_stream(reinterpret_cast<f32x4*>(a.agg + out * D + gl * 4), s_park[w][slot][gl]);
-            if (gl == 0) {
-              const uint32_t v = s_park_cw[w][slot];
-              a.contrib_count[out] = (int32_t)(v & 0xffffu);
-              a.active_count[out] = (int32_t)(v >> 16);
-            }
-          }
-        }
-      }
-      __builtin_amdgcn_wave_barrier();   // the next batch reuses the slots
-      parked = 0;
     };
     // every group of a wave runs the wave's longest group's batches, so the
-    // flush sees the whole wave
+    // parking decisions are taken by the whole wave
     int iters = nvalid;
     if (kPark) {
 #pragma unroll
@@ -759,8 +773,8 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
       uint32_t use;
       gather(i0, word, rv, use);
       sum_batch(i0, word, rv, use);
-      if (kPark) flush();
     }
+    if (kPark && pbase > 0) flush();   // before the parking area holds the chain sums
 
     bool last_open = false, pass = false;
     if (nvalid > 0) {
@@ -774,7 +788,7 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
           s_seg[grp] = (uint32_t)seg;
         }
       } else if (in_first && first_open) {
-        facc = acc; fcc = cc; fww = ww; owner = true;
+        hold_first();
       } else {
         finalize_segment(a, seg + hb, acc, cc, ww, gl, lane_on);
       }
@@ -784,8 +798,8 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
 
     // a group whose first run began before it closes the chain of runs
     if (owner) {
-      f64x4 tot = facc;
-      int tcc = fcc, tww = fww;
+      f64x4 tot = lane_on ? s_first[threadIdx.x] : f64x4{0.0, 0.0, 0.0, 0.0};
+      int tcc = s_fcc[grp], tww = s_fww[grp];
       bool from_prev_tile = true;
       for (int gg = grp - 1; gg >= 0; --gg) {
         tot += s_acc_at(gg * LPR + gl);
