@@ -10,6 +10,8 @@
 // up to 15% of bandwidth to DRAM row conflicts, depending on the buffers'
 // relative addresses).  Each thread accumulates its 16 vectors in float64 in
 // buffer order, so the only rounding is the final one to float.
+#include <algorithm>
+
 #include "gba_device.hpp"
 #include "gba_internal.hpp"
 #include "optim.hpp"
@@ -22,6 +24,7 @@ constexpr int kDenseVecs = 16;                                        // f32x4 p
 constexpr int64_t kDenseSpan = (int64_t)kSumBlock * kDenseVecs;       // vectors per block step
 constexpr int64_t kDenseMaxBlocks = 65535;
 constexpr int64_t kApplyMaxBlocks = 8192;
+constexpr int64_t kDenseRoundsPerLaunch = 1;                           // rounds of resident blocks per launch
 
 static inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
@@ -167,7 +170,7 @@ template <int MODE, bool CARRY>
 __global__ void __launch_bounds__(kSumBlock)
 aggregate_dense_kernel(const float* const* __restrict__ grads, const float* __restrict__ w, int K,
                        int64_t P, float* __restrict__ out, DenseState st, double* __restrict__ run,
-                       double denom, int reset) {
+                       double denom, int reset, int64_t step0, int64_t step_end) {
   __shared__ uint16_t kept[GBA_MAX_K];
   __shared__ float kw[GBA_MAX_K];
   __shared__ uint32_t tmp[kSumBlock / kWave + 1];
@@ -180,7 +183,8 @@ aggregate_dense_kernel(const float* const* __restrict__ grads, const float* __re
                                (reinterpret_cast<uintptr_t>(run) & 31u) == 0;   // null pointers count as aligned
   if (aligned && outputs_aligned) {
     const int64_t nvec = P / 4;
-    for (int64_t b0 = (int64_t)blockIdx.x * kDenseSpan; b0 < nvec; b0 += (int64_t)gridDim.x * kDenseSpan) {
+    for (int64_t s = step0 + blockIdx.x; s < step_end; s += gridDim.x) {
+      const int64_t b0 = s * kDenseSpan;
       // wave w covers vectors [b0 + w * 1024, +1024): lane l takes l, l + 64, ...
       const int64_t vb = b0 + (int64_t)(threadIdx.x / kWave) * (kWave * kDenseVecs) + (threadIdx.x % kWave);
       f64x4 acc[kDenseVecs];
@@ -214,9 +218,9 @@ aggregate_dense_kernel(const float* const* __restrict__ grads, const float* __re
     }
     // the last P % 4 elements
     const int64_t tail0 = nvec * 4;
-    if (blockIdx.x == 0 && threadIdx.x < P - tail0)
+    if (step0 == 0 && blockIdx.x == 0 && threadIdx.x < P - tail0)
       finish_scalar<MODE, CARRY>(grads, kept, kw, nk, tail0 + threadIdx.x, out, st, run, denom, reset);
-  } else {
+  } else if (step0 == 0) {   // the first launch takes every element
     for (int64_t e = (int64_t)blockIdx.x * kSumBlock + threadIdx.x; e < P; e += stride)
       finish_scalar<MODE, CARRY>(grads, kept, kw, nk, e, out, st, run, denom, reset);
   }
@@ -227,14 +231,33 @@ static hipError_t launch_dense_mode(const float* const* grads, const float* w, i
                                     float* out, const DenseState& st, double* run, double denom, int reset,
                                     hipStream_t stream) {
   if (P <= 0) return hipSuccess;
-  // one block step per block where possible; unaligned buffers fall back to
-  // a grid-stride loop over single elements
-  int64_t blocks = ceil_div(ceil_div(P, 4), kDenseSpan);
-  if (blocks > kDenseMaxBlocks) blocks = kDenseMaxBlocks;
-  if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL((aggregate_dense_kernel<MODE, CARRY>), dim3((unsigned)blocks), dim3(kSumBlock), 0, stream,
-                     grads, w, (int)K, P, out, st, run, denom, reset);
-  return hipGetLastError();
+  // One block step per block.  Where the steps outnumber two rounds of the
+  // blocks the GPU holds at once, they are launched one round at a time:
+  // blocks that start together read the same gradient at neighbouring
+  // offsets, while in one long launch the blocks drift apart until they read
+  // all K buffers at once, which costs bandwidth (DRAM row changes).  Unaligned
+  // buffers fall back to a grid-stride loop over single elements in the first
+  // launch.
+  const int64_t steps = std::max<int64_t>(ceil_div(P / 4, kDenseSpan), 1);
+  int64_t round = steps;
+  if (K > 0) {
+    int dev = 0, cus = 0, per_cu = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, aggregate_dense_kernel<MODE, CARRY>, kSumBlock, 0) ==
+            hipSuccess &&
+        cus > 0 && per_cu > 0 && steps > 2 * kDenseRoundsPerLaunch * (int64_t)cus * per_cu)
+      round = kDenseRoundsPerLaunch * (int64_t)cus * per_cu;
+  }
+  for (int64_t s0 = 0; s0 < steps; s0 += round) {
+    const int64_t s1 = std::min(steps, s0 + round);
+    const int64_t blocks = std::min(s1 - s0, kDenseMaxBlocks);
+    hipLaunchKernelGGL((aggregate_dense_kernel<MODE, CARRY>), dim3((unsigned)blocks), dim3(kSumBlock), 0, stream,
+                       grads, w, (int)K, P, out, st, run, denom, reset, s0, s1);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_aggregate_dense(const float* const* grads, const float* w, int32_t K, int64_t P,

@@ -71,6 +71,20 @@ def test_aggregate_dense(K, P):
     assert_exact(got, ref, "g_bar (float64 accumulation in buffer order is exact)")
 
 
+def test_aggregate_dense_launched_in_rounds():
+    """More block steps than two rounds of the blocks the GPU holds at once
+    (each step covers 32,768 elements): the reduction is launched one round at
+    a time, and every element, the ragged tail included, is still summed once."""
+    K, P = 3, 3 * 256 * 32768 + 3      # three rounds of 256 one-block compute units
+    rng = np.random.default_rng(29)
+    grads = [rng.random(P, dtype=np.float32) - np.float32(0.5) for _ in range(K)]
+    w = np.array([1.0, 0.0, 1.0], np.float32)
+    ref = oracle.aggregate_dense(grads, w)
+    out = torch.empty(P, dtype=torch.float32, device=DEV)
+    gba.gba_aggregate_dense(gba.pointer_table([dev(g) for g in grads]), dev(w), P, out)
+    assert_exact(host(out), ref, "g_bar")
+
+
 def test_aggregate_dense_unaligned_and_fractional_weights():
     K, P = 5, 1001
     base = [dev(counter.values_range(3, 100 + m, 0, P + 1, counter.KIND_GRAD, counter.grad_scale(1e-2)))
