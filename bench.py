@@ -234,17 +234,24 @@ def run_workload(name, args, torch, gba_step_mod, sdev, gba):
     dense_b, sparse_b = algorithmic_bytes(w, K_eff, N_act, U, U_act, args.decay == "id_tag")
     step_gbs = (dense_b + sparse_b) / (ms * 1e-3) / 1e9
 
-    # dominant kernel: the dense reduction (one launch per call), fused with
-    # the dense optimiser unless --separate-dense
+    # dominant kernel: the dense reduction, fused with the dense optimiser
+    # unless --separate-dense.  A call is one launch, or one launch per round
+    # of resident blocks at large P; the figures are per launch (the call's
+    # bytes and time over its launches, which split the work evenly but for
+    # the last).
     S = 1 if w.optimizer == "adagrad" else 2
     if args.separate_dense:
-        dense_kernel_bytes = K_eff * w.P * 4 + w.P * 4
-        dk_ms = breakdown["aggregate_dense"]
+        dense_call_bytes = K_eff * w.P * 4 + w.P * 4
+        call_ms = breakdown["aggregate_dense"]
         kname = "aggregate_dense_kernel<0, false>"
+        launches = gba.gba_aggregate_dense_launches(w.P, w.K, gba.DENSE_SUM)
     else:
-        dense_kernel_bytes = K_eff * w.P * 4 + (2 + 2 * S) * w.P * 4
-        dk_ms = breakdown["aggregate_apply_dense"]
+        dense_call_bytes = K_eff * w.P * 4 + (2 + 2 * S) * w.P * 4
+        call_ms = breakdown["aggregate_apply_dense"]
         kname = f"aggregate_dense_kernel<{S}, false>"
+        launches = gba.gba_aggregate_dense_launches(w.P, w.K, gba.DENSE_ADAGRAD if S == 1 else gba.DENSE_ADAM)
+    dense_kernel_bytes = dense_call_bytes / launches
+    dk_ms = call_ms / launches
     dk_gbs = dense_kernel_bytes / (dk_ms * 1e-3) / 1e9
     traffic = measured_traffic(kname, name)
     res = dict(
@@ -255,7 +262,7 @@ def run_workload(name, args, torch, gba_step_mod, sdev, gba):
         breakdown_ms=breakdown, overlap=args.overlap, fused_dense=not args.separate_dense, K_eff=K_eff, N=w.N, N_act=N_act, U=U, U_act=U_act, setup_s=setup_s,
         roofline=dict(kernel=kname, bound="hbm", achieved=dk_gbs, peak=HBM_PEAK_GBS,
                       unit="GB/s", frac=dk_gbs / HBM_PEAK_GBS, traffic=traffic,
-                      alg_bytes_per_launch=dense_kernel_bytes, avg_launch_ms=dk_ms),
+                      alg_bytes_per_launch=dense_kernel_bytes, avg_launch_ms=dk_ms, launches_per_call=launches),
     )
     # the same step with the dense sum taken early, for each J asked for
     res["early_sum"] = []

@@ -185,6 +185,18 @@ gba_status gba_aggregate_apply_dense_adagrad(const float* const* grads, const fl
                                              int64_t P, float* out, float* param, float* accum,
                                              double lr, double eps, hipStream_t stream);
 
+/*
+ * Host query, for profiling and for callers that count graph nodes: the
+ * number of kernel launches one dense call over P elements with K
+ * contributions makes on the current device (the weighted sum of Alg. 2 is
+ * launched one round of resident blocks at a time when it spans more than two
+ * rounds).  opt: 0 gba_aggregate_dense, 1 gba_aggregate_apply_dense_adagrad,
+ * 2 gba_aggregate_apply_dense_adam, 3 gba_accumulate_dense (K = J).
+ * launches   host out; 0 when P == 0.
+ * Errors: GBA_ERR_NULL (launches), GBA_ERR_INVALID_ARG (K, P or opt out of range).
+ */
+gba_status gba_aggregate_dense_launches(int64_t P, int32_t K, int32_t opt, int64_t* launches);
+
 gba_status gba_aggregate_apply_dense_adam(const float* const* grads, const float* w, int32_t K,
                                           int64_t P, float* out, float* param, float* m, float* v,
                                           double lr, double beta1, double beta2, double eps,

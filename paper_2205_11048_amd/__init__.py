@@ -59,6 +59,7 @@ _SIGNATURES = {
     "gba_aggregate_apply_dense_adam": ([_P, _P, _I32, _I64, _P, _P, _P, _P, _F64, _F64, _F64, _F64, _I64, _P],
                                        _I32),
     "gba_accumulate_dense": ([_P, _P, _I32, _I64, _P, _P], _I32),
+    "gba_aggregate_dense_launches": ([_I64, _I32, _I32, ctypes.POINTER(_I64)], _I32),
     "gba_finalize_dense": ([_P, _I32, _I64, _P, _I32, _P], _I32),
     "gba_finalize_apply_dense_adagrad": ([_P, _I32, _I64, _P, _P, _P, _F64, _F64, _I32, _P], _I32),
     "gba_finalize_apply_dense_adam": ([_P, _I32, _I64, _P, _P, _P, _P, _F64, _F64, _F64, _F64, _I64, _I32, _P],
@@ -149,6 +150,16 @@ def gba_aggregate_dense(grads, w, P, out, stream=None):
     _need(w, torch.float32, "w", K)
     _need(out, torch.float32, "out", P)
     _check(lib().gba_aggregate_dense(_ptr(grads), _ptr(w), K, int(P), _ptr(out), _stream(stream)))
+
+
+DENSE_SUM, DENSE_ADAGRAD, DENSE_ADAM, DENSE_ACCUMULATE = 0, 1, 2, 3
+
+
+def gba_aggregate_dense_launches(P, K, opt=DENSE_SUM):
+    """Kernel launches one dense call makes on the current device (host query)."""
+    n = _I64(0)
+    _check(lib().gba_aggregate_dense_launches(int(P), int(K), int(opt), ctypes.byref(n)))
+    return int(n.value)
 
 
 def _dense_common(grads, w, P, out, **state):

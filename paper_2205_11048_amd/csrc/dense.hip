@@ -226,29 +226,37 @@ aggregate_dense_kernel(const float* const* __restrict__ grads, const float* __re
   }
 }
 
+// Block steps of a dense call over P elements and the steps each launch
+// covers.  Where the steps outnumber two rounds of the blocks the GPU holds at
+// once, they are launched one round at a time: blocks that start together read
+// the same gradient at neighbouring offsets, while in one long launch the
+// blocks drift apart until they read all K buffers at once, which costs
+// bandwidth (DRAM row changes).  K == 0 (finishing a running sum) reads no
+// gradients and takes one launch.
 template <int MODE, bool CARRY>
-static hipError_t launch_dense_mode(const float* const* grads, const float* w, int32_t K, int64_t P,
-                                    float* out, const DenseState& st, double* run, double denom, int reset,
-                                    hipStream_t stream) {
-  if (P <= 0) return hipSuccess;
-  // One block step per block.  Where the steps outnumber two rounds of the
-  // blocks the GPU holds at once, they are launched one round at a time:
-  // blocks that start together read the same gradient at neighbouring
-  // offsets, while in one long launch the blocks drift apart until they read
-  // all K buffers at once, which costs bandwidth (DRAM row changes).  Unaligned
-  // buffers fall back to a grid-stride loop over single elements in the first
-  // launch.
-  const int64_t steps = std::max<int64_t>(ceil_div(P / 4, kDenseSpan), 1);
-  int64_t round = steps;
+static void dense_rounds(int64_t P, int32_t K, int64_t* steps, int64_t* round) {
+  *steps = std::max<int64_t>(ceil_div(P / 4, kDenseSpan), 1);
+  *round = *steps;
   if (K > 0) {
     int dev = 0, cus = 0, per_cu = 0;
     if (hipGetDevice(&dev) == hipSuccess &&
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
         hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, aggregate_dense_kernel<MODE, CARRY>, kSumBlock, 0) ==
             hipSuccess &&
-        cus > 0 && per_cu > 0 && steps > 2 * kDenseRoundsPerLaunch * (int64_t)cus * per_cu)
-      round = kDenseRoundsPerLaunch * (int64_t)cus * per_cu;
+        cus > 0 && per_cu > 0 && *steps > 2 * kDenseRoundsPerLaunch * (int64_t)cus * per_cu)
+      *round = kDenseRoundsPerLaunch * (int64_t)cus * per_cu;
   }
+}
+
+template <int MODE, bool CARRY>
+static hipError_t launch_dense_mode(const float* const* grads, const float* w, int32_t K, int64_t P,
+                                    float* out, const DenseState& st, double* run, double denom, int reset,
+                                    hipStream_t stream) {
+  if (P <= 0) return hipSuccess;
+  // one block step per block; unaligned buffers fall back to a grid-stride
+  // loop over single elements in the first launch
+  int64_t steps = 0, round = 0;
+  dense_rounds<MODE, CARRY>(P, K, &steps, &round);
   for (int64_t s0 = 0; s0 < steps; s0 += round) {
     const int64_t s1 = std::min(steps, s0 + round);
     const int64_t blocks = std::min(s1 - s0, kDenseMaxBlocks);
@@ -258,6 +266,18 @@ static hipError_t launch_dense_mode(const float* const* grads, const float* w, i
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
+}
+
+int64_t dense_launch_count(int64_t P, int32_t K, int opt) {
+  if (P <= 0) return 0;
+  int64_t steps = 0, round = 0;
+  switch (opt) {
+    case 1: dense_rounds<kApplyAdagrad, false>(P, K, &steps, &round); break;
+    case 2: dense_rounds<kApplyAdam, false>(P, K, &steps, &round); break;
+    case 3: dense_rounds<kAccumulate, true>(P, K, &steps, &round); break;
+    default: dense_rounds<kStoreOnly, false>(P, K, &steps, &round); break;
+  }
+  return ceil_div(steps, round);
 }
 
 hipError_t launch_aggregate_dense(const float* const* grads, const float* w, int32_t K, int64_t P,

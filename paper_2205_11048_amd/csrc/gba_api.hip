@@ -71,6 +71,13 @@ gba_status gba_aggregate_dense(const float* const* grads, const float* w, int32_
   return from_hip(launch_aggregate_dense(grads, w, K, P, out, stream));
 }
 
+gba_status gba_aggregate_dense_launches(int64_t P, int32_t K, int32_t opt, int64_t* launches) {
+  if (!launches) return GBA_ERR_NULL;
+  if (K < 1 || K > GBA_MAX_K || P < 0 || opt < 0 || opt > 3) return GBA_ERR_INVALID_ARG;
+  *launches = dense_launch_count(P, K, opt);
+  return GBA_OK;
+}
+
 gba_status gba_aggregate_apply_dense_adagrad(const float* const* grads, const float* w, int32_t K,
                                              int64_t P, float* out, float* param, float* accum, double lr,
                                              double eps, hipStream_t stream) {

@@ -17,6 +17,9 @@ hipError_t launch_token_weights(const int64_t* tokens, int32_t K, int64_t step, 
                                 hipStream_t stream);
 
 // ---- dense weighted sum / N_a (Alg. 2)
+// Kernel launches one dense call makes (opt: 0 sum only, 1 fused Adagrad,
+// 2 fused Adam, 3 early accumulation), on the current device.
+int64_t dense_launch_count(int64_t P, int32_t K, int opt);
 hipError_t launch_aggregate_dense(const float* const* grads, const float* w, int32_t K, int64_t P,
                                   float* out, hipStream_t stream);
 

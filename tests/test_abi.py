@@ -60,6 +60,15 @@ def test_host_checks_return_before_any_launch():
                             None, None) == 2
 
 
+def test_dense_launch_query_host_checks():
+    L = gba.lib()
+    assert L.gba_aggregate_dense_launches(10, 3, 0, None) == 1
+    for bad in [(10, 0, 0), (-1, 3, 0), (10, 3, 4), (10, 3, -1)]:
+        with pytest.raises(gba.GBAError):
+            gba.gba_aggregate_dense_launches(*bad)
+    assert gba.gba_aggregate_dense_launches(0, 3) == 0
+
+
 def test_token_of_batch_host_function():
     """The token rule is a host function of the library: no GPU needed."""
     import oracle

@@ -83,6 +83,10 @@ def test_aggregate_dense_launched_in_rounds():
     out = torch.empty(P, dtype=torch.float32, device=DEV)
     gba.gba_aggregate_dense(gba.pointer_table([dev(g) for g in grads]), dev(w), P, out)
     assert_exact(host(out), ref, "g_bar")
+    steps = -(-(P // 4) // 8192)
+    assert 1 < gba.gba_aggregate_dense_launches(P, K) <= steps
+    assert gba.gba_aggregate_dense_launches(100_000, K) == 1
+    assert gba.gba_aggregate_dense_launches(0, K) == 0
 
 
 def test_aggregate_dense_unaligned_and_fractional_weights():
