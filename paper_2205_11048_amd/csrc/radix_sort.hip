@@ -41,7 +41,10 @@ template <int ITEMS>
 constexpr int64_t tile_keys() { return (int64_t)kSortBlock * ITEMS; }
 constexpr int kRadix = 256;
 constexpr int kXcds = 8;   // MI355X: 8 accelerator dies, each with its own L2
-constexpr int kChunk = kSortWaves;                     // tiles per chunk: one hist block
+constexpr int kHistTilesPerWave = 4;
+// tiles per chunk (one hist block): four per wave, so the digit scans read a
+// sixteenth of a count row per tile
+constexpr int kChunk = kSortWaves * kHistTilesPerWave;
 
 // Hot-key plan.
 constexpr int kHotSample = 16384;      // sampled positions (one block sorts them in LDS)
@@ -401,7 +404,7 @@ sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n_arg, const uin
                       int shift, int bits, int64_t R, uint32_t* __restrict__ hist, uint32_t* __restrict__ chunk,
                       HotTables ht, int32_t* __restrict__ err) {
   constexpr bool HOT = MODE == kHotFirst;
-  __shared__ uint32_t h[kSortWaves][kRadix];
+  __shared__ uint32_t h[kChunk][kRadix];
   __shared__ uint32_t s_bucket_w[HOT ? kHotBuckets / 2 : 1];   // uint16 entries
   __shared__ uint32_t s_ids[HOT ? 256 : 1];
   __shared__ uint32_t s_iv[HOT ? kRadix : 1];
@@ -410,7 +413,9 @@ sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n_arg, const uin
   const int64_t tiles = ceil_div(n, tile_keys<ITEMS>());
   const int w = threadIdx.x / kWave;
   const int lane = lane_id();
-  for (int i = lane; i < kRadix; i += kWave) h[w][i] = 0u;
+#pragma unroll
+  for (int k = 0; k < kHistTilesPerWave; ++k)
+    for (int i = lane; i < kRadix; i += kWave) h[w * kHistTilesPerWave + k][i] = 0u;
   HotLookup hl{s_bucket, s_ids, 0u, ht.bshift};
   uint32_t cold_bins = 0;
   if (HOT) {
@@ -422,17 +427,20 @@ sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n_arg, const uin
   } else {
     __builtin_amdgcn_wave_barrier();
   }
-  const int64_t tile = (int64_t)blockIdx.x * kSortWaves + w;
+  // wave w counts the chunk's tiles w * kHistTilesPerWave + k, each into its own row
   bool bad = false;
-  if (tile < tiles) {
+  for (int k = 0; k < kHistTilesPerWave; ++k) {
+    const int r = w * kHistTilesPerWave + k;
+    const int64_t tile = (int64_t)blockIdx.x * kChunk + r;
+    if (tile >= tiles) break;
     const uint32_t mask = (1u << bits) - 1u;
     const int64_t tile0 = tile * tile_keys<ITEMS>();
     if (tile0 + tile_keys<ITEMS>() <= n)
-      bad = count_tile<FIRST, ITEMS, true, HOT>(keys_in, n, tile0, shift, mask, R, h[w], lane, hl, cold_bins, s_iv,
-                                                ht.digit);
+      bad |= count_tile<FIRST, ITEMS, true, HOT>(keys_in, n, tile0, shift, mask, R, h[r], lane, hl, cold_bins, s_iv,
+                                                 ht.digit);
     else
-      bad = count_tile<FIRST, ITEMS, false, HOT>(keys_in, n, tile0, shift, mask, R, h[w], lane, hl, cold_bins,
-                                                 s_iv, ht.digit);
+      bad |= count_tile<FIRST, ITEMS, false, HOT>(keys_in, n, tile0, shift, mask, R, h[r], lane, hl, cold_bins,
+                                                  s_iv, ht.digit);
   }
   __syncthreads();
   // the block's tiles form one chunk: each tile's row holds the counts of the
@@ -440,10 +448,10 @@ sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n_arg, const uin
   // rows), and the chunk row holds the chunk's counts
   {
     const int d = threadIdx.x;
-    const int64_t t0 = (int64_t)blockIdx.x * kSortWaves;
+    const int64_t t0 = (int64_t)blockIdx.x * kChunk;
     uint32_t s = 0;
 #pragma unroll
-    for (int k = 0; k < kSortWaves; ++k) {
+    for (int k = 0; k < kChunk; ++k) {
       if (t0 + k < tiles) hist[(t0 + k) * kRadix + d] = s;
       s += h[k][d];
     }
