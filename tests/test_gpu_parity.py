@@ -288,6 +288,35 @@ def test_sparse_hot_ids_crowded_in_one_bucket(decay):
     _check_sparse(res, ids, rows, off, w, tokens, 1000, 2, tag, decay, expect_exact=True)
 
 
+@pytest.mark.parametrize("K", [256, 300])
+@pytest.mark.parametrize("D", [16, 32])
+@pytest.mark.parametrize("norm", ["per_id_count", "by_k"])
+def test_sparse_means_for_every_count(K, D, norm):
+    """ID r lies in contributions 0..r, so the per-ID counts c_r run through
+    1..K (through the table of reciprocals when K <= 256, past it when K = 300);
+    dyadic rows make the sums exact, so the means match only if every quotient
+    is correctly rounded."""
+    ids_l, sizes = [], []
+    for m in range(K):
+        r = np.arange(m, K, dtype=np.int64)
+        dup = r[(r + m) % 7 == 0]                 # some IDs twice in one contribution
+        part = np.concatenate([r, dup])
+        np.random.default_rng(m).shuffle(part)
+        ids_l.append(part)
+        sizes.append(part.size)
+    ids = np.concatenate(ids_l)
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    N = ids.size
+    rows = counter.values_range(41, counter.STREAM_ROWS, 0, N * D, counter.KIND_DYADIC, 1.0).reshape(N, D)
+    step, iota = 1000, 3
+    tokens = step - (np.arange(K) % 6)            # contributions with staleness 4 and 5 are excluded
+    w, _, _ = oracle.token_weights(tokens, step, iota)
+    for plan in (None, gba.SORT_HOT):
+        res = _run_sparse(ids, rows, off, w, tokens, step, iota, K, norm=norm, plan=plan)
+        ref = _check_sparse(res, ids, rows, off, w, tokens, step, iota, norm=norm, expect_exact=True)
+        assert_exact(ref["contrib_count"], np.arange(1, K + 1, dtype=np.int32), "c_r = r + 1")
+
+
 def test_sparse_empty():
     K, D = 3, 8
     off = np.zeros(K + 1, np.int64)
