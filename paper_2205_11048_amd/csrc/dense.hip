@@ -8,8 +8,10 @@
 // system sees long contiguous runs per gradient wherever the caller placed
 // the K buffers (short runs from many buffers at once were measured to lose
 // up to 15% of bandwidth to DRAM row conflicts, depending on the buffers'
-// relative addresses).  Each thread accumulates its 16 vectors in float64 in
-// buffer order, so the only rounding is the final one to float.
+// relative addresses).  Where P is too small for such blocks to give every
+// compute unit one, threads take 4 vectors (or 1) instead of 16.  Each thread
+// accumulates its vectors in float64 in buffer order, so the only rounding is
+// the final one to float.
 #include <algorithm>
 
 #include "gba_device.hpp"
@@ -20,8 +22,11 @@ namespace gba {
 
 constexpr int kDenseBlock = 256;                                      // elementwise optimiser kernels
 constexpr int kSumBlock = 512;                                        // the reduction: 8 waves
-constexpr int kDenseVecs = 16;                                        // f32x4 per thread
-constexpr int64_t kDenseSpan = (int64_t)kSumBlock * kDenseVecs;       // vectors per block step
+// f32x4 per thread: 16 (each wave reads 16 KB of one gradient in a row); 4 or
+// 1 where P is too small for 16 to give every compute unit a block
+constexpr int kDenseVecs = 16;
+template <int VECS>
+constexpr int64_t dense_span() { return (int64_t)kSumBlock * VECS; }   // vectors per block step
 constexpr int64_t kDenseMaxBlocks = 65535;
 constexpr int64_t kApplyMaxBlocks = 8192;
 constexpr int64_t kDenseRoundsPerLaunch = 1;                           // rounds of resident blocks per launch
@@ -107,26 +112,26 @@ __device__ __forceinline__ void finish_scalar(const float* const* grads, const u
   }
 }
 
-// Vectors q[j] = vb + 64 j (j < kDenseVecs, q < nvec) are finished: g in
+// Vectors q[j] = vb + 64 j (j < VECS, q < nvec) are finished: g in
 // float first (which frees the float64 sums), then the optimiser, with the
 // state of a whole group of vectors requested at once (16 for Adagrad, 8 for
 // Adam: what fits the registers the sums held), so a block's finishing costs
 // one or two memory latencies, not one per vector.
-template <int MODE>
+template <int MODE, int VECS>
 __device__ __forceinline__ void finish_vectors(const f64x4* acc, double denom, int64_t vb, int64_t nvec,
                                                float* out, const DenseState& st) {
-  f32x4 g[kDenseVecs];
+  f32x4 g[VECS];
 #pragma unroll
-  for (int j = 0; j < kDenseVecs; ++j) g[j] = narrow(acc[j] / denom);
+  for (int j = 0; j < VECS; ++j) g[j] = narrow(acc[j] / denom);
   if (out) {
 #pragma unroll
-    for (int j = 0; j < kDenseVecs; ++j)
+    for (int j = 0; j < VECS; ++j)
       if (vb + kWave * j < nvec) store_stream(reinterpret_cast<f32x4*>(out) + vb + kWave * j, g[j]);
   }
   if (MODE == kStoreOnly) return;
-  constexpr int kGroup = (MODE == kApplyAdam) ? 8 : 16;
+  constexpr int kGroup = (MODE == kApplyAdam) ? (VECS < 8 ? VECS : 8) : VECS;
 #pragma unroll
-  for (int j0 = 0; j0 < kDenseVecs; j0 += kGroup) {
+  for (int j0 = 0; j0 < VECS; j0 += kGroup) {
     f32x4 pv[kGroup], sv[kGroup], vv[kGroup];
 #pragma unroll
     for (int jj = 0; jj < kGroup; ++jj) {
@@ -166,7 +171,7 @@ __device__ __forceinline__ void finish_vectors(const f64x4* acc, double denom, i
 // early weighted sum, CARRY: contributions folded in as they arrive, in
 // arrival order, so the result is bitwise the one-shot sum).  Then the
 // MODE's finishing; with CARRY, `reset` clears run[] for the next step.
-template <int MODE, bool CARRY>
+template <int MODE, bool CARRY, int VECS>
 __global__ void __launch_bounds__(kSumBlock)
 aggregate_dense_kernel(const float* const* __restrict__ grads, const float* __restrict__ w, int K,
                        int64_t P, float* __restrict__ out, DenseState st, double* __restrict__ run,
@@ -184,34 +189,34 @@ aggregate_dense_kernel(const float* const* __restrict__ grads, const float* __re
   if (aligned && outputs_aligned) {
     const int64_t nvec = P / 4;
     for (int64_t s = step0 + blockIdx.x; s < step_end; s += gridDim.x) {
-      const int64_t b0 = s * kDenseSpan;
+      const int64_t b0 = s * dense_span<VECS>();
       // wave w covers vectors [b0 + w * 1024, +1024): lane l takes l, l + 64, ...
-      const int64_t vb = b0 + (int64_t)(threadIdx.x / kWave) * (kWave * kDenseVecs) + (threadIdx.x % kWave);
-      f64x4 acc[kDenseVecs];
+      const int64_t vb = b0 + (int64_t)(threadIdx.x / kWave) * (kWave * VECS) + (threadIdx.x % kWave);
+      f64x4 acc[VECS];
 #pragma unroll
-      for (int j = 0; j < kDenseVecs; ++j) {
+      for (int j = 0; j < VECS; ++j) {
         acc[j] = f64x4{0.0, 0.0, 0.0, 0.0};
         if (CARRY && vb + kWave * j < nvec) acc[j] = reinterpret_cast<const f64x4*>(run)[vb + kWave * j];
       }
       for (int i = 0; i < nk; ++i) {
         const f32x4* g = reinterpret_cast<const f32x4*>(grads[kept[i]]) + vb;
-        f32x4 x[kDenseVecs];
+        f32x4 x[VECS];
 #pragma unroll
-        for (int j = 0; j < kDenseVecs; ++j)
+        for (int j = 0; j < VECS; ++j)
           x[j] = (vb + kWave * j < nvec) ? load_stream(g + kWave * j) : f32x4{0.f, 0.f, 0.f, 0.f};
         const double wi = (double)kw[i];
 #pragma unroll
-        for (int j = 0; j < kDenseVecs; ++j) acc[j] += wi * widen(x[j]);
+        for (int j = 0; j < VECS; ++j) acc[j] += wi * widen(x[j]);
       }
       if (MODE == kAccumulate) {
 #pragma unroll
-        for (int j = 0; j < kDenseVecs; ++j)
+        for (int j = 0; j < VECS; ++j)
           if (vb + kWave * j < nvec) reinterpret_cast<f64x4*>(run)[vb + kWave * j] = acc[j];
       } else {
-        finish_vectors<MODE>(acc, denom, vb, nvec, out, st);
+        finish_vectors<MODE, VECS>(acc, denom, vb, nvec, out, st);
         if (CARRY && reset) {
 #pragma unroll
-          for (int j = 0; j < kDenseVecs; ++j)
+          for (int j = 0; j < VECS; ++j)
             if (vb + kWave * j < nvec) reinterpret_cast<f64x4*>(run)[vb + kWave * j] = f64x4{0.0, 0.0, 0.0, 0.0};
         }
       }
@@ -233,19 +238,53 @@ aggregate_dense_kernel(const float* const* __restrict__ grads, const float* __re
 // blocks drift apart until they read all K buffers at once, which costs
 // bandwidth (DRAM row changes).  K == 0 (finishing a running sum) reads no
 // gradients and takes one launch.
-template <int MODE, bool CARRY>
-static void dense_rounds(int64_t P, int32_t K, int64_t* steps, int64_t* round) {
-  *steps = std::max<int64_t>(ceil_div(P / 4, kDenseSpan), 1);
+template <int MODE, bool CARRY, int VECS>
+static void dense_rounds(int64_t P, int32_t K, int cus, int64_t* steps, int64_t* round) {
+  *steps = std::max<int64_t>(ceil_div(P / 4, dense_span<VECS>()), 1);
   *round = *steps;
-  if (K > 0) {
-    int dev = 0, cus = 0, per_cu = 0;
-    if (hipGetDevice(&dev) == hipSuccess &&
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, aggregate_dense_kernel<MODE, CARRY>, kSumBlock, 0) ==
-            hipSuccess &&
-        cus > 0 && per_cu > 0 && *steps > 2 * kDenseRoundsPerLaunch * (int64_t)cus * per_cu)
-      *round = kDenseRoundsPerLaunch * (int64_t)cus * per_cu;
+  int per_cu = 0;
+  if (K > 0 && cus > 0 &&
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, aggregate_dense_kernel<MODE, CARRY, VECS>, kSumBlock,
+                                                   0) == hipSuccess &&
+      per_cu > 0 && *steps > 2 * kDenseRoundsPerLaunch * (int64_t)cus * per_cu)
+    *round = kDenseRoundsPerLaunch * (int64_t)cus * per_cu;
+}
+
+// Compute units of the current device (0 if unknown).
+static int device_cus() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
+                                              hipSuccess)
+    return 0;
+  return cus;
+}
+
+// Vectors per thread for P elements: the most that still give every compute
+// unit a block step.
+static int dense_vecs(int64_t P, int cus) {
+  const int64_t nvec = P / 4;
+  if (cus <= 0 || ceil_div(nvec, dense_span<kDenseVecs>()) >= cus) return kDenseVecs;
+  if (ceil_div(nvec, dense_span<4>()) >= cus) return 4;
+  return 1;
+}
+
+template <int MODE, bool CARRY, int VECS>
+static hipError_t launch_dense_vecs(const float* const* grads, const float* w, int32_t K, int64_t P, float* out,
+                                    const DenseState& st, double* run, double denom, int reset, int cus,
+                                    hipStream_t stream) {
+  // one block step per block; unaligned buffers fall back to a grid-stride
+  // loop over single elements in the first launch
+  int64_t steps = 0, round = 0;
+  dense_rounds<MODE, CARRY, VECS>(P, K, cus, &steps, &round);
+  for (int64_t s0 = 0; s0 < steps; s0 += round) {
+    const int64_t s1 = std::min(steps, s0 + round);
+    const int64_t blocks = std::min(s1 - s0, kDenseMaxBlocks);
+    hipLaunchKernelGGL((aggregate_dense_kernel<MODE, CARRY, VECS>), dim3((unsigned)blocks), dim3(kSumBlock), 0,
+                       stream, grads, w, (int)K, P, out, st, run, denom, reset, s0, s1);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
   }
+  return hipSuccess;
 }
 
 template <int MODE, bool CARRY>
@@ -253,31 +292,35 @@ static hipError_t launch_dense_mode(const float* const* grads, const float* w, i
                                     float* out, const DenseState& st, double* run, double denom, int reset,
                                     hipStream_t stream) {
   if (P <= 0) return hipSuccess;
-  // one block step per block; unaligned buffers fall back to a grid-stride
-  // loop over single elements in the first launch
-  int64_t steps = 0, round = 0;
-  dense_rounds<MODE, CARRY>(P, K, &steps, &round);
-  for (int64_t s0 = 0; s0 < steps; s0 += round) {
-    const int64_t s1 = std::min(steps, s0 + round);
-    const int64_t blocks = std::min(s1 - s0, kDenseMaxBlocks);
-    hipLaunchKernelGGL((aggregate_dense_kernel<MODE, CARRY>), dim3((unsigned)blocks), dim3(kSumBlock), 0, stream,
-                       grads, w, (int)K, P, out, st, run, denom, reset, s0, s1);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+  const int cus = device_cus();
+  switch (dense_vecs(P, cus)) {
+    case 1: return launch_dense_vecs<MODE, CARRY, 1>(grads, w, K, P, out, st, run, denom, reset, cus, stream);
+    case 4: return launch_dense_vecs<MODE, CARRY, 4>(grads, w, K, P, out, st, run, denom, reset, cus, stream);
+    default:
+      return launch_dense_vecs<MODE, CARRY, kDenseVecs>(grads, w, K, P, out, st, run, denom, reset, cus, stream);
   }
-  return hipSuccess;
+}
+
+template <int MODE, bool CARRY>
+static int64_t launch_count(int64_t P, int32_t K) {
+  const int cus = device_cus();
+  int64_t steps = 0, round = 0;
+  switch (dense_vecs(P, cus)) {
+    case 1: dense_rounds<MODE, CARRY, 1>(P, K, cus, &steps, &round); break;
+    case 4: dense_rounds<MODE, CARRY, 4>(P, K, cus, &steps, &round); break;
+    default: dense_rounds<MODE, CARRY, kDenseVecs>(P, K, cus, &steps, &round); break;
+  }
+  return ceil_div(steps, round);
 }
 
 int64_t dense_launch_count(int64_t P, int32_t K, int opt) {
   if (P <= 0) return 0;
-  int64_t steps = 0, round = 0;
   switch (opt) {
-    case 1: dense_rounds<kApplyAdagrad, false>(P, K, &steps, &round); break;
-    case 2: dense_rounds<kApplyAdam, false>(P, K, &steps, &round); break;
-    case 3: dense_rounds<kAccumulate, true>(P, K, &steps, &round); break;
-    default: dense_rounds<kStoreOnly, false>(P, K, &steps, &round); break;
+    case 1: return launch_count<kApplyAdagrad, false>(P, K);
+    case 2: return launch_count<kApplyAdam, false>(P, K);
+    case 3: return launch_count<kAccumulate, true>(P, K);
+    default: return launch_count<kStoreOnly, false>(P, K);
   }
-  return ceil_div(steps, round);
 }
 
 hipError_t launch_aggregate_dense(const float* const* grads, const float* w, int32_t K, int64_t P,
