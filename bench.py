@@ -52,6 +52,8 @@ def parse():
                     help="run the dense path on a second stream, concurrently with the sparse path")
     ap.add_argument("--separate-dense", action="store_true",
                     help="dense sum and dense optimiser as two calls instead of the fused one")
+    ap.add_argument("--separate-sparse", action="store_true",
+                    help="sparse aggregation and row apply as two calls instead of the fused one")
     ap.add_argument("--early-sum", default="16",
                     help="comma list of J: also time the step with the dense sum taken early, J arriving "
                          "contributions folded per call ('' for none)")
@@ -172,6 +174,27 @@ def run_workload(name, args, torch, gba_step_mod, sdev, gba):
             ev["d2"].record(dstream)
         if ev is not None:
             ev["s0"].record(stream)
+        if not args.separate_sparse:
+            # one call: the rows are applied as the aggregation finishes them
+            # (agg kept only where the row width takes the separate apply)
+            agg = None if st.fuses_rows else st.agg
+            sparse = (ds.ids, ds.rows, ds.offsets, w.R, st.w, ds.tokens, ds.step, w.iota, ds.tags, decay,
+                      gba.NORM_PER_ID_COUNT, st.unique_ids, st.seg_offsets, st.contrib_count, st.active_count, agg,
+                      st.num_unique)
+            if w.optimizer == "adagrad":
+                gba.gba_aggregate_apply_sparse_adagrad(*sparse, ds.table, ds.table_slots[0], w.lr, w.eps,
+                                                       st.workspace, st.err, **kw)
+            else:
+                gba.gba_aggregate_apply_sparse_adam(*sparse, ds.table, ds.table_slots[0], ds.table_slots[1], w.lr,
+                                                    w.beta1, w.beta2, w.eps, w.adam_t, st.workspace, st.err, **kw)
+            if ev is not None:
+                ev["s1"].record(stream)
+                ev["s2"].record(stream)
+            if args.overlap:
+                d_done = torch.cuda.Event()
+                d_done.record(dstream)
+                stream.wait_event(d_done)
+            return
         gba.gba_aggregate_sparse(ds.ids, ds.rows, ds.offsets, w.R, st.w, ds.tokens, ds.step, w.iota,
                                  ds.tags, decay, gba.NORM_PER_ID_COUNT, st.unique_ids, st.seg_offsets,
                                  st.contrib_count, st.active_count, st.agg, st.num_unique, st.workspace,
@@ -214,7 +237,10 @@ def run_workload(name, args, torch, gba_step_mod, sdev, gba):
     print(f"[bench] {name}: {args.steps} steps timed", file=sys.stderr, flush=True)
     total_ms = start.elapsed_time(end)
     ms = total_ms / args.steps
-    spans = {"token_weights": ("t0", "t1"), "aggregate_sparse": ("s0", "s1"), "apply_rows": ("s1", "s2")}
+    if args.separate_sparse:
+        spans = {"token_weights": ("t0", "t1"), "aggregate_sparse": ("s0", "s1"), "apply_rows": ("s1", "s2")}
+    else:
+        spans = {"token_weights": ("t0", "t1"), "aggregate_apply_sparse": ("s0", "s1")}
     if args.separate_dense:
         spans.update(aggregate_dense=("d0", "d1"), apply_dense=("d1", "d2"))
     else:
@@ -259,7 +285,7 @@ def run_workload(name, args, torch, gba_step_mod, sdev, gba):
         global_batches_per_s=1000.0 / ms, embedding_grad_rows_per_s=w.N / (ms * 1e-3),
         samples_per_s=w.K * w.B / (ms * 1e-3),
         step_alg_bytes=dense_b + sparse_b, step_alg_gbs=step_gbs, step_frac_of_hbm_peak=step_gbs / HBM_PEAK_GBS,
-        breakdown_ms=breakdown, overlap=args.overlap, fused_dense=not args.separate_dense, K_eff=K_eff, N=w.N, N_act=N_act, U=U, U_act=U_act, setup_s=setup_s,
+        breakdown_ms=breakdown, overlap=args.overlap, fused_dense=not args.separate_dense, fused_sparse=not args.separate_sparse, K_eff=K_eff, N=w.N, N_act=N_act, U=U, U_act=U_act, setup_s=setup_s,
         roofline=dict(kernel=kname, bound="hbm", achieved=dk_gbs, peak=HBM_PEAK_GBS,
                       unit="GB/s", frac=dk_gbs / HBM_PEAK_GBS, traffic=traffic,
                       alg_bytes_per_launch=dense_kernel_bytes, avg_launch_ms=dk_ms, launches_per_call=launches),

@@ -168,6 +168,50 @@ gba_status gba_apply_adam(float* param, float* m, float* v, const float* grad, c
                           int32_t* err, hipStream_t stream);
 
 /*
+ * gba_aggregate_sparse followed by the row form of gba_apply_adagrad /
+ * gba_apply_adam over its active rows (Alg. 2: embeddings are updated by ID
+ * with the per-ID mean; Table 1 names the optimisers), in one call.  Table,
+ * state and every output come out bitwise equal to those of the two separate
+ * calls (the same float64 arithmetic, each stored value rounded once).  For
+ * rows of 20 to 32 floats (16 < D <= 32) the optimiser runs as each ID's segment is
+ * finished, so the mean never makes a round trip through memory; other widths
+ * aggregate first and then apply.
+ * ids ... num_unique   as for gba_aggregate_sparse, except that agg may be
+ *                  NULL (the means are then not stored, or stored in the
+ *                  workspace where they are needed).
+ * table            [R][D] float, the embedding rows, updated in place (only
+ *                  rows with W_r > 0 change).
+ * accum / m, v     [R][D] float optimiser state, updated in place.
+ * lr, eps, beta1, beta2, t   as for gba_apply_adagrad / gba_apply_adam.
+ * workspace        at least gba_aggregate_apply_sparse_workspace_size bytes.
+ * table and state must be 16-byte aligned.  Errors as for
+ * gba_aggregate_sparse; also GBA_ERR_NULL for a missing table or state when
+ * N > 0.
+ */
+gba_status gba_aggregate_apply_sparse_workspace_size(int64_t N, int32_t K, int32_t D, int64_t R,
+                                                     size_t* bytes /* host out */);
+
+gba_status gba_aggregate_apply_sparse_adagrad(const int64_t* ids, const float* rows,
+                                              const int64_t* contrib_offsets, int32_t K, int64_t N,
+                                              int32_t D, int64_t R, const float* w, const int64_t* tokens,
+                                              int64_t step, int64_t iota, int32_t* tag, gba_decay decay,
+                                              gba_norm norm, int64_t* unique_ids, int64_t* seg_offsets,
+                                              int32_t* contrib_count, int32_t* active_count, float* agg,
+                                              int64_t* num_unique, float* table, float* accum, double lr,
+                                              double eps, void* workspace, size_t workspace_bytes,
+                                              int32_t* err, hipStream_t stream);
+
+gba_status gba_aggregate_apply_sparse_adam(const int64_t* ids, const float* rows,
+                                           const int64_t* contrib_offsets, int32_t K, int64_t N, int32_t D,
+                                           int64_t R, const float* w, const int64_t* tokens, int64_t step,
+                                           int64_t iota, int32_t* tag, gba_decay decay, gba_norm norm,
+                                           int64_t* unique_ids, int64_t* seg_offsets, int32_t* contrib_count,
+                                           int32_t* active_count, float* agg, int64_t* num_unique,
+                                           float* table, float* m, float* v, double lr, double beta1,
+                                           double beta2, double eps, int64_t t, void* workspace,
+                                           size_t workspace_bytes, int32_t* err, hipStream_t stream);
+
+/*
  * gba_aggregate_dense followed by the dense form of gba_apply_adagrad /
  * gba_apply_adam, in one pass over memory (Alg. 2: the weighted sum of the
  * dense gradients divided by K, then the Table 1 optimiser on the dense

@@ -60,6 +60,13 @@ _SIGNATURES = {
                                        _I32),
     "gba_accumulate_dense": ([_P, _P, _I32, _I64, _P, _P], _I32),
     "gba_aggregate_dense_launches": ([_I64, _I32, _I32, ctypes.POINTER(_I64)], _I32),
+    "gba_aggregate_apply_sparse_workspace_size": ([_I64, _I32, _I32, _I64, ctypes.POINTER(ctypes.c_size_t)], _I32),
+    "gba_aggregate_apply_sparse_adagrad": ([_P, _P, _P, _I32, _I64, _I32, _I64, _P, _P, _I64, _I64, _P, _I32, _I32,
+                                            _P, _P, _P, _P, _P, _P, _P, _P, _F64, _F64, _P, ctypes.c_size_t, _P,
+                                            _P], _I32),
+    "gba_aggregate_apply_sparse_adam": ([_P, _P, _P, _I32, _I64, _I32, _I64, _P, _P, _I64, _I64, _P, _I32, _I32,
+                                         _P, _P, _P, _P, _P, _P, _P, _P, _P, _F64, _F64, _F64, _F64, _I64, _P,
+                                         ctypes.c_size_t, _P, _P], _I32),
     "gba_finalize_dense": ([_P, _I32, _I64, _P, _I32, _P], _I32),
     "gba_finalize_apply_dense_adagrad": ([_P, _I32, _I64, _P, _P, _P, _F64, _F64, _I32, _P], _I32),
     "gba_finalize_apply_dense_adam": ([_P, _I32, _I64, _P, _P, _P, _P, _F64, _F64, _F64, _F64, _I64, _I32, _P],
@@ -369,6 +376,51 @@ def gba_aggregate_sparse_plan(ids, rows, contrib_offsets, R, w, tokens, step, io
         int(iota), _ptr(tag), int(decay), int(norm), _ptr(unique_ids), _ptr(seg_offsets),
         _ptr(contrib_count), _ptr(active_count), _ptr(agg), _ptr(num_unique), _ptr(workspace),
         workspace.numel(), int(plan), _ptr(err), _stream(stream)))
+
+
+def gba_aggregate_apply_sparse_workspace_size(N, K, D, R) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib().gba_aggregate_apply_sparse_workspace_size(int(N), int(K), int(D), int(R), ctypes.byref(n)))
+    return int(n.value)
+
+
+def _apply_sparse_args(ids, rows, contrib_offsets, R, w, tokens, tag, unique_ids, seg_offsets, contrib_count,
+                       active_count, agg, num_unique, workspace, err, table, state):
+    N, K, D = _sparse_args(ids, rows, contrib_offsets, R, w, tokens, tag, unique_ids, seg_offsets, contrib_count,
+                           active_count, None, num_unique, workspace, err)
+    _need(agg, torch.float32, "agg", N * D)
+    for name, t in [("table", table)] + state:
+        _need(t, torch.float32, name, int(R) * D)
+    return N, K, D
+
+
+def gba_aggregate_apply_sparse_adagrad(ids, rows, contrib_offsets, R, w, tokens, step, iota, tag, decay, norm,
+                                       unique_ids, seg_offsets, contrib_count, active_count, agg, num_unique,
+                                       table, accum, lr, eps, workspace, err=None, stream=None):
+    """gba_aggregate_sparse + the row form of gba_apply_adagrad in one call; ``agg`` may be None."""
+    N, K, D = _apply_sparse_args(ids, rows, contrib_offsets, R, w, tokens, tag, unique_ids, seg_offsets,
+                                 contrib_count, active_count, agg, num_unique, workspace, err, table,
+                                 [("accum", accum)])
+    _check(lib().gba_aggregate_apply_sparse_adagrad(
+        _ptr(ids), _ptr(rows), _ptr(contrib_offsets), K, N, D, int(R), _ptr(w), _ptr(tokens), int(step),
+        int(iota), _ptr(tag), int(decay), int(norm), _ptr(unique_ids), _ptr(seg_offsets),
+        _ptr(contrib_count), _ptr(active_count), _ptr(agg), _ptr(num_unique), _ptr(table), _ptr(accum),
+        float(lr), float(eps), _ptr(workspace), workspace.numel(), _ptr(err), _stream(stream)))
+
+
+def gba_aggregate_apply_sparse_adam(ids, rows, contrib_offsets, R, w, tokens, step, iota, tag, decay, norm,
+                                    unique_ids, seg_offsets, contrib_count, active_count, agg, num_unique,
+                                    table, m, v, lr, beta1, beta2, eps, t, workspace, err=None, stream=None):
+    """gba_aggregate_sparse + the row form of gba_apply_adam in one call; ``agg`` may be None."""
+    N, K, D = _apply_sparse_args(ids, rows, contrib_offsets, R, w, tokens, tag, unique_ids, seg_offsets,
+                                 contrib_count, active_count, agg, num_unique, workspace, err, table,
+                                 [("m", m), ("v", v)])
+    _check(lib().gba_aggregate_apply_sparse_adam(
+        _ptr(ids), _ptr(rows), _ptr(contrib_offsets), K, N, D, int(R), _ptr(w), _ptr(tokens), int(step),
+        int(iota), _ptr(tag), int(decay), int(norm), _ptr(unique_ids), _ptr(seg_offsets),
+        _ptr(contrib_count), _ptr(active_count), _ptr(agg), _ptr(num_unique), _ptr(table), _ptr(m), _ptr(v),
+        float(lr), float(beta1), float(beta2), float(eps), int(t), _ptr(workspace), workspace.numel(), _ptr(err),
+        _stream(stream)))
 
 
 def gba_apply_adagrad(param, accum, grad, lr, eps, rows=None, active=None, num_rows=None, R=0,

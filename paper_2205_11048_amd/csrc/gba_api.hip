@@ -159,13 +159,15 @@ gba_status gba_aggregate_sparse(const int64_t* ids, const float* rows, const int
                                    workspace_bytes, GBA_SORT_AUTO, err, stream);
 }
 
-gba_status gba_aggregate_sparse_plan(const int64_t* ids, const float* rows, const int64_t* contrib_offsets,
-                                     int32_t K, int64_t N, int32_t D, int64_t R, const float* w,
-                                     const int64_t* tokens, int64_t step, int64_t iota, int32_t* tag,
-                                     gba_decay decay, gba_norm norm, int64_t* unique_ids,
-                                     int64_t* seg_offsets, int32_t* contrib_count, int32_t* active_count,
-                                     float* agg, int64_t* num_unique, void* workspace,
-                                     size_t workspace_bytes, int32_t sort_plan, int32_t* err, hipStream_t stream) {
+// The sparse call behind gba_aggregate_sparse(_plan) and the fused
+// aggregate-and-apply calls: ap (may be null) applies the rows as their
+// segments are finished (agg may then be null).
+static gba_status sparse_call(const int64_t* ids, const float* rows, const int64_t* contrib_offsets, int32_t K,
+                              int64_t N, int32_t D, int64_t R, const float* w, const int64_t* tokens, int64_t step,
+                              int64_t iota, int32_t* tag, gba_decay decay, gba_norm norm, int64_t* unique_ids,
+                              int64_t* seg_offsets, int32_t* contrib_count, int32_t* active_count, float* agg,
+                              int64_t* num_unique, void* workspace, size_t workspace_bytes, int32_t sort_plan,
+                              const RowApply* ap, int32_t* err, hipStream_t stream) {
   if (K < 1 || K > GBA_MAX_K || N < 0 || N > kMaxN || R < 1 || R > (int64_t(1) << 32))
     return GBA_ERR_INVALID_ARG;
   if (sort_plan < -1 || sort_plan > 1) return GBA_ERR_INVALID_ARG;
@@ -174,7 +176,7 @@ gba_status gba_aggregate_sparse_plan(const int64_t* ids, const float* rows, cons
   if (!width_ok(D)) return GBA_ERR_UNSUPPORTED;
   if (!contrib_offsets || !w || !tokens || !seg_offsets || !num_unique || !workspace)
     return GBA_ERR_NULL;
-  if (N > 0 && (!ids || !rows || !unique_ids || !contrib_count || !active_count || !agg))
+  if (N > 0 && (!ids || !rows || !unique_ids || !contrib_count || !active_count || (!agg && !ap)))
     return GBA_ERR_NULL;
   if (decay == GBA_DECAY_ID_TAG) {
     if (!tag) return GBA_ERR_NULL;
@@ -185,9 +187,14 @@ gba_status gba_aggregate_sparse_plan(const int64_t* ids, const float* rows, cons
     return GBA_ERR_INVALID_ARG;
   SortPlan plan;
   const size_t need = sparse_bytes(N, D, R, sort_plan, &plan);
-  if (workspace_bytes < need) return GBA_ERR_WORKSPACE;
+  // a row apply at a width the row pass does not fuse goes through agg, in
+  // the workspace when the caller gives none
+  const bool separate = ap && !segments_fuse_apply(D);
+  const size_t agg_ws = (separate && !agg) ? align_up((size_t)N * D * sizeof(float)) : 0;
+  if (workspace_bytes < need + agg_ws) return GBA_ERR_WORKSPACE;
 
   char* ws = static_cast<char*>(workspace);
+  float* g = agg ? agg : (agg_ws ? reinterpret_cast<float*>(ws + need) : nullptr);
   const uint32_t* keys = nullptr;
   const uint32_t* vals = nullptr;
   // with the hot-key plan the frequent IDs are reduced apart from the rest
@@ -219,10 +226,87 @@ gba_status gba_aggregate_sparse_plan(const int64_t* ids, const float* rows, cons
   a.seg_offsets = seg_offsets;
   a.contrib_count = contrib_count;
   a.active_count = active_count;
-  a.agg = agg;
+  a.agg = g;
   a.num_unique = num_unique;
   a.err = err;
-  return from_hip(launch_segments(a, ws + align_up(plan.bytes), stream));
+  if (ap && !separate) a.ap = *ap;
+  e = launch_segments(a, ws + align_up(plan.bytes), stream);
+  if (e != hipSuccess || !separate || N == 0) return from_hip(e);
+  // the rows apply after the aggregation, over the active distinct IDs
+  if (ap->mode == 2)
+    e = launch_rows_adam(ap->p, ap->s1, ap->s2, g, unique_ids, active_count, num_unique, N, D, R,
+                         AdamParams{ap->lr, ap->beta1, ap->beta2, ap->eps, ap->bc1, ap->bc2}, err, stream);
+  else
+    e = launch_rows_adagrad(ap->p, ap->s1, g, unique_ids, active_count, num_unique, N, D, R, ap->lr, ap->eps, err,
+                            stream);
+  return from_hip(e);
+}
+
+gba_status gba_aggregate_sparse_plan(const int64_t* ids, const float* rows, const int64_t* contrib_offsets,
+                                     int32_t K, int64_t N, int32_t D, int64_t R, const float* w,
+                                     const int64_t* tokens, int64_t step, int64_t iota, int32_t* tag,
+                                     gba_decay decay, gba_norm norm, int64_t* unique_ids,
+                                     int64_t* seg_offsets, int32_t* contrib_count, int32_t* active_count,
+                                     float* agg, int64_t* num_unique, void* workspace,
+                                     size_t workspace_bytes, int32_t sort_plan, int32_t* err, hipStream_t stream) {
+  return sparse_call(ids, rows, contrib_offsets, K, N, D, R, w, tokens, step, iota, tag, decay, norm, unique_ids,
+                     seg_offsets, contrib_count, active_count, agg, num_unique, workspace, workspace_bytes, sort_plan,
+                     nullptr, err, stream);
+}
+
+gba_status gba_aggregate_apply_sparse_workspace_size(int64_t N, int32_t K, int32_t D, int64_t R, size_t* bytes) {
+  const gba_status st = gba_aggregate_sparse_workspace_size(N, K, D, R, bytes);
+  if (st == GBA_OK && !segments_fuse_apply(D)) *bytes += align_up((size_t)N * D * sizeof(float));
+  return st;
+}
+
+gba_status gba_aggregate_apply_sparse_adagrad(const int64_t* ids, const float* rows, const int64_t* contrib_offsets,
+                                              int32_t K, int64_t N, int32_t D, int64_t R, const float* w,
+                                              const int64_t* tokens, int64_t step, int64_t iota, int32_t* tag,
+                                              gba_decay decay, gba_norm norm, int64_t* unique_ids,
+                                              int64_t* seg_offsets, int32_t* contrib_count, int32_t* active_count,
+                                              float* agg, int64_t* num_unique, float* table, float* accum,
+                                              double lr, double eps, void* workspace, size_t workspace_bytes,
+                                              int32_t* err, hipStream_t stream) {
+  if (N > 0 && (!table || !accum)) return GBA_ERR_NULL;
+  if ((table && !aligned16(table)) || (accum && !aligned16(accum))) return GBA_ERR_INVALID_ARG;
+  RowApply ap;
+  ap.mode = 1;
+  ap.p = table;
+  ap.s1 = accum;
+  ap.lr = lr;
+  ap.eps = eps;
+  return sparse_call(ids, rows, contrib_offsets, K, N, D, R, w, tokens, step, iota, tag, decay, norm, unique_ids,
+                     seg_offsets, contrib_count, active_count, agg, num_unique, workspace, workspace_bytes,
+                     GBA_SORT_AUTO, &ap, err, stream);
+}
+
+gba_status gba_aggregate_apply_sparse_adam(const int64_t* ids, const float* rows, const int64_t* contrib_offsets,
+                                           int32_t K, int64_t N, int32_t D, int64_t R, const float* w,
+                                           const int64_t* tokens, int64_t step, int64_t iota, int32_t* tag,
+                                           gba_decay decay, gba_norm norm, int64_t* unique_ids,
+                                           int64_t* seg_offsets, int32_t* contrib_count, int32_t* active_count,
+                                           float* agg, int64_t* num_unique, float* table, float* m, float* v,
+                                           double lr, double beta1, double beta2, double eps, int64_t t,
+                                           void* workspace, size_t workspace_bytes, int32_t* err, hipStream_t stream) {
+  if (!adam_args_ok(beta1, beta2, t)) return GBA_ERR_INVALID_ARG;
+  if (N > 0 && (!table || !m || !v)) return GBA_ERR_NULL;
+  if ((table && !aligned16(table)) || (m && !aligned16(m)) || (v && !aligned16(v))) return GBA_ERR_INVALID_ARG;
+  const AdamParams hp = adam_params(lr, beta1, beta2, eps, t);
+  RowApply ap;
+  ap.mode = 2;
+  ap.p = table;
+  ap.s1 = m;
+  ap.s2 = v;
+  ap.lr = hp.lr;
+  ap.eps = hp.eps;
+  ap.beta1 = hp.beta1;
+  ap.beta2 = hp.beta2;
+  ap.bc1 = hp.bc1;
+  ap.bc2 = hp.bc2;
+  return sparse_call(ids, rows, contrib_offsets, K, N, D, R, w, tokens, step, iota, tag, decay, norm, unique_ids,
+                     seg_offsets, contrib_count, active_count, agg, num_unique, workspace, workspace_bytes,
+                     GBA_SORT_AUTO, &ap, err, stream);
 }
 
 gba_status gba_sort_ids_workspace_size(int64_t n, int64_t R, int32_t plan, size_t* bytes) {

@@ -96,6 +96,17 @@ hipError_t launch_sort_ids(const int64_t* ids, int64_t n, int64_t R, const SortP
                            hipStream_t stream, SortHot* split = nullptr);
 
 // ---- segments over the sorted keys: dedup, counts, decayed weighted sums
+// Fused row apply: the optimiser runs on each active row (W_r > 0) as its
+// segment is finished, with the same arithmetic as the separate row apply,
+// instead of the mean making a round trip through agg.
+struct RowApply {
+  int mode = 0;          // 0 none, 1 Adagrad, 2 Adam
+  float* p = nullptr;    // [R][D] table
+  float* s1 = nullptr;   // [R][D] Adagrad accumulator or Adam m
+  float* s2 = nullptr;   // [R][D] Adam v
+  double lr = 0.0, eps = 0.0, beta1 = 0.0, beta2 = 0.0, bc1 = 1.0, bc2 = 1.0;
+};
+
 struct SegmentArgs {
   const uint32_t* keys;        // sorted IDs [N]
   const uint32_t* vals;        // occurrence index of each sorted entry [N]
@@ -119,8 +130,12 @@ struct SegmentArgs {
   // ID order.  Null n_dev: keys/vals hold all N occurrences.
   const uint32_t* n_dev = nullptr;
   SortHot hot;
+  RowApply ap;            // mode 0: agg is written and no row is applied
 };
 size_t segments_workspace_bytes(int64_t N, int32_t D);
+// Whether launch_segments can apply the rows itself (ap.mode != 0) at width D;
+// other widths take the aggregation followed by the separate row apply.
+bool segments_fuse_apply(int32_t D);
 hipError_t launch_segments(const SegmentArgs& a, void* ws, hipStream_t stream);
 
 // ---- runs of equal keys in sorted keys[N]: per 1024-position tile, the number

@@ -30,6 +30,7 @@
 // segment logic) and finished by hot_finish, both in a fixed order.
 #include "gba_device.hpp"
 #include "gba_internal.hpp"
+#include "optim.hpp"
 
 namespace gba {
 
@@ -194,13 +195,58 @@ __device__ __forceinline__ int contribution_global(const int64_t* off, int K, ui
   return m < 0 ? 0 : (m < K ? m : K - 1);
 }
 
-// out: the segment's place among all distinct IDs
+// The optimiser on one lane's 4 floats of a row, with the row apply's
+// arithmetic (float64, one rounding per stored value).
+template <int MODE>
+__device__ __forceinline__ void optimise4(const RowApply& ap, f32x4& pv, f32x4& s1, f32x4& s2, f32x4 g) {
+  float pe[4] = {pv.x, pv.y, pv.z, pv.w}, ae[4] = {s1.x, s1.y, s1.z, s1.w};
+  const float ge[4] = {g.x, g.y, g.z, g.w};
+  if (MODE == 2) {
+    float ve[4] = {s2.x, s2.y, s2.z, s2.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) adam_update(pe[e], ae[e], ve[e], ge[e], ap.lr, ap.beta1, ap.beta2, ap.eps, ap.bc1, ap.bc2);
+    s2 = f32x4{ve[0], ve[1], ve[2], ve[3]};
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) adagrad_update(pe[e], ae[e], ge[e], ap.lr, ap.eps);
+  }
+  pv = f32x4{pe[0], pe[1], pe[2], pe[3]};
+  s1 = f32x4{ae[0], ae[1], ae[2], ae[3]};
+}
+
+// Row r updated with mean g (one lane's 16 bytes): load, optimise, store.
+__device__ __forceinline__ void apply_row_part(const RowApply& ap, int64_t r, int D, int lane, f32x4 g) {
+  const int64_t at = r * D + lane * 4;
+  f32x4 pv = load_stream(reinterpret_cast<const f32x4*>(ap.p + at));
+  f32x4 s1 = load_stream(reinterpret_cast<const f32x4*>(ap.s1 + at));
+  f32x4 s2 = {0.f, 0.f, 0.f, 0.f};
+  if (ap.mode == 2) {
+    s2 = load_stream(reinterpret_cast<const f32x4*>(ap.s2 + at));
+    optimise4<2>(ap, pv, s1, s2, g);
+    store_stream(reinterpret_cast<f32x4*>(ap.s2 + at), s2);
+  } else {
+    optimise4<1>(ap, pv, s1, s2, g);
+  }
+  store_stream(reinterpret_cast<f32x4*>(ap.p + at), pv);
+  store_stream(reinterpret_cast<f32x4*>(ap.s1 + at), s1);
+}
+
+// out: the segment's place among all distinct IDs.  The mean goes to agg
+// (when given) and, with a row apply (mode != 0; a constant in the row pass),
+// into the optimiser update of row `row`, or where row < 0 of the ID the
+// position pass wrote for this place (written by an earlier launch).
 __device__ __forceinline__ void finalize_segment(const SegmentArgs& a, int64_t seg, f64x4 acc,
-                                                 int cc, int ww, int lane, bool lane_on) {
+                                                 int cc, int ww, int lane, bool lane_on, int mode,
+                                                 int64_t row = -1) {
   if (seg < 0 || seg >= a.N) return;   // unreachable when the numbering is consistent
   const double div = (a.norm == GBA_NORM_BY_K) ? (double)a.K : (double)cc;
-  if (lane_on)
-    store_stream(reinterpret_cast<f32x4*>(a.agg + seg * (int64_t)a.D + lane * 4), narrow(div_rounded(acc, div)));   // read once, by the apply
+  const f32x4 g = narrow(div_rounded(acc, div));
+  if (lane_on && a.agg)
+    store_stream(reinterpret_cast<f32x4*>(a.agg + seg * (int64_t)a.D + lane * 4), g);   // read once, by the apply
+  if (mode != 0 && lane_on && ww > 0) {
+    const int64_t r = row >= 0 ? row : a.unique_ids[seg];
+    if (r >= 0 && r < a.R) apply_row_part(a.ap, r, a.D, lane, g);   // always in range when the numbering is consistent
+  }
   if (lane == 0) {
     a.contrib_count[seg] = cc;
     a.active_count[seg] = ww;
@@ -555,33 +601,37 @@ seg_meta_kernel(SegmentArgs a, const uint32_t* __restrict__ tile_seg_base,
   }
 }
 
-// Per-group pass: gather the kept rows and sum every run in float64.
-template <int LPR>
+// Per-group pass: gather the kept rows and sum every run in float64.  APPLY
+// (1 Adagrad, 2 Adam; 32-float rows only) updates each finished segment's row
+// in the table as well.
+template <int LPR, int APPLY>
 __global__ void __launch_bounds__(kSegBlock)
 seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32_t* __restrict__ base32,
                 SegPartials part, const uint32_t* __restrict__ seg_start, const uint32_t* __restrict__ cnum) {
   constexpr int GW = kWave / LPR;            // groups per wave
   constexpr int G = kSegWaves * GW;          // groups per block
   constexpr int64_t TILE = (int64_t)G * kGroupSpan;
-  // With several groups per wave, a segment that closes is parked in LDS
-  // (its float64 sums, place and counts) in the wave's next free slot, and
-  // when the slots run low the wave finishes the parked segments together:
-  // the division, the narrowing and the row stores run with every lane busy,
-  // GW rows per store, instead of in each group as its segments close while
-  // the other groups' lanes idle.
-  constexpr bool kPark = LPR == 8;
-  constexpr int kParkCap = 3 * GW;   // slots per wave
-  __shared__ f64x4 s_park[kPark ? kSegWaves : 1][kPark ? kParkCap : 1][LPR];
-  __shared__ uint32_t s_park_out[kPark ? kSegWaves : 1][kParkCap];
-  __shared__ uint32_t s_park_cw[kPark ? kSegWaves : 1][kParkCap];
+  // With one lane per 16 bytes of a 32-float row (eight groups of eight lanes
+  // per wave), a segment that closes inside a batch is parked in LDS (its
+  // row, place and counts, one slot per group and batch position) and the
+  // wave writes the batch's parked segments together afterwards, eight rows
+  // per store with every lane busy, instead of each group storing as its
+  // segments close while the other groups' lanes idle.
+  // With a row apply the parked segment also keeps its row (its ID), and the
+  // wave updates the batch's rows together: the table and state rows of
+  // several rounds of parked segments are requested before the first is used.
+  constexpr bool kPark = LPR == 8 && GW == kBatch;
+  static_assert(APPLY == 0 || kPark, "the row apply is fused where segments are parked");
+  constexpr int kSlots = GW * kBatch;
+  __shared__ f32x4 s_park[kPark ? kSegWaves : 1][kPark ? kSlots : 1][LPR];
+  __shared__ uint32_t s_park_out[kPark ? kSegWaves : 1][kSlots];
+  __shared__ uint32_t s_park_cw[kPark ? kSegWaves : 1][kSlots];
+  __shared__ uint32_t s_park_list[kPark ? kSegWaves : 1][kSlots];
+  __shared__ uint32_t s_park_key[APPLY ? kSegWaves : 1][APPLY ? kSlots : 1];
   // per-lane chain sums at the end of the groups: in the parking area of the
   // lane's own wave when parking (free by then), else their own array
   static_assert(!kPark || sizeof(s_park[0]) >= kWave * sizeof(f64x4), "chain sums fit a wave's parking area");
   __shared__ f64x4 s_acc_own[kPark ? 1 : kSegBlock];
-  // the sums of the segment each group began inside, held until the chain of
-  // groups before it is known
-  __shared__ f64x4 s_first[kSegBlock];
-  __shared__ int32_t s_fcc[G], s_fww[G];
   auto s_acc_at = [&](int t) -> f64x4& {
     if (kPark) return reinterpret_cast<f64x4*>(&s_park[t / kWave][0][0])[t % kWave];
     return s_acc_own[t];
@@ -627,43 +677,11 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
     uint32_t hnext = hb < H ? s_cnum[hb] : 0xffffffffu;   // positions (and segments) stay below 2^32 - 1
     bool first_open = false;
     bool in_first = true;
+    f64x4 facc = {0.0, 0.0, 0.0, 0.0};
+    int fcc = 0, fww = 0;
     bool owner = false;
-    int pbase = 0;   // parked segments of the wave (the same in every lane)
-    auto hold_first = [&]() {
-      if (lane_on) s_first[threadIdx.x] = acc;
-      if (gl == 0) {
-        s_fcc[grp] = cc;
-        s_fww[grp] = ww;
-      }
-      owner = true;
-    };
-    // The wave's parked segments: each group finishes one per round.
-    auto flush = [&]() {
-      __builtin_amdgcn_wave_barrier();
-      for (int b = 0; b < pbase; b += GW) {
-        const int e = b + lane / LPR;
-        if (e < pbase) {
-          const int64_t out = s_park_out[w][e];
-          const uint32_t v = s_park_cw[w][e];
-          const int c = (int)(v & 0xffffu);
-          if (out < N) {   // always true when the numbering is consistent
-            if (lane_on) {
-              const double div = by_k ? (double)a.K : (double)c;
-              // a segment has at most K contributions: the table covers every count when K is small
-              const double y = by_k ? recip_k : (small_k ? s_recip[c < kRecipMax ? c : kRecipMax] : 1.0 / div);
-              store_stream(reinterpret_cast<f32x4*>(a.agg + out * D + gl * 4),
-                           narrow(div_rounded(s_park[w][e][gl], div, y)));
-            }
-            if (gl == 0) {
-              a.contrib_count[out] = c;
-              a.active_count[out] = (int32_t)(v >> 16);
-            }
-          }
-        }
-      }
-      __builtin_amdgcn_wave_barrier();   // the slots are reused
-      pbase = 0;
-    };
+    uint32_t parked = 0;   // batch positions at which a segment of this group was parked
+    uint32_t cur_key = (APPLY && nvalid > 0) ? a.keys[p0] : 0u;   // row of the open segment (row apply)
     // Words of the batch at i0 (the packed array is padded by a group span, so
     // whole vectors stay in bounds past the group's end).
     auto load_words = [&](int i0, uint32_t (&word)[kBatch]) {
@@ -673,6 +691,21 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
       for (int v = 0; v < kBatch / 4; ++v) {
         const u32x4 x = wp[v];
         word[4 * v] = x.x; word[4 * v + 1] = x.y; word[4 * v + 2] = x.z; word[4 * v + 3] = x.w;
+      }
+    };
+    // Keys of the batch at i0, for the row apply (zero past the sorted positions).
+    auto load_keys = [&](int i0, uint32_t (&kk)[kBatch]) {
+      const int64_t pk = (i0 < nvalid) ? p0 + i0 : 0;
+      if (pk + kBatch <= n) {
+        const u32x4* kp = reinterpret_cast<const u32x4*>(a.keys + pk);
+#pragma unroll
+        for (int v = 0; v < kBatch / 4; ++v) {
+          const u32x4 x = kp[v];
+          kk[4 * v] = x.x; kk[4 * v + 1] = x.y; kk[4 * v + 2] = x.z; kk[4 * v + 3] = x.w;
+        }
+      } else {
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) kk[u] = (pk + u < n) ? a.keys[pk + u] : 0u;
       }
     };
     // Every lane issues all of a batch's gathers: one whose row is not needed
@@ -690,7 +723,8 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
         rv[u] = *reinterpret_cast<const f32x4*>(a.rows + (on ? (int64_t)jv * D + gl * 4 : 0));
       }
     };
-    auto sum_batch = [&](int i0, const uint32_t (&word)[kBatch], f32x4 (&rv)[kBatch], uint32_t use) {
+    auto sum_batch = [&](int i0, const uint32_t (&word)[kBatch], const uint32_t (&kk)[kBatch], f32x4 (&rv)[kBatch],
+                         uint32_t use) {
 #pragma unroll
       for (int u = 0; u < kBatch; ++u)
         if (!((use >> u) & 1u)) rv[u] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -707,31 +741,30 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
         // keep each row's float64 widening next to its use: hoisting all of
         // them costs registers and the waves that keep gathers in flight
         __builtin_amdgcn_sched_barrier(0);
-        // parking: a free slot for every group, the groups' slots numbered in
-        // group order (both wave-wide, so outside the branches below)
-        uint64_t pm = 0;
-        if (kPark) {
-          if (pbase + GW > kParkCap) flush();
-          pm = __ballot(i < nvalid && (word[u] & kHead) && i > 0 && !(in_first && first_open));
-        }
         if (i < nvalid) {
           if (word[u] & kHead) {
             if (i > 0) {
               if (in_first && first_open) {
-                hold_first();
+                facc = acc; fcc = cc; fww = ww; owner = true;
               } else if (kPark) {
-                const int slot = pbase + (__popcll(pm & lanemask_lt()) / LPR);
-                if (lane_on) s_park[w][slot][gl] = acc;
+                const int slot = (lane / LPR) * kBatch + u;
+                const double div = by_k ? (double)a.K : (double)cc;
+                // a segment has at most K contributions: the table covers every count when K is small
+                const double y = by_k ? recip_k : (small_k ? s_recip[cc] : 1.0 / div);
+                if (lane_on) s_park[w][slot][gl] = narrow(div_rounded(acc, div, y));
                 if (gl == 0) {
                   s_park_out[w][slot] = (uint32_t)(seg + hb);
                   s_park_cw[w][slot] = (uint32_t)cc | ((uint32_t)ww << 16);
+                  if (APPLY) s_park_key[w][slot] = cur_key;
                 }
+                parked |= 1u << u;
               } else {
-                finalize_segment(a, seg + hb, acc, cc, ww, gl, lane_on);
+                finalize_segment(a, seg + hb, acc, cc, ww, gl, lane_on, APPLY);
               }
               in_first = false;
             }
             ++seg;
+            if (APPLY) cur_key = kk[u];
             if ((uint32_t)seg >= hnext) {
               do ++hb; while (hb < H && (int64_t)s_cnum[hb] <= seg);
               hnext = hb < H ? s_cnum[hb] : 0xffffffffu;
@@ -752,11 +785,80 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
           cc += nc;
           ww += (nc && !zero) ? 1 : 0;
         }
-        if (kPark) pbase += __popcll(pm) / LPR;
       }
     };
+    // The parked segments of a batch, written by the whole wave: lane L
+    // stands for slot L (group L / 8, batch position L % 8).
+    auto flush = [&]() {
+      const bool mine = (parked >> gl) & 1u;
+      const uint64_t m = __ballot(mine);
+      if (mine) s_park_list[w][__popcll(m & lanemask_lt())] = (uint32_t)lane;
+      __builtin_amdgcn_wave_barrier();
+      const int E = __popcll(m);
+      if (APPLY) {
+        // kR rounds at a time: the table and state rows of all their active
+        // segments are requested, then updated (an inactive or missing one
+        // reads row 0 and is not written)
+        constexpr int kR = APPLY == 2 ? 2 : 4;
+        for (int b = 0; b < E; b += kR * GW) {
+          f32x4 pv[kR], sv[kR], vv[kR];
+          uint32_t slot[kR];
+          int64_t outv[kR], row[kR];
+          bool act[kR];
+#pragma unroll
+          for (int r = 0; r < kR; ++r) {
+            const int e = b + r * GW + lane / LPR;
+            slot[r] = e < E ? s_park_list[w][e] : 0u;
+            outv[r] = e < E ? (int64_t)s_park_out[w][slot[r]] : N;   // out < N when the numbering is consistent
+            act[r] = outv[r] < N && (s_park_cw[w][slot[r]] >> 16) > 0 && lane_on &&
+                     (int64_t)s_park_key[w][slot[r]] < a.R;   // sorted keys are below R
+            row[r] = act[r] ? (int64_t)s_park_key[w][slot[r]] : 0;
+            const int64_t at = row[r] * D + gl * 4;
+            pv[r] = load_stream(reinterpret_cast<const f32x4*>(a.ap.p + at));
+            sv[r] = load_stream(reinterpret_cast<const f32x4*>(a.ap.s1 + at));
+            if (APPLY == 2) vv[r] = load_stream(reinterpret_cast<const f32x4*>(a.ap.s2 + at));
+          }
+#pragma unroll
+          for (int r = 0; r < kR; ++r) {
+            if (outv[r] >= N) continue;
+            const f32x4 g = s_park[w][slot[r]][gl];
+            if (lane_on && a.agg) store_stream(reinterpret_cast<f32x4*>(a.agg + outv[r] * D + gl * 4), g);
+            if (gl == 0) {
+              const uint32_t v = s_park_cw[w][slot[r]];
+              a.contrib_count[outv[r]] = (int32_t)(v & 0xffffu);
+              a.active_count[outv[r]] = (int32_t)(v >> 16);
+            }
+            if (act[r]) {
+              const int64_t at = row[r] * D + gl * 4;
+              optimise4<APPLY>(a.ap, pv[r], sv[r], vv[r], g);
+              store_stream(reinterpret_cast<f32x4*>(a.ap.p + at), pv[r]);
+              store_stream(reinterpret_cast<f32x4*>(a.ap.s1 + at), sv[r]);
+              if (APPLY == 2) store_stream(reinterpret_cast<f32x4*>(a.ap.s2 + at), vv[r]);
+            }
+          }
+        }
+      } else {
+        for (int b = 0; b < E; b += GW) {
+          const int e = b + lane / LPR;
+          if (e < E) {
+            const uint32_t slot = s_park_list[w][e];
+            const int64_t out = s_park_out[w][slot];
+            if (out < N) {   // always true when the numbering is consistent
+              if (lane_on) store_stream(reinterpret_cast<f32x4*>(a.agg + out * D + gl * 4), s_park[w][slot][gl]);
+              if (gl == 0) {
+                const uint32_t v = s_park_cw[w][slot];
+                a.contrib_count[out] = (int32_t)(v & 0xffffu);
+                a.active_count[out] = (int32_t)(v >> 16);
+              }
+            }
+          }
+        }
+      }
+      __builtin_amdgcn_wave_barrier();   // the next batch reuses the slots
+      parked = 0;
+    };
     // every group of a wave runs the wave's longest group's batches, so the
-    // parking decisions are taken by the whole wave
+    // flush sees the whole wave
     int iters = nvalid;
     if (kPark) {
 #pragma unroll
@@ -766,15 +868,16 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
       }
     }
     for (int i0 = 0; i0 < iters; i0 += kBatch) {
-      uint32_t word[kBatch];
+      uint32_t word[kBatch], kk[kBatch];
       load_words(i0, word);
+      if (APPLY) load_keys(i0, kk);
       if (i0 == 0) first_open = !(word[0] & kHead);
       f32x4 rv[kBatch];
       uint32_t use;
       gather(i0, word, rv, use);
-      sum_batch(i0, word, rv, use);
+      sum_batch(i0, word, kk, rv, use);
+      if (kPark) flush();
     }
-    if (kPark && pbase > 0) flush();   // before the parking area holds the chain sums
 
     bool last_open = false, pass = false;
     if (nvalid > 0) {
@@ -788,9 +891,9 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
           s_seg[grp] = (uint32_t)seg;
         }
       } else if (in_first && first_open) {
-        hold_first();
+        facc = acc; fcc = cc; fww = ww; owner = true;
       } else {
-        finalize_segment(a, seg + hb, acc, cc, ww, gl, lane_on);
+        finalize_segment(a, seg + hb, acc, cc, ww, gl, lane_on, APPLY);
       }
     }
     if (gl == 0) s_flags[grp] = (nvalid > 0 ? kValid : 0u) | (last_open ? kOpen : 0u) | (pass ? kPass : 0u);
@@ -798,8 +901,8 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
 
     // a group whose first run began before it closes the chain of runs
     if (owner) {
-      f64x4 tot = lane_on ? s_first[threadIdx.x] : f64x4{0.0, 0.0, 0.0, 0.0};
-      int tcc = s_fcc[grp], tww = s_fww[grp];
+      f64x4 tot = facc;
+      int tcc = fcc, tww = fww;
       bool from_prev_tile = true;
       for (int gg = grp - 1; gg >= 0; --gg) {
         tot += s_acc_at(gg * LPR + gl);
@@ -817,7 +920,7 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
           part.first_ww[tile] = tww;
         }
       } else {
-        finalize_segment(a, (int64_t)gbase - 1 + hb0, tot, tcc, tww, gl, lane_on);
+        finalize_segment(a, (int64_t)gbase - 1 + hb0, tot, tcc, tww, gl, lane_on, APPLY);
       }
     }
     // the chain that runs into the next tile
@@ -901,7 +1004,7 @@ seg_fixup_kernel(SegmentArgs a, SegPartials part) {
         tcc += s_cc[g];
         tww += s_ww[g];
       }
-      finalize_segment(a, seg + hb, tot, tcc, tww, lane, lane_on);
+      finalize_segment(a, seg + hb, tot, tcc, tww, lane, lane_on, a.ap.mode);
     }
     __syncthreads();   // s_acc is rewritten for the next listed tile
   }
@@ -1129,7 +1232,7 @@ hot_finish_kernel(SegmentArgs a, HotPartials hp, const uint32_t* __restrict__ cn
     }
     const int64_t out = (int64_t)h + cnum[h];
     if (out < a.N) {   // always true when the numbering is consistent
-      finalize_segment(a, out, tot, tc, ta, lane, lane_on);
+      finalize_segment(a, out, tot, tc, ta, lane, lane_on, a.ap.mode, (int64_t)key);
       if (lane == 0) {
         a.unique_ids[out] = key;
         a.seg_offsets[out] = (int64_t)below_all + a.hot.prefix[h];
@@ -1169,8 +1272,18 @@ static hipError_t launch_rows(const SegmentArgs& a, const uint32_t* packed, cons
                               SegPartials part, const uint32_t* seg_start, const uint32_t* cnum, HotPartials hp,
                               const int32_t* buckets, int q, int nb, const SegLayout& L, hipStream_t stream) {
   const int64_t tiles = L.row_tiles;
-  hipLaunchKernelGGL(seg_rows_kernel<LPR>, dim3((unsigned)tiles), dim3(kSegBlock), 0, stream, a, packed,
-                     base32, part, seg_start, cnum);
+  const dim3 grid((unsigned)tiles), block(kSegBlock);
+  if constexpr (LPR == 8) {
+    if (a.ap.mode == 1)
+      hipLaunchKernelGGL((seg_rows_kernel<LPR, 1>), grid, block, 0, stream, a, packed, base32, part, seg_start, cnum);
+    else if (a.ap.mode == 2)
+      hipLaunchKernelGGL((seg_rows_kernel<LPR, 2>), grid, block, 0, stream, a, packed, base32, part, seg_start, cnum);
+    else
+      hipLaunchKernelGGL((seg_rows_kernel<LPR, 0>), grid, block, 0, stream, a, packed, base32, part, seg_start, cnum);
+  } else {
+    if (a.ap.mode != 0) return hipErrorInvalidValue;   // the caller applies the rows separately at this width
+    hipLaunchKernelGGL((seg_rows_kernel<LPR, 0>), grid, block, 0, stream, a, packed, base32, part, seg_start, cnum);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // the listed tiles (at most all of them) are spread over a fixed grid
@@ -1187,6 +1300,8 @@ static hipError_t launch_rows(const SegmentArgs& a, const uint32_t* packed, cons
   }
   return hipSuccess;
 }
+
+bool segments_fuse_apply(int32_t D) { return lanes_per_row(D) == 8; }
 
 hipError_t launch_segments(const SegmentArgs& a, void* ws, hipStream_t stream) {
   const SegLayout L = seg_layout(a.N, a.D);

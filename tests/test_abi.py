@@ -96,3 +96,16 @@ def test_sort_workspace_query_and_host_checks():
             gba.gba_sort_ids_workspace_size(*bad)
     assert L.gba_sort_ids(None, 10, 100, 0, None, None, None, 0, None, None) == 1
     assert L.gba_sort_ids(None, 10, 100, 5, None, None, None, 0, None, None) == 2
+
+
+def test_fused_sparse_host_checks():
+    L = gba.lib()
+    # a missing table with occurrences to apply is refused before any launch
+    assert L.gba_aggregate_apply_sparse_adagrad(None, None, None, 3, 10, 32, 100, None, None, 0, 0, None, 0, 0,
+                                                None, None, None, None, None, None, None, None, 0.1, 0.0, None, 0,
+                                                None, None) == 1
+    assert L.gba_aggregate_apply_sparse_adam(None, None, None, 3, 10, 32, 100, None, None, 0, 0, None, 0, 0, None,
+                                             None, None, None, None, None, None, None, None, 0.1, 1.5, 0.9, 0.0, 1,
+                                             None, 0, None, None) == 2
+    with pytest.raises(gba.GBAError):
+        gba.gba_aggregate_apply_sparse_workspace_size(10, 0, 32, 100)

@@ -38,7 +38,7 @@ def test_full_size(name, decay):
            offsets=ds.offsets, param=ds.param, dense_slots=ds.dense_slots, table=ds.table,
            table_slots=ds.table_slots, optimizer=w.optimizer, lr=w.lr, eps=w.eps, beta1=w.beta1,
            beta2=w.beta2, t=w.adam_t, tag=ds.tags,
-           decay=gba.DECAY_ID_TAG if decay == "id_tag" else gba.DECAY_TOKEN)
+           decay=gba.DECAY_ID_TAG if decay == "id_tag" else gba.DECAY_TOKEN, keep_agg=True)
     torch.cuda.synchronize()
     assert int(st.err.item()) == 0
 

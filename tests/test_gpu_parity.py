@@ -11,6 +11,7 @@ import paper_2205_11048_amd as gba
 from compare import assert_exact, assert_rule_t, exact_fraction
 from paper_2205_11048_amd.step import GBAStep
 from synth import counter, workload
+from synth import device as sdev
 from synth.configs import BY_NAME
 
 pytestmark = pytest.mark.gpu
@@ -489,11 +490,16 @@ def test_apply_rows_out_of_range_is_reported():
 
 
 # ------------------------------------------------------------ whole step
-@pytest.mark.parametrize("fused_dense", [True, False])
+@pytest.mark.parametrize("fused", [(True, True), (False, False), (True, False), (False, True)])
+@pytest.mark.parametrize("D", [16, 32])
 @pytest.mark.parametrize("decay", ["token", "id_tag"])
 @pytest.mark.parametrize("opt", ["adagrad", "adam"])
-def test_full_step_small(decay, opt, fused_dense):
-    c = BY_NAME["c0"].scaled(optimizer=opt, lr=0.01 if opt == "adagrad" else 1e-3)
+def test_full_step_small(decay, opt, D, fused):
+    """The whole step against the oracle, with the dense and the sparse calls
+    each fused or separate; D = 32 takes the row pass that applies the rows
+    itself, D = 16 the aggregation followed by the row apply."""
+    fused_dense, fused_sparse = fused
+    c = BY_NAME["c0"].scaled(optimizer=opt, lr=0.01 if opt == "adagrad" else 1e-3, D=D)
     hs = workload.host_step(c)
     stepper = GBAStep(c.K, c.N, c.D, c.R, c.P)
     grads = [dev(g) for g in hs.grads]
@@ -504,7 +510,8 @@ def test_full_step_small(decay, opt, fused_dense):
     stepper.run(tokens=dev(hs.tokens), step=hs.step, iota=c.iota, grads=grads, ids=dev(hs.ids),
                 rows=dev(hs.rows), offsets=dev(hs.offsets), param=param, dense_slots=dslots, table=table,
                 table_slots=tslots, optimizer=opt, lr=c.lr, eps=c.eps, t=c.adam_t, tag=tag,
-                decay=gba.DECAY_ID_TAG if decay == "id_tag" else gba.DECAY_TOKEN, fused_dense=fused_dense)
+                decay=gba.DECAY_ID_TAG if decay == "id_tag" else gba.DECAY_TOKEN, fused_dense=fused_dense,
+                fused_sparse=fused_sparse)
     hp = dict(lr=c.lr, eps=c.eps, beta1=c.beta1, beta2=c.beta2)
     ref = oracle.gba_step(hs.tokens, hs.step, c.iota, hs.grads, hs.ids, hs.rows, hs.offsets, hs.param,
                           hs.dense_slots, lambda r: hs.table[r], lambda k, r: hs.table_slots[k][r], opt, hp,
@@ -539,6 +546,122 @@ def test_sparse_fractional_token_weights(D, plan):
     w = np.array([1.0, 0.5, 0.0, 0.25, 0.0], np.float32)
     res = _run_sparse(ids, rows, off, w, tokens, 1000, 2, 800, plan=plan)
     _check_sparse(res, ids, rows, off, w, tokens, 1000, 2, expect_exact=True)
+
+
+# ------------------------------------------ fused sparse aggregate + row apply
+def _sparse_step(d_ids, d_rows, d_off, d_w, d_tok, step, iota, R, tag, decay, opt, fused, keep_agg, table0,
+                 slots0):
+    """One sparse step on device inputs, fused or as the two separate calls,
+    from copies of the given table and state."""
+    N, D = d_rows.shape
+    K = d_off.numel() - 1
+    cap = max(N, 1)
+    out = dict(unique_ids=torch.full((cap,), -5, dtype=torch.int64, device=DEV),
+               seg_offsets=torch.full((cap + 1,), -5, dtype=torch.int64, device=DEV),
+               contrib_count=torch.full((cap,), -5, dtype=torch.int32, device=DEV),
+               active_count=torch.full((cap,), -5, dtype=torch.int32, device=DEV),
+               agg=torch.full((cap, D), float("nan"), dtype=torch.float32, device=DEV),
+               num_unique=torch.full((1,), -5, dtype=torch.int64, device=DEV))
+    table = table0.clone()
+    slots = [s.clone() for s in slots0]
+    tag_d = dev(tag) if decay == "id_tag" else None
+    dec = gba.DECAY_ID_TAG if decay == "id_tag" else gba.DECAY_TOKEN
+    err = torch.zeros(1, dtype=torch.int32, device=DEV)
+    lr, eps, b1, b2, t = (0.01, 1e-8, 0.9, 0.999, 1) if opt == "adagrad" else (1e-3, 1e-8, 0.9, 0.999, 1001)
+    common = (d_ids, d_rows, d_off, R, d_w, d_tok, step, iota, tag_d, dec, gba.NORM_PER_ID_COUNT,
+              out["unique_ids"], out["seg_offsets"], out["contrib_count"], out["active_count"])
+    if fused:
+        ws = torch.empty(gba.gba_aggregate_apply_sparse_workspace_size(N, K, D, R), dtype=torch.uint8, device=DEV)
+        agg = out["agg"] if keep_agg else None
+        if opt == "adagrad":
+            gba.gba_aggregate_apply_sparse_adagrad(*common, agg, out["num_unique"], table, slots[0], lr, eps, ws, err)
+        else:
+            gba.gba_aggregate_apply_sparse_adam(*common, agg, out["num_unique"], table, slots[0], slots[1], lr, b1,
+                                                b2, eps, t, ws, err)
+    else:
+        ws = torch.empty(gba.gba_aggregate_sparse_workspace_size(N, K, D, R), dtype=torch.uint8, device=DEV)
+        gba.gba_aggregate_sparse(*common, out["agg"], out["num_unique"], ws, err)
+        rows_kw = dict(rows=out["unique_ids"], active=out["active_count"], num_rows=out["num_unique"], R=R, err=err)
+        if opt == "adagrad":
+            gba.gba_apply_adagrad(table, slots[0], out["agg"], lr, eps, **rows_kw)
+        else:
+            gba.gba_apply_adam(table, slots[0], slots[1], out["agg"], lr, b1, b2, eps, t, **rows_kw)
+    torch.cuda.synchronize()
+    res = {k: host(v) for k, v in out.items()}
+    res.update(table=table, slots=slots, err=int(host(err)[0]), tag=host(tag_d) if tag_d is not None else None)
+    return res
+
+
+def _table_and_state(R, D, opt, seed):
+    table = sdev.fill(torch.empty((R, D), dtype=torch.float32, device=DEV), seed, counter.STREAM_TABLE,
+                      counter.KIND_PARAM)
+    kinds = [counter.KIND_ACCUM] if opt == "adagrad" else [counter.KIND_ADAM_M, counter.KIND_ADAM_V]
+    return table, [sdev.fill(torch.empty((R, D), dtype=torch.float32, device=DEV), seed, 90 + i, k)
+                   for i, k in enumerate(kinds)]
+
+
+@pytest.mark.parametrize("keep_agg", [False, True])
+@pytest.mark.parametrize("D", [8, 20, 32, 64])
+@pytest.mark.parametrize("decay", ["token", "id_tag"])
+@pytest.mark.parametrize("opt", ["adagrad", "adam"])
+def test_fused_sparse_matches_separate_calls(opt, decay, D, keep_agg):
+    """gba_aggregate_apply_sparse_* gives bitwise the table, state and outputs
+    of gba_aggregate_sparse followed by the row apply: D = 20 and 32 update the
+    rows in the row pass, 8 and 64 aggregate and then apply."""
+    K = 12
+    sizes = np.random.default_rng(D).integers(0, 12_000, K)
+    R = 40_000
+    ids, rows, off, tokens, tag = _case(K, sizes, R, D, seed=D + 100)
+    step, iota = 1000, 3
+    w, _, _ = oracle.token_weights(tokens, step, iota)
+    table0, slots0 = _table_and_state(R, D, opt, 5)
+    d_in = (dev(ids), dev(rows), dev(off), dev(w), dev(tokens))
+    sep = _sparse_step(*d_in, step, iota, R, tag, decay, opt, False, True, table0, slots0)
+    fus = _sparse_step(*d_in, step, iota, R, tag, decay, opt, True, keep_agg, table0, slots0)
+    assert sep["err"] == 0 and fus["err"] == 0
+    U = int(sep["num_unique"][0])
+    assert int(fus["num_unique"][0]) == U and U > 1000
+    for k in ("unique_ids", "contrib_count", "active_count"):
+        assert_exact(fus[k][:U], sep[k][:U], k)
+    assert_exact(fus["seg_offsets"][:U + 1], sep["seg_offsets"][:U + 1], "seg_offsets")
+    if keep_agg:
+        assert_exact(fus["agg"][:U], sep["agg"][:U], "agg")
+    assert torch.equal(fus["table"], sep["table"]), "table"
+    for i in range(len(slots0)):
+        assert torch.equal(fus["slots"][i], sep["slots"][i]), f"state {i}"
+    assert not torch.equal(fus["table"], table0)
+    if decay == "id_tag":
+        assert_exact(fus["tag"], sep["tag"], "tag")
+
+
+@pytest.mark.parametrize("opt", ["adagrad", "adam"])
+def test_fused_sparse_large_hot_plan(opt):
+    """Above the size where the automatic sort plan takes frequent IDs apart:
+    the hot IDs' rows are applied where their partial sums are joined."""
+    K, n_m, R, D = 8, 600_000, 3_000_000, 32
+    N = K * n_m
+    rng = np.random.default_rng(77)
+    r = rng.zipf(1.1, N).astype(np.int64) % R
+    ids = (r * 2654435761 + 12345) % R                      # skewed, scrambled over the table
+    off = np.arange(K + 1, dtype=np.int64) * n_m
+    step, iota = 1000, 3
+    tokens = step - rng.integers(0, 6, K)
+    w, _, _ = oracle.token_weights(tokens, step, iota)
+    d_rows = sdev.fill(torch.empty((N, D), dtype=torch.float32, device=DEV), 77, counter.STREAM_ROWS,
+                       counter.KIND_GRAD, float(counter.grad_scale(1e-2)))
+    table0, slots0 = _table_and_state(R, D, opt, 6)
+    assert gba.gba_aggregate_apply_sparse_workspace_size(N, K, D, R) == \
+        gba.gba_aggregate_sparse_plan_workspace_size(N, K, D, R, gba.SORT_HOT)
+    d_in = (dev(ids), d_rows, dev(off), dev(w), dev(tokens))
+    sep = _sparse_step(*d_in, step, iota, R, None, "token", opt, False, True, table0, slots0)
+    fus = _sparse_step(*d_in, step, iota, R, None, "token", opt, True, False, table0, slots0)
+    assert sep["err"] == 0 and fus["err"] == 0
+    U = int(sep["num_unique"][0])
+    assert_exact(fus["unique_ids"][:U], sep["unique_ids"][:U], "unique_ids")
+    assert_exact(fus["active_count"][:U], sep["active_count"][:U], "active_count")
+    assert torch.equal(fus["table"], sep["table"]), "table"
+    for i in range(len(slots0)):
+        assert torch.equal(fus["slots"][i], sep["slots"][i]), f"state {i}"
 
 
 # ------------------------------------------------ fused dense sum + optimiser
