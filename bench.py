@@ -177,7 +177,7 @@ def run_workload(name, args, torch, gba_step_mod, sdev, gba):
         if not args.separate_sparse:
             # one call: the rows are applied as the aggregation finishes them
             # (agg kept only where the row width takes the separate apply)
-            agg = None if st.fuses_rows else st.agg
+            agg = None if st.fuses_rows[w.optimizer] else st.agg
             sparse = (ds.ids, ds.rows, ds.offsets, w.R, st.w, ds.tokens, ds.step, w.iota, ds.tags, decay,
                       gba.NORM_PER_ID_COUNT, st.unique_ids, st.seg_offsets, st.contrib_count, st.active_count, agg,
                       st.num_unique)

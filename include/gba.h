@@ -172,10 +172,10 @@ gba_status gba_apply_adam(float* param, float* m, float* v, const float* grad, c
  * gba_apply_adam over its active rows (Alg. 2: embeddings are updated by ID
  * with the per-ID mean; Table 1 names the optimisers), in one call.  Table,
  * state and every output come out bitwise equal to those of the two separate
- * calls (the same float64 arithmetic, each stored value rounded once).  For
- * rows of 20 to 32 floats (16 < D <= 32) the optimiser runs as each ID's segment is
- * finished, so the mean never makes a round trip through memory; other widths
- * aggregate first and then apply.
+ * calls (the same float64 arithmetic, each stored value rounded once).  With
+ * Adagrad on rows of 20 to 32 floats (16 < D <= 32) the optimiser runs as each
+ * ID's segment is finished, so the mean never makes a round trip through
+ * memory; otherwise (other widths, Adam) the call aggregates and then applies.
  * ids ... num_unique   as for gba_aggregate_sparse, except that agg may be
  *                  NULL (the means are then not stored, or stored in the
  *                  workspace where they are needed).
@@ -183,12 +183,16 @@ gba_status gba_apply_adam(float* param, float* m, float* v, const float* grad, c
  *                  rows with W_r > 0 change).
  * accum / m, v     [R][D] float optimiser state, updated in place.
  * lr, eps, beta1, beta2, t   as for gba_apply_adagrad / gba_apply_adam.
- * workspace        at least gba_aggregate_apply_sparse_workspace_size bytes.
+ * workspace        at least gba_aggregate_apply_sparse_workspace_size bytes
+ *                  for the optimiser (it includes room for the means where
+ *                  they must go through memory and agg is NULL).
  * table and state must be 16-byte aligned.  Errors as for
  * gba_aggregate_sparse; also GBA_ERR_NULL for a missing table or state when
  * N > 0.
  */
+enum { GBA_OPTIMIZER_ADAGRAD = 1, GBA_OPTIMIZER_ADAM = 2 };
 gba_status gba_aggregate_apply_sparse_workspace_size(int64_t N, int32_t K, int32_t D, int64_t R,
+                                                     int32_t optimizer /* GBA_OPTIMIZER_* */,
                                                      size_t* bytes /* host out */);
 
 gba_status gba_aggregate_apply_sparse_adagrad(const int64_t* ids, const float* rows,

@@ -60,7 +60,8 @@ _SIGNATURES = {
                                        _I32),
     "gba_accumulate_dense": ([_P, _P, _I32, _I64, _P, _P], _I32),
     "gba_aggregate_dense_launches": ([_I64, _I32, _I32, ctypes.POINTER(_I64)], _I32),
-    "gba_aggregate_apply_sparse_workspace_size": ([_I64, _I32, _I32, _I64, ctypes.POINTER(ctypes.c_size_t)], _I32),
+    "gba_aggregate_apply_sparse_workspace_size": ([_I64, _I32, _I32, _I64, _I32, ctypes.POINTER(ctypes.c_size_t)],
+                                                  _I32),
     "gba_aggregate_apply_sparse_adagrad": ([_P, _P, _P, _I32, _I64, _I32, _I64, _P, _P, _I64, _I64, _P, _I32, _I32,
                                             _P, _P, _P, _P, _P, _P, _P, _P, _F64, _F64, _P, ctypes.c_size_t, _P,
                                             _P], _I32),
@@ -378,9 +379,15 @@ def gba_aggregate_sparse_plan(ids, rows, contrib_offsets, R, w, tokens, step, io
         workspace.numel(), int(plan), _ptr(err), _stream(stream)))
 
 
-def gba_aggregate_apply_sparse_workspace_size(N, K, D, R) -> int:
+OPTIMIZER_ADAGRAD, OPTIMIZER_ADAM = 1, 2
+
+
+def gba_aggregate_apply_sparse_workspace_size(N, K, D, R, optimizer) -> int:
+    """``optimizer``: "adagrad", "adam" or OPTIMIZER_ADAGRAD / OPTIMIZER_ADAM."""
+    opt = {"adagrad": OPTIMIZER_ADAGRAD, "adam": OPTIMIZER_ADAM}.get(optimizer, optimizer)
     n = ctypes.c_size_t(0)
-    _check(lib().gba_aggregate_apply_sparse_workspace_size(int(N), int(K), int(D), int(R), ctypes.byref(n)))
+    _check(lib().gba_aggregate_apply_sparse_workspace_size(int(N), int(K), int(D), int(R), int(opt),
+                                                           ctypes.byref(n)))
     return int(n.value)
 
 

@@ -189,7 +189,7 @@ static gba_status sparse_call(const int64_t* ids, const float* rows, const int64
   const size_t need = sparse_bytes(N, D, R, sort_plan, &plan);
   // a row apply at a width the row pass does not fuse goes through agg, in
   // the workspace when the caller gives none
-  const bool separate = ap && !segments_fuse_apply(D);
+  const bool separate = ap && !segments_fuse_apply(D, ap->mode);
   const size_t agg_ws = (separate && !agg) ? align_up((size_t)N * D * sizeof(float)) : 0;
   if (workspace_bytes < need + agg_ws) return GBA_ERR_WORKSPACE;
 
@@ -254,9 +254,11 @@ gba_status gba_aggregate_sparse_plan(const int64_t* ids, const float* rows, cons
                      nullptr, err, stream);
 }
 
-gba_status gba_aggregate_apply_sparse_workspace_size(int64_t N, int32_t K, int32_t D, int64_t R, size_t* bytes) {
+gba_status gba_aggregate_apply_sparse_workspace_size(int64_t N, int32_t K, int32_t D, int64_t R, int32_t optimizer,
+                                                     size_t* bytes) {
+  if (optimizer != GBA_OPTIMIZER_ADAGRAD && optimizer != GBA_OPTIMIZER_ADAM) return GBA_ERR_INVALID_ARG;
   const gba_status st = gba_aggregate_sparse_workspace_size(N, K, D, R, bytes);
-  if (st == GBA_OK && !segments_fuse_apply(D)) *bytes += align_up((size_t)N * D * sizeof(float));
+  if (st == GBA_OK && !segments_fuse_apply(D, optimizer)) *bytes += align_up((size_t)N * D * sizeof(float));
   return st;
 }
 
@@ -271,7 +273,7 @@ gba_status gba_aggregate_apply_sparse_adagrad(const int64_t* ids, const float* r
   if (N > 0 && (!table || !accum)) return GBA_ERR_NULL;
   if ((table && !aligned16(table)) || (accum && !aligned16(accum))) return GBA_ERR_INVALID_ARG;
   RowApply ap;
-  ap.mode = 1;
+  ap.mode = GBA_OPTIMIZER_ADAGRAD;
   ap.p = table;
   ap.s1 = accum;
   ap.lr = lr;
@@ -294,7 +296,7 @@ gba_status gba_aggregate_apply_sparse_adam(const int64_t* ids, const float* rows
   if ((table && !aligned16(table)) || (m && !aligned16(m)) || (v && !aligned16(v))) return GBA_ERR_INVALID_ARG;
   const AdamParams hp = adam_params(lr, beta1, beta2, eps, t);
   RowApply ap;
-  ap.mode = 2;
+  ap.mode = GBA_OPTIMIZER_ADAM;
   ap.p = table;
   ap.s1 = m;
   ap.s2 = v;

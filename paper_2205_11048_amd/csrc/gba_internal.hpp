@@ -133,9 +133,11 @@ struct SegmentArgs {
   RowApply ap;            // mode 0: agg is written and no row is applied
 };
 size_t segments_workspace_bytes(int64_t N, int32_t D);
-// Whether launch_segments can apply the rows itself (ap.mode != 0) at width D;
-// other widths take the aggregation followed by the separate row apply.
-bool segments_fuse_apply(int32_t D);
+// Whether launch_segments applies the rows itself for this optimiser (ap.mode)
+// at width D: Adagrad on rows of 20 to 32 floats, where it was measured
+// faster than the aggregation followed by the separate row apply (Adam, with
+// two state rows per update, was measured slower fused).
+bool segments_fuse_apply(int32_t D, int mode);
 hipError_t launch_segments(const SegmentArgs& a, void* ws, hipStream_t stream);
 
 // ---- runs of equal keys in sorted keys[N]: per 1024-position tile, the number

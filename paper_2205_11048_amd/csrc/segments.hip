@@ -1273,15 +1273,13 @@ static hipError_t launch_rows(const SegmentArgs& a, const uint32_t* packed, cons
                               const int32_t* buckets, int q, int nb, const SegLayout& L, hipStream_t stream) {
   const int64_t tiles = L.row_tiles;
   const dim3 grid((unsigned)tiles), block(kSegBlock);
+  if (a.ap.mode != 0 && !segments_fuse_apply(a.D, a.ap.mode)) return hipErrorInvalidValue;   // the caller applies
   if constexpr (LPR == 8) {
     if (a.ap.mode == 1)
       hipLaunchKernelGGL((seg_rows_kernel<LPR, 1>), grid, block, 0, stream, a, packed, base32, part, seg_start, cnum);
-    else if (a.ap.mode == 2)
-      hipLaunchKernelGGL((seg_rows_kernel<LPR, 2>), grid, block, 0, stream, a, packed, base32, part, seg_start, cnum);
     else
       hipLaunchKernelGGL((seg_rows_kernel<LPR, 0>), grid, block, 0, stream, a, packed, base32, part, seg_start, cnum);
   } else {
-    if (a.ap.mode != 0) return hipErrorInvalidValue;   // the caller applies the rows separately at this width
     hipLaunchKernelGGL((seg_rows_kernel<LPR, 0>), grid, block, 0, stream, a, packed, base32, part, seg_start, cnum);
   }
   hipError_t e = hipGetLastError();
@@ -1301,7 +1299,7 @@ static hipError_t launch_rows(const SegmentArgs& a, const uint32_t* packed, cons
   return hipSuccess;
 }
 
-bool segments_fuse_apply(int32_t D) { return lanes_per_row(D) == 8; }
+bool segments_fuse_apply(int32_t D, int mode) { return mode == 1 && lanes_per_row(D) == 8; }
 
 hipError_t launch_segments(const SegmentArgs& a, void* ws, hipStream_t stream) {
   const SegLayout L = seg_layout(a.N, a.D);

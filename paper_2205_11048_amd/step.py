@@ -40,8 +40,9 @@ class GBAStep:
         self.num_unique = torch.zeros(1, dtype=torch.int64, device=dev)
         ws = gba_aggregate_sparse_workspace_size(N, K, D, R)
         # the fused sparse call needs no more workspace where it applies the
-        # rows as it goes; at other widths it goes through agg (ours)
-        self.fuses_rows = gba_aggregate_apply_sparse_workspace_size(N, K, D, R) == ws
+        # rows as it goes; otherwise the means go through agg (ours)
+        self.fuses_rows = {opt: gba_aggregate_apply_sparse_workspace_size(N, K, D, R, opt) == ws
+                           for opt in ("adagrad", "adam")}
         self.workspace = torch.empty(ws, dtype=torch.uint8, device=dev)
         self._grad_table = None
         self._grad_table_key = None
@@ -82,7 +83,7 @@ class GBAStep:
                                stream=stream)
         sparse_tag = tag if decay == DECAY_ID_TAG else None
         if fused_sparse:
-            agg = self.agg if (keep_agg or not self.fuses_rows) else None
+            agg = self.agg if (keep_agg or not self.fuses_rows[optimizer]) else None
             if optimizer == "adagrad":
                 gba_aggregate_apply_sparse_adagrad(ids, rows, offsets, self.R, self.w, tokens, step, iota, sparse_tag,
                                                    decay, norm, self.unique_ids, self.seg_offsets, self.contrib_count,

@@ -108,4 +108,13 @@ def test_fused_sparse_host_checks():
                                              None, None, None, None, None, None, None, None, 0.1, 1.5, 0.9, 0.0, 1,
                                              None, 0, None, None) == 2
     with pytest.raises(gba.GBAError):
-        gba.gba_aggregate_apply_sparse_workspace_size(10, 0, 32, 100)
+        gba.gba_aggregate_apply_sparse_workspace_size(10, 0, 32, 100, "adagrad")
+    with pytest.raises(gba.GBAError):
+        gba.gba_aggregate_apply_sparse_workspace_size(10, 3, 32, 100, 3)
+    # the rows are applied in the row pass for Adagrad at 20-32 floats; else the means need room
+    n = 100_000
+    plain = gba.gba_aggregate_sparse_workspace_size(n, 3, 32, 1000)
+    assert gba.gba_aggregate_apply_sparse_workspace_size(n, 3, 32, 1000, "adagrad") == plain
+    assert gba.gba_aggregate_apply_sparse_workspace_size(n, 3, 32, 1000, "adam") >= plain + n * 32 * 4
+    assert gba.gba_aggregate_apply_sparse_workspace_size(n, 3, 64, 1000, "adagrad") >= \
+        gba.gba_aggregate_sparse_workspace_size(n, 3, 64, 1000) + n * 64 * 4

@@ -571,7 +571,8 @@ def _sparse_step(d_ids, d_rows, d_off, d_w, d_tok, step, iota, R, tag, decay, op
     common = (d_ids, d_rows, d_off, R, d_w, d_tok, step, iota, tag_d, dec, gba.NORM_PER_ID_COUNT,
               out["unique_ids"], out["seg_offsets"], out["contrib_count"], out["active_count"])
     if fused:
-        ws = torch.empty(gba.gba_aggregate_apply_sparse_workspace_size(N, K, D, R), dtype=torch.uint8, device=DEV)
+        ws = torch.empty(gba.gba_aggregate_apply_sparse_workspace_size(N, K, D, R, opt), dtype=torch.uint8,
+                         device=DEV)
         agg = out["agg"] if keep_agg else None
         if opt == "adagrad":
             gba.gba_aggregate_apply_sparse_adagrad(*common, agg, out["num_unique"], table, slots[0], lr, eps, ws, err)
@@ -606,8 +607,9 @@ def _table_and_state(R, D, opt, seed):
 @pytest.mark.parametrize("opt", ["adagrad", "adam"])
 def test_fused_sparse_matches_separate_calls(opt, decay, D, keep_agg):
     """gba_aggregate_apply_sparse_* gives bitwise the table, state and outputs
-    of gba_aggregate_sparse followed by the row apply: D = 20 and 32 update the
-    rows in the row pass, 8 and 64 aggregate and then apply."""
+    of gba_aggregate_sparse followed by the row apply: with Adagrad, D = 20 and
+    32 update the rows in the row pass, 8 and 64 aggregate and then apply (as
+    Adam does at every width)."""
     K = 12
     sizes = np.random.default_rng(D).integers(0, 12_000, K)
     R = 40_000
@@ -650,8 +652,9 @@ def test_fused_sparse_large_hot_plan(opt):
     d_rows = sdev.fill(torch.empty((N, D), dtype=torch.float32, device=DEV), 77, counter.STREAM_ROWS,
                        counter.KIND_GRAD, float(counter.grad_scale(1e-2)))
     table0, slots0 = _table_and_state(R, D, opt, 6)
-    assert gba.gba_aggregate_apply_sparse_workspace_size(N, K, D, R) == \
-        gba.gba_aggregate_sparse_plan_workspace_size(N, K, D, R, gba.SORT_HOT)
+    plain = gba.gba_aggregate_sparse_plan_workspace_size(N, K, D, R, gba.SORT_HOT)
+    fused = gba.gba_aggregate_apply_sparse_workspace_size(N, K, D, R, opt)
+    assert fused == (plain if opt == "adagrad" else plain + N * D * 4)   # Adam's means go through memory
     d_in = (dev(ids), d_rows, dev(off), dev(w), dev(tokens))
     sep = _sparse_step(*d_in, step, iota, R, None, "token", opt, False, True, table0, slots0)
     fus = _sparse_step(*d_in, step, iota, R, None, "token", opt, True, False, table0, slots0)
