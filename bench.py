@@ -266,15 +266,20 @@ def run_workload(name, args, torch, gba_step_mod, sdev, gba):
     # bytes and time over its launches, which split the work evenly but for
     # the last).
     S = 1 if w.optimizer == "adagrad" else 2
+    # vectors per thread of the dense kernel: 16 unless P is too small for
+    # 16 to give every compute unit a block step (4, else 1)
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    nvec = w.P // 4
+    vecs = 16 if -(-nvec // (512 * 16)) >= cus else (4 if -(-nvec // (512 * 4)) >= cus else 1)
     if args.separate_dense:
         dense_call_bytes = K_eff * w.P * 4 + w.P * 4
         call_ms = breakdown["aggregate_dense"]
-        kname = "aggregate_dense_kernel<0, false>"
+        kname = f"aggregate_dense_kernel<0, false, {vecs}>"
         launches = gba.gba_aggregate_dense_launches(w.P, w.K, gba.DENSE_SUM)
     else:
         dense_call_bytes = K_eff * w.P * 4 + (2 + 2 * S) * w.P * 4
         call_ms = breakdown["aggregate_apply_dense"]
-        kname = f"aggregate_dense_kernel<{S}, false>"
+        kname = f"aggregate_dense_kernel<{S}, false, {vecs}>"
         launches = gba.gba_aggregate_dense_launches(w.P, w.K, gba.DENSE_ADAGRAD if S == 1 else gba.DENSE_ADAM)
     dense_kernel_bytes = dense_call_bytes / launches
     dk_ms = call_ms / launches
