@@ -636,8 +636,8 @@ def test_fused_sparse_matches_separate_calls(opt, decay, D, keep_agg):
         assert_exact(fus["tag"], sep["tag"], "tag")
 
 
-@pytest.mark.parametrize("opt", ["adagrad", "adam"])
-def test_fused_sparse_large_hot_plan(opt):
+@pytest.mark.parametrize("opt,decay", [("adagrad", "token"), ("adam", "token"), ("adagrad", "id_tag")])
+def test_fused_sparse_large_hot_plan(opt, decay):
     """Above the size where the automatic sort plan takes frequent IDs apart:
     the hot IDs' rows are applied where their partial sums are joined."""
     K, n_m, R, D = 8, 600_000, 3_000_000, 32
@@ -655,9 +655,10 @@ def test_fused_sparse_large_hot_plan(opt):
     plain = gba.gba_aggregate_sparse_plan_workspace_size(N, K, D, R, gba.SORT_HOT)
     fused = gba.gba_aggregate_apply_sparse_workspace_size(N, K, D, R, opt)
     assert fused == (plain if opt == "adagrad" else plain + N * D * 4)   # Adam's means go through memory
+    tag = workload.tag_values(77, np.arange(R), step) if decay == "id_tag" else None
     d_in = (dev(ids), d_rows, dev(off), dev(w), dev(tokens))
-    sep = _sparse_step(*d_in, step, iota, R, None, "token", opt, False, True, table0, slots0)
-    fus = _sparse_step(*d_in, step, iota, R, None, "token", opt, True, False, table0, slots0)
+    sep = _sparse_step(*d_in, step, iota, R, tag, decay, opt, False, True, table0, slots0)
+    fus = _sparse_step(*d_in, step, iota, R, tag, decay, opt, True, False, table0, slots0)
     assert sep["err"] == 0 and fus["err"] == 0
     U = int(sep["num_unique"][0])
     assert_exact(fus["unique_ids"][:U], sep["unique_ids"][:U], "unique_ids")
@@ -665,6 +666,8 @@ def test_fused_sparse_large_hot_plan(opt):
     assert torch.equal(fus["table"], sep["table"]), "table"
     for i in range(len(slots0)):
         assert torch.equal(fus["slots"][i], sep["slots"][i]), f"state {i}"
+    if decay == "id_tag":
+        assert_exact(fus["tag"], sep["tag"], "tag")
 
 
 # ------------------------------------------------ fused dense sum + optimiser
