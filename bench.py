@@ -411,8 +411,11 @@ def hash_leg(w, ds, st, gba, torch, stream, decay, start, end, n):
     num_rows = torch.zeros(1, dtype=torch.int64, device="cuda")
     rows_of = torch.empty(w.N, dtype=torch.int64, device="cuda")
     hws = torch.empty(gba.gba_hash_workspace_size(w.N), dtype=torch.uint8, device="cuda")
-    sws = torch.empty(gba.gba_aggregate_sparse_workspace_size(w.N, w.K, w.D, pool_rows), dtype=torch.uint8,
-                      device="cuda")
+    # the fused sparse call, agg kept only where the means must go through memory
+    fused_ws = gba.gba_aggregate_apply_sparse_workspace_size(w.N, w.K, w.D, pool_rows, w.optimizer)
+    plain_ws = gba.gba_aggregate_sparse_workspace_size(w.N, w.K, w.D, pool_rows)
+    agg = None if fused_ws == plain_ws else st.agg
+    sws = torch.empty(plain_ws, dtype=torch.uint8, device="cuda")
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
 
     def step(e=None):
@@ -428,16 +431,14 @@ def hash_leg(w, ds, st, gba, torch, stream, decay, start, end, n):
         gba.gba_hash_find_or_insert(slot_ids, slot_rows, ids64, rows_of, num_rows, pool_rows, hws, err=st.err)
         if e is not None:
             e[1].record(stream)
-        gba.gba_aggregate_sparse(rows_of, ds.rows, ds.offsets, pool_rows, st.w, ds.tokens, ds.step, w.iota,
-                                 ds.tags, decay, gba.NORM_PER_ID_COUNT, st.unique_ids, st.seg_offsets,
-                                 st.contrib_count, st.active_count, st.agg, st.num_unique, sws, st.err)
+        sparse = (rows_of, ds.rows, ds.offsets, pool_rows, st.w, ds.tokens, ds.step, w.iota, ds.tags, decay,
+                  gba.NORM_PER_ID_COUNT, st.unique_ids, st.seg_offsets, st.contrib_count, st.active_count, agg,
+                  st.num_unique)
         if w.optimizer == "adagrad":
-            gba.gba_apply_adagrad(ds.table, ds.table_slots[0], st.agg, w.lr, w.eps, rows=st.unique_ids,
-                                  active=st.active_count, num_rows=st.num_unique, R=pool_rows, err=st.err)
+            gba.gba_aggregate_apply_sparse_adagrad(*sparse, ds.table, ds.table_slots[0], w.lr, w.eps, sws, st.err)
         else:
-            gba.gba_apply_adam(ds.table, ds.table_slots[0], ds.table_slots[1], st.agg, w.lr, w.beta1, w.beta2, w.eps,
-                               w.adam_t, rows=st.unique_ids, active=st.active_count, num_rows=st.num_unique,
-                               R=pool_rows, err=st.err)
+            gba.gba_aggregate_apply_sparse_adam(*sparse, ds.table, ds.table_slots[0], ds.table_slots[1], w.lr,
+                                                w.beta1, w.beta2, w.eps, w.adam_t, sws, st.err)
 
     for _ in range(2):
         step()

@@ -39,7 +39,8 @@ constexpr int kSegWaves = kSegBlock / kWave;                 // 4
 constexpr int kRounds = 4;                                   // 16-byte loads per lane in seg_heads
 constexpr int64_t kMetaTile = (int64_t)kSegBlock * kRounds;  // 1024 positions: 4 per thread of a block
 static_assert(kMetaTile == kRunTile, "run-head tiles are the per-position tiles");
-constexpr int kGroupSpan = 128;                              // positions per lane group in seg_rows
+constexpr int kGroupSpan = 128;                              // positions per lane group (most; hot_rows)
+constexpr int kBase32Span = 32;                              // the segment count is kept every 32 positions
 constexpr int kBatch = 8;                                    // row gathers per batch of a group
 constexpr int kMaxBuckets = 1024;                            // contribution lookup buckets
 
@@ -60,8 +61,13 @@ static int lanes_per_row(int D) {
   while (l < 64 && l * 4 < D) l <<= 1;
   return l;
 }
-// positions per seg_rows tile: 4 waves x (64 / LPR) groups x kGroupSpan positions
-static int64_t rows_tile(int lpr) { return (int64_t)kSegWaves * (kWave / lpr) * kGroupSpan; }
+// Positions per lane group of the cold row pass: 128 for large inputs, fewer
+// below, so that a pass over a few million positions still has waves enough
+// to keep the memory busy (each group walks its span in batches, one after
+// the other).
+static int rows_span(int64_t N) { return N >= (int64_t(1) << 25) ? 128 : (N >= (int64_t(1) << 23) ? 64 : 32); }
+// positions per row-pass tile: 4 waves x (64 / LPR) groups x span positions
+static int64_t rows_tile(int lpr, int span) { return (int64_t)kSegWaves * (kWave / lpr) * span; }
 
 // Bucket width 2^q so that at most kMaxBuckets buckets cover [0, N).
 static int bucket_shift(int64_t N) {
@@ -94,7 +100,7 @@ struct SegLayout {
 static SegLayout seg_layout(int64_t N, int32_t D) {
   SegLayout L{};
   L.meta_tiles = N > 0 ? ceil_div(N, kMetaTile) : 1;
-  L.row_tiles = N > 0 ? ceil_div(N, rows_tile(lanes_per_row(D))) : 1;
+  L.row_tiles = N > 0 ? ceil_div(N, rows_tile(lanes_per_row(D), rows_span(N))) : 1;
   const size_t mt = (size_t)L.meta_tiles, rt = (size_t)L.row_tiles;
   const size_t n = (size_t)(N > 0 ? N : 1);
   size_t o = 0;
@@ -103,7 +109,7 @@ static SegLayout seg_layout(int64_t N, int32_t D) {
   L.off_scan = o;      o += align_up(run_heads_workspace_bytes(N));
   L.off_buckets = o;   o += align_up(kMaxBuckets * 4);
   L.off_packed = o;    o += align_up((n + kGroupSpan) * 4);   // padded: whole-group vector loads stay inside
-  L.off_base32 = o;    o += align_up((n / kGroupSpan + 2) * 4);
+  L.off_base32 = o;    o += align_up((n / kBase32Span + 2) * 4);
   L.off_cnt = o;       o += align_up(rt * 16);
   L.off_fix = o;       o += 256 + align_up(rt * 16);  // count, then the list
   L.off_first_acc = o; o += align_up(rt * (size_t)D * 8);
@@ -113,7 +119,7 @@ static SegLayout seg_layout(int64_t N, int32_t D) {
   // per hot ID: the cold segments below it, then the chunk prefix of its run
   L.off_cnum = o;      o += align_up(2 * (kHotSlots + 1) * 4);
   // per chunk of a hot run: float64 sums and (contributions, active, first and last contribution)
-  L.hot_chunks = rt + kHotSlots;
+  L.hot_chunks = (N > 0 ? ceil_div(N, rows_tile(lanes_per_row(D), kGroupSpan)) : 1) + kHotSlots;
   L.off_hot_acc = o;   o += align_up((size_t)L.hot_chunks * D * 8);
   L.off_hot_cnt = o;   o += align_up((size_t)L.hot_chunks * 16);
   L.bytes = o;
@@ -545,7 +551,7 @@ seg_meta_kernel(SegmentArgs a, const uint32_t* __restrict__ tile_seg_base,
     uint32_t before = seg_base + incl - heads;
     for (int k = 0; k < w; ++k) before += s_wave_heads[k];
     // segments that start before each group-aligned position
-    if ((p0 & (kGroupSpan - 1)) == 0 && p0 < n) base32[p0 / kGroupSpan] = before;
+    if ((p0 & (kBase32Span - 1)) == 0 && p0 < n) base32[p0 / kBase32Span] = before;
 #pragma unroll
     for (int e = 0; e < kMetaPer; ++e) {
       if ((head_bits >> e) & 1u) {
@@ -604,13 +610,14 @@ seg_meta_kernel(SegmentArgs a, const uint32_t* __restrict__ tile_seg_base,
 // Per-group pass: gather the kept rows and sum every run in float64.  APPLY
 // (1 Adagrad, 2 Adam; 32-float rows only) updates each finished segment's row
 // in the table as well.
-template <int LPR, int APPLY>
+template <int LPR, int APPLY, int SPAN>
 __global__ void __launch_bounds__(kSegBlock)
 seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32_t* __restrict__ base32,
                 SegPartials part, const uint32_t* __restrict__ seg_start, const uint32_t* __restrict__ cnum) {
   constexpr int GW = kWave / LPR;            // groups per wave
   constexpr int G = kSegWaves * GW;          // groups per block
-  constexpr int64_t TILE = (int64_t)G * kGroupSpan;
+  constexpr int64_t TILE = (int64_t)G * SPAN;
+  static_assert(SPAN % kBatch == 0 && SPAN % kBase32Span == 0 && SPAN <= kGroupSpan, "whole batches per group");
   // With one lane per 16 bytes of a 32-float row (eight groups of eight lanes
   // per wave), a segment that closes inside a batch is parked in LDS (its
   // row, place and counts, one slot per group and batch position) and the
@@ -664,9 +671,9 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
 
   {
     const int64_t tile = blockIdx.x;
-    const int64_t p0 = tile * TILE + (int64_t)grp * kGroupSpan;
-    const int nvalid = (n - p0) >= kGroupSpan ? kGroupSpan : (n - p0 > 0 ? (int)(n - p0) : 0);
-    const uint32_t gbase = nvalid > 0 ? base32[p0 / kGroupSpan] : 0u;
+    const int64_t p0 = tile * TILE + (int64_t)grp * SPAN;
+    const int nvalid = (n - p0) >= SPAN ? SPAN : (n - p0 > 0 ? (int)(n - p0) : 0);
+    const uint32_t gbase = nvalid > 0 ? base32[p0 / kBase32Span] : 0u;
     f64x4 acc = {0.0, 0.0, 0.0, 0.0};
     int cc = 0, ww = 0;
     int64_t seg = (int64_t)gbase - 1;
@@ -881,7 +888,7 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
 
     bool last_open = false, pass = false;
     if (nvalid > 0) {
-      last_open = nvalid == kGroupSpan && (p0 + kGroupSpan) < n && !(packed[p0 + kGroupSpan] & kHead);
+      last_open = nvalid == SPAN && (p0 + SPAN) < n && !(packed[p0 + SPAN] & kHead);
       if (last_open) {
         pass = in_first && first_open;
         s_acc_at(threadIdx.x) = acc;
@@ -1274,14 +1281,24 @@ static hipError_t launch_rows(const SegmentArgs& a, const uint32_t* packed, cons
   const int64_t tiles = L.row_tiles;
   const dim3 grid((unsigned)tiles), block(kSegBlock);
   if (a.ap.mode != 0 && !segments_fuse_apply(a.D, a.ap.mode)) return hipErrorInvalidValue;   // the caller applies
+  const int span = rows_span(a.N);   // the layout's tiles were sized with the same span
+#define GBA_ROWS_SPAN(AP, SP) \
+  hipLaunchKernelGGL((seg_rows_kernel<LPR, AP, SP>), grid, block, 0, stream, a, packed, base32, part, seg_start, cnum)
+#define GBA_ROWS_SPANS(AP)                 \
+  if (span == 128) GBA_ROWS_SPAN(AP, 128); \
+  else if (span == 64) GBA_ROWS_SPAN(AP, 64); \
+  else GBA_ROWS_SPAN(AP, 32);
   if constexpr (LPR == 8) {
-    if (a.ap.mode == 1)
-      hipLaunchKernelGGL((seg_rows_kernel<LPR, 1>), grid, block, 0, stream, a, packed, base32, part, seg_start, cnum);
-    else
-      hipLaunchKernelGGL((seg_rows_kernel<LPR, 0>), grid, block, 0, stream, a, packed, base32, part, seg_start, cnum);
+    if (a.ap.mode == 1) {
+      GBA_ROWS_SPANS(1)
+    } else {
+      GBA_ROWS_SPANS(0)
+    }
   } else {
-    hipLaunchKernelGGL((seg_rows_kernel<LPR, 0>), grid, block, 0, stream, a, packed, base32, part, seg_start, cnum);
+    GBA_ROWS_SPANS(0)
   }
+#undef GBA_ROWS_SPANS
+#undef GBA_ROWS_SPAN
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   // the listed tiles (at most all of them) are spread over a fixed grid
