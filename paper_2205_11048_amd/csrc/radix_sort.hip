@@ -41,10 +41,12 @@ template <int ITEMS>
 constexpr int64_t tile_keys() { return (int64_t)kSortBlock * ITEMS; }
 constexpr int kRadix = 256;
 constexpr int kXcds = 8;   // MI355X: 8 accelerator dies, each with its own L2
-constexpr int kHistTilesPerWave = 4;
-// tiles per chunk (one hist block): four per wave, so the digit scans read a
-// sixteenth of a count row per tile
-constexpr int kChunk = kSortWaves * kHistTilesPerWave;
+// Tiles per chunk (one hist block): one per wave, or four per wave where a
+// pass has tiles enough (the digit scans then read a quarter of the chunk
+// rows, while small passes keep their hist blocks spread over the chip).
+constexpr int kChunk = kSortWaves;                       // the smallest chunk
+constexpr int64_t kWideChunkTiles = 8192;                // tiles from which a pass takes 4 per wave
+static int hist_tiles_per_wave(int64_t tiles) { return tiles >= kWideChunkTiles ? 4 : 1; }
 
 // Hot-key plan.
 constexpr int kHotSample = 16384;      // sampled positions (one block sorts them in LDS)
@@ -398,13 +400,14 @@ __device__ __forceinline__ bool count_tile(const void* __restrict__ keys_in, int
 // one count per run of equal digits among each lane's 4 consecutive keys.
 // kCold reads the key count from n_dev; kHotFirst also writes the chunk's
 // counts of cold keys by the number of hot IDs below them.
-template <bool FIRST, int ITEMS, int MODE>
+template <bool FIRST, int ITEMS, int MODE, int TPW>
 __global__ void __launch_bounds__(kSortBlock)
 sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n_arg, const uint32_t* __restrict__ n_dev,
                       int shift, int bits, int64_t R, uint32_t* __restrict__ hist, uint32_t* __restrict__ chunk,
                       HotTables ht, int32_t* __restrict__ err) {
   constexpr bool HOT = MODE == kHotFirst;
-  __shared__ uint32_t h[kChunk][kRadix];
+  constexpr int kTiles = kSortWaves * TPW;   // the chunk
+  __shared__ uint32_t h[kTiles][kRadix];
   __shared__ uint32_t s_bucket_w[HOT ? kHotBuckets / 2 : 1];   // uint16 entries
   __shared__ uint32_t s_ids[HOT ? 256 : 1];
   __shared__ uint32_t s_iv[HOT ? kRadix : 1];
@@ -414,8 +417,8 @@ sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n_arg, const uin
   const int w = threadIdx.x / kWave;
   const int lane = lane_id();
 #pragma unroll
-  for (int k = 0; k < kHistTilesPerWave; ++k)
-    for (int i = lane; i < kRadix; i += kWave) h[w * kHistTilesPerWave + k][i] = 0u;
+  for (int k = 0; k < TPW; ++k)
+    for (int i = lane; i < kRadix; i += kWave) h[w * TPW + k][i] = 0u;
   HotLookup hl{s_bucket, s_ids, 0u, ht.bshift};
   uint32_t cold_bins = 0;
   if (HOT) {
@@ -427,11 +430,11 @@ sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n_arg, const uin
   } else {
     __builtin_amdgcn_wave_barrier();
   }
-  // wave w counts the chunk's tiles w * kHistTilesPerWave + k, each into its own row
+  // wave w counts the chunk's tiles w * TPW + k, each into its own row
   bool bad = false;
-  for (int k = 0; k < kHistTilesPerWave; ++k) {
-    const int r = w * kHistTilesPerWave + k;
-    const int64_t tile = (int64_t)blockIdx.x * kChunk + r;
+  for (int k = 0; k < TPW; ++k) {
+    const int r = w * TPW + k;
+    const int64_t tile = (int64_t)blockIdx.x * kTiles + r;
     if (tile >= tiles) break;
     const uint32_t mask = (1u << bits) - 1u;
     const int64_t tile0 = tile * tile_keys<ITEMS>();
@@ -448,10 +451,10 @@ sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n_arg, const uin
   // rows), and the chunk row holds the chunk's counts
   {
     const int d = threadIdx.x;
-    const int64_t t0 = (int64_t)blockIdx.x * kChunk;
+    const int64_t t0 = (int64_t)blockIdx.x * kTiles;
     uint32_t s = 0;
 #pragma unroll
-    for (int k = 0; k < kChunk; ++k) {
+    for (int k = 0; k < kTiles; ++k) {
       if (t0 + k < tiles) hist[(t0 + k) * kRadix + d] = s;
       s += h[k][d];
     }
@@ -555,7 +558,7 @@ scatter_tile(const void* __restrict__ keys_in, const uint32_t* __restrict__ vals
              uint32_t* __restrict__ keys_fin, uint32_t* __restrict__ vals_fin, int64_t n_arg,
              const uint32_t* __restrict__ n_dev, int64_t n_total, int shift, int bits, int64_t R,
              const uint32_t* __restrict__ hist, const uint32_t* __restrict__ chunk,
-             const uint32_t* __restrict__ total, const HotTables& ht) {
+             const uint32_t* __restrict__ total, const HotTables& ht, int chunk_shift) {
   constexpr bool HOT = MODE == kHotFirst;
   constexpr bool DYN = MODE == kCold || MODE == kColdLast;
   constexpr bool GAP = MODE == kColdLast;
@@ -580,7 +583,7 @@ scatter_tile(const void* __restrict__ keys_in, const uint32_t* __restrict__ vals
   // after the ranking, where one scan finds both the digit starts and the
   // tile's own digit offsets.
   const int d = threadIdx.x;
-  const uint32_t off = chunk[(tile / kChunk) * kRadix + d] + hist[tile * kRadix + d];
+  const uint32_t off = chunk[(tile >> chunk_shift) * kRadix + d] + hist[tile * kRadix + d];
   const uint32_t tot = total[d];
   // hot bin d (ID d - cold_bins) starts after the cold keys with at most
   // d - cold_bins hot IDs below them: thread d takes column d - cold_bins
@@ -769,9 +772,10 @@ scatter_tile(const void* __restrict__ keys_in, const uint32_t* __restrict__ vals
       uint32_t* __restrict__ vals_out, uint32_t* __restrict__ keys_fin, uint32_t* __restrict__ vals_fin,   \
       int64_t n_arg, const uint32_t* __restrict__ n_dev, int64_t n_total, int shift, int bits, int64_t R,   \
       const uint32_t* __restrict__ hist, const uint32_t* __restrict__ chunk,                               \
-      const uint32_t* __restrict__ total, HotTables ht
-#define GBA_SCATTER_ARGS \
-  keys_in, vals_in, keys_out, vals_out, keys_fin, vals_fin, n_arg, n_dev, n_total, shift, bits, R, hist, chunk, total, ht
+      const uint32_t* __restrict__ total, HotTables ht, int chunk_shift
+#define GBA_SCATTER_ARGS                                                                                         \
+  keys_in, vals_in, keys_out, vals_out, keys_fin, vals_fin, n_arg, n_dev, n_total, shift, bits, R, hist, chunk, total, \
+      ht, chunk_shift
 
 template <bool FIRST, int ITEMS, int MODE>
 __global__ void __launch_bounds__(kSortBlock) sort_scatter_kernel(GBA_SCATTER_PARAMS) {
@@ -866,20 +870,29 @@ hipError_t launch_sort_ids(const int64_t* ids, int64_t n, int64_t R, const SortP
     const void* kin = pass == 0 ? (const void*)ids : (const void*)keys[cur];
     const int64_t tiles = ceil_div(n, pass > 0 ? tile_keys<kItemsRest>()
                                                : (plan.hot ? tile_keys<kItemsHotFirst>() : tile_keys<kItemsFirst>()));
-    const int64_t nchunks = ceil_div(tiles, kChunk);
-    const dim3 grid((unsigned)tiles);
-    if (pass == 0 && plan.hot)
-      hipLaunchKernelGGL((sort_tile_hist_kernel<true, kItemsHotFirst, kHotFirst>), dim3((unsigned)nchunks), block, 0,
-                         stream, kin, n, (const uint32_t*)nullptr, shift, bits, R, hist, chunk, ht, err);
-    else if (pass == 0)
-      hipLaunchKernelGGL((sort_tile_hist_kernel<true, kItemsFirst, kPlain>), dim3((unsigned)nchunks), block, 0,
-                         stream, kin, n, (const uint32_t*)nullptr, shift, bits, R, hist, chunk, ht, err);
-    else if (plan.hot)
-      hipLaunchKernelGGL((sort_tile_hist_kernel<false, kItemsRest, kCold>), dim3((unsigned)nchunks), block, 0,
-                         stream, kin, n, n_cold, shift, bits, R, hist, chunk, ht, err);
-    else
-      hipLaunchKernelGGL((sort_tile_hist_kernel<false, kItemsRest, kPlain>), dim3((unsigned)nchunks), block, 0,
-                         stream, kin, n, (const uint32_t*)nullptr, shift, bits, R, hist, chunk, ht, err);
+    const int tpw = hist_tiles_per_wave(tiles);
+    const int chunk_tiles = kSortWaves * tpw;
+    const int chunk_shift = chunk_tiles == 16 ? 4 : 2;
+    const int64_t nchunks = ceil_div(tiles, chunk_tiles);
+    const dim3 grid((unsigned)tiles), hgrid((unsigned)nchunks);
+#define GBA_HIST(F, IT, MD, NDEV)                                                                            \
+  if (tpw == 4)                                                                                              \
+    hipLaunchKernelGGL((sort_tile_hist_kernel<F, IT, MD, 4>), hgrid, block, 0, stream, kin, n, NDEV, shift, bits, R, \
+                       hist, chunk, ht, err);                                                                \
+  else                                                                                                       \
+    hipLaunchKernelGGL((sort_tile_hist_kernel<F, IT, MD, 1>), hgrid, block, 0, stream, kin, n, NDEV, shift, bits, R, \
+                       hist, chunk, ht, err);
+    static_assert(kSortWaves == 4, "chunk_shift assumes 4 or 16 tiles per chunk");
+    if (pass == 0 && plan.hot) {
+      GBA_HIST(true, kItemsHotFirst, kHotFirst, (const uint32_t*)nullptr)
+    } else if (pass == 0) {
+      GBA_HIST(true, kItemsFirst, kPlain, (const uint32_t*)nullptr)
+    } else if (plan.hot) {
+      GBA_HIST(false, kItemsRest, kCold, n_cold)
+    } else {
+      GBA_HIST(false, kItemsRest, kPlain, (const uint32_t*)nullptr)
+    }
+#undef GBA_HIST
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const bool with_iv = pass == 0 && plan.hot;
     hipLaunchKernelGGL(sort_digit_scan_kernel, dim3(with_iv ? 2 * kRadix : kRadix), block, 0, stream, chunk,
@@ -889,24 +902,25 @@ hipError_t launch_sort_ids(const int64_t* ids, int64_t n, int64_t R, const SortP
     if (pass == 0 && plan.hot)
       hipLaunchKernelGGL(sort_scatter_hot_first_kernel, grid, block, 0, stream, kin, vin,
                          keys[0], vals[0], keys[2], vals[2], n, (const uint32_t*)nullptr, n, shift, bits, R,
-                         (const uint32_t*)hist, (const uint32_t*)chunk, (const uint32_t*)total, ht);
+                         (const uint32_t*)hist, (const uint32_t*)chunk, (const uint32_t*)total, ht, chunk_shift);
     else if (pass == 0)
       hipLaunchKernelGGL((sort_scatter_kernel<true, kItemsFirst, kPlain>), grid, block, 0, stream, kin, vin,
                          keys[0], vals[0], (uint32_t*)nullptr, (uint32_t*)nullptr, n, (const uint32_t*)nullptr, n,
-                         shift, bits, R, (const uint32_t*)hist, (const uint32_t*)chunk, (const uint32_t*)total, ht);
+                         shift, bits, R, (const uint32_t*)hist, (const uint32_t*)chunk, (const uint32_t*)total, ht,
+                         chunk_shift);
     else if (gap)
       hipLaunchKernelGGL((sort_scatter_kernel<false, kItemsRest, kColdLast>), grid, block, 0, stream, kin, vin,
                          keys[out], vals[out], (uint32_t*)nullptr, (uint32_t*)nullptr, n, n_cold, n, shift, bits,
-                         R, (const uint32_t*)hist, (const uint32_t*)chunk, (const uint32_t*)total, ht);
+                         R, (const uint32_t*)hist, (const uint32_t*)chunk, (const uint32_t*)total, ht, chunk_shift);
     else if (plan.hot)
       hipLaunchKernelGGL((sort_scatter_kernel<false, kItemsRest, kCold>), grid, block, 0, stream, kin, vin,
                          keys[out], vals[out], (uint32_t*)nullptr, (uint32_t*)nullptr, n, n_cold, n, shift, bits,
-                         R, (const uint32_t*)hist, (const uint32_t*)chunk, (const uint32_t*)total, ht);
+                         R, (const uint32_t*)hist, (const uint32_t*)chunk, (const uint32_t*)total, ht, chunk_shift);
     else
       hipLaunchKernelGGL((sort_scatter_kernel<false, kItemsRest, kPlain>), grid, block, 0, stream, kin, vin,
                          keys[out], vals[out], (uint32_t*)nullptr, (uint32_t*)nullptr, n, (const uint32_t*)nullptr,
                          n, shift, bits, R, (const uint32_t*)hist, (const uint32_t*)chunk, (const uint32_t*)total,
-                         ht);
+                         ht, chunk_shift);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     cur = out;
   }
