@@ -496,8 +496,8 @@ seg_meta_kernel(SegmentArgs a, const uint32_t* __restrict__ tile_seg_base,
   const int lane = lane_id();
   // One tile: key/jv are this lane's 4 positions from p0, kprev/jprev the
   // position before p0 (when p0 > 0), seg_base the segments before the tile.
-  auto tile_body = [&](int64_t tile, int64_t p0, const uint32_t* key, const uint32_t* jv, uint32_t kprev,
-                       uint32_t jprev, uint32_t seg_base) {
+  auto tile_body = [&](int64_t p0, const uint32_t* key, const uint32_t* jv, uint32_t kprev, uint32_t jprev,
+                       uint32_t seg_base) {
     int m[kMetaPer];
 #pragma unroll
     for (int e = 0; e < kMetaPer; ++e)
@@ -583,7 +583,7 @@ seg_meta_kernel(SegmentArgs a, const uint32_t* __restrict__ tile_seg_base,
       const int64_t p0 = blk0 + kt * kMetaTile + (int64_t)threadIdx.x * kMetaPer;
       const uint32_t key[kMetaPer] = {kv[kt].x, kv[kt].y, kv[kt].z, kv[kt].w};
       const uint32_t jv[kMetaPer] = {vv[kt].x, vv[kt].y, vv[kt].z, vv[kt].w};
-      tile_body((int64_t)blockIdx.x * kMetaTilesPerBlock + kt, p0, key, jv, kpv[kt], jpv[kt], sb[kt]);
+      tile_body(p0, key, jv, kpv[kt], jpv[kt], sb[kt]);
     }
     return;
   }
@@ -603,7 +603,7 @@ seg_meta_kernel(SegmentArgs a, const uint32_t* __restrict__ tile_seg_base,
       kprev = a.keys[p0 - 1];
       jprev = a.vals[p0 - 1];
     }
-    tile_body(tile, p0, key, jv, kprev, jprev, tile_seg_base[tile]);
+    tile_body(p0, key, jv, kprev, jprev, tile_seg_base[tile]);
   }
 }
 
@@ -804,8 +804,8 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
       const int E = __popcll(m);
       if (APPLY) {
         // kR rounds at a time: the table and state rows of all their active
-        // segments are requested, then updated (an inactive or missing one
-        // reads row 0 and is not written)
+        // segments are requested, then updated (a lane without one reads the
+        // table's first 16 bytes and writes nothing)
         constexpr int kR = APPLY == 2 ? 2 : 4;
         for (int b = 0; b < E; b += kR * GW) {
           f32x4 pv[kR], sv[kR], vv[kR];
@@ -820,7 +820,7 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
             act[r] = outv[r] < N && (s_park_cw[w][slot[r]] >> 16) > 0 && lane_on &&
                      (int64_t)s_park_key[w][slot[r]] < a.R;   // sorted keys are below R
             row[r] = act[r] ? (int64_t)s_park_key[w][slot[r]] : 0;
-            const int64_t at = row[r] * D + gl * 4;
+            const int64_t at = act[r] ? row[r] * D + gl * 4 : 0;   // inactive lanes read the table's first 16 bytes
             pv[r] = load_stream(reinterpret_cast<const f32x4*>(a.ap.p + at));
             sv[r] = load_stream(reinterpret_cast<const f32x4*>(a.ap.s1 + at));
             if (APPLY == 2) vv[r] = load_stream(reinterpret_cast<const f32x4*>(a.ap.s2 + at));

@@ -636,6 +636,32 @@ def test_fused_sparse_matches_separate_calls(opt, decay, D, keep_agg):
         assert_exact(fus["tag"], sep["tag"], "tag")
 
 
+@pytest.mark.parametrize("R", [1, 3])
+@pytest.mark.parametrize("D", [20, 32])
+def test_fused_sparse_tiny_table(D, R):
+    """A table of one or three rows: few, long segments, and at D = 20 lanes past
+    the row width, which must read and write nothing outside the table."""
+    K = 3
+    rng = np.random.default_rng(R * 100 + D)
+    sizes = np.array([3000, 11, 5000])
+    N = int(sizes.sum())
+    ids = rng.integers(0, R, N).astype(np.int64)
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    rows = counter.values_range(8, counter.STREAM_ROWS, 0, N * D, counter.KIND_DYADIC).reshape(N, D)
+    step, iota = 1000, 3
+    tokens = np.array([1000, 996, 999])
+    w, _, _ = oracle.token_weights(tokens, step, iota)
+    table0, slots0 = _table_and_state(R, D, "adagrad", 9)
+    d_in = (dev(ids), dev(rows), dev(off), dev(w), dev(tokens))
+    sep = _sparse_step(*d_in, step, iota, R, None, "token", "adagrad", False, True, table0, slots0)
+    fus = _sparse_step(*d_in, step, iota, R, None, "token", "adagrad", True, True, table0, slots0)
+    assert sep["err"] == 0 and fus["err"] == 0
+    U = int(sep["num_unique"][0])
+    assert int(fus["num_unique"][0]) == U
+    assert_exact(fus["agg"][:U], sep["agg"][:U], "agg")
+    assert torch.equal(fus["table"], sep["table"]) and torch.equal(fus["slots"][0], sep["slots"][0])
+
+
 @pytest.mark.parametrize("opt,decay", [("adagrad", "token"), ("adam", "token"), ("adagrad", "id_tag")])
 def test_fused_sparse_large_hot_plan(opt, decay):
     """Above the size where the automatic sort plan takes frequent IDs apart:
