@@ -550,7 +550,7 @@ def test_sparse_fractional_token_weights(D, plan):
 
 # ------------------------------------------ fused sparse aggregate + row apply
 def _sparse_step(d_ids, d_rows, d_off, d_w, d_tok, step, iota, R, tag, decay, opt, fused, keep_agg, table0,
-                 slots0):
+                 slots0, norm="per_id_count"):
     """One sparse step on device inputs, fused or as the two separate calls,
     from copies of the given table and state."""
     N, D = d_rows.shape
@@ -568,7 +568,8 @@ def _sparse_step(d_ids, d_rows, d_off, d_w, d_tok, step, iota, R, tag, decay, op
     dec = gba.DECAY_ID_TAG if decay == "id_tag" else gba.DECAY_TOKEN
     err = torch.zeros(1, dtype=torch.int32, device=DEV)
     lr, eps, b1, b2, t = (0.01, 1e-8, 0.9, 0.999, 1) if opt == "adagrad" else (1e-3, 1e-8, 0.9, 0.999, 1001)
-    common = (d_ids, d_rows, d_off, R, d_w, d_tok, step, iota, tag_d, dec, gba.NORM_PER_ID_COUNT,
+    nrm = gba.NORM_BY_K if norm == "by_k" else gba.NORM_PER_ID_COUNT
+    common = (d_ids, d_rows, d_off, R, d_w, d_tok, step, iota, tag_d, dec, nrm,
               out["unique_ids"], out["seg_offsets"], out["contrib_count"], out["active_count"])
     if fused:
         ws = torch.empty(gba.gba_aggregate_apply_sparse_workspace_size(N, K, D, R, opt), dtype=torch.uint8,
@@ -1129,6 +1130,41 @@ def test_sparse_random_shapes(K, n_max, R, D, decay, norm, seed, dyadic, zipf_s,
                       plan=plan)
     _check_sparse(res, ids, rows, off, w, tokens, 1000, 2, tag if decay == "id_tag" else None, decay, norm,
                   expect_exact=dyadic)
+
+
+@settings(max_examples=40, deadline=None, derandomize=True,
+          suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large])
+@given(K=hst.integers(1, 12), n_max=hst.integers(0, 3000), R=hst.sampled_from([1, 2, 17, 1000, 70_000]),
+       D=hst.sampled_from([4, 16, 20, 24, 28, 32, 64]), decay=hst.sampled_from(["token", "id_tag"]),
+       norm=hst.sampled_from(["per_id_count", "by_k"]), seed=hst.integers(0, 2 ** 31 - 1),
+       opt=hst.sampled_from(["adagrad", "adam"]), keep_agg=hst.booleans())
+def test_fused_sparse_random_shapes(K, n_max, R, D, decay, norm, seed, opt, keep_agg):
+    """Random shapes, empty contributions and tiny tables: the fused sparse call
+    gives bitwise the outputs, table and state of the two separate calls."""
+    rng = np.random.default_rng(seed)
+    sizes = rng.integers(0, n_max + 1, K)
+    sizes[rng.random(K) < 0.2] = 0
+    ids, rows, off, tokens, tag = _case(K, sizes, R, D, seed % 100_000, stale_hi=4)
+    step, iota = 1000, 2
+    w, _, _ = oracle.token_weights(tokens, step, iota)
+    table0, slots0 = _table_and_state(R, D, opt, seed % 1000)
+    d_in = (dev(ids), dev(rows.reshape(-1, D)), dev(off), dev(w), dev(tokens))
+    args = (step, iota, R, tag if decay == "id_tag" else None, decay, opt)
+    sep = _sparse_step(*d_in, *args, False, True, table0, slots0, norm=norm)
+    fus = _sparse_step(*d_in, *args, True, keep_agg, table0, slots0, norm=norm)
+    assert sep["err"] == 0 and fus["err"] == 0
+    U = int(sep["num_unique"][0])
+    assert int(fus["num_unique"][0]) == U
+    for k in ("unique_ids", "contrib_count", "active_count"):
+        assert_exact(fus[k][:U], sep[k][:U], k)
+    assert_exact(fus["seg_offsets"][:U + 1], sep["seg_offsets"][:U + 1], "seg_offsets")
+    if keep_agg:
+        assert_exact(fus["agg"][:U], sep["agg"][:U], "agg")
+    assert torch.equal(fus["table"], sep["table"]), "table"
+    for i in range(len(slots0)):
+        assert torch.equal(fus["slots"][i], sep["slots"][i]), f"state {i}"
+    if decay == "id_tag":
+        assert_exact(fus["tag"], sep["tag"], "tag")
 
 
 @settings(max_examples=40, deadline=None, derandomize=True, suppress_health_check=[HealthCheck.too_slow])
