@@ -2,6 +2,8 @@
 at sizes that span several tiles and ragged tails, plus the degenerate
 cases of the method (empty contributions, a single hot ID, all IDs
 distinct, every contribution excluded, nothing at all)."""
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -1109,9 +1111,17 @@ def test_hash_find_or_insert_empty_request():
 # ------------------------------------------------ randomised shapes (hypothesis)
 from hypothesis import HealthCheck, given, settings, strategies as hst   # noqa: E402
 
+# GBA_HYPOTHESIS_SCALE=n runs n times the examples below, drawn at random
+# instead of from the fixed derandomised sequence (a longer search for rare
+# shapes; the default run stays short and repeatable).
+_HYP_SCALE = max(1, int(os.environ.get("GBA_HYPOTHESIS_SCALE", "1")))
 
-@settings(max_examples=60, deadline=None, derandomize=True,
-          suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large])
+
+def _hyp(n, **kw):
+    return settings(max_examples=n * _HYP_SCALE, deadline=None, derandomize=_HYP_SCALE == 1, database=None, **kw)
+
+
+@_hyp(60, suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large])
 @given(K=hst.integers(1, 12), n_max=hst.integers(0, 3000), R=hst.sampled_from([1, 2, 17, 1000, 70_000, 1 << 20]),
        D=hst.sampled_from([4, 8, 12, 32, 64, 256]), decay=hst.sampled_from(["token", "id_tag"]),
        norm=hst.sampled_from(["per_id_count", "by_k"]), seed=hst.integers(0, 2 ** 31 - 1),
@@ -1132,8 +1142,7 @@ def test_sparse_random_shapes(K, n_max, R, D, decay, norm, seed, dyadic, zipf_s,
                   expect_exact=dyadic)
 
 
-@settings(max_examples=40, deadline=None, derandomize=True,
-          suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large])
+@_hyp(40, suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large])
 @given(K=hst.integers(1, 12), n_max=hst.integers(0, 3000), R=hst.sampled_from([1, 2, 17, 1000, 70_000]),
        D=hst.sampled_from([4, 16, 20, 24, 28, 32, 64]), decay=hst.sampled_from(["token", "id_tag"]),
        norm=hst.sampled_from(["per_id_count", "by_k"]), seed=hst.integers(0, 2 ** 31 - 1),
@@ -1167,7 +1176,7 @@ def test_fused_sparse_random_shapes(K, n_max, R, D, decay, norm, seed, opt, keep
         assert_exact(fus["tag"], sep["tag"], "tag")
 
 
-@settings(max_examples=40, deadline=None, derandomize=True, suppress_health_check=[HealthCheck.too_slow])
+@_hyp(40, suppress_health_check=[HealthCheck.too_slow])
 @given(K=hst.integers(1, 70), P=hst.integers(1, 150_000), offset=hst.sampled_from([0, 0, 1, 3]),
        frac=hst.booleans(), seed=hst.integers(0, 2 ** 31 - 1), J=hst.integers(1, 9),
        opt=hst.sampled_from(["adagrad", "adam"]))
