@@ -1223,3 +1223,45 @@ def test_dense_random_shapes(K, P, offset, frac, seed, J, opt):
     for other in runs[1:]:
         for a, b in zip(runs[0], other):
             assert_exact(b, a, "fused / early vs separate")
+
+
+@_hyp(40, suppress_health_check=[HealthCheck.too_slow])
+@given(calls=hst.integers(1, 4), n_max=hst.integers(0, 4000), pool=hst.integers(1, 3000),
+       spare=hst.integers(0, 2), clustered=hst.booleans(), seed=hst.integers(0, 2 ** 31 - 1))
+def test_hash_random_sequences(calls, n_max, pool, spare, clustered, seed):
+    """A sequence of find-or-insert calls against a dictionary model: a known ID
+    keeps its row, each call's distinct new IDs take the next rows (one each,
+    the same for every occurrence), the count of new IDs and of rows in use
+    follow the model, and the reverse map names each row's ID.  The index is
+    at most half full; clustered IDs are consecutive values (neighbours in the
+    key space, scattered only by the hash)."""
+    rng = np.random.default_rng(seed)
+    if clustered:
+        ids_pool = rng.integers(-(2 ** 62), 2 ** 62) + np.arange(pool, dtype=np.int64)
+    else:
+        ids_pool = rng.integers(-(2 ** 63), 2 ** 63 - 1, pool, dtype=np.int64)
+    ids_pool = np.unique(ids_pool[ids_pool != gba.EMPTY_ID])
+    capacity = 1 << (int(2 * ids_pool.size - 1).bit_length() + spare)
+    st = _HashStore(capacity, max_rows=ids_pool.size, n_max=max(n_max, 1))
+    model = {}
+    for _ in range(calls):
+        n = int(rng.integers(0, n_max + 1))
+        pick = np.where(rng.random(n) < 0.3, 0, rng.integers(0, ids_pool.size, n))   # a frequent ID among the rest
+        ids = ids_pool[pick]
+        rows, nn = st.rows_of(ids)
+        assert int(host(st.err)[0]) == 0
+        before = len(model)
+        new_ids = [int(x) for x in np.unique(ids) if int(x) not in model]
+        assert nn == len(new_ids)
+        got = {}
+        for x, r in zip(ids.tolist(), rows.tolist()):
+            if x in model:
+                assert r == model[x], "a known ID kept its row"
+            else:
+                assert got.setdefault(x, r) == r, "every occurrence of a new ID has one row"
+        assert sorted(got.values()) == list(range(before, before + len(new_ids)))
+        model.update(got)
+        assert int(host(st.num_rows)[0]) == len(model)
+    row_ids = host(st.row_ids)
+    for x, r in model.items():
+        assert int(row_ids[r]) == x
