@@ -339,9 +339,10 @@ gba_status gba_aggregate_sparse_plan(const int64_t* ids, const float* rows,
  * gba_token_of_batch (host function, no device work): the token handed out
  * with the i-th batch of the data list, t_i = floor(i / M) with M = K the
  * number of gradients aggregated per step: tokens start at 0 and each value
- * repeats M times, in ascending order.  (The paper prints floor(i / K) with K
- * the number of updates, which contradicts "each value repeats M times"; the
- * repetition rule is the one followed.)  Returns -1 if i < 0 or M < 1.
+ * repeats M times, in ascending order.  (The formula printed in Sec. 3.1
+ * divides by the number of updates K instead, which would contradict the rule
+ * stated beside it that every token value occurs M times; that rule is the one
+ * followed.)  Returns -1 if i < 0 or M < 1.
  *
  * gba_pull_rows: the embedding rows for a worker's request, looked up once per
  * distinct ID.
@@ -384,11 +385,15 @@ gba_status gba_pull_rows(const int64_t* ids, int64_t n, int64_t R, const float* 
  *   num_rows   one int64 on the device: rows in use (read and advanced).
  *   max_rows   size of the row pool (<= 2^31 - 1).
  *   row_ids    [max_rows] int64 out, row -> ID for the new rows; may be NULL.
- *   num_new    one int64 out on the device: IDs inserted by this call; may be NULL.
+ *   num_new    one int64 out on the device: IDs that asked for a row in this
+ *              call (inserted now, or left without a row by an earlier call on
+ *              a full pool); may be NULL.
  *   workspace  gba_hash_workspace_size(n) bytes.
  *   err        GBA_DERR_ID_RANGE for an ID equal to GBA_EMPTY_ID,
  *              GBA_DERR_TABLE_FULL when the index or the pool is full (those
- *              positions get row -1).
+ *              positions get row -1).  An ID that was given a slot but no
+ *              row, because the pool was full, gets a row from a later call
+ *              once the pool has room (a larger max_rows).
  * Which slot and which row an ID gets depends on the order in which threads
  * win their races; every other output is deterministic.
  *

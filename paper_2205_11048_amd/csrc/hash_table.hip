@@ -6,10 +6,13 @@
 //
 // find-or-insert is three launches, so no thread ever waits for another's
 // write: (1) every position claims or finds its ID's slot (compare-and-swap on
-// the slot's ID; IDs are never removed, so a non-empty slot never changes) and
-// the slots it claimed are appended to a list, one atomic per wave; (2) the
-// claimed slots get the next rows of the pool, in list order; (3) every
-// position reads its slot's row.
+// the slot's ID; IDs are never removed, so a non-empty slot never changes);
+// a slot that holds no row yet (claimed now, or by an earlier call that found
+// the pool full) is appended to a list once, by the one position whose
+// compare-and-swap marks its row as pending, one list atomic per wave; (2)
+// the listed slots get the next rows of the pool, in list order (a slot past
+// the end of the pool is left without a row, to be served by a later call);
+// (3) every position reads its slot's row.
 #include "gba_device.hpp"
 #include "gba_internal.hpp"
 
@@ -49,6 +52,11 @@ __device__ __forceinline__ uint64_t mix64(uint64_t h) {
   return h;
 }
 
+// Row of a slot: kNoRow until the pool hands it one; kPendingRow while it is
+// listed for a row inside one find-or-insert.
+constexpr int32_t kNoRow = -1;
+constexpr int32_t kPendingRow = -2;
+
 __global__ void hash_count_reset_kernel(uint32_t* __restrict__ claimed_count) { *claimed_count = 0u; }
 
 __global__ void __launch_bounds__(kHashBlock)
@@ -86,8 +94,8 @@ __device__ __forceinline__ int64_t claim_or_find(int64_t* slot_ids, int64_t mask
 }
 
 __global__ void __launch_bounds__(kHashBlock)
-hash_claim_kernel(int64_t* __restrict__ slot_ids, int64_t mask, const int64_t* __restrict__ ids, int64_t n,
-                  int32_t* __restrict__ slot_of, int32_t* __restrict__ claimed_slots,
+hash_claim_kernel(int64_t* __restrict__ slot_ids, int32_t* __restrict__ slot_rows, int64_t mask,
+                  const int64_t* __restrict__ ids, int64_t n, int32_t* __restrict__ slot_of, int32_t* __restrict__ claimed_slots,
                   uint32_t* __restrict__ claimed_count, int32_t* __restrict__ err) {
   const int64_t stride = (int64_t)gridDim.x * kHashBlock;
   const uint64_t lt = lanemask_lt();
@@ -102,8 +110,16 @@ hash_claim_kernel(int64_t* __restrict__ slot_ids, int64_t mask, const int64_t* _
       if (id == GBA_EMPTY_ID) {
         raise_error(err, GBA_DERR_ID_RANGE);
       } else {
-        s = claim_or_find(slot_ids, mask, id, &claimed);
-        if (s < 0) raise_error(err, GBA_DERR_TABLE_FULL);
+        bool fresh = false;
+        s = claim_or_find(slot_ids, mask, id, &fresh);
+        if (s < 0) {
+          raise_error(err, GBA_DERR_TABLE_FULL);
+        } else if (slot_rows[s] == kNoRow) {
+          // the slot has no row yet: exactly one position lists it (rows are
+          // written only by the next launch, so kNoRow cannot turn into a row
+          // during this one)
+          claimed = atomicCAS(slot_rows + s, kNoRow, kPendingRow) == kNoRow;
+        }
       }
       slot_of[i] = (int32_t)s;
     }
@@ -129,7 +145,8 @@ hash_assign_kernel(const int64_t* __restrict__ slot_ids, int32_t* __restrict__ s
   for (int64_t j = (int64_t)blockIdx.x * kHashBlock + threadIdx.x; j < c; j += stride) {
     const int64_t s = claimed_slots[j];
     const int64_t r = r0 + j;
-    if (r >= max_rows) {   // the pool is full: the slot keeps no row
+    if (r >= max_rows) {   // the pool is full: the slot keeps no row, and a later call lists it again
+      slot_rows[s] = kNoRow;
       raise_error(err, GBA_DERR_TABLE_FULL);
       continue;
     }
@@ -146,14 +163,19 @@ __global__ void hash_count_kernel(const uint32_t* __restrict__ claimed_count, in
   if (num_new) *num_new = c;
 }
 
+// A position whose ID has no slot or no row gets -1 and reports the table full.
 __global__ void __launch_bounds__(kHashBlock)
 hash_rows_kernel(const int32_t* __restrict__ slot_rows, const int32_t* __restrict__ slot_of, int64_t n,
-                 int64_t* __restrict__ rows_out) {
+                 int64_t* __restrict__ rows_out, int32_t* __restrict__ err) {
   const int64_t stride = (int64_t)gridDim.x * kHashBlock;
+  bool full = false;
   for (int64_t i = (int64_t)blockIdx.x * kHashBlock + threadIdx.x; i < n; i += stride) {
     const int32_t s = slot_of[i];
-    rows_out[i] = s < 0 ? -1 : (int64_t)slot_rows[s];
+    const int32_t r = s < 0 ? -1 : slot_rows[s];
+    full |= r < 0;
+    rows_out[i] = r < 0 ? -1 : (int64_t)r;
   }
+  if (full) raise_error(err, GBA_DERR_TABLE_FULL);
 }
 
 // Re-insert every (ID, row) of the old index into the new one; each ID is
@@ -203,8 +225,8 @@ hipError_t launch_hash_find_or_insert(int64_t* slot_ids, int32_t* slot_rows, int
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (n > 0) {
-    hipLaunchKernelGGL(hash_claim_kernel, grid_for(n), dim3(kHashBlock), 0, stream, slot_ids, capacity - 1, ids, n,
-                       slot_of, claimed, count, err);
+    hipLaunchKernelGGL(hash_claim_kernel, grid_for(n), dim3(kHashBlock), 0, stream, slot_ids, slot_rows, capacity - 1,
+                       ids, n, slot_of, claimed, count, err);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(hash_assign_kernel, grid_for(n), dim3(kHashBlock), 0, stream, (const int64_t*)slot_ids,
                        slot_rows, (const int32_t*)claimed, (const uint32_t*)count, (const int64_t*)num_rows, max_rows,
@@ -216,7 +238,7 @@ hipError_t launch_hash_find_or_insert(int64_t* slot_ids, int32_t* slot_rows, int
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (n > 0) {
     hipLaunchKernelGGL(hash_rows_kernel, grid_for(n), dim3(kHashBlock), 0, stream, (const int32_t*)slot_rows,
-                       (const int32_t*)slot_of, n, rows_out);
+                       (const int32_t*)slot_of, n, rows_out, err);
     e = hipGetLastError();
   }
   return e;

@@ -201,44 +201,30 @@ __device__ __forceinline__ int contribution_global(const int64_t* off, int K, ui
   return m < 0 ? 0 : (m < K ? m : K - 1);
 }
 
-// The optimiser on one lane's 4 floats of a row, with the row apply's
-// arithmetic (float64, one rounding per stored value).
-template <int MODE>
-__device__ __forceinline__ void optimise4(const RowApply& ap, f32x4& pv, f32x4& s1, f32x4& s2, f32x4 g) {
+// Adagrad on one lane's 4 floats of a row, with the row apply's arithmetic
+// (float64, one rounding per stored value).  The fused row pass applies
+// Adagrad only (segments_fuse_apply); Adam goes through the separate apply.
+__device__ __forceinline__ void adagrad4(const RowApply& ap, f32x4& pv, f32x4& s1, f32x4 g) {
   float pe[4] = {pv.x, pv.y, pv.z, pv.w}, ae[4] = {s1.x, s1.y, s1.z, s1.w};
   const float ge[4] = {g.x, g.y, g.z, g.w};
-  if (MODE == 2) {
-    float ve[4] = {s2.x, s2.y, s2.z, s2.w};
 #pragma unroll
-    for (int e = 0; e < 4; ++e) adam_update(pe[e], ae[e], ve[e], ge[e], ap.lr, ap.beta1, ap.beta2, ap.eps, ap.bc1, ap.bc2);
-    s2 = f32x4{ve[0], ve[1], ve[2], ve[3]};
-  } else {
-#pragma unroll
-    for (int e = 0; e < 4; ++e) adagrad_update(pe[e], ae[e], ge[e], ap.lr, ap.eps);
-  }
+  for (int e = 0; e < 4; ++e) adagrad_update(pe[e], ae[e], ge[e], ap.lr, ap.eps);
   pv = f32x4{pe[0], pe[1], pe[2], pe[3]};
   s1 = f32x4{ae[0], ae[1], ae[2], ae[3]};
 }
 
-// Row r updated with mean g (one lane's 16 bytes): load, optimise, store.
+// Row r updated with mean g (one lane's 16 bytes): load, Adagrad, store.
 __device__ __forceinline__ void apply_row_part(const RowApply& ap, int64_t r, int D, int lane, f32x4 g) {
   const int64_t at = r * D + lane * 4;
   f32x4 pv = load_stream(reinterpret_cast<const f32x4*>(ap.p + at));
   f32x4 s1 = load_stream(reinterpret_cast<const f32x4*>(ap.s1 + at));
-  f32x4 s2 = {0.f, 0.f, 0.f, 0.f};
-  if (ap.mode == 2) {
-    s2 = load_stream(reinterpret_cast<const f32x4*>(ap.s2 + at));
-    optimise4<2>(ap, pv, s1, s2, g);
-    store_stream(reinterpret_cast<f32x4*>(ap.s2 + at), s2);
-  } else {
-    optimise4<1>(ap, pv, s1, s2, g);
-  }
+  adagrad4(ap, pv, s1, g);
   store_stream(reinterpret_cast<f32x4*>(ap.p + at), pv);
   store_stream(reinterpret_cast<f32x4*>(ap.s1 + at), s1);
 }
 
 // out: the segment's place among all distinct IDs.  The mean goes to agg
-// (when given) and, with a row apply (mode != 0; a constant in the row pass),
+// (when given) and, with the fused Adagrad apply (mode 1; a constant in the row pass),
 // into the optimiser update of row `row`, or where row < 0 of the ID the
 // position pass wrote for this place (written by an earlier launch).
 __device__ __forceinline__ void finalize_segment(const SegmentArgs& a, int64_t seg, f64x4 acc,
@@ -608,8 +594,8 @@ seg_meta_kernel(SegmentArgs a, const uint32_t* __restrict__ tile_seg_base,
 }
 
 // Per-group pass: gather the kept rows and sum every run in float64.  APPLY
-// (1 Adagrad, 2 Adam; 32-float rows only) updates each finished segment's row
-// in the table as well.
+// (1: Adagrad, on rows of 20 to 32 floats only) updates each finished
+// segment's row in the table as well.
 template <int LPR, int APPLY, int SPAN>
 __global__ void __launch_bounds__(kSegBlock)
 seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32_t* __restrict__ base32,
@@ -629,6 +615,7 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
   // several rounds of parked segments are requested before the first is used.
   constexpr bool kPark = LPR == 8 && GW == kBatch;
   static_assert(APPLY == 0 || kPark, "the row apply is fused where segments are parked");
+  static_assert(APPLY == 0 || APPLY == 1, "the fused row apply is Adagrad only");
   constexpr int kSlots = GW * kBatch;
   __shared__ f32x4 s_park[kPark ? kSegWaves : 1][kPark ? kSlots : 1][LPR];
   __shared__ uint32_t s_park_out[kPark ? kSegWaves : 1][kSlots];
@@ -806,9 +793,9 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
         // kR rounds at a time: the table and state rows of all their active
         // segments are requested, then updated (a lane without one reads the
         // table's first 16 bytes and writes nothing)
-        constexpr int kR = APPLY == 2 ? 2 : 4;
+        constexpr int kR = 4;
         for (int b = 0; b < E; b += kR * GW) {
-          f32x4 pv[kR], sv[kR], vv[kR];
+          f32x4 pv[kR], sv[kR];
           uint32_t slot[kR];
           int64_t outv[kR], row[kR];
           bool act[kR];
@@ -823,7 +810,6 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
             const int64_t at = act[r] ? row[r] * D + gl * 4 : 0;   // inactive lanes read the table's first 16 bytes
             pv[r] = load_stream(reinterpret_cast<const f32x4*>(a.ap.p + at));
             sv[r] = load_stream(reinterpret_cast<const f32x4*>(a.ap.s1 + at));
-            if (APPLY == 2) vv[r] = load_stream(reinterpret_cast<const f32x4*>(a.ap.s2 + at));
           }
 #pragma unroll
           for (int r = 0; r < kR; ++r) {
@@ -837,10 +823,9 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
             }
             if (act[r]) {
               const int64_t at = row[r] * D + gl * 4;
-              optimise4<APPLY>(a.ap, pv[r], sv[r], vv[r], g);
+              adagrad4(a.ap, pv[r], sv[r], g);
               store_stream(reinterpret_cast<f32x4*>(a.ap.p + at), pv[r]);
               store_stream(reinterpret_cast<f32x4*>(a.ap.s1 + at), sv[r]);
-              if (APPLY == 2) store_stream(reinterpret_cast<f32x4*>(a.ap.s2 + at), vv[r]);
             }
           }
         }

@@ -537,6 +537,62 @@ def test_full_step_small(decay, opt, D, fused):
         assert_exact(host(tag), ref["sparse"]["new_tag"], "tag")
 
 
+@pytest.mark.parametrize("iota", [np.iinfo(np.int64).max, -1])
+@pytest.mark.parametrize("decay", ["token", "id_tag"])
+@pytest.mark.parametrize("opt", ["adagrad", "adam"])
+def test_eq1_limits_through_the_step(opt, decay, iota):
+    """Eq. 1 at its two limits, through the weights and the whole fused step
+    (as the benchmark launches it): a threshold above every staleness keeps
+    every contribution (the bulk-synchronous limit: every weight 1 and W_r =
+    c_r for every ID, in both decay modes), and iota = -1 excludes every
+    contribution (no row is applied or re-tagged; the dense update still runs,
+    with a zero gradient)."""
+    c = BY_NAME["c0"].scaled(optimizer=opt, lr=0.01 if opt == "adagrad" else 1e-3, D=32)
+    hs = workload.host_step(c)
+    stepper = GBAStep(c.K, c.N, c.D, c.R, c.P)
+    grads = [dev(g) for g in hs.grads]
+    param, table = dev(hs.param), dev(hs.table)
+    dslots = [dev(s) for s in hs.dense_slots]
+    tslots = [dev(s) for s in hs.table_slots]
+    tag = dev(hs.tags)
+    stepper.run(tokens=dev(hs.tokens), step=hs.step, iota=int(iota), grads=grads, ids=dev(hs.ids),
+                rows=dev(hs.rows), offsets=dev(hs.offsets), param=param, dense_slots=dslots, table=table,
+                table_slots=tslots, optimizer=opt, lr=c.lr, eps=c.eps, t=c.adam_t, tag=tag,
+                decay=gba.DECAY_ID_TAG if decay == "id_tag" else gba.DECAY_TOKEN, keep_agg=True)
+    hp = dict(lr=c.lr, eps=c.eps, beta1=c.beta1, beta2=c.beta2)
+    ref = oracle.gba_step(hs.tokens, hs.step, int(iota), hs.grads, hs.ids, hs.rows, hs.offsets, hs.param,
+                          hs.dense_slots, lambda r: hs.table[r], lambda k, r: hs.table_slots[k][r], opt, hp,
+                          tag=hs.tags, decay=decay, t=c.adam_t)
+    keep_all = iota > 0
+    assert int(host(stepper.err)[0]) == 0
+    assert_exact(host(stepper.w), ref["w"], "w")
+    assert_exact(ref["w"], np.full(c.K, 1.0 if keep_all else 0.0, np.float32), "oracle w at the limit")
+    assert int(host(stepper.num_excluded)[0]) == ref["num_excluded"] == (0 if keep_all else c.K)
+    assert_exact(host(stepper.g_bar), ref["g_bar"], "g_bar")
+    assert_rule_t(host(param), ref["param"], None, "param")
+    for k, s in enumerate(ref["dense_slots"]):
+        assert_rule_t(host(dslots[k]), s, None, f"dense slot {k}")
+    sp = ref["sparse"]
+    U = int(host(stepper.num_unique)[0])
+    assert U == sp["num_unique"]
+    W = host(stepper.active_count)[:U]
+    assert_exact(W, sp["active_count"], "W_r")
+    assert_exact(W, sp["contrib_count"] if keep_all else np.zeros(U, np.int32), "W_r at the limit")
+    assert_rule_t(host(stepper.agg)[:U], sp["agg"], sp["agg_mu"], "agg")
+    t_after = host(table)
+    act = ref["active_ids"]
+    assert act.size == (U if keep_all else 0)
+    if act.size:
+        assert_rule_t(t_after[act], ref["table_rows"], None, "table rows")
+        for k, s in enumerate(ref["table_slot_rows"]):
+            assert_rule_t(host(tslots[k])[act], s, None, f"table slot {k}")
+    untouched = np.ones(c.R, bool)
+    untouched[act] = False
+    assert_exact(t_after[untouched], hs.table[untouched], "untouched rows")
+    if decay == "id_tag":
+        assert_exact(host(tag), sp["new_tag"], "tag")
+
+
 @pytest.mark.parametrize("plan", [None, gba.SORT_HOT])
 @pytest.mark.parametrize("D", [8, 32])
 def test_sparse_fractional_token_weights(D, plan):
@@ -951,10 +1007,26 @@ def test_hash_full_index_full_pool_and_reserved_id():
     st = _HashStore(16, max_rows=100, n_max=64)
     st.rows_of(np.arange(20, dtype=np.int64) * 7 + 3)
     assert int(host(st.err)[0]) & gba.DERR_TABLE_FULL
-    st = _HashStore(64, max_rows=10, n_max=64)
-    rows, _ = st.rows_of(np.arange(20, dtype=np.int64) + 100)
+    st = _HashStore(64, max_rows=30, n_max=64)
+    st.max_rows = 10
+    ids = np.repeat(np.arange(20, dtype=np.int64) + 100, 2)
+    rows, _ = st.rows_of(ids)
     assert int(host(st.err)[0]) & gba.DERR_TABLE_FULL
-    assert int(host(st.num_rows)[0]) == 10 and (rows == -1).sum() == 10
+    assert int(host(st.num_rows)[0]) == 10 and (rows == -1).sum() == 20
+    # the pool grows: the IDs left without a row get the next rows, the others keep theirs
+    st.max_rows = 30
+    st.err.zero_()
+    rows2, nn = st.rows_of(ids)
+    assert int(host(st.err)[0]) == 0 and nn == 10
+    kept = rows >= 0
+    assert_exact(rows2[kept], rows[kept], "rows kept")
+    assert_exact(np.unique(rows2[~kept]), np.arange(10, 20), "rows handed out later")
+    assert_exact(rows2[0::2], rows2[1::2], "one row per ID")
+    assert int(host(st.num_rows)[0]) == 20
+    assert_exact(host(st.row_ids)[rows2], ids, "row -> ID")
+    rows3, nn3 = st.rows_of(ids[::-1].copy())
+    assert int(host(st.err)[0]) == 0 and nn3 == 0
+    assert_exact(rows3[::-1], rows2, "rows of a third call")
     st = _HashStore(64, max_rows=10, n_max=64)
     st.rows_of(np.array([4, gba.EMPTY_ID, 4], np.int64))
     assert int(host(st.err)[0]) & gba.DERR_ID_RANGE

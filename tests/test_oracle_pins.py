@@ -452,3 +452,198 @@ def test_results_follow_the_id_not_its_value(decay):
         assert np.array_equal(b[k], a[k][order]), k
     if decay == "id_tag":
         assert np.array_equal(b["new_tag"][perm], a["new_tag"])
+
+
+# ------------------------------------------- magnitude companions of the float rule
+# The comparison rule passes a float x against the oracle's r when
+# |x - r| <= 1e-5 max(|r|, mu).  mu comes from the oracle's *_magnitude
+# functions and agg_mu; these pins check them against a second worked example
+# (tests/golden/magnitudes.json, mixed signs so that mu != |r| where a sum
+# cancels), against brute-force sums of absolute terms in exact arithmetic,
+# and against the error they must cover.
+MAG = os.path.join(os.path.dirname(__file__), "golden", "magnitudes.json")
+
+
+@pytest.fixture(scope="module")
+def mag():
+    with open(MAG) as f:
+        return json.load(f)
+
+
+def _fr(v):
+    return np.array([float(Fraction(x)) for x in v])
+
+
+def _mag_inputs(m):
+    grads = np.array(m["dense_grads"], np.float32)
+    ids = np.array(m["ids"], np.int64)
+    rows = np.array(m["rows"], np.float32)
+    off = np.array(m["offsets"], np.int64)
+    tag = np.full(16, -7, np.int32)
+    for r, t in m["tag_before"].items():
+        tag[int(r)] = t
+    w, _, _ = oracle.token_weights(m["tokens"], m["step"], m["iota"])
+    return grads, ids, rows, off, tag, w
+
+
+def test_magnitude_of_the_dense_sum(mag):
+    grads, _, _, _, _, w = _mag_inputs(mag)
+    assert list(w) == mag["w"]
+    np.testing.assert_array_equal(oracle.aggregate_dense(grads, w), _fr(mag["g_bar"]).astype(np.float32))
+    # the stale contribution's 100s must not count: (|1| + |-3|) / 3 and (|-6| + |2|) / 3
+    np.testing.assert_array_equal(oracle.aggregate_dense_magnitude(grads, w), _fr(mag["g_bar_mu"]))
+
+
+@pytest.mark.parametrize("decay", ["token", "id_tag"])
+def test_magnitude_of_the_row_sums(mag, decay):
+    _, ids, rows, off, tag, w = _mag_inputs(mag)
+    out = oracle.aggregate_sparse(ids, rows, off, w, mag["tokens"], mag["step"], mag["iota"], tag=tag, decay=decay)
+    assert list(out["unique_ids"]) == mag["unique_ids"]
+    assert list(out["contrib_count"]) == mag["contrib_count"]
+    assert list(out["active_count"]) == mag[decay]["active_count"]
+    np.testing.assert_array_equal(out["agg"][:, 0], _fr(mag[decay]["agg"]).astype(np.float32))
+    np.testing.assert_array_equal(out["agg_mu"][:, 0], _fr(mag[decay]["agg_mu"]))
+
+
+def test_magnitudes_of_adagrad(mag):
+    grads, ids, rows, off, tag, w = _mag_inputs(mag)
+    a = mag["adagrad"]
+    lr, eps = float(Fraction(a["lr"])), float(a["eps"])
+    g = oracle.aggregate_dense(grads, w)
+    gmu = oracle.aggregate_dense_magnitude(grads, w)
+    d = a["dense"]
+    p0, a0 = _fr(d["param_before"]).astype(np.float32), _fr(d["accum_before"]).astype(np.float32)
+    p1, a1 = oracle.adagrad(p0, a0, g, lr, eps)
+    np.testing.assert_allclose(p1, _fr(d["param_after"]), rtol=1e-6)
+    np.testing.assert_allclose(a1, _fr(d["accum_after"]), rtol=1e-6)
+    mu_p, mu_a = oracle.adagrad_magnitude(p0, a0, g, gmu, lr, eps)
+    np.testing.assert_allclose(mu_p, _fr(d["mu_param"]), rtol=1e-6)
+    np.testing.assert_allclose(mu_a, _fr(d["mu_accum"]), rtol=1e-6)
+    # table rows, with the row means and their companions
+    sp = oracle.aggregate_sparse(ids, rows, off, w, mag["tokens"], mag["step"], mag["iota"])
+    tr = a["token_rows"]
+    assert list(sp["unique_ids"]) == tr["ids"]
+    E0, A0 = _fr(tr["param_before"]).astype(np.float32)[:, None], _fr(tr["accum_before"]).astype(np.float32)[:, None]
+    E1, A1 = oracle.adagrad(E0, A0, sp["agg"], lr, eps)
+    np.testing.assert_allclose(E1[:, 0], _fr(tr["param_after"]), rtol=1e-6)
+    np.testing.assert_allclose(A1[:, 0], _fr(tr["accum_after"]), rtol=1e-6)
+    mu_p, mu_a = oracle.adagrad_magnitude(E0, A0, sp["agg"], sp["agg_mu"], lr, eps)
+    np.testing.assert_allclose(mu_p[:, 0], _fr(tr["mu_param"]), rtol=1e-6)
+    np.testing.assert_allclose(mu_a[:, 0], _fr(tr["mu_accum"]), rtol=1e-6)
+
+
+def test_magnitudes_of_adam(mag):
+    grads, _, _, _, _, w = _mag_inputs(mag)
+    a = mag["adam"]
+    lr, b1, b2 = (float(Fraction(a[k])) for k in ("lr", "beta1", "beta2"))
+    eps, t = float(a["eps"]), a["t"]
+    g = oracle.aggregate_dense(grads, w)
+    gmu = oracle.aggregate_dense_magnitude(grads, w)
+    d = a["dense"]
+    p0, m0, v0 = (_fr(d[k]).astype(np.float32) for k in ("param_before", "m_before", "v_before"))
+    p1, m1, v1 = oracle.adam(p0, m0, v0, g, lr, b1, b2, eps, t)
+    np.testing.assert_allclose(p1, _fr(d["param_after"]), rtol=1e-6)
+    np.testing.assert_allclose(m1, _fr(d["m_after"]), rtol=1e-6)
+    np.testing.assert_allclose(v1, _fr(d["v_after"]), rtol=1e-6)
+    mu_p, mu_m, mu_v = oracle.adam_magnitude(p0, m0, v0, g, gmu, lr, b1, b2, eps, t)
+    np.testing.assert_allclose(mu_p, _fr(d["mu_param"]), rtol=1e-6)
+    np.testing.assert_allclose(mu_m, _fr(d["mu_m"]), rtol=1e-6)
+    np.testing.assert_allclose(mu_v, _fr(d["mu_v"]), rtol=1e-6)
+
+
+@pytest.mark.parametrize("seed", range(8))
+@pytest.mark.parametrize("decay", ["token", "id_tag"])
+@pytest.mark.parametrize("norm", ["per_id_count", "by_k"])
+def test_magnitudes_are_sums_of_absolute_terms(seed, decay, norm):
+    """Brute force in exact rational arithmetic, organised per contribution and
+    occurrence: mu of the dense sum is sum over kept m of |w_m g_m| / K, and mu
+    of a row mean is sum over its kept occurrences of |w x| / c_r (or / K).
+    Dyadic inputs make the oracle's float64 sums exact, so after the one
+    correctly rounded division both sides agree bit for bit."""
+    rng = np.random.default_rng(4000 + seed)
+    K, P, D, R = int(rng.integers(1, 6)), int(rng.integers(1, 7)), int(rng.integers(1, 4)), int(rng.integers(1, 9))
+    step, iota = 20, int(rng.integers(0, 4))
+    tokens = step - rng.integers(0, 6, K)
+    w, _, _ = oracle.token_weights(tokens, step, iota)
+    w = (w * rng.choice([1.0, 0.5, 0.75, 0.25], K)).astype(np.float32)    # fractional policies (token mode)
+    grads = (rng.integers(-64, 65, (K, P)) / 8).astype(np.float32)
+    sizes = rng.integers(0, 5, K)
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    N = int(off[-1])
+    ids = rng.integers(0, R, N).astype(np.int64)
+    rows = (rng.integers(-64, 65, (N, D)) / 16).astype(np.float32)
+    tag = rng.integers(-1, step, R).astype(np.int32)
+
+    F = Fraction
+    want = [sum((abs(F(float(w[m])) * F(float(grads[m, i]))) for m in range(K) if w[m] != 0), F(0)) / K
+            for i in range(P)]
+    np.testing.assert_array_equal(oracle.aggregate_dense_magnitude(grads, w), np.array([float(x) for x in want]))
+
+    if N == 0:
+        return
+    seen, total = {}, {}
+    for m in range(K):
+        for j in range(int(off[m]), int(off[m + 1])):
+            r = int(ids[j])
+            seen.setdefault(r, set()).add(m)
+            if decay == "token":
+                wt = F(float(w[m]))
+            else:
+                wt = F(1) if max(0, int(tag[r]) - int(tokens[m]) + 1) <= iota else F(0)
+            acc = total.setdefault(r, [F(0)] * D)
+            if wt != 0:
+                for d_ in range(D):
+                    acc[d_] += abs(wt * F(float(rows[j, d_])))
+    out = oracle.aggregate_sparse(ids, rows, off, w, tokens, step, iota, tag=tag, decay=decay, norm=norm)
+    keys = sorted(total)
+    assert list(out["unique_ids"]) == keys
+    for u, r in enumerate(keys):
+        div = len(seen[r]) if norm == "per_id_count" else K
+        np.testing.assert_array_equal(out["agg_mu"][u], np.array([float(x / div) for x in total[r]]))
+
+
+def test_rule_t_rejects_an_error_of_twice_the_bound():
+    from compare import assert_rule_t
+    ref = np.array([1.0, -2.0, 1e-3, 0.0])
+    mu = np.array([3.0, 2.0, 10.0, 4.0])
+    assert_rule_t(ref + 0.9e-5 * mu, ref, mu, "inside")
+    assert_rule_t(ref - 0.9e-5 * mu, ref, mu, "inside")
+    for i in range(ref.size):
+        bad = ref.copy()
+        bad[i] += 2e-5 * mu[i]
+        with pytest.raises(AssertionError):
+            assert_rule_t(bad, ref, mu, "outside")
+    # without a companion the bound is relative to |r|
+    with pytest.raises(AssertionError):
+        assert_rule_t(np.array([1.0 + 2e-5]), np.array([1.0]), None, "relative")
+    assert_rule_t(np.array([1.0 + 0.5e-5]), np.array([1.0]), None, "relative")
+    with pytest.raises(AssertionError):
+        assert_rule_t(np.array([np.nan]), np.array([1.0]), None, "nan")
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_optimiser_magnitudes_cover_the_gradient_tolerance(seed):
+    """A gradient that is itself within 1e-5 mu_g of the oracle's moves each
+    optimiser output by at most 1e-5 of that output's companion: the companions
+    carry the tolerance of their input through the update.  State values are
+    those of a warm parameter server (the generator's accumulator and moment
+    ranges), and mu_g runs up to 20 |g| (cancelling sums)."""
+    rng = np.random.default_rng(77 + seed)
+    n = 20000
+    g = rng.normal(0.0, 1e-2, n).astype(np.float32)
+    gmu = np.abs(g.astype(np.float64)) * rng.uniform(1.0, 20.0, n)
+    delta = rng.uniform(-0.99, 0.99, n) * 1e-5 * gmu
+    g2 = (g.astype(np.float64) + delta).astype(np.float32)
+    p = rng.uniform(-1 / 16, 1 / 16, n).astype(np.float32)
+    lr, eps = 0.01, 1e-8
+    a = rng.uniform(1 / 16, 5 / 16, n).astype(np.float32)
+    mu_p, mu_a = oracle.adagrad_magnitude(p, a, g, gmu, lr, eps)
+    for x, y, mu in zip(oracle.adagrad(p, a, g, lr, eps), oracle.adagrad(p, a, g2, lr, eps), (mu_p, mu_a)):
+        assert np.all(np.abs(y.astype(np.float64) - x) <= 1e-5 * mu)
+    m = rng.uniform(-1e-3, 1e-3, n).astype(np.float32)
+    v = rng.uniform(2.0 ** -18, 5 * 2.0 ** -18, n).astype(np.float32)
+    b1, b2, t = 0.9, 0.999, 1001
+    mu_p, mu_m, mu_v = oracle.adam_magnitude(p, m, v, g, gmu, 1e-3, b1, b2, eps, t)
+    for x, y, mu in zip(oracle.adam(p, m, v, g, 1e-3, b1, b2, eps, t), oracle.adam(p, m, v, g2, 1e-3, b1, b2, eps, t),
+                        (mu_p, mu_m, mu_v)):
+        assert np.all(np.abs(y.astype(np.float64) - x) <= 1e-5 * mu)
