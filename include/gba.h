@@ -42,7 +42,8 @@ typedef enum gba_status {
   GBA_ERR_INVALID_ARG = 2,   /* a size or mode is out of range               */
   GBA_ERR_UNSUPPORTED = 3,   /* valid but not supported (e.g. width D)       */
   GBA_ERR_WORKSPACE = 4,     /* workspace smaller than the size query asked  */
-  GBA_ERR_HIP = 5            /* a HIP launch failed                          */
+  GBA_ERR_HIP = 5,           /* a HIP launch failed                          */
+  GBA_ERR_SCRATCH_LIMIT = 6  /* sizes beyond the no-allocation call's array   */
 } gba_status;
 
 /* Bits OR-ed into *err by device code. */
@@ -166,6 +167,34 @@ gba_status gba_apply_adam(float* param, float* m, float* v, const float* grad, c
                           const int32_t* active, const int64_t* num_rows, int64_t n, int32_t D,
                           int64_t R, double lr, double beta1, double beta2, double eps, int64_t t,
                           int32_t* err, hipStream_t stream);
+
+/*
+ * gba_aggregate_sparse without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  The call allocates nothing: its scratch
+ * is a fixed device array of GBA_NOALLOC_SCRATCH_BYTES inside the library, one
+ * per device, created when the library's code is first loaded on that device
+ * and held until the process ends.  The first call on each device looks up the
+ * array's address (make that first call outside graph capture).
+ * Arguments, outputs, limits and errors as for gba_aggregate_sparse (agg is
+ * required), plus GBA_ERR_SCRATCH_LIMIT, returned before any device work, when
+ * gba_aggregate_sparse_workspace_size(N, K, D, R) exceeds the array (for
+ * example N above 2^20 occurrences at D = 256, or about 2.5 * 2^20 at D = 32).
+ * The outputs equal those of gba_aggregate_sparse bit for bit.
+ * Every call on one device shares that device's array, and a call leaves its
+ * contents behind (nothing in it must start at zero): calls that overlap in
+ * time on one device, on different streams or from different host threads,
+ * race on it and must be serialised by the caller.
+ */
+#define GBA_NOALLOC_SCRATCH_BYTES (64ull << 20)
+
+gba_status gba_aggregate_sparse_noalloc(const int64_t* ids, const float* rows,
+                                        const int64_t* contrib_offsets, int32_t K, int64_t N, int32_t D,
+                                        int64_t R, const float* w, const int64_t* tokens, int64_t step,
+                                        int64_t iota, int32_t* tag, gba_decay decay, gba_norm norm,
+                                        int64_t* unique_ids, int64_t* seg_offsets, int32_t* contrib_count,
+                                        int32_t* active_count, float* agg, int64_t* num_unique,
+                                        int32_t* err, hipStream_t stream);
 
 /*
  * gba_aggregate_sparse followed by the row form of gba_apply_adagrad /

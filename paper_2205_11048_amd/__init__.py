@@ -21,7 +21,8 @@ __all__ = [
     "gba_token_of_batch", "gba_pull_workspace_size", "gba_pull_rows", "gba_hash_clear",
     "gba_hash_workspace_size", "gba_hash_find_or_insert", "gba_hash_rehash", "EMPTY_ID", "DERR_TABLE_FULL",
     "gba_sort_ids_workspace_size", "gba_sort_ids", "SORT_AUTO", "SORT_PLAIN", "SORT_HOT",
-    "gba_aggregate_sparse_plan_workspace_size", "gba_aggregate_sparse_plan",
+    "gba_aggregate_sparse_plan_workspace_size", "gba_aggregate_sparse_plan", "gba_aggregate_sparse_noalloc",
+    "NOALLOC_SCRATCH_BYTES", "ERR_SCRATCH_LIMIT",
     "pointer_table", "DECAY_TOKEN", "DECAY_ID_TAG", "NORM_PER_ID_COUNT", "NORM_BY_K",
     "DERR_ID_RANGE", "DERR_FUTURE_TOKEN", "DERR_OFFSETS", "DERR_ROW_RANGE", "MAX_K", "MAX_D",
     "LIB_PATH",
@@ -38,6 +39,8 @@ DERR_ID_RANGE, DERR_FUTURE_TOKEN, DERR_OFFSETS, DERR_ROW_RANGE, DERR_TABLE_FULL 
 EMPTY_ID = -1
 SORT_AUTO, SORT_PLAIN, SORT_HOT = -1, 0, 1
 MAX_K, MAX_D = 4096, 256
+NOALLOC_SCRATCH_BYTES = 64 << 20     # GBA_NOALLOC_SCRATCH_BYTES
+ERR_SCRATCH_LIMIT = 6
 
 _P = ctypes.c_void_p
 _I32 = ctypes.c_int32
@@ -55,6 +58,8 @@ _SIGNATURES = {
                                                  _I32),
     "gba_aggregate_sparse_plan": ([_P, _P, _P, _I32, _I64, _I32, _I64, _P, _P, _I64, _I64, _P, _I32, _I32,
                                    _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _I32, _P, _P], _I32),
+    "gba_aggregate_sparse_noalloc": ([_P, _P, _P, _I32, _I64, _I32, _I64, _P, _P, _I64, _I64, _P, _I32, _I32,
+                                      _P, _P, _P, _P, _P, _P, _P, _P], _I32),
     "gba_aggregate_apply_dense_adagrad": ([_P, _P, _I32, _I64, _P, _P, _P, _F64, _F64, _P], _I32),
     "gba_aggregate_apply_dense_adam": ([_P, _P, _I32, _I64, _P, _P, _P, _P, _F64, _F64, _F64, _F64, _I64, _P],
                                        _I32),
@@ -379,6 +384,34 @@ def gba_aggregate_sparse_plan(ids, rows, contrib_offsets, R, w, tokens, step, io
         workspace.numel(), int(plan), _ptr(err), _stream(stream)))
 
 
+def gba_aggregate_sparse_noalloc(ids, rows, contrib_offsets, R, w, tokens, step, iota, tag, decay, norm,
+                                 unique_ids, seg_offsets, contrib_count, active_count, agg, num_unique,
+                                 err=None, stream=None):
+    """gba_aggregate_sparse with the library's fixed device scratch array
+    instead of a workspace (the call allocates nothing); sizes whose workspace
+    would exceed NOALLOC_SCRATCH_BYTES raise GBAError (status ERR_SCRATCH_LIMIT)."""
+    N = ids.numel()
+    K = contrib_offsets.numel() - 1
+    D = rows.shape[-1]
+    _need(ids, torch.int64, "ids")
+    _need(rows, torch.float32, "rows", N * D)
+    _need(contrib_offsets, torch.int64, "contrib_offsets")
+    _need(w, torch.float32, "w", K)
+    _need(tokens, torch.int64, "tokens", K)
+    _need(tag, torch.int32, "tag", R if tag is not None else None)
+    _need(unique_ids, torch.int64, "unique_ids", N)
+    _need(seg_offsets, torch.int64, "seg_offsets", N + 1)
+    _need(contrib_count, torch.int32, "contrib_count", N)
+    _need(active_count, torch.int32, "active_count", N)
+    _need(agg, torch.float32, "agg", N * D)
+    _need(num_unique, torch.int64, "num_unique", 1)
+    _need(err, torch.int32, "err", 1)
+    _check(lib().gba_aggregate_sparse_noalloc(
+        _ptr(ids), _ptr(rows), _ptr(contrib_offsets), K, N, D, int(R), _ptr(w), _ptr(tokens), int(step),
+        int(iota), _ptr(tag), int(decay), int(norm), _ptr(unique_ids), _ptr(seg_offsets),
+        _ptr(contrib_count), _ptr(active_count), _ptr(agg), _ptr(num_unique), _ptr(err), _stream(stream)))
+
+
 OPTIMIZER_ADAGRAD, OPTIMIZER_ADAM = 1, 2
 
 
@@ -472,3 +505,4 @@ def gba_apply_adam(param, m, v, grad, lr, beta1, beta2, eps, t, rows=None, activ
     _check(lib().gba_apply_adam(_ptr(param), _ptr(m), _ptr(v), _ptr(grad), _ptr(rows), _ptr(active),
                                 _ptr(num_rows), n, D, int(R), float(lr), float(beta1), float(beta2),
                                 float(eps), int(t), _ptr(err), _stream(stream)))
+

@@ -2,6 +2,7 @@
 // workspace layout and launch order.  No allocation, no synchronisation.
 #include <cmath>
 #include <cstdint>
+#include <mutex>
 
 #include "gba_internal.hpp"
 
@@ -41,6 +42,40 @@ AdamParams adam_params(double lr, double beta1, double beta2, double eps, int64_
 
 }  // namespace
 
+// ------------------------------------------------- the no-allocation variant
+// Scratch of gba_aggregate_sparse_noalloc: one array per device, created when
+// the code object is loaded there and held until the process ends.  Host code
+// never passes `scratch` itself to a kernel (in host code the name is only a
+// stand-in for the device symbol); it passes the device address looked up
+// once per device below.
+static __device__ __align__(256) unsigned char scratch[GBA_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};   // per device id; set once, under g_scratch_mu
+
+// Device address of the current device's copy of `scratch`.
+hipError_t current_device_scratch(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
+
+}  // namespace
+
 extern "C" {
 
 const char* gba_status_string(gba_status s) {
@@ -51,6 +86,8 @@ const char* gba_status_string(gba_status s) {
     case GBA_ERR_UNSUPPORTED: return "unsupported size or width";
     case GBA_ERR_WORKSPACE: return "workspace too small";
     case GBA_ERR_HIP: return "a HIP launch failed";
+    case GBA_ERR_SCRATCH_LIMIT:
+      return "sizes need more scratch than the fixed device array of the no-allocation call holds";
   }
   return "unknown status";
 }
@@ -252,6 +289,26 @@ gba_status gba_aggregate_sparse_plan(const int64_t* ids, const float* rows, cons
   return sparse_call(ids, rows, contrib_offsets, K, N, D, R, w, tokens, step, iota, tag, decay, norm, unique_ids,
                      seg_offsets, contrib_count, active_count, agg, num_unique, workspace, workspace_bytes, sort_plan,
                      nullptr, err, stream);
+}
+
+gba_status gba_aggregate_sparse_noalloc(const int64_t* ids, const float* rows, const int64_t* contrib_offsets,
+                                        int32_t K, int64_t N, int32_t D, int64_t R, const float* w,
+                                        const int64_t* tokens, int64_t step, int64_t iota, int32_t* tag,
+                                        gba_decay decay, gba_norm norm, int64_t* unique_ids,
+                                        int64_t* seg_offsets, int32_t* contrib_count, int32_t* active_count,
+                                        float* agg, int64_t* num_unique, int32_t* err, hipStream_t stream) {
+  // sizes first: a call the fixed array cannot hold is refused before any
+  // device work (and before the first-call symbol lookup)
+  if (K < 1 || K > GBA_MAX_K || N < 0 || N > kMaxN || R < 1 || R > (int64_t(1) << 32))
+    return GBA_ERR_INVALID_ARG;
+  if (!width_ok(D)) return GBA_ERR_UNSUPPORTED;
+  if (sparse_bytes(N, D, R, GBA_SORT_AUTO, nullptr) > (size_t)GBA_NOALLOC_SCRATCH_BYTES)
+    return GBA_ERR_SCRATCH_LIMIT;
+  void* ws = nullptr;
+  if (current_device_scratch(&ws) != hipSuccess) return GBA_ERR_HIP;
+  return sparse_call(ids, rows, contrib_offsets, K, N, D, R, w, tokens, step, iota, tag, decay, norm, unique_ids,
+                     seg_offsets, contrib_count, active_count, agg, num_unique, ws,
+                     (size_t)GBA_NOALLOC_SCRATCH_BYTES, GBA_SORT_AUTO, nullptr, err, stream);
 }
 
 gba_status gba_aggregate_apply_sparse_workspace_size(int64_t N, int32_t K, int32_t D, int64_t R, int32_t optimizer,

@@ -8,13 +8,18 @@ import pytest
 
 import paper_2205_11048_amd as gba
 
-HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "gba.h")
+INCLUDE = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
 
 
 def declared_functions():
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w[\w\s\*]*?\b(gba_\w+)\s*\(", text, flags=re.M)))
+    names = set()
+    for h in sorted(os.listdir(INCLUDE)):
+        if not h.endswith(".h"):
+            continue
+        text = open(os.path.join(INCLUDE, h)).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        names |= set(re.findall(r"^\s*(?:const\s+)?\w[\w\s\*]*?\b(gba_\w+)\s*\(", text, flags=re.M))
+    return sorted(names)
 
 
 def test_header_declares_the_five_calls():
@@ -50,6 +55,16 @@ def test_status_strings_and_workspace_query():
 
 def test_host_checks_return_before_any_launch():
     L = gba.lib()
+    # the no-allocation sparse call refuses sizes beyond its fixed array before
+    # any device work (D = 256 just above 2^20 occurrences)
+    assert b"no-allocation" in L.gba_status_string(6)
+    assert gba.gba_aggregate_sparse_workspace_size(1_100_000, 4, 256, 1000) > gba.NOALLOC_SCRATCH_BYTES
+    assert L.gba_aggregate_sparse_noalloc(None, None, None, 4, 1_100_000, 256, 1000, None, None, 0, 0, None, 0, 0,
+                                          None, None, None, None, None, None, None, None) == 6
+    assert L.gba_aggregate_sparse_noalloc(None, None, None, 0, 10, 16, 1000, None, None, 0, 0, None, 0, 0,
+                                          None, None, None, None, None, None, None, None) == 2
+    assert L.gba_aggregate_sparse_noalloc(None, None, None, 4, 10, 6, 1000, None, None, 0, 0, None, 0, 0,
+                                          None, None, None, None, None, None, None, None) == 3
     # null pointers and bad sizes are refused on the host, without touching a GPU
     assert L.gba_token_weights(None, 4, 0, 0, None, None, None, None, None) == 1
     assert L.gba_token_weights(None, 0, 0, 0, None, None, None, None, None) == 1
