@@ -63,7 +63,11 @@ def parse():
                     help="skip the leg that replays the step from a captured HIP graph")
     ap.add_argument("--step-only", action="store_true",
                     help="time the step only: no early-sum, pull or hash-storage legs (for kernel profiles)")
-    ap.add_argument("--cpu-sample", type=int, default=4, help="1/S of the workload for the oracle timing")
+    ap.add_argument("--cpu-sample", type=int, default=0,
+                    help="time the oracle on 1/S of the workload, scaled by S (default 0: over the whole workload, "
+                         "about a minute of host time at c4)")
+    ap.add_argument("--no-ceilings", dest="ceilings", action="store_false",
+                    help="skip the measurement kernels (read stream, copy stream, random row gathers)")
     return ap.parse_args()
 
 
@@ -215,6 +219,8 @@ def run_workload(name, args, torch, gba_step_mod, sdev, gba):
             d_done.record(dstream)
             stream.wait_event(d_done)
 
+    full_cpu = args.cpu_sample <= 0 and not args.no_cpu_baseline and name == args.workload
+    pre = capture_state(w, ds, torch) if full_cpu else None
     for _ in range(args.warmup):
         one_step()
     torch.cuda.synchronize()
@@ -343,6 +349,16 @@ def run_workload(name, args, torch, gba_step_mod, sdev, gba):
     if args.hash_storage:
         res["hash_storage"] = hash_leg(w, ds, st, gba, torch, stream, decay, start, end, max(3, args.steps // 2))
 
+    # the bandwidth of the step's access patterns (measurement kernels)
+    if args.ceilings and name == args.workload:
+        res["ceilings"] = ceilings(w, ds.table, gba, torch, stream)
+        print(f"[bench] {name}: ceilings measured", file=sys.stderr, flush=True)
+
+    if full_cpu:
+        res["cpu_baseline"] = cpu_baseline_full(w, ds, pre)
+        del pre
+        print(f"[bench] {name}: oracle timed over the whole workload", file=sys.stderr, flush=True)
+
     # pull side: one worker's request (the IDs of one contribution), rows looked
     # up once per distinct ID
     if args.step_only:
@@ -455,6 +471,84 @@ def hash_leg(w, ds, st, gba, torch, stream, decay, start, end, n):
                 find_or_insert_ms=float(np.mean([a.elapsed_time(b) for a, b in ev])))
 
 
+def ceilings(w, table, gba, torch, stream):
+    """Bandwidth of the step's access patterns on this GPU, each from the
+    plainest kernel that has it (include/gba_ceilings.h): a 4 GiB stream of
+    16-byte non-temporal reads (the dense sum's pattern), a 2 GiB stream copy,
+    and N gathers of random whole rows of the workload's table (the row
+    passes' pattern).  Each is timed over 5 launches per grid size, after one
+    warm-up, for a few grid sizes; the best grid is reported."""
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def timed(fn, reps=5):
+        fn()
+        start.record(stream)
+        for _ in range(reps):
+            fn()
+        end.record(stream)
+        torch.cuda.synchronize()
+        return start.elapsed_time(end) / reps
+
+    out = {}
+    grids = (1024, 2048, 4096, 8192)
+    sink = torch.empty(gba.gba_ceiling_sink_words(max(grids)), dtype=torch.int32, device="cuda")
+    src = torch.empty(1 << 30, dtype=torch.float32, device="cuda")        # 4 GiB
+    best = min((timed(lambda: gba.gba_ceiling_read(src, sink, b)), b) for b in grids)
+    nbytes = src.numel() * 4
+    out["read_stream"] = dict(bytes=nbytes, blocks=best[1], us=best[0] * 1e3, gbs=nbytes / (best[0] * 1e-3) / 1e9)
+    del src
+    a = torch.empty(1 << 29, dtype=torch.float32, device="cuda")           # 2 GiB each way
+    b_ = torch.empty_like(a)
+    best = min((timed(lambda: gba.gba_ceiling_copy(a, b_, b)), b) for b in grids)
+    nbytes = a.numel() * 4
+    out["copy_stream"] = dict(bytes_read=nbytes, bytes_written=nbytes, blocks=best[1], us=best[0] * 1e3,
+                              gbs=2 * nbytes / (best[0] * 1e-3) / 1e9)
+    del a, b_
+    g = torch.Generator(device="cuda")
+    g.manual_seed(2205110480)
+    rows = torch.randint(0, w.R, (w.N,), device="cuda", generator=g, dtype=torch.int64)
+    best = min((timed(lambda: gba.gba_ceiling_gather_rows(table, rows, sink, b)), b) for b in grids)
+    nbytes = w.N * w.D * 4 + w.N * 8
+    out["random_row_gather"] = dict(rows=w.N, row_bytes=w.D * 4, table_rows=w.R, bytes=nbytes, blocks=best[1],
+                                    us=best[0] * 1e3, gbs=nbytes / (best[0] * 1e-3) / 1e9)
+    del rows, sink
+    torch.cuda.empty_cache()
+    return out
+
+
+def host_cpu():
+    """CPU model of this host and the cores this process may run on."""
+    model = platform.processor() or platform.machine()
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        avail = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        avail = os.cpu_count()
+    return dict(cpu_model=model, nproc=os.cpu_count(), cores_available=avail)
+
+
+class _OracleClock:
+    """Wall and process CPU time spent inside oracle calls only."""
+
+    def __init__(self):
+        self.wall = 0.0
+        self.cpu = 0.0
+
+    def __call__(self, fn, *a, **kw):
+        w0, c0 = time.perf_counter(), time.process_time()
+        out = fn(*a, **kw)
+        self.wall += time.perf_counter() - w0
+        self.cpu += time.process_time() - c0
+        return out
+
+
 def cpu_baseline(name, S):
     """The oracle, untuned, on 1/S of the workload (all K contributions, B/S
     samples each, P/S dense parameters), one host thread; the measured time is
@@ -487,16 +581,76 @@ def cpu_baseline(name, S):
         return trows[k][np.searchsorted(uniq, r)]
 
     hp = dict(lr=ws.lr, eps=ws.eps, beta1=ws.beta1, beta2=ws.beta2)
-    t0 = time.perf_counter()
-    oracle.gba_step(tok, 1000, ws.iota, grads, ids, rows, off, param, dslots, rows_of, slot_rows_of,
-                    ws.optimizer, hp, t=ws.adam_t)
-    dt = time.perf_counter() - t0
+    clock = _OracleClock()
+    clock(oracle.gba_step, tok, 1000, ws.iota, grads, ids, rows, off, param, dslots, rows_of, slot_rows_of,
+          ws.optimizer, hp, t=ws.adam_t)
+    dt = clock.wall
     full_s = dt * S
     return dict(value=1.0 / full_s, unit="global batches/s", cores=1, kind="oracle",
                 sample=f"{name} at 1/{S}: K={ws.K} contributions of B={ws.B} samples x L={ws.L} IDs "
                        f"(N={ws.N}), P={ws.P} dense params, same Zipf law and R; oracle time {dt:.2f} s x {S}",
-                seconds_measured=dt, host=platform.processor() or platform.machine(),
-                nproc=os.cpu_count())
+                seconds_measured=dt, cpu_seconds=clock.cpu, **host_cpu())
+
+
+def capture_state(w, ds, torch):
+    """Host copies of the step's state before any step runs: the dense
+    parameters and optimiser slots, and for every distinct ID its table row
+    and slot rows (what the oracle reads; the generator's values)."""
+    uq = np.unique(ds.ids_host)
+    uq_t = torch.from_numpy(uq).to(ds.table.device)
+    st = dict(uq=uq, param=ds.param.cpu().numpy(), dslots=[x.cpu().numpy() for x in ds.dense_slots],
+              E=ds.table[uq_t].cpu().numpy(), S=[x[uq_t].cpu().numpy() for x in ds.table_slots])
+    del uq_t
+    return st
+
+
+def cpu_baseline_full(w, ds, pre, J=16):
+    """The oracle, untuned, over the whole workload on one host thread.  Its
+    inputs are the ones the device step reads, copied to the host and never
+    timed: the contributions as the generator wrote them (gradients, IDs,
+    rows) and the state captured before any step ran; only the oracle's calls
+    are timed.  The dense gradients arrive J contributions at a time and are
+    folded into the float64 running sum by the oracle's early weighted sum
+    (App. B), which in buffer order is bit for bit its one-shot sum; the
+    embedding part takes all N occurrences at once."""
+    import oracle
+    from synth.configs import STEP
+    clock = _OracleClock()
+    t0 = time.perf_counter()
+    tok = ds.tokens_host
+    wts, _, _ = clock(oracle.token_weights, tok, STEP, w.iota)
+    run = np.zeros(w.P, dtype=np.float64)
+    for lo in range(0, w.K, J):
+        hi = min(w.K, lo + J)
+        chunk = [ds.grads[m].cpu().numpy() if wts[m] != 0 else None for m in range(lo, hi)]
+        clock(oracle.accumulate_dense, run, chunk, wts[lo:hi])
+        del chunk
+    g_bar = clock(oracle.finalize_dense, run, w.K)
+    del run
+    hp = dict(lr=w.lr, eps=w.eps, beta1=w.beta1, beta2=w.beta2)
+    if w.optimizer == "adagrad":
+        clock(oracle.adagrad, pre["param"], pre["dslots"][0], g_bar, hp["lr"], hp["eps"])
+    else:
+        clock(oracle.adam, pre["param"], pre["dslots"][0], pre["dslots"][1], g_bar, hp["lr"], hp["beta1"],
+              hp["beta2"], hp["eps"], w.adam_t)
+    rows = ds.rows.cpu().numpy()
+    sp = clock(oracle.aggregate_sparse, ds.ids_host, rows, ds.offsets_host, wts, tok, STEP, w.iota)
+    del rows
+    assert np.array_equal(sp["unique_ids"], pre["uq"])
+    act = sp["active_count"] > 0
+    if w.optimizer == "adagrad":
+        clock(oracle.adagrad, pre["E"][act], pre["S"][0][act], sp["agg"][act], hp["lr"], hp["eps"])
+    else:
+        clock(oracle.adam, pre["E"][act], pre["S"][0][act], pre["S"][1][act], sp["agg"][act], hp["lr"],
+              hp["beta1"], hp["beta2"], hp["eps"], w.adam_t)
+    total_s = time.perf_counter() - t0
+    return dict(value=1.0 / clock.wall, unit="global batches/s", cores=1, kind="oracle",
+                sample=f"{w.name} in full: K={w.K} contributions of B={w.B} samples x L={w.L} IDs (N={w.N}), "
+                       f"P={w.P} dense params; dense gradients handed over {J} contributions at a time and "
+                       f"folded by the oracle's early weighted sum; oracle time {clock.wall:.1f} s (copies to "
+                       f"the host, not timed, {total_s - clock.wall:.1f} s)",
+                seconds_measured=clock.wall, cpu_seconds=clock.cpu, U=int(sp["num_unique"]),
+                U_act=int(act.sum()), **host_cpu())
 
 
 def main():
@@ -548,6 +702,7 @@ def main():
         "breakdown_ms": head["breakdown_ms"],
         "realised": {k: head[k] for k in ("K_eff", "N", "N_act", "U", "U_act", "step_alg_bytes")},
         "roofline": head["roofline"],
+        "ceilings": head.get("ceilings"),
         "early_weighted_sum": head["early_sum"],
         "pull": head.get("pull"),
         "hash_storage": head.get("hash_storage"),
@@ -555,7 +710,7 @@ def main():
         "other_workloads": others,
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_sample)
+        out["cpu_baseline"] = head.get("cpu_baseline") or cpu_baseline(args.workload, max(1, args.cpu_sample))
     print(json.dumps(out))
 
 

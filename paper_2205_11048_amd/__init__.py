@@ -22,7 +22,8 @@ __all__ = [
     "gba_hash_workspace_size", "gba_hash_find_or_insert", "gba_hash_rehash", "EMPTY_ID", "DERR_TABLE_FULL",
     "gba_sort_ids_workspace_size", "gba_sort_ids", "SORT_AUTO", "SORT_PLAIN", "SORT_HOT",
     "gba_aggregate_sparse_plan_workspace_size", "gba_aggregate_sparse_plan", "gba_aggregate_sparse_noalloc",
-    "NOALLOC_SCRATCH_BYTES", "ERR_SCRATCH_LIMIT",
+    "NOALLOC_SCRATCH_BYTES", "ERR_SCRATCH_LIMIT", "gba_ceiling_read", "gba_ceiling_copy",
+    "gba_ceiling_gather_rows", "gba_ceiling_sink_words",
     "pointer_table", "DECAY_TOKEN", "DECAY_ID_TAG", "NORM_PER_ID_COUNT", "NORM_BY_K",
     "DERR_ID_RANGE", "DERR_FUTURE_TOKEN", "DERR_OFFSETS", "DERR_ROW_RANGE", "MAX_K", "MAX_D",
     "LIB_PATH",
@@ -58,6 +59,10 @@ _SIGNATURES = {
                                                  _I32),
     "gba_aggregate_sparse_plan": ([_P, _P, _P, _I32, _I64, _I32, _I64, _P, _P, _I64, _I64, _P, _I32, _I32,
                                    _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _I32, _P, _P], _I32),
+    "gba_ceiling_read": ([_P, _I64, _P, _I32, _P], _I32),
+    "gba_ceiling_copy": ([_P, _P, _I64, _I32, _P], _I32),
+    "gba_ceiling_gather_rows": ([_P, _I64, _I32, _P, _I64, _P, _I32, _P], _I32),
+    "gba_ceiling_sink_words": ([_I32], _I64),
     "gba_aggregate_sparse_noalloc": ([_P, _P, _P, _I32, _I64, _I32, _I64, _P, _P, _I64, _I64, _P, _I32, _I32,
                                       _P, _P, _P, _P, _P, _P, _P, _P], _I32),
     "gba_aggregate_apply_dense_adagrad": ([_P, _P, _I32, _I64, _P, _P, _P, _F64, _F64, _P], _I32),
@@ -506,3 +511,38 @@ def gba_apply_adam(param, m, v, grad, lr, beta1, beta2, eps, t, rows=None, activ
                                 _ptr(num_rows), n, D, int(R), float(lr), float(beta1), float(beta2),
                                 float(eps), int(t), _ptr(err), _stream(stream)))
 
+
+# ------------------------------------------------- measurement kernels
+# (include/gba_ceilings.h: the bandwidth of the step's access patterns)
+def gba_ceiling_sink_words(blocks) -> int:
+    return int(lib().gba_ceiling_sink_words(int(blocks)))
+
+
+def _bytes16(t, name):
+    if not t.is_cuda or not t.is_contiguous():
+        raise GBAError(f"{name}: expected a contiguous tensor on the GPU")
+    return t.numel() * t.element_size() // 16
+
+
+def gba_ceiling_read(src, sink, blocks, stream=None):
+    """Reads every whole 16-byte vector of ``src`` once (non-temporal loads)."""
+    _need(sink, torch.int32, "sink", gba_ceiling_sink_words(blocks))
+    _check(lib().gba_ceiling_read(_ptr(src), _bytes16(src, "src"), _ptr(sink), int(blocks), _stream(stream)))
+
+
+def gba_ceiling_copy(src, dst, blocks, stream=None):
+    """Copies the whole 16-byte vectors of ``src`` to ``dst``."""
+    n16 = _bytes16(src, "src")
+    if _bytes16(dst, "dst") < n16:
+        raise GBAError("dst: smaller than src")
+    _check(lib().gba_ceiling_copy(_ptr(src), _ptr(dst), n16, int(blocks), _stream(stream)))
+
+
+def gba_ceiling_gather_rows(table, rows, sink, blocks, stream=None):
+    """Gathers table[rows[i]] for every i (rows: int64 on the GPU)."""
+    _need(table, torch.float32, "table")
+    _need(rows, torch.int64, "rows")
+    _need(sink, torch.int32, "sink", gba_ceiling_sink_words(blocks))
+    R, D = table.shape
+    _check(lib().gba_ceiling_gather_rows(_ptr(table), int(R), int(D), _ptr(rows), rows.numel(), _ptr(sink),
+                                         int(blocks), _stream(stream)))
