@@ -125,14 +125,26 @@ static HotTables hot_tables(char* ws, const SortLayout& L, int key_bits) {
   return t;
 }
 
-// Mask of the active lanes whose digit equals this lane's digit.
+// Mask of the active lanes whose digit equals this lane's digit.  Per bit,
+// the lanes that differ from this one are the ballot of the bit, flipped
+// where this lane's bit is 1: ballot ^ (0 or all ones), OR-ed into a mask of
+// mismatches (one sign-extending bit extract, a compare for the ballot and
+// one three-input bit operation per 32-lane half).
 __device__ __forceinline__ uint64_t match_digit(uint32_t digit, int bits, bool active) {
-  uint64_t m = __ballot(active);
-  for (int b = 0; b < bits; ++b) {
-    const bool bit = (digit >> b) & 1u;
-    const uint64_t bal = __ballot(bit);
-    m &= bit ? bal : ~bal;
+  uint32_t diff_lo, diff_hi;
+  {
+    const uint64_t on = __ballot(active);
+    diff_lo = ~(uint32_t)on;
+    diff_hi = ~(uint32_t)(on >> 32);
   }
+  for (int b = 0; b < bits; ++b) {
+    const uint32_t x = (uint32_t)((int32_t)(digit << (31 - b)) >> 31);   // 0 or all ones: the lane's bit b
+    const uint64_t bal = __ballot(x != 0u);
+    // diff | (ballot ^ x) in one gfx950 three-input bit operation (table: S0 | (S1 ^ S2))
+    diff_lo = __builtin_amdgcn_bitop3_b32(diff_lo, (uint32_t)bal, x, 0xF6);
+    diff_hi = __builtin_amdgcn_bitop3_b32(diff_hi, (uint32_t)(bal >> 32), x, 0xF6);
+  }
+  const uint64_t m = ~(((uint64_t)diff_hi << 32) | diff_lo);
   return active ? m : 0ull;
 }
 
