@@ -84,7 +84,6 @@ struct SortHot {
   const uint16_t* bucket = nullptr;     // [1024] hot IDs whose key >> bshift is below the index
   const uint32_t* prefix = nullptr;     // [256] hot occurrences of the hot IDs before h; [H] = all
   const uint32_t* meta = nullptr;       // [0] = H
-  const uint32_t* iv_total = nullptr;   // [256] cold keys with exactly h hot IDs below them
   int bshift = 0;
 };
 // Sorts ids (int64 [n], each checked against [0, R)) by value, stably.  The

@@ -321,7 +321,7 @@ __device__ __forceinline__ uint32_t hot_first_digit(uint32_t key, uint32_t mask,
 // drops the bounds checks, so no branch waits on a load and a phase's loads
 // are in flight together; only the last tile of a pass can be partial.
 // Returns whether an ID outside [0, R) was seen (first pass).
-template <bool FIRST, int ITEMS, bool FULL, bool HOT>
+template <bool FIRST, int ITEMS, bool FULL, bool HOT, bool IV>
 __device__ __forceinline__ bool count_tile(const void* __restrict__ keys_in, int64_t n, int64_t tile0, int shift,
                                            uint32_t mask, int64_t R, uint32_t* h_row, int lane,
                                            const HotLookup& hl, uint32_t cold_bins, uint32_t* iv,
@@ -367,7 +367,7 @@ __device__ __forceinline__ bool count_tile(const void* __restrict__ keys_in, int
           bool hot;
           uint32_t below;
           digit[4 * cc + e] = hot_first_digit(k4[e], mask, cold_bins, hl, &hot, &below);
-          if (!hot && (FULL || i0 + e < n)) atomicAdd(&iv[below], 1u);
+          if (IV && !hot && (FULL || i0 + e < n)) atomicAdd(&iv[below], 1u);
         } else {
           digit[4 * cc + e] = (k4[e] >> shift) & mask;
         }
@@ -450,12 +450,24 @@ sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n_arg, const uin
     if (tile >= tiles) break;
     const uint32_t mask = (1u << bits) - 1u;
     const int64_t tile0 = tile * tile_keys<ITEMS>();
-    if (tile0 + tile_keys<ITEMS>() <= n)
-      bad |= count_tile<FIRST, ITEMS, true, HOT>(keys_in, n, tile0, shift, mask, R, h[r], lane, hl, cold_bins, s_iv,
-                                                 ht.digit);
-    else
-      bad |= count_tile<FIRST, ITEMS, false, HOT>(keys_in, n, tile0, shift, mask, R, h[r], lane, hl, cold_bins,
-                                                  s_iv, ht.digit);
+    // the cold keys' counts by hot IDs below them are needed only for the
+    // merged output (split: the segment pass finds them from the sorted keys)
+    const bool full = tile0 + tile_keys<ITEMS>() <= n;
+    if (HOT && !ht.split) {
+      if (full)
+        bad |= count_tile<FIRST, ITEMS, true, HOT, true>(keys_in, n, tile0, shift, mask, R, h[r], lane, hl, cold_bins,
+                                                         s_iv, ht.digit);
+      else
+        bad |= count_tile<FIRST, ITEMS, false, HOT, true>(keys_in, n, tile0, shift, mask, R, h[r], lane, hl,
+                                                          cold_bins, s_iv, ht.digit);
+    } else {
+      if (full)
+        bad |= count_tile<FIRST, ITEMS, true, HOT, false>(keys_in, n, tile0, shift, mask, R, h[r], lane, hl,
+                                                          cold_bins, s_iv, ht.digit);
+      else
+        bad |= count_tile<FIRST, ITEMS, false, HOT, false>(keys_in, n, tile0, shift, mask, R, h[r], lane, hl,
+                                                           cold_bins, s_iv, ht.digit);
+    }
   }
   __syncthreads();
   // the block's tiles form one chunk: each tile's row holds the counts of the
@@ -471,7 +483,7 @@ sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n_arg, const uin
       s += h[k][d];
     }
     chunk[(int64_t)blockIdx.x * kRadix + d] = s;
-    if (HOT) ht.iv_chunk[(int64_t)blockIdx.x * kRadix + d] = s_iv[d];
+    if (HOT && !ht.split) ht.iv_chunk[(int64_t)blockIdx.x * kRadix + d] = s_iv[d];
   }
   if (FIRST && bad) raise_error(err, GBA_DERR_ID_RANGE);
 }
@@ -600,7 +612,7 @@ scatter_tile(const void* __restrict__ keys_in, const uint32_t* __restrict__ vals
   // hot bin d (ID d - cold_bins) starts after the cold keys with at most
   // d - cold_bins hot IDs below them: thread d takes column d - cold_bins
   uint32_t iv_tot = 0;
-  if (HOT && d >= (1 << bits)) iv_tot = ht.iv_total[d - (1 << bits)];
+  if (HOT && !ht.split && d >= (1 << bits)) iv_tot = ht.iv_total[d - (1 << bits)];
   // kColdLast: this thread's share of the hot tables, parked in registers
   // until the ranking is done with cnt
   uint32_t g_prefix = 0, g_id = 0, g_bucket0 = 0, g_bucket1 = 0, g_H = 0;
@@ -857,7 +869,6 @@ hipError_t launch_sort_ids(const int64_t* ids, int64_t n, int64_t R, const SortP
       split->bucket = ht.bucket;
       split->prefix = ht.prefix;
       split->meta = ht.meta;
-      split->iv_total = ht.iv_total;
       split->bshift = ht.bshift;
     }
   }
@@ -906,7 +917,7 @@ hipError_t launch_sort_ids(const int64_t* ids, int64_t n, int64_t R, const SortP
     }
 #undef GBA_HIST
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    const bool with_iv = pass == 0 && plan.hot;
+    const bool with_iv = pass == 0 && plan.hot && !ht.split;
     hipLaunchKernelGGL(sort_digit_scan_kernel, dim3(with_iv ? 2 * kRadix : kRadix), block, 0, stream, chunk,
                        nchunks, total, (const uint32_t*)ht.iv_chunk, ht.iv_total);
     if ((e = hipGetLastError()) != hipSuccess) return e;

@@ -116,8 +116,9 @@ static SegLayout seg_layout(int64_t N, int32_t D) {
   L.off_last_acc = o;  o += align_up(rt * (size_t)D * 8);
   // the position where each (cold) segment starts, and its end
   L.off_start = o;     o += align_up((n + 1) * 4);
-  // per hot ID: the cold segments below it, then the chunk prefix of its run
-  L.off_cnum = o;      o += align_up(2 * (kHotSlots + 1) * 4);
+  // per hot ID: the cold segments below it, the chunk prefix of its run, and
+  // the cold positions below it
+  L.off_cnum = o;      o += align_up(3 * (kHotSlots + 1) * 4);
   // per chunk of a hot run: float64 sums and (contributions, active, first and last contribution)
   L.hot_chunks = (N > 0 ? ceil_div(N, rows_tile(lanes_per_row(D), kGroupSpan)) : 1) + kHotSlots;
   L.off_hot_acc = o;   o += align_up((size_t)L.hot_chunks * D * 8);
@@ -393,7 +394,7 @@ seg_heads_kernel(const uint32_t* __restrict__ keys, int64_t N_arg, const uint32_
 // cold segment above them.
 __global__ void __launch_bounds__(kSegBlock)
 seg_finish_kernel(const SegmentArgs a, const uint32_t* __restrict__ total, uint32_t* __restrict__ seg_start,
-                  uint32_t* __restrict__ cnum, uint32_t* __restrict__ fix_count) {
+                  uint32_t* __restrict__ cnum, uint32_t* __restrict__ cold_below, uint32_t* __restrict__ fix_count) {
   const uint32_t U = *total;
   const uint32_t H = a.n_dev ? *a.hot.meta : 0u;
   const int64_t n = a.n_dev ? (int64_t)*a.n_dev : a.N;
@@ -403,7 +404,10 @@ seg_finish_kernel(const SegmentArgs a, const uint32_t* __restrict__ total, uint3
     seg_start[U] = (uint32_t)n;
     *fix_count = 0u;   // the row pass appends to the fixup list
   }
-  for (uint32_t h = threadIdx.x; h < H; h += kSegBlock) cnum[h] = U;
+  for (uint32_t h = threadIdx.x; h < H; h += kSegBlock) {
+    cnum[h] = U;
+    cold_below[h] = (uint32_t)n;
+  }
 }
 
 // Per-position pass: numbering, segment IDs and starts, packed words.
@@ -417,7 +421,7 @@ __global__ void __launch_bounds__(kSegBlock)
 seg_meta_kernel(SegmentArgs a, const uint32_t* __restrict__ tile_seg_base,
                 const int32_t* __restrict__ buckets, int q, int nbuckets, int64_t num_tiles,
                 uint32_t* __restrict__ packed, uint32_t* __restrict__ base32, uint32_t* __restrict__ seg_start,
-                uint32_t* __restrict__ cnum) {
+                uint32_t* __restrict__ cnum, uint32_t* __restrict__ cold_below) {
   extern __shared__ int32_t s_dyn[];
   __shared__ uint32_t s_wave_heads[kSegWaves];
   // split plan: the hot IDs, their buckets and the hot occurrences below each
@@ -549,7 +553,10 @@ seg_meta_kernel(SegmentArgs a, const uint32_t* __restrict__ tile_seg_base,
           below = hot_below(key[e], hbucket, s_hids, H, a.hot.bshift);
           const uint32_t kprev = e == 0 ? kp : key[e - 1];
           const uint32_t from = (p0 + e > 0) ? hot_below(kprev, hbucket, s_hids, H, a.hot.bshift) : 0u;
-          for (uint32_t h = from; h < below; ++h) cnum[h] = before;
+          for (uint32_t h = from; h < below; ++h) {
+            cnum[h] = before;
+            cold_below[h] = (uint32_t)(p0 + e);
+          }
         }
         const int64_t out = (int64_t)before + below;
         if (out < N) {   // always true when the numbering is consistent
@@ -1148,11 +1155,11 @@ hot_rows_kernel(SegmentArgs a, const int32_t* __restrict__ buckets, int q, int n
 // W_r and the weighted sum divided by c_r (or K).
 template <int LPR>
 __global__ void __launch_bounds__(kFixBlock)
-hot_finish_kernel(SegmentArgs a, HotPartials hp, const uint32_t* __restrict__ cnum) {
+hot_finish_kernel(SegmentArgs a, HotPartials hp, const uint32_t* __restrict__ cnum,
+                  const uint32_t* __restrict__ cold_below) {
   constexpr int G = kFixBlock / LPR;
   __shared__ f64x4 s_acc[kFixBlock];
   __shared__ int32_t s_c[G], s_a[G];
-  __shared__ uint32_t s_tmp[kFixBlock / kWave + 1];
   const uint32_t H = *a.hot.meta;
   const uint32_t h = blockIdx.x;
   if (h >= H) return;
@@ -1163,9 +1170,8 @@ hot_finish_kernel(SegmentArgs a, HotPartials hp, const uint32_t* __restrict__ cn
   const bool lane_on = lane * 4 < D;
   const int64_t key = a.hot.ids[h];
   const int64_t tg = (a.decay == GBA_DECAY_ID_TAG && key < a.R) ? (int64_t)a.tag[key] : -1;
-  // cold occurrences below the hot ID: cold keys with at most h hot IDs below them
-  uint32_t below_all;
-  (void)block_exclusive_scan<kFixBlock>((uint32_t)t <= h ? a.hot.iv_total[t] : 0u, s_tmp, &below_all);
+  // cold occurrences below the hot ID (found by the position pass)
+  const uint32_t below_all = cold_below[h];
   const uint32_t b0 = hp.cp[h], b1 = hp.cp[h + 1];
   f64x4 acc = {0.0, 0.0, 0.0, 0.0};
   int C = 0, A = 0;
@@ -1295,7 +1301,8 @@ static hipError_t launch_rows(const SegmentArgs& a, const uint32_t* packed, cons
     hipLaunchKernelGGL(hot_rows_kernel<LPR>, dim3((unsigned)L.hot_chunks), dim3(kSegBlock), lds, stream, a, buckets,
                        q, nb, hp);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(hot_finish_kernel<LPR>, dim3(kHotSlots), dim3(kFixBlock), 0, stream, a, hp, cnum);
+    hipLaunchKernelGGL(hot_finish_kernel<LPR>, dim3(kHotSlots), dim3(kFixBlock), 0, stream, a, hp, cnum,
+                       cnum + 2 * (kHotSlots + 1));
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   return hipSuccess;
@@ -1328,6 +1335,7 @@ hipError_t launch_segments(const SegmentArgs& a, void* ws, hipStream_t stream) {
   hp.acc = reinterpret_cast<double*>(base + L.off_hot_acc);
   hp.cnt = reinterpret_cast<int32_t*>(base + L.off_hot_cnt);
   hp.cp = cnum + kHotSlots + 1;
+  uint32_t* cold_below = cnum + 2 * (kHotSlots + 1);
 
   hipLaunchKernelGGL(check_offsets_kernel, dim3(1), dim3(256), 0, stream, a.offsets, a.K, a.N, a.err);
   hipError_t e = hipGetLastError();
@@ -1335,7 +1343,7 @@ hipError_t launch_segments(const SegmentArgs& a, void* ws, hipStream_t stream) {
   e = launch_run_heads(a.keys, a.N, heads, total, scan_ws, stream, a.n_dev);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(seg_finish_kernel, dim3(1), dim3(kSegBlock), 0, stream, a, (const uint32_t*)total, seg_start,
-                     cnum, part.fix_count);
+                     cnum, cold_below, part.fix_count);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (a.N <= 0) return hipSuccess;
 
@@ -1347,7 +1355,7 @@ hipError_t launch_segments(const SegmentArgs& a, void* ws, hipStream_t stream) {
   const size_t lds = (size_t)(3 * a.K + 1 + nb) * sizeof(int32_t);
   hipLaunchKernelGGL(seg_meta_kernel, dim3((unsigned)ceil_div(L.meta_tiles, kMetaTilesPerBlock)),
                      dim3(kSegBlock), lds, stream, a, (const uint32_t*)heads, (const int32_t*)buckets, q, nb,
-                     L.meta_tiles, packed, base32, seg_start, cnum);
+                     L.meta_tiles, packed, base32, seg_start, cnum, cold_below);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   switch (lanes_per_row(a.D)) {
     case 1: e = launch_rows<1>(a, packed, base32, part, seg_start, cnum, hp, buckets, q, nb, L, stream); break;
