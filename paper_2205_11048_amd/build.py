@@ -65,7 +65,35 @@ def build_all(jobs=8):
     return [build_gba(jobs), build_synth(jobs)]
 
 
+def build_gba_host_sanitized(jobs=8):
+    """libgba.so with AddressSanitizer and UndefinedBehaviorSanitizer on its
+    host code only (argument checks, workspace layout, launch logic; device
+    code is built as usual), into _build_sanitized/.  Load it with
+    GBA_LIBRARY and the clang ASan runtime preloaded."""
+    csrc = os.path.join(PKG, "csrc")
+    srcs = sorted(os.path.join(csrc, f) for f in os.listdir(csrc) if f.endswith(".hip"))
+    out_dir = os.path.join(PKG, "_build_sanitized")
+    os.makedirs(out_dir, exist_ok=True)
+    san = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+           "-Xarch_host", "-fno-omit-frame-pointer", "-g"]
+    inc = [f"-I{csrc}", f"-I{os.path.join(ROOT, 'include')}"]
+
+    def compile_one(src):
+        obj = os.path.join(out_dir, os.path.splitext(os.path.basename(src))[0] + ".o")
+        _run([HIPCC, *FLAGS, *san, *inc, "-c", src, "-o", obj])
+        return obj
+
+    with ThreadPoolExecutor(max_workers=jobs) as ex:
+        objs = list(ex.map(compile_one, srcs))
+    out_so = os.path.join(out_dir, "libgba_sanitized.so")
+    _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *san, *objs, "-o", out_so])
+    return out_so
+
+
 if __name__ == "__main__":
+    if "--sanitize-host" in sys.argv:
+        print("built", build_gba_host_sanitized())
+        sys.exit(0)
     for p in build_all():
         print("built", p)
     sys.exit(0)
