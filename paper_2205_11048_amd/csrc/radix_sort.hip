@@ -327,9 +327,10 @@ __device__ __forceinline__ bool count_tile(const void* __restrict__ keys_in, int
                                            const HotLookup& hl, uint32_t cold_bins, uint32_t* iv,
                                            uint8_t* __restrict__ dig_out) {
   constexpr int kHistKeys = 4 * ITEMS;   // keys per lane
-  // eight vectors (32 keys) per lane per phase, all in flight together (four
-  // with the hot lookup, whose registers would otherwise halve residency)
-  constexpr int kVecs = HOT ? 4 : 8;
+  // eight vectors (32 keys) per lane per phase, all in flight together (two
+  // with the hot lookup, which keeps the first pass at 8 waves per SIMD: its
+  // whole grid is then resident at once)
+  constexpr int kVecs = HOT ? 2 : 8;
   static_assert(kHistKeys % (4 * kVecs) == 0, "whole phases per tile");
   bool bad = false;
 #pragma unroll
@@ -413,7 +414,9 @@ __device__ __forceinline__ bool count_tile(const void* __restrict__ keys_in, int
 // kCold reads the key count from n_dev; kHotFirst also writes the chunk's
 // counts of cold keys by the number of hot IDs below them.
 template <bool FIRST, int ITEMS, int MODE, int TPW>
-__global__ void __launch_bounds__(kSortBlock)
+// Eight waves per SIMD (eight blocks of 20 KB of LDS fill a compute unit's
+// 160 KB): at 65.5 M keys the hot-key first pass has 2000 blocks, one round.
+__global__ void __launch_bounds__(kSortBlock) __attribute__((amdgpu_waves_per_eu(8, 8)))
 sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n_arg, const uint32_t* __restrict__ n_dev,
                       int shift, int bits, int64_t R, uint32_t* __restrict__ hist, uint32_t* __restrict__ chunk,
                       HotTables ht, int32_t* __restrict__ err) {
