@@ -142,7 +142,10 @@ gba_status gba_aggregate_sparse(const int64_t* ids, const float* rows,
 /*
  * Optimiser apply (Table 1 names Adagrad and Adam; rules of Duchi et al. 2011
  * and Kingma and Ba 2015).  Arithmetic in float64 from the float32 state,
- * each stored value rounded once.
+ * each stored value rounded once, except Adagrad in the row form (and in the
+ * fused sparse call): float32, with the hardware square root and reciprocal
+ * (each within 1 ulp), so the step lr * g / (sqrt(a') + eps) is within a few
+ * float32 ulps and p', a' are rounded once more.
  *
  * Dense form (rows == NULL): elementwise over n elements of param/state/grad.
  * Row form (rows != NULL): for i < *num_rows (device int64, <= n), when
@@ -201,7 +204,7 @@ gba_status gba_aggregate_sparse_noalloc(const int64_t* ids, const float* rows,
  * gba_apply_adam over its active rows (Alg. 2: embeddings are updated by ID
  * with the per-ID mean; Table 1 names the optimisers), in one call.  Table,
  * state and every output come out bitwise equal to those of the two separate
- * calls (the same float64 arithmetic, each stored value rounded once).  With
+ * calls (the same arithmetic and the same roundings).  With
  * Adagrad on rows of 20 to 32 floats (16 < D <= 32) the optimiser runs as each
  * ID's segment is finished, so the mean never makes a round trip through
  * memory; otherwise (other widths, Adam) the call aggregates and then applies.

@@ -331,7 +331,7 @@ def adam_magnitude(param, m, v, grad, grad_mu, lr, beta1, beta2, eps, t):
 # --------------------------------------------------------------------------
 def gba_step(tokens, step, iota, grads, ids, rows, offsets, param, dense_slots,
              table_rows_of, table_slot_rows_of, optimizer: str, hp: dict,
-             tag=None, decay=DECAY_TOKEN, norm=NORM_PER_ID_COUNT, t=None):
+             tag=None, decay=DECAY_TOKEN, norm=NORM_PER_ID_COUNT, t=None, magnitudes=False):
     """One global step on one shard.
 
     ``table_rows_of(r_array)`` and ``table_slot_rows_of(slot, r_array)`` return
@@ -340,24 +340,42 @@ def gba_step(tokens, step, iota, grads, ids, rows, offsets, param, dense_slots,
 
     Returns a dict: w, s, num_excluded, g_bar, param', dense slots', the
     sparse aggregate (see ``aggregate_sparse``), and for the active rows the
-    updated table rows and slot rows (keyed by ``active_ids``)."""
+    updated table rows and slot rows (keyed by ``active_ids``).  With
+    ``magnitudes``, also each updated value's magnitude companion (``*_mu``)
+    for the comparison rule."""
     w, s, n_ex = token_weights(tokens, step, iota)
     g_bar = aggregate_dense(grads, w)
     sp = aggregate_sparse(ids, rows, offsets, w, tokens, step, iota, tag, decay, norm)
     active = sp["unique_ids"][sp["active_count"] > 0]
     act_agg = sp["agg"][sp["active_count"] > 0]
     E = table_rows_of(active)
+    act_mu = sp["agg_mu"][sp["active_count"] > 0]
+    g_mu = aggregate_dense_magnitude(grads, w) if magnitudes else None
     if optimizer == "adagrad":
         p_new, a_new = adagrad(param, dense_slots[0], g_bar, hp["lr"], hp["eps"])
-        e_new, ea_new = adagrad(E, table_slot_rows_of(0, active), act_agg, hp["lr"], hp["eps"])
+        S0 = table_slot_rows_of(0, active)
+        e_new, ea_new = adagrad(E, S0, act_agg, hp["lr"], hp["eps"])
         dense_new, rows_new = [a_new], [ea_new]
+        if magnitudes:
+            mu_p, mu_a = adagrad_magnitude(param, dense_slots[0], g_bar, g_mu, hp["lr"], hp["eps"])
+            mu_e, mu_ea = adagrad_magnitude(E, S0, act_agg, act_mu, hp["lr"], hp["eps"])
+            dense_mu, rows_mu = [mu_a], [mu_ea]
     elif optimizer == "adam":
         p_new, m_new, v_new = adam(param, dense_slots[0], dense_slots[1], g_bar, hp["lr"],
                                    hp["beta1"], hp["beta2"], hp["eps"], t)
-        e_new, em_new, ev_new = adam(E, table_slot_rows_of(0, active), table_slot_rows_of(1, active),
-                                     act_agg, hp["lr"], hp["beta1"], hp["beta2"], hp["eps"], t)
+        S0, S1 = table_slot_rows_of(0, active), table_slot_rows_of(1, active)
+        e_new, em_new, ev_new = adam(E, S0, S1, act_agg, hp["lr"], hp["beta1"], hp["beta2"], hp["eps"], t)
         dense_new, rows_new = [m_new, v_new], [em_new, ev_new]
+        if magnitudes:
+            mu_p, mu_m, mu_v = adam_magnitude(param, dense_slots[0], dense_slots[1], g_bar, g_mu, hp["lr"],
+                                              hp["beta1"], hp["beta2"], hp["eps"], t)
+            mu_e, mu_em, mu_ev = adam_magnitude(E, S0, S1, act_agg, act_mu, hp["lr"], hp["beta1"],
+                                                hp["beta2"], hp["eps"], t)
+            dense_mu, rows_mu = [mu_m, mu_v], [mu_em, mu_ev]
     else:
         raise ValueError(optimizer)
-    return dict(w=w, s=s, num_excluded=n_ex, g_bar=g_bar, param=p_new, dense_slots=dense_new,
-                sparse=sp, active_ids=active, table_rows=e_new, table_slot_rows=rows_new)
+    out = dict(w=w, s=s, num_excluded=n_ex, g_bar=g_bar, param=p_new, dense_slots=dense_new,
+               sparse=sp, active_ids=active, table_rows=e_new, table_slot_rows=rows_new)
+    if magnitudes:
+        out.update(param_mu=mu_p, dense_slots_mu=dense_mu, table_rows_mu=mu_e, table_slot_rows_mu=rows_mu)
+    return out

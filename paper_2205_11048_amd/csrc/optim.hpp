@@ -1,6 +1,7 @@
-// Optimiser updates of one float32 element, computed in float64 and rounded
-// once per stored value.  Table 1 of the paper names Adagrad and Adam; the
-// rules are the textbook ones.
+// Optimiser updates of one float32 element.  Table 1 of the paper names
+// Adagrad and Adam; the rules are the textbook ones.  The dense updates and
+// Adam compute in float64 and round once per stored value; the Adagrad update
+// of table rows computes in float32 (below).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -14,6 +15,21 @@ __device__ __forceinline__ void adagrad_update(float& p, float& a, float g, doub
   const double pn = (double)p - lr * gd / (sqrt(an) + eps);
   p = (float)pn;
   a = (float)an;
+}
+
+// Adagrad on embedding-table rows: the same rule in float32, with the
+// hardware square root and reciprocal (v_sqrt_f32, v_rcp_f32: each within
+// 1 ulp).  The step lr g / (sqrt(a') + eps) comes out within a few float32
+// ulps of its exact value, and p' and a' take one rounding each, so the error
+// is a few 1e-7 of |p| + |step| and of a'.  The row passes gather random rows
+// and issue the update for every touched row: this form takes 8 instructions
+// per element, the float64 one some 35, among them a correctly rounded
+// float64 square root and division.
+__device__ __forceinline__ void adagrad_update_f32(float& p, float& a, float g, float lr, float eps) {
+  const float an = a + g * g;
+  const float den = __builtin_amdgcn_sqrtf(an) + eps;
+  p = p - (lr * g) * __builtin_amdgcn_rcpf(den);
+  a = an;
 }
 
 // Adam (Kingma and Ba 2015) with bias corrections bc1 = 1 - b1^t, bc2 = 1 - b2^t.

@@ -34,6 +34,7 @@ rows_apply_kernel(float* __restrict__ p, float* __restrict__ s1, float* __restri
   const int grp = threadIdx.x / LPR;
   int64_t count = *num_rows;
   if (count > n) count = n;
+  const float lr_f = (float)lr, eps_f = (float)eps;   // Adagrad on rows runs in float32
   bool bad = false;
   const int64_t stride = (int64_t)gridDim.x * G * kRowBatch;
   for (int64_t i0 = ((int64_t)blockIdx.x * G + grp) * kRowBatch; i0 < count; i0 += stride) {
@@ -76,7 +77,7 @@ rows_apply_kernel(float* __restrict__ p, float* __restrict__ s1, float* __restri
           store_stream(reinterpret_cast<f32x4*>(s2 + at), f32x4{ve[0], ve[1], ve[2], ve[3]});
         } else {
 #pragma unroll
-          for (int e = 0; e < 4; ++e) adagrad_update(pe[e], ae[e], ge[e], lr, eps);
+          for (int e = 0; e < 4; ++e) adagrad_update_f32(pe[e], ae[e], ge[e], lr_f, eps_f);
         }
         store_stream(reinterpret_cast<f32x4*>(p + at), f32x4{pe[0], pe[1], pe[2], pe[3]});
         store_stream(reinterpret_cast<f32x4*>(s1 + at), f32x4{ae[0], ae[1], ae[2], ae[3]});

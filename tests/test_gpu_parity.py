@@ -463,16 +463,20 @@ def test_apply_rows(opt, D):
     sel = np.nonzero(active[:count] > 0)[0]
     upd[rows[sel]] = True
     et, e1, e2 = table.copy(), s1.copy(), s2.copy()
+    mt, m1 = None, None
     if opt == "adagrad":
         et[rows[sel]], e1[rows[sel]] = oracle.adagrad(table[rows[sel]], s1[rows[sel]], g[sel], 0.01, 1e-8)
+        mt, m1 = np.abs(table).astype(np.float64), np.abs(s1).astype(np.float64)
+        mt[rows[sel]], m1[rows[sel]] = oracle.adagrad_magnitude(table[rows[sel]], s1[rows[sel]], g[sel],
+                                                                np.abs(g[sel]), 0.01, 1e-8)
     else:
         et[rows[sel]], e1[rows[sel]], e2[rows[sel]] = oracle.adam(table[rows[sel]], s1[rows[sel]], s2[rows[sel]],
                                                                   g[sel], 1e-3, 0.9, 0.999, 1e-8, 7)
     gt, g1, g2 = host(td), host(s1d), host(s2d)
     assert_exact(gt[~upd], table[~upd], "untouched rows")
     assert_exact(g1[~upd], s1[~upd], "untouched state")
-    assert_rule_t(gt, et, None, "table")
-    assert_rule_t(g1, e1, None, "slot1")
+    assert_rule_t(gt, et, mt, "table")
+    assert_rule_t(g1, e1, m1, "slot1")
     if opt == "adam":
         assert_rule_t(g2, e2, None, "slot2")
     assert int(host(err)[0]) == 0
@@ -517,7 +521,7 @@ def test_full_step_small(decay, opt, D, fused):
     hp = dict(lr=c.lr, eps=c.eps, beta1=c.beta1, beta2=c.beta2)
     ref = oracle.gba_step(hs.tokens, hs.step, c.iota, hs.grads, hs.ids, hs.rows, hs.offsets, hs.param,
                           hs.dense_slots, lambda r: hs.table[r], lambda k, r: hs.table_slots[k][r], opt, hp,
-                          tag=hs.tags, decay=decay, t=c.adam_t)
+                          tag=hs.tags, decay=decay, t=c.adam_t, magnitudes=True)
     assert int(host(stepper.err)[0]) == 0
     assert_exact(host(stepper.w), ref["w"], "w")
     assert int(host(stepper.num_excluded)[0]) == ref["num_excluded"]
@@ -527,12 +531,12 @@ def test_full_step_small(decay, opt, D, fused):
         assert_rule_t(host(dslots[k]), s, None, f"dense slot {k}")
     t_after = host(table)
     act = ref["active_ids"]
-    assert_rule_t(t_after[act], ref["table_rows"], None, "table rows")
+    assert_rule_t(t_after[act], ref["table_rows"], ref["table_rows_mu"], "table rows")
     untouched = np.ones(c.R, bool)
     untouched[act] = False
     assert_exact(t_after[untouched], hs.table[untouched], "untouched rows")
-    for k, s in enumerate(ref["table_slot_rows"]):
-        assert_rule_t(host(tslots[k])[act], s, None, f"table slot {k}")
+    for k, (s, mu) in enumerate(zip(ref["table_slot_rows"], ref["table_slot_rows_mu"])):
+        assert_rule_t(host(tslots[k])[act], s, mu, f"table slot {k}")
     if decay == "id_tag":
         assert_exact(host(tag), ref["sparse"]["new_tag"], "tag")
 
@@ -562,7 +566,7 @@ def test_eq1_limits_through_the_step(opt, decay, iota):
     hp = dict(lr=c.lr, eps=c.eps, beta1=c.beta1, beta2=c.beta2)
     ref = oracle.gba_step(hs.tokens, hs.step, int(iota), hs.grads, hs.ids, hs.rows, hs.offsets, hs.param,
                           hs.dense_slots, lambda r: hs.table[r], lambda k, r: hs.table_slots[k][r], opt, hp,
-                          tag=hs.tags, decay=decay, t=c.adam_t)
+                          tag=hs.tags, decay=decay, t=c.adam_t, magnitudes=True)
     keep_all = iota > 0
     assert int(host(stepper.err)[0]) == 0
     assert_exact(host(stepper.w), ref["w"], "w")
@@ -583,9 +587,9 @@ def test_eq1_limits_through_the_step(opt, decay, iota):
     act = ref["active_ids"]
     assert act.size == (U if keep_all else 0)
     if act.size:
-        assert_rule_t(t_after[act], ref["table_rows"], None, "table rows")
-        for k, s in enumerate(ref["table_slot_rows"]):
-            assert_rule_t(host(tslots[k])[act], s, None, f"table slot {k}")
+        assert_rule_t(t_after[act], ref["table_rows"], ref["table_rows_mu"], "table rows")
+        for k, (s, mu) in enumerate(zip(ref["table_slot_rows"], ref["table_slot_rows_mu"])):
+            assert_rule_t(host(tslots[k])[act], s, mu, f"table slot {k}")
     untouched = np.ones(c.R, bool)
     untouched[act] = False
     assert_exact(t_after[untouched], hs.table[untouched], "untouched rows")
@@ -1087,12 +1091,12 @@ def test_hash_backed_push_step(opt):
     hp = dict(lr=c.lr, eps=c.eps, beta1=c.beta1, beta2=c.beta2)
     ref = oracle.gba_step(hs.tokens, hs.step, c.iota, hs.grads, hs.ids, hs.rows, hs.offsets, hs.param,
                           hs.dense_slots, lambda r: hs.table[r], lambda k, r: hs.table_slots[k][r], opt, hp,
-                          t=c.adam_t)
+                          t=c.adam_t, magnitudes=True)
     row_of_orig = dict(zip(orig_of_row.tolist(), range(U)))
     act_rows = np.array([row_of_orig[r] for r in ref["active_ids"]])
-    assert_rule_t(host(pool)[act_rows], ref["table_rows"], None, "rows")
-    for k, s_ in enumerate(ref["table_slot_rows"]):
-        assert_rule_t(host(pslots[k])[act_rows], s_, None, f"slot {k}")
+    assert_rule_t(host(pool)[act_rows], ref["table_rows"], ref["table_rows_mu"], "rows")
+    for k, (s_, mu) in enumerate(zip(ref["table_slot_rows"], ref["table_slot_rows_mu"])):
+        assert_rule_t(host(pslots[k])[act_rows], s_, mu, f"slot {k}")
 
 
 # ------------------------------------------------ capture in a HIP graph
