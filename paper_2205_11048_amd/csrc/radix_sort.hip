@@ -327,10 +327,10 @@ __device__ __forceinline__ bool count_tile(const void* __restrict__ keys_in, int
                                            const HotLookup& hl, uint32_t cold_bins, uint32_t* iv,
                                            uint8_t* __restrict__ dig_out) {
   constexpr int kHistKeys = 4 * ITEMS;   // keys per lane
-  // eight vectors (32 keys) per lane per phase, all in flight together (two
-  // with the hot lookup, which keeps the first pass at 8 waves per SIMD: its
-  // whole grid is then resident at once)
-  constexpr int kVecs = HOT ? 2 : 8;
+  // eight vectors (32 keys) per lane per phase, all in flight together; on
+  // the first pass, whose 8-byte IDs take twice the registers, four (two with
+  // the hot lookup), which keeps the kernel at 8 waves per SIMD
+  constexpr int kVecs = HOT ? 2 : (FIRST ? 4 : 8);
   static_assert(kHistKeys % (4 * kVecs) == 0, "whole phases per tile");
   bool bad = false;
 #pragma unroll
@@ -409,19 +409,21 @@ __device__ __forceinline__ bool count_tile(const void* __restrict__ keys_in, int
   return bad;
 }
 
-// Digit counts of the four tiles of one chunk, one wave per tile; each adds
-// one count per run of equal digits among each lane's 4 consecutive keys.
+// Digit counts of the tiles of one chunk (4 or 16), one wave per tile; each
+// adds one count per run of equal digits among each lane's 4 consecutive keys.
 // kCold reads the key count from n_dev; kHotFirst also writes the chunk's
 // counts of cold keys by the number of hot IDs below them.
+// Eight waves per SIMD: the blocks of a pass are then all resident at once
+// where the grid allows (at 65.5 M keys the hot-key first pass has 2000
+// blocks of 16 waves; the cold passes have some 500 active blocks).
 template <bool FIRST, int ITEMS, int MODE, int TPW>
-// Eight waves per SIMD (eight blocks of 20 KB of LDS fill a compute unit's
-// 160 KB): at 65.5 M keys the hot-key first pass has 2000 blocks, one round.
-__global__ void __launch_bounds__(kSortBlock) __attribute__((amdgpu_waves_per_eu(8, 8)))
+__global__ void __launch_bounds__(kSortWaves * TPW * kWave) __attribute__((amdgpu_waves_per_eu(8, 8)))
 sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n_arg, const uint32_t* __restrict__ n_dev,
                       int shift, int bits, int64_t R, uint32_t* __restrict__ hist, uint32_t* __restrict__ chunk,
                       HotTables ht, int32_t* __restrict__ err) {
   constexpr bool HOT = MODE == kHotFirst;
-  constexpr int kTiles = kSortWaves * TPW;   // the chunk
+  constexpr int kTiles = kSortWaves * TPW;   // the chunk: one tile per wave
+  static_assert(kTiles * kWave >= kRadix, "a thread per digit for the chunk rows");
   __shared__ uint32_t h[kTiles][kRadix];
   __shared__ uint32_t s_bucket_w[HOT ? kHotBuckets / 2 : 1];   // uint16 entries
   __shared__ uint32_t s_ids[HOT ? 256 : 1];
@@ -431,26 +433,22 @@ sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n_arg, const uin
   const int64_t tiles = ceil_div(n, tile_keys<ITEMS>());
   const int w = threadIdx.x / kWave;
   const int lane = lane_id();
-#pragma unroll
-  for (int k = 0; k < TPW; ++k)
-    for (int i = lane; i < kRadix; i += kWave) h[w * TPW + k][i] = 0u;
+  for (int i = lane; i < kRadix; i += kWave) h[w][i] = 0u;
   HotLookup hl{s_bucket, s_ids, 0u, ht.bshift};
   uint32_t cold_bins = 0;
   if (HOT) {
     load_hot_tables(ht, s_bucket, s_ids);
-    s_iv[threadIdx.x] = 0u;
+    if (threadIdx.x < kRadix) s_iv[threadIdx.x] = 0u;
     hl.H = ht.meta[0];
     cold_bins = 1u << bits;
     __syncthreads();
   } else {
     __builtin_amdgcn_wave_barrier();
   }
-  // wave w counts the chunk's tiles w * TPW + k, each into its own row
+  // wave w counts the chunk's tile w into row w
   bool bad = false;
-  for (int k = 0; k < TPW; ++k) {
-    const int r = w * TPW + k;
-    const int64_t tile = (int64_t)blockIdx.x * kTiles + r;
-    if (tile >= tiles) break;
+  const int64_t tile = (int64_t)blockIdx.x * kTiles + w;
+  if (tile < tiles) {
     const uint32_t mask = (1u << bits) - 1u;
     const int64_t tile0 = tile * tile_keys<ITEMS>();
     // the cold keys' counts by hot IDs below them are needed only for the
@@ -458,17 +456,17 @@ sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n_arg, const uin
     const bool full = tile0 + tile_keys<ITEMS>() <= n;
     if (HOT && !ht.split) {
       if (full)
-        bad |= count_tile<FIRST, ITEMS, true, HOT, true>(keys_in, n, tile0, shift, mask, R, h[r], lane, hl, cold_bins,
+        bad |= count_tile<FIRST, ITEMS, true, HOT, true>(keys_in, n, tile0, shift, mask, R, h[w], lane, hl, cold_bins,
                                                          s_iv, ht.digit);
       else
-        bad |= count_tile<FIRST, ITEMS, false, HOT, true>(keys_in, n, tile0, shift, mask, R, h[r], lane, hl,
+        bad |= count_tile<FIRST, ITEMS, false, HOT, true>(keys_in, n, tile0, shift, mask, R, h[w], lane, hl,
                                                           cold_bins, s_iv, ht.digit);
     } else {
       if (full)
-        bad |= count_tile<FIRST, ITEMS, true, HOT, false>(keys_in, n, tile0, shift, mask, R, h[r], lane, hl,
+        bad |= count_tile<FIRST, ITEMS, true, HOT, false>(keys_in, n, tile0, shift, mask, R, h[w], lane, hl,
                                                           cold_bins, s_iv, ht.digit);
       else
-        bad |= count_tile<FIRST, ITEMS, false, HOT, false>(keys_in, n, tile0, shift, mask, R, h[r], lane, hl,
+        bad |= count_tile<FIRST, ITEMS, false, HOT, false>(keys_in, n, tile0, shift, mask, R, h[w], lane, hl,
                                                            cold_bins, s_iv, ht.digit);
     }
   }
@@ -476,7 +474,7 @@ sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n_arg, const uin
   // the block's tiles form one chunk: each tile's row holds the counts of the
   // chunk's earlier tiles (so the scatter needs one row, not a loop over
   // rows), and the chunk row holds the chunk's counts
-  {
+  if (threadIdx.x < kRadix) {
     const int d = threadIdx.x;
     const int64_t t0 = (int64_t)blockIdx.x * kTiles;
     uint32_t s = 0;
@@ -903,11 +901,11 @@ hipError_t launch_sort_ids(const int64_t* ids, int64_t n, int64_t R, const SortP
     const dim3 grid((unsigned)tiles), hgrid((unsigned)nchunks);
 #define GBA_HIST(F, IT, MD, NDEV)                                                                            \
   if (tpw == 4)                                                                                              \
-    hipLaunchKernelGGL((sort_tile_hist_kernel<F, IT, MD, 4>), hgrid, block, 0, stream, kin, n, NDEV, shift, bits, R, \
-                       hist, chunk, ht, err);                                                                \
+    hipLaunchKernelGGL((sort_tile_hist_kernel<F, IT, MD, 4>), hgrid, dim3(4 * kSortWaves * kWave), 0, stream, kin, n, \
+                       NDEV, shift, bits, R, hist, chunk, ht, err);                                          \
   else                                                                                                       \
-    hipLaunchKernelGGL((sort_tile_hist_kernel<F, IT, MD, 1>), hgrid, block, 0, stream, kin, n, NDEV, shift, bits, R, \
-                       hist, chunk, ht, err);
+    hipLaunchKernelGGL((sort_tile_hist_kernel<F, IT, MD, 1>), hgrid, dim3(kSortWaves * kWave), 0, stream, kin, n,     \
+                       NDEV, shift, bits, R, hist, chunk, ht, err);
     static_assert(kSortWaves == 4, "chunk_shift assumes 4 or 16 tiles per chunk");
     if (pass == 0 && plan.hot) {
       GBA_HIST(true, kItemsHotFirst, kHotFirst, (const uint32_t*)nullptr)
