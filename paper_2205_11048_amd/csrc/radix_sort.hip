@@ -315,6 +315,11 @@ __device__ __forceinline__ uint32_t hot_first_digit(uint32_t key, uint32_t mask,
   return *hot ? cold_bins + *below : (key & mask);
 }
 
+// Copies of each digit counter in a histogram row, interleaved (lane l adds
+// to copy l % kHistCopies, in the next LDS bank): lanes that add to the same
+// frequent digit (a hot ID) touch different words.
+constexpr int kHistCopies = 4;
+
 // Digit counts of one tile into the wave's LDS row h_row.  Lane l holds keys
 // tile0 + 4 * (l + 64 * c) + e, c < ITEMS, e < 4: each vector load of the
 // wave covers 1 KB of consecutive keys.  FULL (every key of the tile exists)
@@ -397,13 +402,13 @@ __device__ __forceinline__ bool count_tile(const void* __restrict__ keys_in, int
           if (digit[4 * cc + e] == cur) {
             ++len;
           } else {
-            atomicAdd(&h_row[cur], len);
+            atomicAdd(&h_row[cur * kHistCopies + (lane % kHistCopies)], len);
             cur = digit[4 * cc + e];
             len = 1;
           }
         }
       }
-      if (len) atomicAdd(&h_row[cur], len);
+      if (len) atomicAdd(&h_row[cur * kHistCopies + (lane % kHistCopies)], len);
     }
   }
   return bad;
@@ -424,7 +429,7 @@ sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n_arg, const uin
   constexpr bool HOT = MODE == kHotFirst;
   constexpr int kTiles = kSortWaves * TPW;   // the chunk: one tile per wave
   static_assert(kTiles * kWave >= kRadix, "a thread per digit for the chunk rows");
-  __shared__ uint32_t h[kTiles][kRadix];
+  __shared__ uint32_t h[kTiles][kRadix * kHistCopies];
   __shared__ uint32_t s_bucket_w[HOT ? kHotBuckets / 2 : 1];   // uint16 entries
   __shared__ uint32_t s_ids[HOT ? 256 : 1];
   __shared__ uint32_t s_iv[HOT ? kRadix : 1];
@@ -433,7 +438,7 @@ sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n_arg, const uin
   const int64_t tiles = ceil_div(n, tile_keys<ITEMS>());
   const int w = threadIdx.x / kWave;
   const int lane = lane_id();
-  for (int i = lane; i < kRadix; i += kWave) h[w][i] = 0u;
+  for (int i = lane; i < kRadix * kHistCopies; i += kWave) h[w][i] = 0u;
   HotLookup hl{s_bucket, s_ids, 0u, ht.bshift};
   uint32_t cold_bins = 0;
   if (HOT) {
@@ -481,7 +486,10 @@ sort_tile_hist_kernel(const void* __restrict__ keys_in, int64_t n_arg, const uin
 #pragma unroll
     for (int k = 0; k < kTiles; ++k) {
       if (t0 + k < tiles) hist[(t0 + k) * kRadix + d] = s;
-      s += h[k][d];
+      uint32_t c = 0;
+#pragma unroll
+      for (int j = 0; j < kHistCopies; ++j) c += h[k][d * kHistCopies + j];
+      s += c;
     }
     chunk[(int64_t)blockIdx.x * kRadix + d] = s;
     if (HOT && !ht.split) ht.iv_chunk[(int64_t)blockIdx.x * kRadix + d] = s_iv[d];
