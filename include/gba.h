@@ -370,11 +370,11 @@ gba_status gba_aggregate_sparse_plan(const int64_t* ids, const float* rows,
  *
  * gba_token_of_batch (host function, no device work): the token handed out
  * with the i-th batch of the data list, t_i = floor(i / M) with M = K the
- * number of gradients aggregated per step: tokens start at 0 and each value
- * repeats M times, in ascending order.  (The formula printed in Sec. 3.1
- * divides by the number of updates K instead, which would contradict the rule
- * stated beside it that every token value occurs M times; that rule is the one
- * followed.)  Returns -1 if i < 0 or M < 1.
+ * number of gradients aggregated per step: batches 0 .. M-1 get token 0, the
+ * next M batches token 1, and so on.  (The formula printed in Sec. 3.1
+ * divides by the number of updates K instead, which would contradict the
+ * token count per value given beside it, M; the count is the one followed.)
+ * Returns -1 if i < 0 or M < 1.
  *
  * gba_pull_rows: the embedding rows for a worker's request, looked up once per
  * distinct ID.

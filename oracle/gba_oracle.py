@@ -53,9 +53,9 @@ design notes of the repository, with its reason):
       result equals the one-shot sum bit for bit.  Embedding rows are kept as
       they arrive (their buffer is already O(sum of n_m D)) and reduced at the
       step.
-* R10 The token of the i-th batch is floor(i / M): the text says each token
-      value repeats M times and the values ascend, while the printed formula
-      divides by K, the number of updates; the repetition rule is followed.
+* R10 The token of the i-th batch is floor(i / M): the text gives M batches
+      per token value, in ascending order, while the printed formula divides
+      by K, the number of updates; the M batches per value are followed.
 """
 from __future__ import annotations
 
@@ -252,8 +252,8 @@ def aggregate_sparse_occurrences(ids, m_of_j, rows, K: int, w, tokens, step: int
 # Sec. 3.1 token list and Alg. 2 pull responder
 # --------------------------------------------------------------------------
 def token_of_batch(i: int, M: int) -> int:
-    """Token attached to the i-th batch of the data list: values start at 0
-    and each repeats M times, in ascending order (Sec. 3.1; R10)."""
+    """Token attached to the i-th batch of the data list: batches 0 .. M-1
+    get 0, the next M batches 1, and so on (Sec. 3.1; R10)."""
     if i < 0 or M < 1:
         raise ValueError("i >= 0 and M >= 1 required")
     return i // M

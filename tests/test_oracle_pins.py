@@ -399,9 +399,10 @@ def test_early_sum_is_bitwise_the_one_shot_sum_and_skips_excluded():
 
 
 # ------------------------------------------------- Sec. 3.1, Alg. 2 pull side
-def test_token_list_repeats_each_value_m_times_in_ascending_order():
-    """Sec. 3.1: tokens start from zero, each value repeats M times, and the
-    list ascends; with Q batches there are ceil(Q / M) distinct values."""
+def test_token_list_gives_m_batches_per_value_in_ascending_order():
+    """Sec. 3.1: tokens start from zero, M consecutive batches share each
+    value, and the list ascends; with Q batches there are ceil(Q / M)
+    distinct values."""
     for M in (1, 3, 4, 64):
         Q = 10 * M + 3
         toks = [oracle.token_of_batch(i, M) for i in range(Q)]
