@@ -41,7 +41,11 @@ constexpr int64_t kMetaTile = (int64_t)kSegBlock * kRounds;  // 1024 positions: 
 static_assert(kMetaTile == kRunTile, "run-head tiles are the per-position tiles");
 constexpr int kGroupSpan = 128;                              // positions per lane group (most; hot_rows)
 constexpr int kBase32Span = 32;                              // the segment count is kept every 32 positions
-constexpr int kBatch = 8;                                    // row gathers per batch of a group
+constexpr int kBatch = 8;                                    // positions per batch of a group
+// Row gathers in flight per group: a batch's rows are gathered and summed in
+// two parts of four, which leaves the fused row pass 121 VGPRs (4 waves per
+// SIMD) instead of 139 (3): more waves in flight beat more loads per wave.
+constexpr int kBatchPart = 4;
 constexpr int kMaxBuckets = 1024;                            // contribution lookup buckets
 
 // packed word of a sorted position
@@ -625,6 +629,9 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
   static_assert(APPLY == 0 || kPark, "the row apply is fused where segments are parked");
   static_assert(APPLY == 0 || APPLY == 1, "the fused row apply is Adagrad only");
   constexpr int kSlots = GW * kBatch;
+  // rows gathered at a time: the batch in parts of kPart (registers: each
+  // lane holds kPart 16-byte row pieces while they are in flight)
+  constexpr int kPart = kBatchPart;
   __shared__ f32x4 s_park[kPark ? kSegWaves : 1][kPark ? kSlots : 1][LPR];
   __shared__ uint32_t s_park_out[kPark ? kSegWaves : 1][kSlots];
   __shared__ uint32_t s_park_cw[kPark ? kSegWaves : 1][kSlots];
@@ -715,30 +722,26 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
     // bytes of the rows, which stay in cache, and is zeroed when summed.  With
     // no load inside a branch, the compiler can count the loads in flight and
     // never waits for all of them at once.
-    auto gather = [&](int i0, const uint32_t (&word)[kBatch], f32x4 (&rv)[kBatch], uint32_t& use) {
-      use = 0;
+    // rows u0 .. u0 + kPart - 1 of the batch into rv[0 .. kPart)
+    auto gather = [&](int i0, int u0, const uint32_t (&word)[kBatch], f32x4 (&rv)[kPart], uint32_t& use) {
 #pragma unroll
-      for (int u = 0; u < kBatch; ++u) {
+      for (int v = 0; v < kPart; ++v) {
+        const int u = u0 + v;
         const uint32_t jv = word[u] & kIndexMask;
         const bool on = i0 + u < nvalid && !(word[u] & kZeroW) && lane_on && (int64_t)jv < N;
         use |= on ? (1u << u) : 0u;
-        rv[u] = *reinterpret_cast<const f32x4*>(a.rows + (on ? (int64_t)jv * D + gl * 4 : 0));
+        rv[v] = *reinterpret_cast<const f32x4*>(a.rows + (on ? (int64_t)jv * D + gl * 4 : 0));
       }
     };
-    auto sum_batch = [&](int i0, const uint32_t (&word)[kBatch], const uint32_t (&kk)[kBatch], f32x4 (&rv)[kBatch],
-                         uint32_t use) {
+    // positions u0 .. u0 + kPart - 1 of the batch, their rows in rv[0 .. kPart)
+    auto sum_batch = [&](int i0, int u0, const uint32_t (&word)[kBatch], const uint32_t (&kk)[kBatch],
+                         f32x4 (&rv)[kPart], uint32_t use, bool weighted) {
 #pragma unroll
-      for (int u = 0; u < kBatch; ++u)
-        if (!((use >> u) & 1u)) rv[u] = f32x4{0.f, 0.f, 0.f, 0.f};
-      // weights other than 0 and 1 are rare: unless some position of the
-      // wave's batch has one, rows are added without a multiply (a weight-0
-      // row was zeroed above), a branch the whole wave takes together
-      bool nonunit = false;
+      for (int v = 0; v < kPart; ++v)
+        if (!((use >> (u0 + v)) & 1u)) rv[v] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int u = 0; u < kBatch; ++u) nonunit |= i0 + u < nvalid && (word[u] & kNonUnit);
-      const bool weighted = __ballot(nonunit) != 0ull;
-#pragma unroll
-      for (int u = 0; u < kBatch; ++u) {
+      for (int v = 0; v < kPart; ++v) {
+        const int u = u0 + v;
         const int i = i0 + u;
         // keep each row's float64 widening next to its use: hoisting all of
         // them costs registers and the waves that keep gathers in flight
@@ -776,12 +779,12 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
           }
           const bool zero = word[u] & kZeroW;
           if (!weighted) {
-            acc += widen(rv[u]);
+            acc += widen(rv[v]);
           } else if (!zero) {
             double wd = 1.0;
             if (word[u] & kNonUnit)   // a weight other than 0 or 1: look up its contribution
               wd = (double)a.w[contribution_global(a.offsets, a.K, word[u] & kIndexMask)];
-            acc += wd * widen(rv[u]);
+            acc += wd * widen(rv[v]);
           }
           const int nc = (word[u] & kNewC) ? 1 : 0;
           cc += nc;
@@ -872,10 +875,20 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
       load_words(i0, word);
       if (APPLY) load_keys(i0, kk);
       if (i0 == 0) first_open = !(word[0] & kHead);
-      f32x4 rv[kBatch];
-      uint32_t use;
-      gather(i0, word, rv, use);
-      sum_batch(i0, word, kk, rv, use);
+      // weights other than 0 and 1 are rare: unless some position of the
+      // wave's batch has one, rows are added without a multiply (a weight-0
+      // row is zeroed), a branch the whole wave takes together
+      bool nonunit = false;
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) nonunit |= i0 + u < nvalid && (word[u] & kNonUnit);
+      const bool weighted = __ballot(nonunit) != 0ull;
+      uint32_t use = 0;
+#pragma unroll
+      for (int u0 = 0; u0 < kBatch; u0 += kPart) {
+        f32x4 rv[kPart];
+        gather(i0, u0, word, rv, use);
+        sum_batch(i0, u0, word, kk, rv, use, weighted);
+      }
       if (kPark) flush();
     }
 
