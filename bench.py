@@ -351,7 +351,7 @@ def run_workload(name, args, torch, gba_step_mod, sdev, gba):
 
     # the bandwidth of the step's access patterns (measurement kernels)
     if args.ceilings and name == args.workload:
-        res["ceilings"] = ceilings(w, ds.table, gba, torch, stream)
+        res["ceilings"] = ceilings(w, ds.table, ds.rows, gba, torch, stream)
         print(f"[bench] {name}: ceilings measured", file=sys.stderr, flush=True)
 
     if full_cpu:
@@ -471,13 +471,15 @@ def hash_leg(w, ds, st, gba, torch, stream, decay, start, end, n):
                 find_or_insert_ms=float(np.mean([a.elapsed_time(b) for a, b in ev])))
 
 
-def ceilings(w, table, gba, torch, stream):
+def ceilings(w, table, contrib_rows, gba, torch, stream):
     """Bandwidth of the step's access patterns on this GPU, each from the
     plainest kernel that has it (include/gba_ceilings.h): a 4 GiB stream of
     16-byte non-temporal reads (the dense sum's pattern), a 2 GiB stream copy,
-    and N gathers of random whole rows of the workload's table (the row
-    passes' pattern).  Each is timed over 5 launches per grid size, after one
-    warm-up, for a few grid sizes; the best grid is reported."""
+    N gathers of random whole rows of the workload's table, and N/2 gathers of
+    random rows of the contribution rows [N][D] (the row passes' pattern, at
+    about the hot-ID pass's count and footprint).  Each is timed over 5
+    launches per grid size, after one warm-up, for a few grid sizes; the best
+    grid is reported."""
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
 
     def timed(fn, reps=5):
@@ -511,6 +513,18 @@ def ceilings(w, table, gba, torch, stream):
     nbytes = w.N * w.D * 4 + w.N * 8
     out["random_row_gather"] = dict(rows=w.N, row_bytes=w.D * 4, table_rows=w.R, bytes=nbytes, blocks=best[1],
                                     us=best[0] * 1e3, gbs=nbytes / (best[0] * 1e-3) / 1e9)
+    del rows
+    # the row passes' own pattern: half as many random rows as occurrences
+    # (about the hot occurrences at c4) from the contribution rows [N][D]
+    n_half = max(1, w.N // 2)
+    rows = torch.randint(0, w.N, (n_half,), device="cuda", generator=g, dtype=torch.int64)
+    gg = grids + (16384,)
+    sink = torch.empty(gba.gba_ceiling_sink_words(max(gg)), dtype=torch.int32, device="cuda")
+    best = min((timed(lambda: gba.gba_ceiling_gather_rows(contrib_rows, rows, sink, b)), b) for b in gg)
+    nbytes = n_half * w.D * 4 + n_half * 8
+    out["random_contribution_row_gather"] = dict(rows=n_half, row_bytes=w.D * 4, table_rows=w.N, bytes=nbytes,
+                                                 blocks=best[1], us=best[0] * 1e3,
+                                                 gbs=nbytes / (best[0] * 1e-3) / 1e9)
     del rows, sink
     torch.cuda.empty_cache()
     return out
