@@ -68,8 +68,11 @@ def build_all(jobs=8):
 def build_gba_host_sanitized(jobs=8):
     """libgba.so with AddressSanitizer and UndefinedBehaviorSanitizer on its
     host code only (argument checks, workspace layout, launch logic; device
-    code is built as usual), into _build_sanitized/.  Load it with
-    GBA_LIBRARY and the clang ASan runtime preloaded."""
+    code is built as usual), into _build_sanitized/.  Load it by naming it in
+    GBA_LIBRARY, with the clang AddressSanitizer runtime in LD_PRELOAD (its
+    libclang_rt.asan-x86_64.so under /opt/rocm/llvm/lib/clang/*/lib/linux/),
+    on a machine without a GPU: the host-path tests then run every entry
+    point's checks and layout arithmetic under the sanitizers."""
     csrc = os.path.join(PKG, "csrc")
     srcs = sorted(os.path.join(csrc, f) for f in os.listdir(csrc) if f.endswith(".hip"))
     out_dir = os.path.join(PKG, "_build_sanitized")
