@@ -1,7 +1,7 @@
 // Optimiser updates of one float32 element.  Table 1 of the paper names
-// Adagrad and Adam; the rules are the textbook ones.  The dense updates and
-// Adam compute in float64 and round once per stored value; the Adagrad update
-// of table rows computes in float32 (below).
+// Adagrad and Adam; the rules are the textbook ones.  The dense updates
+// compute in float64 and round once per stored value; the updates of
+// embedding-table rows compute in float32 (the *_f32 forms below).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -45,6 +45,22 @@ __device__ __forceinline__ void adam_update(float& p, float& m, float& v, float 
   p = (float)pn;
   m = (float)mn;
   v = (float)vn;
+}
+
+// Adam on embedding-table rows in float32: the same rule with the hardware
+// square root and reciprocal, the constants rounded once from double (omb1 =
+// 1 - beta1, omb2 = 1 - beta2, rbc1 = 1 / bc1, rbc2 = 1 / bc2).  m' and v'
+// are within a few float32 ulps of b1 |m| + (1 - b1) |g| and of v', the step
+// within a few ulps of its value, and p' takes one more rounding.
+__device__ __forceinline__ void adam_update_f32(float& p, float& m, float& v, float g, float lr, float b1,
+                                                float omb1, float b2, float omb2, float eps, float rbc1,
+                                                float rbc2) {
+  const float mn = b1 * m + omb1 * g;
+  const float vn = b2 * v + omb2 * (g * g);
+  const float den = __builtin_amdgcn_sqrtf(vn * rbc2) + eps;
+  p = p - (lr * (mn * rbc1)) * __builtin_amdgcn_rcpf(den);
+  m = mn;
+  v = vn;
 }
 
 }  // namespace gba

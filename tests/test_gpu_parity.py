@@ -472,13 +472,16 @@ def test_apply_rows(opt, D):
     else:
         et[rows[sel]], e1[rows[sel]], e2[rows[sel]] = oracle.adam(table[rows[sel]], s1[rows[sel]], s2[rows[sel]],
                                                                   g[sel], 1e-3, 0.9, 0.999, 1e-8, 7)
+        mt, m1, m2 = (np.abs(x).astype(np.float64) for x in (table, s1, s2))
+        mt[rows[sel]], m1[rows[sel]], m2[rows[sel]] = oracle.adam_magnitude(
+            table[rows[sel]], s1[rows[sel]], s2[rows[sel]], g[sel], np.abs(g[sel]), 1e-3, 0.9, 0.999, 1e-8, 7)
     gt, g1, g2 = host(td), host(s1d), host(s2d)
     assert_exact(gt[~upd], table[~upd], "untouched rows")
     assert_exact(g1[~upd], s1[~upd], "untouched state")
     assert_rule_t(gt, et, mt, "table")
     assert_rule_t(g1, e1, m1, "slot1")
     if opt == "adam":
-        assert_rule_t(g2, e2, None, "slot2")
+        assert_rule_t(g2, e2, m2, "slot2")
     assert int(host(err)[0]) == 0
 
 

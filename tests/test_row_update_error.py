@@ -1,14 +1,19 @@
-"""The float32 Adagrad of the row apply stays inside the comparison rule.
+"""The float32 optimiser updates of table rows stay inside the comparison rule.
 
-The row form of the optimiser apply (and the fused sparse call) computes
-Adagrad (Duchi et al. 2011; Table 1 names it) in float32: a' = a + g*g, then
-p' = p - (lr g) * rcp(sqrt(a') + eps) with the hardware square root and
-reciprocal, each within 1 ulp of the exact value.  This emulates that
-arithmetic in numpy, with every rounding of the square root and the
-reciprocal pushed one ulp either way, and checks the result against the
-oracle under the parity rule with the oracle's magnitude companion: the error
-is a few 1e-7 of |p| + |step|, far inside 1e-5, also where p' cancels to
-almost nothing.  (CPU only: no device code runs here.)"""
+The row form of the optimiser apply (and the fused sparse calls) computes
+Adagrad (Duchi et al. 2011) and Adam (Kingma and Ba 2015), the optimisers
+Table 1 names, in float32 with the hardware square root and reciprocal, each
+within 1 ulp of the exact value:
+  Adagrad: a' = a + g*g, p' = p - (lr g) * rcp(sqrt(a') + eps);
+  Adam:    m' = b1 m + (1 - b1) g, v' = b2 v + (1 - b2) g*g,
+           p' = p - (lr m' / bc1) * rcp(sqrt(v' / bc2) + eps),
+with the constants 1 - b1, 1 - b2, 1 / bc1 and 1 / bc2 rounded once to
+float32.  This emulates that arithmetic in numpy, with every rounding of the
+square root and the reciprocal pushed one ulp either way, and checks the
+result against the oracle under the parity rule with the oracle's magnitude
+companions: the error is a few 1e-7 of the companion, far inside 1e-5, also
+where p' or m' cancels to almost nothing.  (CPU only: no device code runs
+here.)"""
 import itertools
 import os
 import sys
@@ -89,3 +94,36 @@ def test_row_adagrad_plain_rule_would_fail_on_cancellation():
     got_p, _ = _row_adagrad_f32(p, a, g, lr, eps, 1, 1)
     err = np.abs(got_p.astype(np.float64) - ref_p.astype(np.float64))
     assert np.any(err > 1e-5 * np.abs(ref_p.astype(np.float64)) + 1e-30)
+
+
+def _row_adam_f32(p, m, v, g, lr, b1, b2, eps, t, ks, kr):
+    p, m, v, g = F(p), F(m), F(v), F(g)
+    bc1, bc2 = 1.0 - b1 ** t, 1.0 - b2 ** t
+    mn = (F(b1) * m + F(1.0 - b1) * g).astype(F)
+    vn = (F(b2) * v + F(1.0 - b2) * (g * g).astype(F)).astype(F)
+    s = _ulp_shift(np.sqrt((vn * F(1.0 / bc2)).astype(F)).astype(F), ks)
+    den = (s + F(eps)).astype(F)
+    r = _ulp_shift((F(1.0) / den).astype(F), kr)
+    step = ((F(lr) * (mn * F(1.0 / bc1)).astype(F)).astype(F) * r).astype(F)
+    return (p - step).astype(F), mn, vn
+
+
+def test_row_adam_f32_within_rule_with_companion():
+    rng = np.random.default_rng(21)
+    n = 20000
+    p = rng.uniform(-1.0, 1.0, n).astype(F)
+    m = (rng.standard_normal(n) * 1e-3).astype(F)
+    v = (rng.uniform(0.0, 1.0, n) * 1e-6).astype(F)
+    g = (rng.standard_normal(n) * 10.0 ** rng.uniform(-6, 0, n)).astype(F)
+    lr, b1, b2, eps, t = 1e-3, 0.9, 0.999, 1e-8, 7
+    # cancelling first moments: b1 m = -(1 - b1) g to a few ulps
+    c = rng.random(n) < 0.25
+    m[c] = (-(1.0 - b1) * g[c].astype(np.float64) / b1 * (1.0 + rng.integers(-4, 5, c.sum()) * 2.0 ** -24)).astype(F)
+    g[:50] = 0.0
+    v[50:100] = 0.0
+    ref = oracle.adam(p, m, v, g, lr, b1, b2, eps, t)
+    mu = oracle.adam_magnitude(p, m, v, g, np.abs(g), lr, b1, b2, eps, t)
+    for ks, kr in itertools.product((-1, 0, 1), repeat=2):
+        got = _row_adam_f32(p, m, v, g, lr, b1, b2, eps, t, ks, kr)
+        for x, r, u, what in zip(got, ref, mu, ("p'", "m'", "v'")):
+            assert_rule_t(x, r, u, f"{what} (sqrt {ks:+d} ulp, rcp {kr:+d} ulp)")
