@@ -103,7 +103,7 @@ __device__ __forceinline__ void finish_scalar(const float* const* grads, const u
                                               int nk, int64_t e, float* out, const DenseState& st,
                                               double* run, double denom, int reset) {
   double acc = CARRY ? run[e] : 0.0;
-  for (int i = 0; i < nk; ++i) acc += (double)kw[i] * (double)grads[kept[i]][e];
+  for (int i = 0; i < nk; ++i) acc = __builtin_fma((double)kw[i], (double)grads[kept[i]][e], acc);   // exact product
   if (MODE == kAccumulate) {
     run[e] = acc;
   } else {
@@ -198,15 +198,19 @@ aggregate_dense_kernel(const float* const* __restrict__ grads, const float* __re
         acc[j] = f64x4{0.0, 0.0, 0.0, 0.0};
         if (CARRY && vb + kWave * j < nvec) acc[j] = reinterpret_cast<const f64x4*>(run)[vb + kWave * j];
       }
+      // the next gradient's address is fetched while this one's loads are in
+      // flight (global loads: the LDS and scalar reads for it do not wait on them)
+      const f32x4* g_next = nk > 0 ? reinterpret_cast<const f32x4*>(grads[kept[0]]) : nullptr;
       for (int i = 0; i < nk; ++i) {
-        const f32x4* g = reinterpret_cast<const f32x4*>(grads[kept[i]]) + vb;
+        const f32x4* g = g_next + vb;
         f32x4 x[VECS];
 #pragma unroll
         for (int j = 0; j < VECS; ++j)
-          x[j] = (vb + kWave * j < nvec) ? load_stream(g + kWave * j) : f32x4{0.f, 0.f, 0.f, 0.f};
+          x[j] = (vb + kWave * j < nvec) ? load_stream_global(g + kWave * j) : f32x4{0.f, 0.f, 0.f, 0.f};
+        if (i + 1 < nk) g_next = reinterpret_cast<const f32x4*>(grads[kept[i + 1]]);
         const double wi = (double)kw[i];
 #pragma unroll
-        for (int j = 0; j < VECS; ++j) acc[j] += wi * widen(x[j]);
+        for (int j = 0; j < VECS; ++j) acc[j] = fma_widen(wi, x[j], acc[j]);
       }
       if (MODE == kAccumulate) {
 #pragma unroll

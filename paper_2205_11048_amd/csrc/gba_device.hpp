@@ -69,10 +69,24 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // Loads and stores marked non-temporal, for data touched exactly once.
 __device__ __forceinline__ f32x4 load_stream(const f32x4* p) { return __builtin_nontemporal_load(p); }
+// The same from a pointer known to be in device global memory: a global (not
+// flat) load, counted by the vector-memory counter only, so that waiting for
+// an LDS or scalar load does not also wait for it.
+typedef __attribute__((address_space(1))) const f32x4 global_f32x4;
+__device__ __forceinline__ f32x4 load_stream_global(const f32x4* p) {
+  return __builtin_nontemporal_load((global_f32x4*)p);
+}
 __device__ __forceinline__ void store_stream(f32x4* p, f32x4 v) { __builtin_nontemporal_store(v, p); }
 
 __device__ __forceinline__ f64x4 widen(f32x4 v) {
   return f64x4{(double)v.x, (double)v.y, (double)v.z, (double)v.w};
+}
+// acc + w * x for a float32 weight w (widened) and a float32 row x: the
+// product of two float32 values is exact in float64, so one fused
+// multiply-add rounds exactly as the product followed by the sum does.
+__device__ __forceinline__ f64x4 fma_widen(double w, f32x4 x, f64x4 acc) {
+  return f64x4{__builtin_fma(w, (double)x.x, acc.x), __builtin_fma(w, (double)x.y, acc.y),
+               __builtin_fma(w, (double)x.z, acc.z), __builtin_fma(w, (double)x.w, acc.w)};
 }
 __device__ __forceinline__ f32x4 narrow(f64x4 v) {
   return f32x4{(float)v.x, (float)v.y, (float)v.z, (float)v.w};

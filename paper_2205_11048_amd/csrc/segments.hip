@@ -784,7 +784,7 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
             double wd = 1.0;
             if (word[u] & kNonUnit)   // a weight other than 0 or 1: look up its contribution
               wd = (double)a.w[contribution_global(a.offsets, a.K, word[u] & kIndexMask)];
-            acc += wd * widen(rv[v]);
+            acc = fma_widen(wd, rv[v], acc);
           }
           const int nc = (word[u] & kNewC) ? 1 : 0;
           cc += nc;
@@ -1119,7 +1119,7 @@ hot_rows_kernel(SegmentArgs a, const int32_t* __restrict__ buckets, int q, int n
     for (int u = 0; u < kBatch; ++u) {
       __builtin_amdgcn_sched_barrier(0);
       if (i0 + u < nvalid) {
-        if ((use >> u) & 1u) acc += (double)wt[u] * widen(rv[u]);
+        if ((use >> u) & 1u) acc = fma_widen((double)wt[u], rv[u], acc);
         const bool newc = m[u] != last;   // occurrences of one contribution are consecutive
         cg += newc ? 1 : 0;
         ag += (newc && wt[u] != 0.0f) ? 1 : 0;
