@@ -141,11 +141,11 @@ gba_status gba_aggregate_sparse(const int64_t* ids, const float* rows,
 
 /*
  * Optimiser apply (Table 1 names Adagrad and Adam; rules of Duchi et al. 2011
- * and Kingma and Ba 2015).  Dense form: arithmetic in float64 from the
- * float32 state, each stored value rounded once.  Row form (and the fused
- * sparse calls): float32, with the hardware square root and reciprocal (each
- * within 1 ulp), so each step is within a few float32 ulps and the stored
- * values take one more rounding.
+ * and Kingma and Ba 2015).  Arithmetic in float32 from the float32 state and
+ * gradient (in every call that applies an optimiser), with the hardware
+ * square root and reciprocal (each within 1 ulp) and the constants rounded
+ * once from double, so each step is within a few float32 ulps and every
+ * stored value takes one more rounding.
  *
  * Dense form (rows == NULL): elementwise over n elements of param/state/grad.
  * Row form (rows != NULL): for i < *num_rows (device int64, <= n), when

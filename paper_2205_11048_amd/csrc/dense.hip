@@ -77,7 +77,7 @@ struct DenseState {
   float* p;
   float* s1;   // Adagrad accumulator or Adam m
   float* s2;   // Adam v
-  double lr, eps, beta1, beta2, bc1, bc2;
+  OptF32 c;    // the optimiser's float32 constants
 };
 
 template <int MODE>
@@ -85,12 +85,12 @@ __device__ __forceinline__ void finish_element(float g, int64_t e, float* out, c
   if (out) out[e] = g;
   if (MODE == kApplyAdagrad) {
     float pe = st.p[e], ae = st.s1[e];
-    adagrad_update(pe, ae, g, st.lr, st.eps);
+    adagrad_update_f32(pe, ae, g, st.c);
     st.p[e] = pe;
     st.s1[e] = ae;
   } else if (MODE == kApplyAdam) {
     float pe = st.p[e], me = st.s1[e], ve = st.s2[e];
-    adam_update(pe, me, ve, g, st.lr, st.beta1, st.beta2, st.eps, st.bc1, st.bc2);
+    adam_update_f32(pe, me, ve, g, st.c);
     st.p[e] = pe;
     st.s1[e] = me;
     st.s2[e] = ve;
@@ -153,12 +153,11 @@ __device__ __forceinline__ void finish_vectors(const f64x4* acc, double denom, i
       if (MODE == kApplyAdam) {
         float ve[4] = {vv[jj].x, vv[jj].y, vv[jj].z, vv[jj].w};
 #pragma unroll
-        for (int k = 0; k < 4; ++k)
-          adam_update(pe[k], se[k], ve[k], ge[k], st.lr, st.beta1, st.beta2, st.eps, st.bc1, st.bc2);
+        for (int k = 0; k < 4; ++k) adam_update_f32(pe[k], se[k], ve[k], ge[k], st.c);
         store_stream(reinterpret_cast<f32x4*>(st.s2) + q, f32x4{ve[0], ve[1], ve[2], ve[3]});
       } else {
 #pragma unroll
-        for (int k = 0; k < 4; ++k) adagrad_update(pe[k], se[k], ge[k], st.lr, st.eps);
+        for (int k = 0; k < 4; ++k) adagrad_update_f32(pe[k], se[k], ge[k], st.c);
       }
       store_stream(reinterpret_cast<f32x4*>(st.p) + q, f32x4{pe[0], pe[1], pe[2], pe[3]});
       store_stream(reinterpret_cast<f32x4*>(st.s1) + q, f32x4{se[0], se[1], se[2], se[3]});
@@ -333,16 +332,11 @@ hipError_t launch_aggregate_dense(const float* const* grads, const float* w, int
 }
 
 static DenseState adagrad_state(float* p, float* a, double lr, double eps) {
-  DenseState st{};
-  st.p = p;
-  st.s1 = a;
-  st.lr = lr;
-  st.eps = eps;
-  return st;
+  return DenseState{p, a, nullptr, opt_f32(lr, eps)};
 }
 
 static DenseState adam_state(float* p, float* m, float* v, const AdamParams& hp) {
-  return DenseState{p, m, v, hp.lr, hp.eps, hp.beta1, hp.beta2, hp.bc1, hp.bc2};
+  return DenseState{p, m, v, opt_f32(hp.lr, hp.eps, hp.beta1, hp.beta2, hp.bc1, hp.bc2)};
 }
 
 hipError_t launch_aggregate_apply_dense_adagrad(const float* const* grads, const float* w, int32_t K,
@@ -392,7 +386,7 @@ __device__ __forceinline__ bool all_aligned16(const void* a, const void* b, cons
 
 __global__ void __launch_bounds__(kDenseBlock)
 dense_adagrad_kernel(float* __restrict__ p, float* __restrict__ a, const float* __restrict__ g,
-                     int64_t n, double lr, double eps) {
+                     int64_t n, OptF32 c) {
   const int64_t stride = (int64_t)gridDim.x * kDenseBlock;
   const int64_t t0 = (int64_t)blockIdx.x * kDenseBlock + threadIdx.x;
   if (all_aligned16(p, a, g, p)) {
@@ -404,21 +398,21 @@ dense_adagrad_kernel(float* __restrict__ p, float* __restrict__ a, const float* 
       float pe[4] = {pv.x, pv.y, pv.z, pv.w}, ae[4] = {av.x, av.y, av.z, av.w};
       const float ge[4] = {gv.x, gv.y, gv.z, gv.w};
 #pragma unroll
-      for (int k = 0; k < 4; ++k) adagrad_update(pe[k], ae[k], ge[k], lr, eps);
+      for (int k = 0; k < 4; ++k) adagrad_update_f32(pe[k], ae[k], ge[k], c);
       store_stream(reinterpret_cast<f32x4*>(p) + v, f32x4{pe[0], pe[1], pe[2], pe[3]});
       store_stream(reinterpret_cast<f32x4*>(a) + v, f32x4{ae[0], ae[1], ae[2], ae[3]});
     }
     // the last n % 4 elements
     for (int64_t e = nvec * 4 + threadIdx.x; blockIdx.x == 0 && e < n; e += kDenseBlock) {
       float pe = p[e], ae = a[e];
-      adagrad_update(pe, ae, g[e], lr, eps);
+      adagrad_update_f32(pe, ae, g[e], c);
       p[e] = pe;
       a[e] = ae;
     }
   } else {
     for (int64_t e = t0; e < n; e += stride) {
       float pe = p[e], ae = a[e];
-      adagrad_update(pe, ae, g[e], lr, eps);
+      adagrad_update_f32(pe, ae, g[e], c);
       p[e] = pe;
       a[e] = ae;
     }
@@ -427,8 +421,7 @@ dense_adagrad_kernel(float* __restrict__ p, float* __restrict__ a, const float* 
 
 __global__ void __launch_bounds__(kDenseBlock)
 dense_adam_kernel(float* __restrict__ p, float* __restrict__ m, float* __restrict__ v,
-                  const float* __restrict__ g, int64_t n, double lr, double b1, double b2,
-                  double eps, double bc1, double bc2) {
+                  const float* __restrict__ g, int64_t n, OptF32 c) {
   const int64_t stride = (int64_t)gridDim.x * kDenseBlock;
   const int64_t t0 = (int64_t)blockIdx.x * kDenseBlock + threadIdx.x;
   if (all_aligned16(p, m, v, g)) {
@@ -442,7 +435,7 @@ dense_adam_kernel(float* __restrict__ p, float* __restrict__ m, float* __restric
       float ve[4] = {vv.x, vv.y, vv.z, vv.w};
       const float ge[4] = {gv.x, gv.y, gv.z, gv.w};
 #pragma unroll
-      for (int k = 0; k < 4; ++k) adam_update(pe[k], me[k], ve[k], ge[k], lr, b1, b2, eps, bc1, bc2);
+      for (int k = 0; k < 4; ++k) adam_update_f32(pe[k], me[k], ve[k], ge[k], c);
       store_stream(reinterpret_cast<f32x4*>(p) + q, f32x4{pe[0], pe[1], pe[2], pe[3]});
       store_stream(reinterpret_cast<f32x4*>(m) + q, f32x4{me[0], me[1], me[2], me[3]});
       store_stream(reinterpret_cast<f32x4*>(v) + q, f32x4{ve[0], ve[1], ve[2], ve[3]});
@@ -450,7 +443,7 @@ dense_adam_kernel(float* __restrict__ p, float* __restrict__ m, float* __restric
     // the last n % 4 elements
     for (int64_t e = nvec * 4 + threadIdx.x; blockIdx.x == 0 && e < n; e += kDenseBlock) {
       float pe = p[e], me = m[e], ve = v[e];
-      adam_update(pe, me, ve, g[e], lr, b1, b2, eps, bc1, bc2);
+      adam_update_f32(pe, me, ve, g[e], c);
       p[e] = pe;
       m[e] = me;
       v[e] = ve;
@@ -458,7 +451,7 @@ dense_adam_kernel(float* __restrict__ p, float* __restrict__ m, float* __restric
   } else {
     for (int64_t e = t0; e < n; e += stride) {
       float pe = p[e], me = m[e], ve = v[e];
-      adam_update(pe, me, ve, g[e], lr, b1, b2, eps, bc1, bc2);
+      adam_update_f32(pe, me, ve, g[e], c);
       p[e] = pe;
       m[e] = me;
       v[e] = ve;
@@ -472,7 +465,7 @@ hipError_t launch_dense_adagrad(float* p, float* a, const float* g, int64_t n, d
   int64_t blocks = ceil_div(ceil_div(n, 4), kDenseBlock);
   if (blocks > kApplyMaxBlocks) blocks = kApplyMaxBlocks;
   hipLaunchKernelGGL(dense_adagrad_kernel, dim3((unsigned)blocks), dim3(kDenseBlock), 0, stream, p,
-                     a, g, n, lr, eps);
+                     a, g, n, opt_f32(lr, eps));
   return hipGetLastError();
 }
 
@@ -482,7 +475,7 @@ hipError_t launch_dense_adam(float* p, float* m, float* v, const float* g, int64
   int64_t blocks = ceil_div(ceil_div(n, 4), kDenseBlock);
   if (blocks > kApplyMaxBlocks) blocks = kApplyMaxBlocks;
   hipLaunchKernelGGL(dense_adam_kernel, dim3((unsigned)blocks), dim3(kDenseBlock), 0, stream, p, m,
-                     v, g, n, hp.lr, hp.beta1, hp.beta2, hp.eps, hp.bc1, hp.bc2);
+                     v, g, n, opt_f32(hp.lr, hp.eps, hp.beta1, hp.beta2, hp.bc1, hp.bc2));
   return hipGetLastError();
 }
 

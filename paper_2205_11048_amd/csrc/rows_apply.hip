@@ -34,9 +34,7 @@ rows_apply_kernel(float* __restrict__ p, float* __restrict__ s1, float* __restri
   const int grp = threadIdx.x / LPR;
   int64_t count = *num_rows;
   if (count > n) count = n;
-  const float lr_f = (float)lr, eps_f = (float)eps;   // the row updates run in float32
-  const float b1_f = (float)b1, omb1_f = (float)(1.0 - b1), b2_f = (float)b2, omb2_f = (float)(1.0 - b2),
-              rbc1_f = (float)(1.0 / bc1), rbc2_f = (float)(1.0 / bc2);
+  const OptF32 oc = opt_f32(lr, eps, b1, b2, bc1, bc2);
   bool bad = false;
   const int64_t stride = (int64_t)gridDim.x * G * kRowBatch;
   for (int64_t i0 = ((int64_t)blockIdx.x * G + grp) * kRowBatch; i0 < count; i0 += stride) {
@@ -76,11 +74,11 @@ rows_apply_kernel(float* __restrict__ p, float* __restrict__ s1, float* __restri
           float ve[4] = {vk.x, vk.y, vk.z, vk.w};
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            adam_update_f32(pe[e], ae[e], ve[e], ge[e], lr_f, b1_f, omb1_f, b2_f, omb2_f, eps_f, rbc1_f, rbc2_f);
+            adam_update_f32(pe[e], ae[e], ve[e], ge[e], oc);
           store_stream(reinterpret_cast<f32x4*>(s2 + at), f32x4{ve[0], ve[1], ve[2], ve[3]});
         } else {
 #pragma unroll
-          for (int e = 0; e < 4; ++e) adagrad_update_f32(pe[e], ae[e], ge[e], lr_f, eps_f);
+          for (int e = 0; e < 4; ++e) adagrad_update_f32(pe[e], ae[e], ge[e], oc);
         }
         store_stream(reinterpret_cast<f32x4*>(p + at), f32x4{pe[0], pe[1], pe[2], pe[3]});
         store_stream(reinterpret_cast<f32x4*>(s1 + at), f32x4{ae[0], ae[1], ae[2], ae[3]});

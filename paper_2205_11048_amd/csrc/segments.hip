@@ -206,15 +206,14 @@ __device__ __forceinline__ int contribution_global(const int64_t* off, int K, ui
   return m < 0 ? 0 : (m < K ? m : K - 1);
 }
 
-// Adagrad on one lane's 4 floats of a row, with the row apply's arithmetic
-// (float32, hardware square root and reciprocal).  The fused row pass applies
+// Adagrad on one lane's 4 floats of a row, with the row apply's arithmetic.  The fused row pass applies
 // Adagrad only (segments_fuse_apply); Adam goes through the separate apply.
 __device__ __forceinline__ void adagrad4(const RowApply& ap, f32x4& pv, f32x4& s1, f32x4 g) {
   float pe[4] = {pv.x, pv.y, pv.z, pv.w}, ae[4] = {s1.x, s1.y, s1.z, s1.w};
   const float ge[4] = {g.x, g.y, g.z, g.w};
-  const float lr = (float)ap.lr, eps = (float)ap.eps;
+  const OptF32 c = opt_f32(ap.lr, ap.eps);
 #pragma unroll
-  for (int e = 0; e < 4; ++e) adagrad_update_f32(pe[e], ae[e], ge[e], lr, eps);
+  for (int e = 0; e < 4; ++e) adagrad_update_f32(pe[e], ae[e], ge[e], c);
   pv = f32x4{pe[0], pe[1], pe[2], pe[3]};
   s1 = f32x4{ae[0], ae[1], ae[2], ae[3]};
 }

@@ -38,9 +38,3 @@ def assert_rule_t(got, ref, mu=None, name="", rtol=RTOL):
         i = tuple(np.argwhere(bad)[0])
         raise AssertionError(f"{name}: {int(bad.sum())} of {bad.size} outside the 1e-5 rule; first at {i}: "
                              f"got {got[i]!r} want {ref[i]!r} (bound {bound[i]:.3g})")
-
-
-def exact_fraction(got, ref):
-    got = np.asarray(got)
-    ref = np.asarray(ref)
-    return float(np.mean(got == ref)) if got.size else 1.0

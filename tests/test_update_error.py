@@ -1,19 +1,19 @@
-"""The float32 optimiser updates of table rows stay inside the comparison rule.
+"""The float32 optimiser updates stay inside the comparison rule.
 
-The row form of the optimiser apply (and the fused sparse calls) computes
-Adagrad (Duchi et al. 2011) and Adam (Kingma and Ba 2015), the optimisers
-Table 1 names, in float32 with the hardware square root and reciprocal, each
-within 1 ulp of the exact value:
+Every optimiser update (dense and table rows, separate and fused calls)
+computes Adagrad (Duchi et al. 2011) and Adam (Kingma and Ba 2015), the
+optimisers Table 1 names, in float32 with the hardware square root and
+reciprocal, each within 1 ulp of the exact value:
   Adagrad: a' = a + g*g, p' = p - (lr g) * rcp(sqrt(a') + eps);
   Adam:    m' = b1 m + (1 - b1) g, v' = b2 v + (1 - b2) g*g,
            p' = p - (lr m' / bc1) * rcp(sqrt(v' / bc2) + eps),
-with the constants 1 - b1, 1 - b2, 1 / bc1 and 1 / bc2 rounded once to
-float32.  This emulates that arithmetic in numpy, with every rounding of the
-square root and the reciprocal pushed one ulp either way, and checks the
-result against the oracle under the parity rule with the oracle's magnitude
-companions: the error is a few 1e-7 of the companion, far inside 1e-5, also
-where p' or m' cancels to almost nothing.  (CPU only: no device code runs
-here.)"""
+with lr, eps, b1, b2 and the constants 1 - b1, 1 - b2, 1 / bc1 and 1 / bc2
+rounded once to float32.  This emulates that arithmetic in numpy, with every
+rounding of the square root and the reciprocal pushed one ulp either way, and
+checks the result against the oracle under the parity rule with the oracle's
+magnitude companions: the error is a few 1e-7 of the companion, far inside
+1e-5, also where p' or m' cancels to almost nothing.  (CPU only: no device
+code runs here.)"""
 import itertools
 import os
 import sys
