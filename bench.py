@@ -672,6 +672,24 @@ def cpu_baseline_full(w, ds, pre, J=16):
                 U_act=int(act.sum()), **host_cpu())
 
 
+# The paper's own figures, placed beside the result as context and not as a
+# target: whole training jobs on a cluster of Tesla V100S GPUs and Skylake CPUs
+# shared with other jobs (Sec. 4.1); global QPS from Table 2, AUC and local
+# QPS of the private task from Table 3.  The paper times no parameter-server
+# step of its own, so none of these is comparable with a step time.
+PAPER_CONTEXT = {
+    "hardware": "training cluster of Tesla V100S GPUs and Skylake CPUs, shared with other jobs (Sec. 4.1)",
+    "global_qps_samples_per_s": {
+        "criteo_deepfm": {"gba": 3240e3, "sync": 1436e3, "async": 3253e3},
+        "alimama_dien": {"gba": 399e3, "sync": 182e3, "async": 403e3},
+        "private_youtubednn": {"gba": 87e3, "sync": 43e3, "async": 90e3},
+    },
+    "private_task_auc": {"sync": 0.7864, "gba": [0.7864, 0.7866, 0.7865]},
+    "source": "Table 2 (global QPS), Table 3 (AUC of the private task at three local batch sizes)",
+    "comparable": False,
+}
+
+
 def main():
     args = parse()
     if args.step_only:
@@ -727,6 +745,7 @@ def main():
         "hash_storage": head.get("hash_storage"),
         "graph": head.get("graph"),
         "other_workloads": others,
+        "paper_context": PAPER_CONTEXT,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = head.get("cpu_baseline") or cpu_baseline(args.workload, max(1, args.cpu_sample))
