@@ -148,6 +148,34 @@ __device__ __forceinline__ uint64_t match_digit(uint32_t digit, int bits, bool a
   return active ? m : 0ull;
 }
 
+// The same match for a digit width known at compile time (the loop unrolled).
+template <int BITS>
+__device__ __forceinline__ uint64_t match_digit_n(uint32_t digit, bool active) {
+  uint32_t diff_lo, diff_hi;
+  {
+    const uint64_t on = __ballot(active);
+    diff_lo = ~(uint32_t)on;
+    diff_hi = ~(uint32_t)(on >> 32);
+  }
+#pragma unroll
+  for (int b = 0; b < BITS; ++b) {
+    const uint32_t x = (uint32_t)((int32_t)(digit << (31 - b)) >> 31);
+    const uint64_t bal = __ballot(x != 0u);
+    diff_lo = __builtin_amdgcn_bitop3_b32(diff_lo, (uint32_t)bal, x, 0xF6);
+    diff_hi = __builtin_amdgcn_bitop3_b32(diff_hi, (uint32_t)(bal >> 32), x, 0xF6);
+  }
+  const uint64_t m = ~(((uint64_t)diff_hi << 32) | diff_lo);
+  return active ? m : 0ull;
+}
+
+// A copy of x that the compiler cannot tie to earlier uses of x, so values
+// derived from it (LDS addresses) are recomputed where needed instead of
+// being held in registers across a phase.
+__device__ __forceinline__ uint32_t opaque(uint32_t x) {
+  asm volatile("" : "+v"(x));
+  return x;
+}
+
 // Number of hot IDs below `key`, and whether `key` is one of them.  The bucket
 // table narrows the search to the hot IDs that share the key's top bits: up
 // to two are compared without a branch (no loop, so the lookups of a lane's
@@ -550,6 +578,23 @@ __device__ __forceinline__ int64_t xcd_tile(int64_t b, int64_t tiles) {
   return x * q + (x < r ? x : r) + i;
 }
 
+// Tile of scatter block b with the tiles handed to the XCDs in chunks of C
+// consecutive tiles (chunk c on XCD c % 8), for the 8-bit passes: all XCDs
+// write inside one window of each digit's output (fewer, denser write
+// streams than one eighth of the tiles per XCD), and the neighbouring tiles
+// of a chunk still share an L2.  Tiles past the last whole round of 8 C
+// chunks keep their own index; a pass with fewer tiles than one round uses
+// the eighths.
+constexpr int kXcdChunk = 64;
+template <int C>
+__device__ __forceinline__ int64_t xcd_chunk_tile(int64_t b, int64_t tiles) {
+  const int64_t round = (int64_t)kXcds * C;
+  if (tiles < round) return xcd_tile(b, tiles);
+  if (b >= (tiles / round) * round) return b;   // the tail, in order
+  const int64_t x = b % kXcds, i = b / kXcds;
+  return ((i / C) * kXcds + x) * C + i % C;
+}
+
 // Exclusive scans of V values over the block, behind one barrier: every
 // thread adds up the totals of the waves before its own.  `tmp` holds
 // V * kSortWaves words.
@@ -584,6 +629,10 @@ __device__ __forceinline__ void block_exclusive_scan_v(const uint32_t (&x)[V], u
 // ID, from 0, with no cold keys between them); kColdLast writes the
 // cold keys to keys_out/vals_out (the final arrays), each past the hot runs of
 // the hot IDs below it.  n_total bounds the final arrays.
+// Every pass but the hot-key first stages its keys and then its values through
+// one LDS buffer (a key's output place follows from the key, and is kept in a
+// register for its value), so a block needs 22 KB of LDS instead of 38 KB;
+// the hot-key first pass, whose digits travel beside the keys, stages both.
 template <bool FIRST, int ITEMS, int MODE>
 __device__ __forceinline__ void
 scatter_tile(const void* __restrict__ keys_in, const uint32_t* __restrict__ vals_in,
@@ -595,6 +644,7 @@ scatter_tile(const void* __restrict__ keys_in, const uint32_t* __restrict__ vals
   constexpr bool HOT = MODE == kHotFirst;
   constexpr bool DYN = MODE == kCold || MODE == kColdLast;
   constexpr bool GAP = MODE == kColdLast;
+  constexpr bool ONE_BUF = !HOT;
   // per (wave, digit): the wave's count, then the tile position of the wave's
   // first key of that digit (kColdLast: then the hot tables)
   __shared__ uint32_t cnt[kSortWaves][kRadix];
@@ -603,13 +653,13 @@ scatter_tile(const void* __restrict__ keys_in, const uint32_t* __restrict__ vals
   __shared__ uint32_t gshift[kRadix];
   __shared__ uint32_t s_tot[kRadix];
   __shared__ uint32_t tmp[4 * kSortWaves];
-  constexpr int64_t kTile = tile_keys<ITEMS>();
+  constexpr int kTile = (int)tile_keys<ITEMS>();
   __shared__ uint32_t s_keys[kTile];
-  __shared__ uint32_t s_vals[kTile];
+  __shared__ uint32_t s_vals[ONE_BUF ? 1 : kTile];
   const int64_t n = DYN ? (int64_t)*n_dev : n_arg;
   const int64_t tiles = DYN ? ceil_div(n, kTile) : (int64_t)gridDim.x;
   if (DYN && (int64_t)blockIdx.x >= tiles) return;   // the grid is sized for every key
-  const int64_t tile = xcd_tile(blockIdx.x, tiles);
+  const int64_t tile = HOT ? xcd_tile(blockIdx.x, tiles) : xcd_chunk_tile<kXcdChunk>(blockIdx.x, tiles);
   // Where the tile's keys of digit d go: where the digit starts (scan of the
   // digit totals), plus its count in earlier chunks, plus in earlier tiles of
   // this tile's chunk.  The loads are issued with the keys' and used only
@@ -635,7 +685,10 @@ scatter_tile(const void* __restrict__ keys_in, const uint32_t* __restrict__ vals
   }
   const int w = threadIdx.x / kWave;
   const int64_t tile0 = tile * kTile;
-  const int64_t base = tile0 + (int64_t)w * (kWave * ITEMS) + lane_id();
+  // keys in this tile (only the last tile of a pass is partial), and the tile
+  // position of this lane's first key: indices inside a tile are 32-bit
+  const int tile_n = (n - tile0) < kTile ? (int)(n - tile0) : kTile;
+  const int lbase = w * (kWave * ITEMS) + lane_id();
   const uint32_t mask = (1u << bits) - 1u;
   const uint64_t lt = lanemask_lt();
   const int bshift = ht.bshift;
@@ -651,8 +704,8 @@ scatter_tile(const void* __restrict__ keys_in, const uint32_t* __restrict__ vals
     uint64_t raw[FIRST ? ITEMS : 1];
 #pragma unroll
     for (int r = 0; r < ITEMS; ++r) {
-      const int64_t i = base + (int64_t)r * kWave;
-      const int64_t ic = i < n ? i : n - 1;
+      const int li = lbase + r * kWave;
+      const int64_t ic = tile0 + (li < tile_n ? li : tile_n - 1);
       if (FIRST) {
         raw[r] = static_cast<const uint64_t*>(keys_in)[ic];
         if (HOT) dig_hot[r / 4] |= (uint32_t)ht.digit[ic] << (8 * (r % 4));
@@ -678,20 +731,24 @@ scatter_tile(const void* __restrict__ keys_in, const uint32_t* __restrict__ vals
   auto dig = [&](int r) -> uint32_t {
     return HOT ? (dig_hot[r / 4] >> (8 * (r % 4))) & 0xffu : (key[r] >> shift) & mask;
   };
+  auto active_at = [&](int r) -> bool { return lbase + r * kWave < tile_n; };
   // Stable rank within (wave, digit): rounds in index order, lanes in order.
-  const int match_bits = HOT ? 8 : bits;
+  // Every pass but a plain first one has 8-bit digits (hot-key first: digit bytes).
+  constexpr bool kBits8 = HOT || !FIRST;
 #pragma unroll
   for (int r = 0; r < ITEMS; ++r) {
-    const int64_t i = base + (int64_t)r * kWave;
-    const bool active = i < n;
+    const bool active = active_at(r);
     const uint32_t digit = dig(r);
-    const uint64_t m = match_digit(digit, match_bits, active);
+    const uint64_t m = kBits8 ? match_digit_n<8>(digit, active) : match_digit(digit, bits, active);
     uint32_t before = 0;
     if (active) before = cnt[w][digit];
     // every lane of the wave has read the counter before the leader updates it
     __builtin_amdgcn_wave_barrier();
     if (active && (m & lt) == 0) cnt[w][digit] = before + (uint32_t)__popcll(m);
-    rank[r] = before + (uint32_t)__popcll(m & lt);
+    // (materialised here: a rank held as its 64-bit lane mask takes two registers)
+    // (on the hot-key first pass the compiler's own placement is kept: at
+    // more than 5 waves per SIMD that VALU-bound pass runs slower)
+    rank[r] = HOT ? before + (uint32_t)__popcll(m & lt) : opaque(before + (uint32_t)__popcll(m & lt));
     __builtin_amdgcn_wave_barrier();
   }
   __syncthreads();
@@ -739,59 +796,90 @@ scatter_tile(const void* __restrict__ keys_in, const uint32_t* __restrict__ vals
     }
   }
   __syncthreads();
+  if (ONE_BUF) {
+    // each key's tile position in digit order, then the keys staged
+    // (the digit taken again from the key: the counter addresses of the
+    // ranking are not held through the scan)
+    uint32_t pos[ITEMS];
 #pragma unroll
-  for (int r = 0; r < ITEMS; ++r) {
-    const int64_t i = base + (int64_t)r * kWave;
-    if (i < n) {
-      const uint32_t pos = cnt[w][dig(r)] + rank[r];
-      s_keys[pos] = key[r];
-      // kHotFirst: the digit beside the key's place in the tile
-      s_vals[pos] = HOT ? (uint32_t)(i - tile0) | (dig(r) << 16) : (FIRST ? (uint32_t)i : val[r]);
-    }
-  }
-  __syncthreads();
-  const int64_t tile_n = (n - tile0) < kTile ? (n - tile0) : kTile;
-  if (GAP) {
-    // cnt is free now: the hot prefix [0, 256), hot IDs [256, 512), buckets [512, 1024)
-    uint32_t* c32 = &cnt[0][0];
-    c32[d] = g_prefix;
-    c32[256 + d] = g_id;
-    c32[512 + d] = g_bucket0;
-    c32[512 + kSortBlock + d] = g_bucket1;
+    for (int r = 0; r < ITEMS; ++r) pos[r] = cnt[w][(opaque(key[r]) >> shift) & mask] + rank[r];
+#pragma unroll
+    for (int r = 0; r < ITEMS; ++r)
+      if (active_at(r)) s_keys[pos[r]] = key[r];
     __syncthreads();
-    const HotLookup gl{reinterpret_cast<const uint16_t*>(c32 + 512), c32 + 256, g_H, bshift};
-    const uint32_t* prefix = c32;
-    auto put = [&](int64_t i) {
-      const uint32_t k = s_keys[i];
-      bool hot;
-      const uint32_t below = gl.rank(k, &hot);
-      const uint32_t g = gshift[(k >> shift) & mask] + (uint32_t)i + prefix[below];
-      if ((int64_t)g < n_total) {   // always true when the counts are consistent
-        keys_out[g] = k;
-        vals_out[g] = s_vals[i];
-      }
-    };
-    if (tile_n == kTile) {
+    // staged position i = threadIdx.x + r * kSortBlock goes to out[r]
+    uint32_t out[ITEMS];
+    const int64_t bound = GAP ? n_total : n;   // always above out when the counts are consistent
+    if (GAP) {
+      // cnt is free now: the hot prefix [0, 256), hot IDs [256, 512), buckets [512, 1024)
+      uint32_t* c32 = &cnt[0][0];
+      c32[d] = g_prefix;
+      c32[256 + d] = g_id;
+      c32[512 + d] = g_bucket0;
+      c32[512 + kSortBlock + d] = g_bucket1;
+      __syncthreads();
+      const HotLookup gl{reinterpret_cast<const uint16_t*>(c32 + 512), c32 + 256, g_H, bshift};
 #pragma unroll
-      for (int r = 0; r < ITEMS; ++r) put(threadIdx.x + (int64_t)r * kSortBlock);
+      for (int r = 0; r < ITEMS; ++r) {
+        const int i = threadIdx.x + r * kSortBlock;
+        out[r] = 0u;
+        if (i < tile_n) {
+          const uint32_t k = s_keys[i];
+          bool hot;
+          const uint32_t below = gl.rank(k, &hot);
+          out[r] = gshift[(k >> shift) & mask] + (uint32_t)i + c32[below];
+          if ((int64_t)out[r] < bound) keys_out[out[r]] = k;
+        }
+      }
     } else {
-      for (int64_t i = threadIdx.x; i < tile_n; i += kSortBlock) put(i);
+#pragma unroll
+      for (int r = 0; r < ITEMS; ++r) {
+        const int i = threadIdx.x + r * kSortBlock;
+        out[r] = 0u;
+        if (i < tile_n) {
+          const uint32_t k = s_keys[i];
+          out[r] = gshift[(k >> shift) & mask] + (uint32_t)i;
+          if ((int64_t)out[r] < bound) keys_out[out[r]] = k;
+        }
+      }
+    }
+    __syncthreads();   // every key is read out before the values take the buffer
+#pragma unroll
+    for (int r = 0; r < ITEMS; ++r)
+      if (active_at(r)) s_keys[pos[r]] = FIRST ? (uint32_t)(tile0 + lbase + r * kWave) : val[r];
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < ITEMS; ++r) {
+      const int i = threadIdx.x + r * kSortBlock;
+      if (i < tile_n && (int64_t)out[r] < bound) vals_out[out[r]] = s_keys[i];
     }
     return;
   }
+#pragma unroll
+  for (int r = 0; r < ITEMS; ++r) {
+    if (active_at(r)) {
+      const int li = lbase + r * kWave;
+      const uint32_t dr = dig(r);
+      const uint32_t pos = cnt[w][dr] + rank[r];
+      s_keys[pos] = key[r];
+      // kHotFirst: the digit beside the key's place in the tile
+      s_vals[pos] = (uint32_t)li | (dr << 16);
+    }
+  }
+  __syncthreads();
   for (int i = threadIdx.x; i < tile_n; i += kSortBlock) {
     const uint32_t k = s_keys[i];
     const uint32_t v = s_vals[i];
-    const uint32_t digit = HOT ? v >> 16 : (k >> shift) & mask;
-    const uint32_t val_out = HOT ? (uint32_t)tile0 + (v & 0xffffu) : v;
+    const uint32_t digit = v >> 16;
+    const uint32_t val_out = (uint32_t)tile0 + (v & 0xffffu);
     const uint32_t g = gshift[digit] + (uint32_t)i;
     uint32_t* ko = keys_out;
     uint32_t* vo = vals_out;
     bool store_key = true;
-    if (HOT && digit >= cold_bins) {   // a hot ID: straight to its final place
+    if (digit >= cold_bins) {   // a hot ID: straight to its final place
       ko = keys_fin;
       vo = vals_fin;
-      store_key = !ht.split;           // split: only the occurrence indices are read
+      store_key = !ht.split;    // split: only the occurrence indices are read
     }
     if ((int64_t)g < n) {   // always true when the counts are consistent
       if (store_key) ko[g] = k;
