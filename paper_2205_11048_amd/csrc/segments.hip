@@ -1165,13 +1165,15 @@ hot_rows_kernel(SegmentArgs a, const int32_t* __restrict__ buckets, int q, int n
 // One block per hot ID: joins the chunks of its run in a fixed order and
 // writes its place among all IDs (after the cold segments below it, cnum),
 // its start (the cold occurrences below it plus the hot ones before it), c_r,
-// W_r and the weighted sum divided by c_r (or K).
+// W_r and the weighted sum divided by c_r (or K).  1024 threads: the hottest
+// ID of a large input has some 1,800 chunks, joined by 128 lane groups.
+constexpr int kHotFinBlock = 1024;
 template <int LPR>
-__global__ void __launch_bounds__(kFixBlock)
+__global__ void __launch_bounds__(kHotFinBlock)
 hot_finish_kernel(SegmentArgs a, HotPartials hp, const uint32_t* __restrict__ cnum,
                   const uint32_t* __restrict__ cold_below) {
-  constexpr int G = kFixBlock / LPR;
-  __shared__ f64x4 s_acc[kFixBlock];
+  constexpr int G = kHotFinBlock / LPR;
+  __shared__ f64x4 s_acc[kHotFinBlock];
   __shared__ int32_t s_c[G], s_a[G];
   const uint32_t H = *a.hot.meta;
   const uint32_t h = blockIdx.x;
@@ -1314,7 +1316,7 @@ static hipError_t launch_rows(const SegmentArgs& a, const uint32_t* packed, cons
     hipLaunchKernelGGL(hot_rows_kernel<LPR>, dim3((unsigned)L.hot_chunks), dim3(kSegBlock), lds, stream, a, buckets,
                        q, nb, hp);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(hot_finish_kernel<LPR>, dim3(kHotSlots), dim3(kFixBlock), 0, stream, a, hp, cnum,
+    hipLaunchKernelGGL(hot_finish_kernel<LPR>, dim3(kHotSlots), dim3(kHotFinBlock), 0, stream, a, hp, cnum,
                        cnum + 2 * (kHotSlots + 1));
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
