@@ -973,52 +973,100 @@ seg_rows_kernel(SegmentArgs a, const uint32_t* __restrict__ packed, const uint32
 // Joins, for each segment that runs past the end of the tile holding its
 // head, the partial sums of every later tile it covers.  Only the tiles the
 // row pass listed are visited (about a third of them for Zipf IDs), spread
-// over a fixed grid; 256/LPR groups with eight loads in flight each sum the
-// longest chain (the hottest ID: some 1700 tiles at 65M positions).
+// over a fixed grid.  A lane group takes one listed tile whose segment covers
+// at most kFixShort (and at most 256/LPR) later tiles, which is nearly all of
+// them (the hot IDs have their own pass), with all its loads in flight at
+// once; a longer chain (some 1700 tiles for the hottest ID at 65M positions
+// without the hot-key plan) is summed by the whole block, 256/LPR groups with
+// eight loads in flight each.  Both add the tail of the first tile, then the
+// later tiles' partials in tile order.
 constexpr int kFixBlock = 256;
 constexpr int64_t kFixGrid = 2048;
+constexpr int kFixShort = 8;
 template <int LPR>
 __global__ void __launch_bounds__(kFixBlock)
 seg_fixup_kernel(SegmentArgs a, SegPartials part) {
   constexpr int G = kFixBlock / LPR;
+  // a chain of at most G later tiles is summed in the same order by both paths
+  constexpr int kShort = kFixShort < G ? kFixShort : G;
   __shared__ f64x4 s_acc[kFixBlock];
   __shared__ int32_t s_cc[G], s_ww[G];
+  __shared__ uint32_t s_long[G];
+  __shared__ uint32_t s_nlong;
   const int lane = threadIdx.x % LPR;
   const int grp = threadIdx.x / LPR;
   const bool lane_on = lane * 4 < a.D;
   const int D = a.D;
   const uint32_t count = *part.fix_count;
   // the listed tiles in any order: each one's sum is taken in a fixed order
-  for (uint32_t k = blockIdx.x; k < count; k += gridDim.x) {
-    const u32x4 rec = part.fix_list[k];
-    const int64_t b = rec.x, seg = rec.y, b_end = rec.z, hb = rec.w;   // hb: hot IDs before it (split plan)
-    if (seg >= a.N) continue;   // unreachable when the numbering is consistent (block-uniform)
-    f64x4 acc = {0.0, 0.0, 0.0, 0.0};
-    int cc = 0, ww = 0;
-#pragma unroll 8
-    for (int64_t bb = b + 1 + grp; bb <= b_end; bb += G) {
-      if (lane_on) acc += *reinterpret_cast<const f64x4*>(part.first_acc + bb * D + lane * 4);
-      cc += part.first_cc[bb];
-      ww += part.first_ww[bb];
-    }
-    s_acc[threadIdx.x] = acc;
-    if (lane == 0) {
-      s_cc[grp] = cc;
-      s_ww[grp] = ww;
+  for (uint32_t k0 = blockIdx.x * (uint32_t)G; k0 < count; k0 += gridDim.x * (uint32_t)G) {
+    if (threadIdx.x == 0) s_nlong = 0u;
+    __syncthreads();
+    const uint32_t k = k0 + grp;
+    if (k < count) {
+      const u32x4 rec = part.fix_list[k];
+      const int64_t b = rec.x, seg = rec.y, b_end = rec.z, hb = rec.w;   // hb: hot IDs before it (split plan)
+      if (seg < a.N) {   // always true when the numbering is consistent
+        if (b_end - b <= kShort) {
+          f64x4 v[kShort];
+          int32_t c[kShort], ww[kShort];
+#pragma unroll
+          for (int u = 0; u < kShort; ++u) {
+            const int64_t bb = b + 1 + u;
+            const int64_t bc = bb <= b_end ? bb : b;   // clamped: read, then ignored
+            v[u] = lane_on ? *reinterpret_cast<const f64x4*>(part.first_acc + bc * D + lane * 4)
+                           : f64x4{0.0, 0.0, 0.0, 0.0};
+            c[u] = part.first_cc[bc];
+            ww[u] = part.first_ww[bc];
+          }
+          f64x4 tot = lane_on ? *reinterpret_cast<const f64x4*>(part.last_acc + b * D + lane * 4)
+                              : f64x4{0.0, 0.0, 0.0, 0.0};
+          int tcc = part.last_cc[b], tww = part.last_ww[b];
+#pragma unroll
+          for (int u = 0; u < kShort; ++u) {
+            if (b + 1 + u > b_end) break;
+            tot += v[u];
+            tcc += c[u];
+            tww += ww[u];
+          }
+          finalize_segment(a, seg + hb, tot, tcc, tww, lane, lane_on, a.ap.mode);
+        } else if (lane == 0) {
+          s_long[atomicAdd(&s_nlong, 1u)] = k;
+        }
+      }
     }
     __syncthreads();
-    if (grp == 0) {
-      f64x4 tot = lane_on ? *reinterpret_cast<const f64x4*>(part.last_acc + b * D + lane * 4)
-                          : f64x4{0.0, 0.0, 0.0, 0.0};
-      int tcc = part.last_cc[b], tww = part.last_ww[b];
-      for (int g = 0; g < G; ++g) {
-        tot += s_acc[g * LPR + lane];
-        tcc += s_cc[g];
-        tww += s_ww[g];
+    const uint32_t nlong = s_nlong;
+    for (uint32_t i = 0; i < nlong; ++i) {
+      const u32x4 rec = part.fix_list[s_long[i]];
+      const int64_t b = rec.x, seg = rec.y, b_end = rec.z, hb = rec.w;
+      f64x4 acc = {0.0, 0.0, 0.0, 0.0};
+      int cc = 0, ww = 0;
+#pragma unroll 8
+      for (int64_t bb = b + 1 + grp; bb <= b_end; bb += G) {
+        if (lane_on) acc += *reinterpret_cast<const f64x4*>(part.first_acc + bb * D + lane * 4);
+        cc += part.first_cc[bb];
+        ww += part.first_ww[bb];
       }
-      finalize_segment(a, seg + hb, tot, tcc, tww, lane, lane_on, a.ap.mode);
+      s_acc[threadIdx.x] = acc;
+      if (lane == 0) {
+        s_cc[grp] = cc;
+        s_ww[grp] = ww;
+      }
+      __syncthreads();
+      if (grp == 0) {
+        f64x4 tot = lane_on ? *reinterpret_cast<const f64x4*>(part.last_acc + b * D + lane * 4)
+                            : f64x4{0.0, 0.0, 0.0, 0.0};
+        int tcc = part.last_cc[b], tww = part.last_ww[b];
+        for (int g = 0; g < G; ++g) {
+          tot += s_acc[g * LPR + lane];
+          tcc += s_cc[g];
+          tww += s_ww[g];
+        }
+        finalize_segment(a, seg + hb, tot, tcc, tww, lane, lane_on, a.ap.mode);
+      }
+      __syncthreads();   // s_acc is rewritten for the next long chain
     }
-    __syncthreads();   // s_acc is rewritten for the next listed tile
   }
 }
 
@@ -1165,15 +1213,15 @@ hot_rows_kernel(SegmentArgs a, const int32_t* __restrict__ buckets, int q, int n
 // One block per hot ID: joins the chunks of its run in a fixed order and
 // writes its place among all IDs (after the cold segments below it, cnum),
 // its start (the cold occurrences below it plus the hot ones before it), c_r,
-// W_r and the weighted sum divided by c_r (or K).  1024 threads: the hottest
-// ID of a large input has some 1,800 chunks, joined by 128 lane groups.
-constexpr int kHotFinBlock = 1024;
-template <int LPR>
-__global__ void __launch_bounds__(kHotFinBlock)
+// W_r and the weighted sum divided by c_r (or K).  From 2^25 occurrences the
+// blocks have 1024 threads (the hottest ID then has some 1,800 chunks, joined
+// by 128 lane groups), below that 256.
+template <int LPR, int BLOCK>
+__global__ void __launch_bounds__(BLOCK)
 hot_finish_kernel(SegmentArgs a, HotPartials hp, const uint32_t* __restrict__ cnum,
                   const uint32_t* __restrict__ cold_below) {
-  constexpr int G = kHotFinBlock / LPR;
-  __shared__ f64x4 s_acc[kHotFinBlock];
+  constexpr int G = BLOCK / LPR;
+  __shared__ f64x4 s_acc[BLOCK];
   __shared__ int32_t s_c[G], s_a[G];
   const uint32_t H = *a.hot.meta;
   const uint32_t h = blockIdx.x;
@@ -1316,8 +1364,12 @@ static hipError_t launch_rows(const SegmentArgs& a, const uint32_t* packed, cons
     hipLaunchKernelGGL(hot_rows_kernel<LPR>, dim3((unsigned)L.hot_chunks), dim3(kSegBlock), lds, stream, a, buckets,
                        q, nb, hp);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    hipLaunchKernelGGL(hot_finish_kernel<LPR>, dim3(kHotSlots), dim3(kHotFinBlock), 0, stream, a, hp, cnum,
-                       cnum + 2 * (kHotSlots + 1));
+    if (a.N >= (int64_t(1) << 25))
+      hipLaunchKernelGGL((hot_finish_kernel<LPR, 1024>), dim3(kHotSlots), dim3(1024), 0, stream, a, hp, cnum,
+                         cnum + 2 * (kHotSlots + 1));
+    else
+      hipLaunchKernelGGL((hot_finish_kernel<LPR, 256>), dim3(kHotSlots), dim3(256), 0, stream, a, hp, cnum,
+                         cnum + 2 * (kHotSlots + 1));
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   return hipSuccess;
