@@ -500,7 +500,7 @@ def ceilings(w, table, contrib_rows, gba, torch, stream):
     grids = (1024, 2048, 4096, 8192)
     sink = torch.empty(gba.gba_ceiling_sink_words(max(grids)), dtype=torch.int32, device="cuda")
     src = torch.empty(1 << 30, dtype=torch.float32, device="cuda")        # 4 GiB
-    best = min((timed(lambda: gba.gba_ceiling_read(src, sink, b)), b) for b in grids)
+    best = min((timed(lambda: gba.gba_ceiling_read(src, sink, b)), b) for b in (512,) + grids)
     nbytes = src.numel() * 4
     out["read_stream"] = dict(bytes=nbytes, blocks=best[1], us=best[0] * 1e3, gbs=nbytes / (best[0] * 1e-3) / 1e9)
     del src

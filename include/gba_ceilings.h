@@ -28,7 +28,7 @@ extern "C" {
  *   src     [n16 * 16] bytes, 16-byte aligned; any contents.
  *   sink    [gba_ceiling_sink_words(blocks)] uint32 out: one word per wave
  *           (an XOR of what the wave read, so the loads are not removed).
- *   blocks  workgroups of 256 threads (>= 1); each takes 8 vectors per thread
+ *   blocks  workgroups of 256 threads (>= 1); each takes 4 vectors per thread
  *           per round and walks the array in a grid-stride loop.
  * Bytes moved: 16 * n16 read, 4 per wave written.
  */
@@ -37,7 +37,8 @@ gba_status gba_ceiling_read(const void* src, int64_t n16, uint32_t* sink, int32_
 /*
  * Copies n16 16-byte vectors from src to dst (non-temporal loads and stores).
  *   src, dst  [n16 * 16] bytes each, 16-byte aligned, not overlapping.
- *   blocks    as for gba_ceiling_read.
+ *   blocks    workgroups of 256 threads (>= 1); each takes 8 vectors per
+ *             thread per round and walks the arrays in a grid-stride loop.
  * Bytes moved: 16 * n16 read, 16 * n16 written.
  */
 gba_status gba_ceiling_copy(const void* src, void* dst, int64_t n16, int32_t blocks, hipStream_t stream);

@@ -8,6 +8,10 @@ namespace gba {
 
 constexpr int kCeilBlock = 256;
 constexpr int kCeilUnroll = 8;   // vectors (or rows) in flight per lane
+// the read stream: 4 vectors per lane (of the shapes tried, 256 or 512
+// threads with 4, 8 or 16 vectors per lane, lane-consecutive or in runs of
+// 1-16 KB per wave, at 512-16384 blocks, this one read fastest)
+constexpr int kCeilReadUnroll = 4;
 constexpr int kCeilWaves = kCeilBlock / kWave;
 
 __device__ __forceinline__ uint32_t bits_of(f32x4 v) {
@@ -20,21 +24,21 @@ __device__ __forceinline__ void put_wave_word(uint32_t x, uint32_t* sink) {
   if (lane_id() == 0) sink[(int64_t)blockIdx.x * kCeilWaves + threadIdx.x / kWave] = x;
 }
 
-// Each round a block reads kCeilUnroll * kCeilBlock consecutive vectors
-// (32 KB), lane-consecutive, all loads issued before the first is used.
+// Each round a block reads kCeilReadUnroll * kCeilBlock consecutive vectors
+// (16 KB), lane-consecutive, all loads issued before the first is used.
 __global__ void __launch_bounds__(kCeilBlock)
 ceiling_read_kernel(const f32x4* __restrict__ src, int64_t n, uint32_t* __restrict__ sink) {
-  constexpr int64_t kSpan = (int64_t)kCeilBlock * kCeilUnroll;
+  constexpr int64_t kSpan = (int64_t)kCeilBlock * kCeilReadUnroll;
   uint32_t x = 0;
   for (int64_t b = (int64_t)blockIdx.x * kSpan; b < n; b += (int64_t)gridDim.x * kSpan) {
-    f32x4 v[kCeilUnroll];
+    f32x4 v[kCeilReadUnroll];
 #pragma unroll
-    for (int u = 0; u < kCeilUnroll; ++u) {
+    for (int u = 0; u < kCeilReadUnroll; ++u) {
       const int64_t i = b + (int64_t)u * kCeilBlock + threadIdx.x;
       v[u] = i < n ? load_stream(src + i) : f32x4{0.f, 0.f, 0.f, 0.f};
     }
 #pragma unroll
-    for (int u = 0; u < kCeilUnroll; ++u) x ^= bits_of(v[u]);
+    for (int u = 0; u < kCeilReadUnroll; ++u) x ^= bits_of(v[u]);
   }
   put_wave_word(x, sink);
 }
