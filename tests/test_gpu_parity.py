@@ -222,6 +222,30 @@ def test_sparse_one_hot_id_spans_many_blocks(D, plan):
     _check_sparse(res, ids, rows, off, w, tokens, 100, 3, expect_exact=True)
 
 
+@pytest.mark.parametrize("D,tile,short", [(4, 8192, 8), (32, 1024, 8), (256, 128, 4)])
+def test_sparse_fixup_chain_lengths(D, tile, short):
+    """Segments that run on past their head's row-pass tile by exactly the
+    chain length the fix-up sums in one lane group (`short` later tiles), and by
+    one and two more, which the whole block sums.  Under 2^23 occurrences a
+    row-pass tile holds 32 positions per lane group (4 waves, 64 / (D / 4)
+    groups per wave)."""
+    K = 3
+    nA = short * tile + 1                  # head at position 0, ends at the first position of tile `short`
+    nB = (short + 1) * tile                # head in tile `short`, runs on over short + 1 later tiles
+    nC = (short + 2) * tile
+    rng = np.random.default_rng(D)
+    ids = rng.permutation(np.repeat(np.array([5, 9, 13], np.int64), [nA, nB, nC]))
+    N = ids.size
+    cut = np.sort(rng.choice(np.arange(1, N), K - 1, replace=False))
+    off = np.concatenate([[0], cut, [N]]).astype(np.int64)
+    rows = counter.values_range(11, counter.STREAM_ROWS, 0, N * D, counter.KIND_DYADIC).reshape(N, D)
+    tokens = np.array([50, 49, 47])
+    w, _, _ = oracle.token_weights(tokens, 50, 2)
+    res = _run_sparse(ids, rows, off, w, tokens, 50, 2, 20)
+    ref = _check_sparse(res, ids, rows, off, w, tokens, 50, 2, expect_exact=True)
+    assert list(ref["seg_offsets"]) == [0, nA, nA + nB, N]
+
+
 @pytest.mark.parametrize("plan", [None, gba.SORT_HOT])
 def test_sparse_single_id_everywhere(plan):
     """Every occurrence holds one ID (with the hot-key plan: no cold key at all)."""
