@@ -54,6 +54,16 @@ def test_sort_zipf(n, R, plan):
     check(zipf_ids(rng, n, R, 1.1), R, plan)
 
 
+@pytest.mark.parametrize("n", [511 * 4096, 512 * 4096, 512 * 4096 + 1])
+def test_sort_tile_order_around_one_round_of_xcd_chunks(n):
+    """Passes of 511, 512 and 513 tiles of 4096 keys (and 1022, 1024, 1025 of
+    2048 on the first pass): below one round of 8 chunks of 64 tiles the tiles
+    are split in eighths over the XCDs, from one round on in chunks, with the
+    tiles past the last whole round in order."""
+    rng = np.random.default_rng(n)
+    check(zipf_ids(rng, n, 1 << 24, 1.1), 1 << 24, gba.SORT_PLAIN)
+
+
 @pytest.mark.parametrize("plan", [gba.SORT_PLAIN, gba.SORT_HOT, gba.SORT_AUTO])
 def test_sort_large_skewed_auto_picks_the_hot_plan(plan):
     # above the size where the automatic plan takes the hot keys apart
