@@ -6,13 +6,15 @@
 //
 // find-or-insert is three launches, so no thread ever waits for another's
 // write: (1) every position claims or finds its ID's slot (compare-and-swap on
-// the slot's ID; IDs are never removed, so a non-empty slot never changes);
-// a slot that holds no row yet (claimed now, or by an earlier call that found
-// the pool full) is appended to a list once, by the one position whose
-// compare-and-swap marks its row as pending, one list atomic per wave; (2)
-// the listed slots get the next rows of the pool, in list order (a slot past
-// the end of the pool is left without a row, to be served by a later call);
-// (3) every position reads its slot's row.
+// the slot's ID; IDs are never removed, so a non-empty slot never changes) and
+// writes its row where the slot already has one; a slot that holds no row yet
+// (claimed now, or by an earlier call that found the pool full) is appended to
+// a list once, by the one position whose compare-and-swap marks its row as
+// pending, and every position of such a slot to a second list, one list
+// atomic per wave each; (2) the listed slots get the next rows of the pool, in
+// list order (a slot past the end of the pool is left without a row, to be
+// served by a later call); (3) the listed positions read their slot's row.
+// Once every ID is known, (2) and (3) find empty lists.
 #include "gba_device.hpp"
 #include "gba_internal.hpp"
 
@@ -25,16 +27,16 @@ static inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 static inline size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
 
 struct HashLayout {
-  size_t off_slot, off_claimed, off_count, bytes;
+  size_t off_pending, off_claimed, off_count, bytes;
 };
 
 static HashLayout hash_layout(int64_t n) {
   HashLayout L{};
   const size_t m = (size_t)(n > 0 ? n : 1);
   size_t o = 0;
-  L.off_slot = o;    o += align_up(m * 4);    // slot of each position
-  L.off_claimed = o; o += align_up(m * 4);    // slots claimed by this call
-  L.off_count = o;   o += 256;                // number of claimed slots
+  L.off_pending = o; o += align_up(m * 8);    // (position, slot) of the positions waiting for a row
+  L.off_claimed = o; o += align_up(m * 4);    // slots listed for a row by this call
+  L.off_count = o;   o += 256;                // [0] listed slots, [1] waiting positions
   L.bytes = o;
   return L;
 }
@@ -57,7 +59,22 @@ __device__ __forceinline__ uint64_t mix64(uint64_t h) {
 constexpr int32_t kNoRow = -1;
 constexpr int32_t kPendingRow = -2;
 
-__global__ void hash_count_reset_kernel(uint32_t* __restrict__ claimed_count) { *claimed_count = 0u; }
+__global__ void hash_count_reset_kernel(uint32_t* __restrict__ counts) {
+  counts[0] = 0u;
+  counts[1] = 0u;
+}
+
+// Appends this lane's `value` to list[] when `on`, one atomic per wave.
+template <typename T>
+__device__ __forceinline__ void wave_append(bool on, T value, T* __restrict__ list, uint32_t* __restrict__ count) {
+  const uint64_t m = __ballot(on);
+  if (!m) return;
+  const int leader = __ffsll((unsigned long long)m) - 1;
+  uint32_t at = 0;
+  if (lane_id() == leader) at = atomicAdd(count, (uint32_t)__popcll(m));
+  at = __shfl(at, leader, kWave);
+  if (on) list[at + __popcll(m & lanemask_lt())] = value;
+}
 
 __global__ void __launch_bounds__(kHashBlock)
 hash_clear_kernel(int64_t* __restrict__ slot_ids, int32_t* __restrict__ slot_rows, int64_t capacity) {
@@ -95,18 +112,19 @@ __device__ __forceinline__ int64_t claim_or_find(int64_t* slot_ids, int64_t mask
 
 __global__ void __launch_bounds__(kHashBlock)
 hash_claim_kernel(int64_t* __restrict__ slot_ids, int32_t* __restrict__ slot_rows, int64_t mask,
-                  const int64_t* __restrict__ ids, int64_t n, int32_t* __restrict__ slot_of, int32_t* __restrict__ claimed_slots,
-                  uint32_t* __restrict__ claimed_count, int32_t* __restrict__ err) {
+                  const int64_t* __restrict__ ids, int64_t n, int64_t* __restrict__ rows_out,
+                  int2* __restrict__ pending, int32_t* __restrict__ claimed_slots, uint32_t* __restrict__ counts,
+                  int32_t* __restrict__ err) {
   const int64_t stride = (int64_t)gridDim.x * kHashBlock;
-  const uint64_t lt = lanemask_lt();
-  // every lane of a wave runs the same number of rounds, so the ballots below
-  // see the whole wave
+  // every lane of a wave runs the same number of rounds, so the ballots of
+  // the list appends see the whole wave
   for (int64_t base = (int64_t)blockIdx.x * kHashBlock + (threadIdx.x & ~(kWave - 1)); base < n; base += stride) {
     const int64_t i = base + lane_id();
-    bool claimed = false;
+    bool claimed = false, waits = false;
     int64_t s = -1;
     if (i < n) {
       const int64_t id = ids[i];
+      int64_t row = -1;
       if (id == GBA_EMPTY_ID) {
         raise_error(err, GBA_DERR_ID_RANGE);
       } else {
@@ -114,22 +132,23 @@ hash_claim_kernel(int64_t* __restrict__ slot_ids, int32_t* __restrict__ slot_row
         s = claim_or_find(slot_ids, mask, id, &fresh);
         if (s < 0) {
           raise_error(err, GBA_DERR_TABLE_FULL);
-        } else if (slot_rows[s] == kNoRow) {
-          // the slot has no row yet: exactly one position lists it (rows are
-          // written only by the next launch, so kNoRow cannot turn into a row
-          // during this one)
-          claimed = atomicCAS(slot_rows + s, kNoRow, kPendingRow) == kNoRow;
+        } else {
+          const int32_t r = slot_rows[s];
+          if (r >= 0) {
+            row = r;   // rows are handed out only by the next launch: a row never changes
+          } else {
+            // the slot has no row yet: exactly one position lists it (kNoRow
+            // cannot turn into a row during this launch), and every position
+            // of the slot reads its row after the rows are handed out
+            if (r == kNoRow) claimed = atomicCAS(slot_rows + s, kNoRow, kPendingRow) == kNoRow;
+            waits = true;
+          }
         }
       }
-      slot_of[i] = (int32_t)s;
+      if (!waits) rows_out[i] = row;
     }
-    const uint64_t m = __ballot(claimed);
-    if (m) {
-      uint32_t at = 0;
-      if (lane_id() == __ffsll((unsigned long long)m) - 1) at = atomicAdd(claimed_count, (uint32_t)__popcll(m));
-      at = __shfl(at, __ffsll((unsigned long long)m) - 1, kWave);
-      if (claimed) claimed_slots[at + __popcll(m & lt)] = (int32_t)s;
-    }
+    wave_append(claimed, (int32_t)s, claimed_slots, counts);
+    wave_append(waits, make_int2((int32_t)i, (int32_t)s), pending, counts + 1);
   }
 }
 
@@ -163,17 +182,19 @@ __global__ void hash_count_kernel(const uint32_t* __restrict__ claimed_count, in
   if (num_new) *num_new = c;
 }
 
-// A position whose ID has no slot or no row gets -1 and reports the table full.
+// The positions that waited for a row read it; one whose slot got none (the
+// pool is full) gets -1 and reports the table full.
 __global__ void __launch_bounds__(kHashBlock)
-hash_rows_kernel(const int32_t* __restrict__ slot_rows, const int32_t* __restrict__ slot_of, int64_t n,
-                 int64_t* __restrict__ rows_out, int32_t* __restrict__ err) {
+hash_rows_kernel(const int32_t* __restrict__ slot_rows, const int2* __restrict__ pending,
+                 const uint32_t* __restrict__ counts, int64_t* __restrict__ rows_out, int32_t* __restrict__ err) {
+  const int64_t c = counts[1];
   const int64_t stride = (int64_t)gridDim.x * kHashBlock;
   bool full = false;
-  for (int64_t i = (int64_t)blockIdx.x * kHashBlock + threadIdx.x; i < n; i += stride) {
-    const int32_t s = slot_of[i];
-    const int32_t r = s < 0 ? -1 : slot_rows[s];
+  for (int64_t j = (int64_t)blockIdx.x * kHashBlock + threadIdx.x; j < c; j += stride) {
+    const int2 p = pending[j];
+    const int32_t r = slot_rows[p.y];
     full |= r < 0;
-    rows_out[i] = r < 0 ? -1 : (int64_t)r;
+    rows_out[p.x] = r < 0 ? -1 : (int64_t)r;
   }
   if (full) raise_error(err, GBA_DERR_TABLE_FULL);
 }
@@ -216,7 +237,7 @@ hipError_t launch_hash_find_or_insert(int64_t* slot_ids, int32_t* slot_rows, int
                                       hipStream_t stream) {
   const HashLayout L = hash_layout(n);
   char* base = static_cast<char*>(ws);
-  int32_t* slot_of = reinterpret_cast<int32_t*>(base + L.off_slot);
+  int2* pending = reinterpret_cast<int2*>(base + L.off_pending);
   int32_t* claimed = reinterpret_cast<int32_t*>(base + L.off_claimed);
   uint32_t* count = reinterpret_cast<uint32_t*>(base + L.off_count);
   // the counter is cleared by a kernel, not a memset, so the sequence can be
@@ -226,7 +247,7 @@ hipError_t launch_hash_find_or_insert(int64_t* slot_ids, int32_t* slot_rows, int
   if (e != hipSuccess) return e;
   if (n > 0) {
     hipLaunchKernelGGL(hash_claim_kernel, grid_for(n), dim3(kHashBlock), 0, stream, slot_ids, slot_rows, capacity - 1,
-                       ids, n, slot_of, claimed, count, err);
+                       ids, n, rows_out, pending, claimed, count, err);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(hash_assign_kernel, grid_for(n), dim3(kHashBlock), 0, stream, (const int64_t*)slot_ids,
                        slot_rows, (const int32_t*)claimed, (const uint32_t*)count, (const int64_t*)num_rows, max_rows,
@@ -238,7 +259,7 @@ hipError_t launch_hash_find_or_insert(int64_t* slot_ids, int32_t* slot_rows, int
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (n > 0) {
     hipLaunchKernelGGL(hash_rows_kernel, grid_for(n), dim3(kHashBlock), 0, stream, (const int32_t*)slot_rows,
-                       (const int32_t*)slot_of, n, rows_out, err);
+                       (const int2*)pending, (const uint32_t*)count, rows_out, err);
     e = hipGetLastError();
   }
   return e;
