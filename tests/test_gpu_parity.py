@@ -1243,6 +1243,36 @@ def test_sparse_random_shapes(K, n_max, R, D, decay, norm, seed, dyadic, zipf_s,
                   expect_exact=dyadic)
 
 
+@_hyp(8, suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large])
+@given(K=hst.integers(1, 300), n_target=hst.sampled_from([200_000, 700_000, 2_000_000, 4_500_000, 6_000_000]),
+       R=hst.sampled_from([1000, 70_000, 1 << 22, 20_000_000, 500_000_000]),
+       D=hst.sampled_from([4, 16, 32, 64, 256]), decay=hst.sampled_from(["token", "id_tag"]),
+       norm=hst.sampled_from(["per_id_count", "by_k"]), seed=hst.integers(0, 2 ** 31 - 1),
+       dyadic=hst.booleans(), zipf_s=hst.sampled_from([0.7, 1.05, 1.2, 2.0]),
+       plan=hst.sampled_from([None, gba.SORT_HOT]))
+def test_sparse_random_medium_shapes(K, n_target, R, D, decay, norm, seed, dyadic, zipf_s, plan):
+    """Random inputs of 0.2 M to 6 M occurrences (many sort tiles, row-pass
+    tiles and hot chunks, segments running across tiles, the automatic plan
+    turning to hot keys from 2^22 occurrences), uneven and empty
+    contributions: the GPU equals the oracle (exactly on dyadic values)."""
+    rng = np.random.default_rng(seed)
+    n_target = min(n_target, 64_000_000 // D)          # at most 256 MB of rows
+    sizes = rng.integers(0, 2 * n_target // K + 2, K)
+    sizes[rng.random(K) < 0.2] = 0
+    if R > 50_000_000:
+        decay = "token"                                 # tags are drawn for tables up to 50 M rows
+    kind = counter.KIND_DYADIC if dyadic else counter.KIND_GRAD
+    print(f"medium sparse case K={K} N={int(sizes.sum())} R={R} D={D} decay={decay} norm={norm} "
+          f"s={zipf_s} plan={plan} seed={seed}", flush=True)
+    ids, rows, off, tokens, tag = _case(K, sizes, R, D, seed % 100_000, zipf_s=zipf_s, kind=kind, stale_hi=6)
+    iota = 3
+    w, _, _ = oracle.token_weights(tokens, 1000, iota)
+    res = _run_sparse(ids, rows, off, w, tokens, 1000, iota, R, tag if decay == "id_tag" else None, decay, norm,
+                      plan=plan)
+    _check_sparse(res, ids, rows, off, w, tokens, 1000, iota, tag if decay == "id_tag" else None, decay, norm,
+                  expect_exact=dyadic)
+
+
 @_hyp(40, suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large])
 @given(K=hst.integers(1, 12), n_max=hst.integers(0, 3000), R=hst.sampled_from([1, 2, 17, 1000, 70_000]),
        D=hst.sampled_from([4, 16, 20, 24, 28, 32, 64]), decay=hst.sampled_from(["token", "id_tag"]),
