@@ -1273,17 +1273,9 @@ def test_sparse_random_medium_shapes(K, n_target, R, D, decay, norm, seed, dyadi
                   expect_exact=dyadic)
 
 
-@_hyp(40, suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large])
-@given(K=hst.integers(1, 12), n_max=hst.integers(0, 3000), R=hst.sampled_from([1, 2, 17, 1000, 70_000]),
-       D=hst.sampled_from([4, 16, 20, 24, 28, 32, 64]), decay=hst.sampled_from(["token", "id_tag"]),
-       norm=hst.sampled_from(["per_id_count", "by_k"]), seed=hst.integers(0, 2 ** 31 - 1),
-       opt=hst.sampled_from(["adagrad", "adam"]), keep_agg=hst.booleans())
-def test_fused_sparse_random_shapes(K, n_max, R, D, decay, norm, seed, opt, keep_agg):
-    """Random shapes, empty contributions and tiny tables: the fused sparse call
-    gives bitwise the outputs, table and state of the two separate calls."""
-    rng = np.random.default_rng(seed)
-    sizes = rng.integers(0, n_max + 1, K)
-    sizes[rng.random(K) < 0.2] = 0
+def _fused_vs_separate(K, sizes, R, D, decay, norm, seed, opt, keep_agg):
+    """The fused sparse call against the aggregation and the row apply as two
+    calls, from the same table and state: outputs, table and state bitwise."""
     ids, rows, off, tokens, tag = _case(K, sizes, R, D, seed % 100_000, stale_hi=4)
     step, iota = 1000, 2
     w, _, _ = oracle.token_weights(tokens, step, iota)
@@ -1305,6 +1297,39 @@ def test_fused_sparse_random_shapes(K, n_max, R, D, decay, norm, seed, opt, keep
         assert torch.equal(fus["slots"][i], sep["slots"][i]), f"state {i}"
     if decay == "id_tag":
         assert_exact(fus["tag"], sep["tag"], "tag")
+
+
+@_hyp(40, suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large])
+@given(K=hst.integers(1, 12), n_max=hst.integers(0, 3000), R=hst.sampled_from([1, 2, 17, 1000, 70_000]),
+       D=hst.sampled_from([4, 16, 20, 24, 28, 32, 64]), decay=hst.sampled_from(["token", "id_tag"]),
+       norm=hst.sampled_from(["per_id_count", "by_k"]), seed=hst.integers(0, 2 ** 31 - 1),
+       opt=hst.sampled_from(["adagrad", "adam"]), keep_agg=hst.booleans())
+def test_fused_sparse_random_shapes(K, n_max, R, D, decay, norm, seed, opt, keep_agg):
+    """Random shapes, empty contributions and tiny tables: the fused sparse call
+    gives bitwise the outputs, table and state of the two separate calls."""
+    rng = np.random.default_rng(seed)
+    sizes = rng.integers(0, n_max + 1, K)
+    sizes[rng.random(K) < 0.2] = 0
+    _fused_vs_separate(K, sizes, R, D, decay, norm, seed, opt, keep_agg)
+
+
+@_hyp(6, suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large])
+@given(K=hst.integers(1, 300), n_target=hst.sampled_from([200_000, 700_000, 2_000_000, 4_500_000]),
+       R=hst.sampled_from([70_000, 1 << 22, 20_000_000]), D=hst.sampled_from([16, 20, 24, 28, 32, 64]),
+       decay=hst.sampled_from(["token", "id_tag"]), norm=hst.sampled_from(["per_id_count", "by_k"]),
+       seed=hst.integers(0, 2 ** 31 - 1), opt=hst.sampled_from(["adagrad", "adam"]), keep_agg=hst.booleans())
+def test_fused_sparse_random_medium_shapes(K, n_target, R, D, decay, norm, seed, opt, keep_agg):
+    """0.2 M to 4.5 M occurrences (the row pass over many tiles, with the rows
+    updated as their segments close where Adagrad meets rows of 20 to 32
+    floats): the fused call gives bitwise the outputs, table and state of the
+    two separate calls."""
+    rng = np.random.default_rng(seed)
+    n_target = min(n_target, 64_000_000 // D)
+    sizes = rng.integers(0, 2 * n_target // K + 2, K)
+    sizes[rng.random(K) < 0.2] = 0
+    print(f"medium fused case K={K} N={int(sizes.sum())} R={R} D={D} decay={decay} norm={norm} opt={opt} "
+          f"keep_agg={keep_agg} seed={seed}", flush=True)
+    _fused_vs_separate(K, sizes, R, D, decay, norm, seed, opt, keep_agg)
 
 
 @_hyp(40, suppress_health_check=[HealthCheck.too_slow])
