@@ -952,6 +952,33 @@ def test_pull_rows(n, R, D, kind):
     assert_exact(got["rows"][:U], rows, "rows")
 
 
+@pytest.mark.parametrize("n,R,D,s", [(100_000, 1000, 32, 1.1), (1_000_000, 70_000, 16, 0.7),
+                                     (1_000_000, 1 << 22, 32, 2.0), (4_500_000, 1 << 22, 4, 1.1),
+                                     (4_500_000, 20_000_000, 4, 0.7)])
+def test_pull_rows_medium(n, R, D, s):
+    """Requests of 0.1 M to 4.5 M IDs (the largest take the hot-key sort plan)
+    over tables up to 20 M rows: unique IDs, inverse map and rows equal the
+    oracle's."""
+    print(f"pull case n={n} R={R} D={D} s={s}", flush=True)
+    from synth.zipf import ZipfRejectionInversion, rank_to_row
+    ids = rank_to_row(ZipfRejectionInversion(R, s).ranks(n + 3, np.arange(n)) - 1, R).astype(np.int64)
+    seed = n + R
+    table_d = sdev.fill(torch.empty((R, D), dtype=torch.float32, device=DEV), seed, counter.STREAM_TABLE,
+                        counter.KIND_PARAM)
+    table = host(table_d)
+    for r in np.random.default_rng(seed).integers(0, R, 64):   # the device generator's rows are the host's
+        assert_exact(table[r], counter.values_range(seed, counter.STREAM_TABLE, int(r) * D, D, counter.KIND_PARAM),
+                     "generated table row")
+    got, err = _pull(ids, table_d, R)
+    assert err == 0
+    u, inv, rows = oracle.pull_rows(ids, table)
+    U = int(got["nu"][0])
+    assert U == u.size
+    assert_exact(got["u"][:U], u, "unique_ids")
+    assert_exact(got["inv"][:n], inv, "inverse")
+    assert_exact(got["rows"][:U], rows, "rows")
+
+
 def test_pull_rows_reports_out_of_range_ids():
     R, D = 100, 4
     ids = np.array([3, 100, 7, -1, 3], np.int64)
