@@ -115,23 +115,6 @@ __device__ __forceinline__ int64_t claim_or_find(int64_t* slot_ids, int64_t mask
   return -1;
 }
 
-// Each block keeps the IDs it has resolved in LDS.  Zipf-skewed IDs repeat
-// over a block's positions; a repeat then needs neither the index probe nor
-// the row read, and a frequent ID that is new to the index is claimed with one
-// compare-and-swap per block instead of one per occurrence.  An entry belongs
-// for the whole launch to the first ID that takes it (a compare-and-swap on
-// the entry's ID word); that lane then writes the entry's value once: the
-// slot, and the slot's row or, where the slot has none yet, that it waits
-// for one.
-constexpr int kClaimCache = 2048;                     // entries (a power of two)
-constexpr unsigned long long kCacheUnset = ~0ull;     // value not written yet
-__device__ __forceinline__ unsigned long long lds_load(const unsigned long long* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-}
-__device__ __forceinline__ unsigned long long cache_value(int64_t slot, int32_t row) {
-  return (unsigned long long)(uint32_t)slot | ((unsigned long long)(uint32_t)row << 32);
-}
-
 // Block b takes positions [b * chunk, (b + 1) * chunk) in rounds of one
 // position per thread, and lists its slots and waiting positions in position
 // order at the same offsets of claimed_slots and pending; counts[b] and
@@ -141,14 +124,7 @@ hash_claim_kernel(int64_t* __restrict__ slot_ids, int32_t* __restrict__ slot_row
                   const int64_t* __restrict__ ids, int64_t n, int64_t chunk, int64_t* __restrict__ rows_out,
                   int2* __restrict__ pending, int32_t* __restrict__ claimed_slots, uint32_t* __restrict__ counts,
                   int32_t* __restrict__ err) {
-  __shared__ unsigned long long s_cid[kClaimCache];
-  __shared__ unsigned long long s_cval[kClaimCache];
   __shared__ uint32_t s_nc[kHashWaves], s_nw[kHashWaves];
-  for (int e = threadIdx.x; e < kClaimCache; e += kHashBlock) {
-    s_cid[e] = (unsigned long long)(int64_t)GBA_EMPTY_ID;
-    s_cval[e] = kCacheUnset;
-  }
-  __syncthreads();
   const int64_t p0 = (int64_t)blockIdx.x * chunk;
   const int64_t p1 = p0 + chunk < n ? p0 + chunk : n;
   const int w = threadIdx.x / kWave;
@@ -163,44 +139,29 @@ hash_claim_kernel(int64_t* __restrict__ slot_ids, int32_t* __restrict__ slot_row
       if (id == GBA_EMPTY_ID) {
         raise_error(err, GBA_DERR_ID_RANGE);
       } else {
-        const uint64_t h = mix64((uint64_t)id);
-        const int e = (int)(h >> 40) & (kClaimCache - 1);   // other bits than the slot's
-        // 64-bit LDS words read and written whole (relaxed atomics): a value
-        // that is not unset is the one its entry's owner wrote, for that ID
-        const unsigned long long v =
-            lds_load(&s_cid[e]) == (unsigned long long)id ? lds_load(&s_cval[e]) : kCacheUnset;
-        if (v != kCacheUnset) {
-          // resolved by this block before: a row never changes, and a slot
-          // without one is already listed for one
-          s = (int64_t)(uint32_t)v;
-          const int32_t r = (int32_t)(v >> 32);
-          if (r >= 0) row = r; else waits = true;
+        bool fresh = false;
+        s = claim_or_find(slot_ids, mask, id, mix64((uint64_t)id), &fresh);
+        if (s < 0) {
+          raise_error(err, GBA_DERR_TABLE_FULL);
         } else {
-          bool fresh = false;
-          s = claim_or_find(slot_ids, mask, id, h, &fresh);
-          if (s < 0) {
-            raise_error(err, GBA_DERR_TABLE_FULL);
+          const int32_t r = slot_rows[s];
+          if (r >= 0) {
+            row = r;   // rows are handed out only by the next launch: a row never changes
           } else {
-            const int32_t r = slot_rows[s];
-            if (r >= 0) {
-              row = r;   // rows are handed out only by the next launch: a row never changes
-            } else {
-              // the slot has no row yet: exactly one position lists it (kNoRow
-              // cannot turn into a row during this launch), and every position
-              // of the slot reads its row after the rows are handed out
-              if (r == kNoRow) claimed = atomicCAS(slot_rows + s, kNoRow, kPendingRow) == kNoRow;
-              waits = true;
-            }
-            constexpr unsigned long long kFree = (unsigned long long)(int64_t)GBA_EMPTY_ID;
-            if (lds_load(&s_cid[e]) == kFree && atomicCAS(&s_cid[e], kFree, (unsigned long long)id) == kFree)
-              __hip_atomic_store(&s_cval[e], cache_value(s, r >= 0 ? r : kPendingRow), __ATOMIC_RELAXED,
-                                 __HIP_MEMORY_SCOPE_WORKGROUP);
+            // the slot has no row yet: exactly one position lists it (kNoRow
+            // cannot turn into a row during this launch), and every position
+            // of the slot reads its row after the rows are handed out
+            if (r == kNoRow) claimed = atomicCAS(slot_rows + s, kNoRow, kPendingRow) == kNoRow;
+            waits = true;
           }
         }
       }
       if (!waits) rows_out[i] = row;
     }
     // block-ordered appends: the waves before this one, then the lanes before
+    // (a round with nothing to list, as every round once the IDs are known,
+    // ends at the first barrier)
+    if (!__syncthreads_or(claimed || waits)) continue;
     const uint64_t mc = __ballot(claimed), mw = __ballot(waits);
     if (lane_id() == 0) {
       s_nc[w] = (uint32_t)__popcll(mc);
@@ -218,7 +179,7 @@ hash_claim_kernel(int64_t* __restrict__ slot_ids, int32_t* __restrict__ slot_row
     }
     if (claimed) claimed_slots[p0 + bc + __popcll(mc & lanemask_lt())] = (int32_t)s;
     if (waits) pending[p0 + bw + __popcll(mw & lanemask_lt())] = make_int2((int32_t)i, (int32_t)s);
-    __syncthreads();   // s_nc and s_nw are rewritten by the next round
+    // s_nc and s_nw are rewritten only after the next round's first barrier
   }
   if (threadIdx.x == 0) {
     counts[blockIdx.x] = listed;
