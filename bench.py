@@ -389,7 +389,7 @@ def run_workload(name, args, torch, gba_step_mod, sdev, gba):
     end.record(stream)
     torch.cuda.synchronize()
     pull_ms = start.elapsed_time(end) / n_pull
-    # the same request replayed from a captured HIP graph: the 18 small launches
+    # the same request replayed from a captured HIP graph: the 17 small launches
     # of one request then cost no host work
     pg = torch.cuda.CUDAGraph()
     side = torch.cuda.Stream()
