@@ -37,6 +37,10 @@ constexpr int kSortWaves = kSortBlock / kWave;
 constexpr int kItemsFirst = 8;
 constexpr int kItemsRest = 16;
 constexpr int kItemsHotFirst = 8;   // the first pass of the hot-key plan
+// Below this many keys the plain plan keeps 2048-key tiles on every pass: the
+// later passes then have twice the blocks (at 256 K keys, 125 instead of 63
+// for 256 compute units), where long write runs matter less than filling the chip.
+constexpr int64_t kNarrowTilesBelow = int64_t(1) << 20;
 template <int ITEMS>
 constexpr int64_t tile_keys() { return (int64_t)kSortBlock * ITEMS; }
 constexpr int kRadix = 256;
@@ -977,6 +981,7 @@ hipError_t launch_sort_ids(const int64_t* ids, int64_t n, int64_t R, const SortP
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   int cur = 0;
+  const bool narrow = !plan.hot && n < kNarrowTilesBelow;
   // the narrowest digit goes first: the first pass sees keys in arrival order,
   // and fewer bins there mean longer runs of equal digits to write
   const int first_bits = plan.first_bits;
@@ -988,8 +993,9 @@ hipError_t launch_sort_ids(const int64_t* ids, int64_t n, int64_t R, const SortP
     const bool gap = plan.hot && last && !ht.split;   // merged output: the cold keys make room for the hot runs
     const int out = pass == 0 ? 0 : (gap ? 2 : 1 - cur);
     const void* kin = pass == 0 ? (const void*)ids : (const void*)keys[cur];
-    const int64_t tiles = ceil_div(n, pass > 0 ? tile_keys<kItemsRest>()
-                                               : (plan.hot ? tile_keys<kItemsHotFirst>() : tile_keys<kItemsFirst>()));
+    const int64_t tiles =
+        ceil_div(n, pass > 0 ? (narrow ? tile_keys<kItemsFirst>() : tile_keys<kItemsRest>())
+                             : (plan.hot ? tile_keys<kItemsHotFirst>() : tile_keys<kItemsFirst>()));
     const int tpw = hist_tiles_per_wave(tiles);
     const int chunk_tiles = kSortWaves * tpw;
     const int chunk_shift = chunk_tiles == 16 ? 4 : 2;
@@ -1009,6 +1015,8 @@ hipError_t launch_sort_ids(const int64_t* ids, int64_t n, int64_t R, const SortP
       GBA_HIST(true, kItemsFirst, kPlain, (const uint32_t*)nullptr)
     } else if (plan.hot) {
       GBA_HIST(false, kItemsRest, kCold, n_cold)
+    } else if (narrow) {
+      GBA_HIST(false, kItemsFirst, kPlain, (const uint32_t*)nullptr)
     } else {
       GBA_HIST(false, kItemsRest, kPlain, (const uint32_t*)nullptr)
     }
@@ -1036,6 +1044,11 @@ hipError_t launch_sort_ids(const int64_t* ids, int64_t n, int64_t R, const SortP
       hipLaunchKernelGGL((sort_scatter_kernel<false, kItemsRest, kCold>), grid, block, 0, stream, kin, vin,
                          keys[out], vals[out], (uint32_t*)nullptr, (uint32_t*)nullptr, n, n_cold, n, shift, bits,
                          R, (const uint32_t*)hist, (const uint32_t*)chunk, (const uint32_t*)total, ht, chunk_shift);
+    else if (narrow)
+      hipLaunchKernelGGL((sort_scatter_kernel<false, kItemsFirst, kPlain>), grid, block, 0, stream, kin, vin,
+                         keys[out], vals[out], (uint32_t*)nullptr, (uint32_t*)nullptr, n, (const uint32_t*)nullptr,
+                         n, shift, bits, R, (const uint32_t*)hist, (const uint32_t*)chunk, (const uint32_t*)total,
+                         ht, chunk_shift);
     else
       hipLaunchKernelGGL((sort_scatter_kernel<false, kItemsRest, kPlain>), grid, block, 0, stream, kin, vin,
                          keys[out], vals[out], (uint32_t*)nullptr, (uint32_t*)nullptr, n, (const uint32_t*)nullptr,
